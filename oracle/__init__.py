@@ -1,0 +1,36 @@
+"""fp64 CPU oracle for the LoRA-adapted linear layer -- TEST INFRASTRUCTURE.
+
+Only the tests, the package smoke check and the benchmark's CPU-baseline leg
+may import this package.  The product path (the HIP library and its Python
+binding) never calls it and shares no code with it.
+
+What it computes is the plain definition of the method, evaluated in float64
+on the exact decoded bfloat16 inputs:
+
+  Eq. 1 (Section 3, "Model Transfer API"):  output = W0 x + b0 + B A x,
+  written row-major over m tokens with the conventional LoRA scale s = alpha/r
+  (the configuration of Listing 3 carries LORA_R and LORA_ALPHA; with the
+  defaults r = alpha = 16 the scale is 1, exactly Eq. 1):
+
+      U  = X A^T                       [m, r]
+      Y  = X W^T + s U B^T             [m, n]     (b0 = 0)
+
+  and its chain-rule backward for the trainable A, B (W0 frozen, so no dW;
+  Section 3 names B and A as the trainable weights), for an upstream dY:
+
+      dU = s dY B                      [m, r]
+      dX = dY W + dU A                 [m, k]
+      dB = s dY^T U                    [n, r]
+      dA = dU^T X                      [r, k]
+
+Each step is one numpy float64 matrix product; there is no blocking, fusion or
+reordering beyond the definition.  Pins that tie this to the paper and to the
+mathematics (merge identity, B = 0 and A = 0 invariants, finite differences,
+a hand-worked example, brute-force loops, closed forms) live in
+tests/test_oracle_pins.py.
+"""
+from .lora_oracle import (bf16_bits_to_f64, lora_scale, lora_forward, lora_backward,
+                          lora_forward_rows, lora_backward_rows, f64_to_bf16_bits)
+
+__all__ = ["bf16_bits_to_f64", "lora_scale", "lora_forward", "lora_backward",
+           "lora_forward_rows", "lora_backward_rows", "f64_to_bf16_bits"]

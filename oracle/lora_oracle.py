@@ -1,0 +1,94 @@
+"""Plain fp64 oracle of the LoRA linear forward and backward -- TEST INFRASTRUCTURE.
+
+Not part of the product path; see the package docstring for who may call it.
+All arrays are row-major numpy arrays.  Inputs arrive as bfloat16 bit patterns
+(uint16) and are decoded exactly to float64 here; every product below is a
+float64 numpy matmul.
+"""
+from __future__ import annotations
+
+from typing import Optional, Sequence, Tuple
+
+import numpy as np
+
+
+def bf16_bits_to_f64(bits: np.ndarray) -> np.ndarray:
+    """Exact decode of bfloat16 bit patterns: the 16 bits are the top half of a float32."""
+    u32 = np.asarray(bits, dtype=np.uint16).astype(np.uint32) << 16
+    return u32.view(np.float32).astype(np.float64)
+
+
+def f64_to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """Round float64 values to bfloat16 (nearest, ties to even) for bit-exact checks.
+
+    Goes through float32 first; that double rounding is harmless for the
+    small-integer values this is used on."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    return ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
+
+
+def lora_scale(alpha: float, r: int) -> float:
+    """LoRA scale s = alpha / r.  The paper's Eq. 1 shows no scale; its config
+    (Listing 3) carries LORA_ALPHA and LORA_R, whose defaults (16, 16) give s = 1,
+    which is Eq. 1 as printed."""
+    return float(alpha) / float(r)
+
+
+def _f64(a: np.ndarray) -> np.ndarray:
+    a = np.asarray(a)
+    if a.dtype == np.uint16:
+        return bf16_bits_to_f64(a)
+    return a.astype(np.float64, copy=False)
+
+
+def lora_forward(X, W, A, B, alpha: float) -> Tuple[np.ndarray, np.ndarray]:
+    """Eq. 1 (Section 3): U = X A^T; Y = X W^T + s U B^T, with b0 = 0.
+
+    X [m,k], W [n,k] (frozen W0, stored out x in), A [r,k], B [n,r].
+    Returns (U [m,r], Y [m,n]) in float64."""
+    X, W, A, B = _f64(X), _f64(W), _f64(A), _f64(B)
+    s = lora_scale(alpha, A.shape[0])
+    U = X @ A.T
+    Y = X @ W.T + s * (U @ B.T)
+    return U, Y
+
+
+def lora_backward(dY, X, W, A, B, alpha: float
+                  ) -> Tuple[np.ndarray, np.ndarray, np.ndarray, np.ndarray]:
+    """Chain rule through Eq. 1 for the trainable A and B (W0 frozen: no dW).
+
+    Returns (dU [m,r], dX [m,k], dA [r,k], dB [n,r]) in float64, where
+    dU = s dY B is the gradient of the rank-r activation U = X A^T."""
+    dY, X, W, A, B = _f64(dY), _f64(X), _f64(W), _f64(A), _f64(B)
+    s = lora_scale(alpha, A.shape[0])
+    U = X @ A.T
+    dU = s * (dY @ B)
+    dX = dY @ W + dU @ A
+    dB = s * (dY.T @ U)
+    dA = dU.T @ X
+    return dU, dX, dA, dB
+
+
+def lora_forward_rows(X, W, A, B, alpha: float, rows: Sequence[int]
+                      ) -> Tuple[np.ndarray, np.ndarray]:
+    """The forward restricted to the token rows `rows` (each output row of Eq. 1
+    depends only on the same row of X).  Returns (U[rows], Y[rows])."""
+    idx = np.asarray(rows, dtype=np.int64)
+    return lora_forward(np.asarray(X)[idx], W, A, B, alpha)
+
+
+def lora_backward_rows(dY, X, W, A, B, alpha: float, rows: Optional[Sequence[int]]
+                       ) -> Tuple[np.ndarray, np.ndarray, np.ndarray, np.ndarray]:
+    """Backward with dX evaluated only at token rows `rows` (dX row i depends only
+    on row i of dY).  dU, dA and dB reduce over all tokens and are returned whole.
+
+    Returns (dU [m,r], dX[rows] [len(rows),k], dA [r,k], dB [n,r])."""
+    dY64, X64, W64, A64, B64 = _f64(dY), _f64(X), _f64(W), _f64(A), _f64(B)
+    s = lora_scale(alpha, A64.shape[0])
+    U = X64 @ A64.T
+    dU = s * (dY64 @ B64)
+    idx = np.arange(dY64.shape[0]) if rows is None else np.asarray(rows, dtype=np.int64)
+    dX = dY64[idx] @ W64 + dU[idx] @ A64
+    dB = s * (dY64.T @ U)
+    dA = dU.T @ X64
+    return dU, dX, dA, dB
