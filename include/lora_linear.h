@@ -1,0 +1,118 @@
+/*
+ * lora_linear.h -- C ABI of the LoRA-adapted linear layer for AMD MI355X (gfx950).
+ *
+ * The operation is Eq. 1 of JORA (arXiv 2403.11366, Section 3, "Model Transfer
+ * API"): output = W0 x + b0 + B A x, where W0 is a frozen weight and the rank-r
+ * factors B and A are the only trainable parameters.  This library evaluates it
+ * row-major over m tokens, without bias, with the conventional LoRA scale
+ * s = alpha / r (the configuration of Listing 3 carries LORA_R and LORA_ALPHA):
+ *
+ *     U  = X A^T                 [m, r]   (saved for the backward)
+ *     Y  = X W^T + s U B^T       [m, n]
+ *
+ * and its chain-rule backward for an upstream gradient dY (W0 frozen: no dW):
+ *
+ *     dU = s dY B,  dX = dY W + dU A,  dB = s dY^T U,  dA = dU^T X.
+ *
+ * Conventions shared by every entry point:
+ *   - Matrices are dense, row-major, leading dimension = row length.
+ *   - Matrix pointers are DEVICE pointers (hipMalloc'd or from a framework's
+ *     device allocator) and must be 16-byte aligned.  The caller owns every
+ *     buffer, including the workspace; the library allocates nothing, frees
+ *     nothing and never synchronises.
+ *   - bfloat16 values are passed as raw 16-bit patterns (lora_bf16).
+ *   - Shapes: m >= 1 (any value; tails are masked); n, k >= 8 and multiples of
+ *     8 (rows must be 16-byte aligned); 1 <= r <= 64.
+ *   - `stream` is a hipStream_t (NULL = the default stream).  Calls enqueue
+ *     kernels on it and return; results are valid once the stream has been
+ *     synchronised.  Calls that share buffers must be ordered by the caller.
+ *   - Outputs are overwritten (no accumulation into existing contents).
+ *   - All arguments are validated before anything is enqueued.  On an error
+ *     nothing is launched and every output is left untouched.  No C++ exception
+ *     crosses this interface.
+ *   - Arithmetic: bf16 operands, fp32 accumulation on the matrix cores, bf16
+ *     outputs rounded to nearest-even.  The rank-r intermediates U and dU enter
+ *     the matrix cores as a bf16 high part plus a bf16 low part, so they keep
+ *     about 16 significant bits.  Reductions use a fixed order: repeated calls
+ *     on the same inputs give bit-identical results.
+ */
+#ifndef LORA_LINEAR_H
+#define LORA_LINEAR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef uint16_t lora_bf16;
+
+typedef enum {
+  LORA_OK = 0,
+  LORA_ERR_NULL = 1,        /* a required pointer is NULL */
+  LORA_ERR_SHAPE = 2,       /* m < 1, n or k < 8 or not a multiple of 8, r < 1, or size overflow */
+  LORA_ERR_ALIGN = 3,       /* a matrix pointer is not 16-byte aligned */
+  LORA_ERR_UNSUPPORTED = 4, /* r > 64, or a dimension beyond the supported range */
+  LORA_ERR_WORKSPACE = 5,   /* workspace missing or smaller than lora_linear_bwd_workspace_size() */
+  LORA_ERR_ALIAS = 6,       /* an output overlaps an input or another output */
+  LORA_ERR_HIP = 7          /* the HIP runtime reported an error at launch */
+} lora_status;
+
+/*
+ * Forward of Eq. 1 (Section 3): Y = X W^T + (alpha/r) (X A^T) B^T, and U = X A^T.
+ *
+ *   X  [m, k]  layer input (bf16), read only
+ *   W  [n, k]  frozen weight W0, stored [out, in] (bf16), read only
+ *   A  [r, k]  LoRA down projection (bf16), read only
+ *   B  [n, r]  LoRA up projection (bf16), read only
+ *   Y  [m, n]  output (bf16), written
+ *   U  [m, r]  output (fp32), written: the unscaled X A^T, needed by the backward
+ *   alpha      LoRA alpha; the scale is s = alpha / r, computed in fp32
+ *
+ * One kernel: a bf16 matrix-core GEMM over k that streams each X tile through
+ * LDS once for both W and A, then adds s U B^T to the accumulators in its
+ * epilogue before rounding Y to bf16.
+ */
+lora_status lora_linear_fwd(const lora_bf16* X, const lora_bf16* W, const lora_bf16* A,
+                            const lora_bf16* B, lora_bf16* Y, float* U,
+                            int64_t m, int64_t n, int64_t k, int64_t r, float alpha,
+                            void* stream);
+
+/*
+ * Bytes of device workspace lora_linear_bwd needs for this shape (0 on an
+ * invalid shape).  The workspace holds transposed and split copies of the
+ * rank-r operands and the fixed-order split-K partial sums of dA and dB.
+ */
+size_t lora_linear_bwd_workspace_size(int64_t m, int64_t n, int64_t k, int64_t r);
+
+/*
+ * Backward of Eq. 1 for the trainable A and B (Section 3: B and A are the
+ * trainable weights; W0 is frozen, so no dW is formed).
+ *
+ *   dY [m, n]  upstream gradient (bf16), read only
+ *   X  [m, k]  the forward's input (bf16), read only
+ *   W, A, B    as in lora_linear_fwd, read only
+ *   U  [m, r]  the forward's U output (fp32), read only
+ *   dX [m, k]  output (bf16), written:  dY W + dU A, with dU = s dY B
+ *   dA [r, k]  output (fp32), written:  dU^T X
+ *   dB [n, r]  output (fp32), written:  s dY^T U
+ *   workspace  device buffer of at least lora_linear_bwd_workspace_size(m,n,k,r)
+ *              bytes, 16-byte aligned; contents on entry are ignored.  It must not
+ *              be used concurrently by another call.
+ */
+lora_status lora_linear_bwd(const lora_bf16* dY, const lora_bf16* X, const lora_bf16* W,
+                            const lora_bf16* A, const lora_bf16* B, const float* U,
+                            lora_bf16* dX, float* dA, float* dB,
+                            void* workspace, size_t workspace_bytes,
+                            int64_t m, int64_t n, int64_t k, int64_t r, float alpha,
+                            void* stream);
+
+/* Static, human-readable name of a status code. */
+const char* lora_status_string(lora_status s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LORA_LINEAR_H */

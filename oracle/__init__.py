@@ -29,8 +29,8 @@ mathematics (merge identity, B = 0 and A = 0 invariants, finite differences,
 a hand-worked example, brute-force loops, closed forms) live in
 tests/test_oracle_pins.py.
 """
-from .lora_oracle import (bf16_bits_to_f64, lora_scale, lora_forward, lora_backward,
-                          lora_forward_rows, lora_backward_rows, f64_to_bf16_bits)
+from .lora_oracle import (bf16_bits_to_f64, lora_scale, lora_rank_activation, lora_forward,
+                          lora_backward, lora_forward_rows, lora_backward_rows, f64_to_bf16_bits)
 
-__all__ = ["bf16_bits_to_f64", "lora_scale", "lora_forward", "lora_backward",
-           "lora_forward_rows", "lora_backward_rows", "f64_to_bf16_bits"]
+__all__ = ["bf16_bits_to_f64", "lora_scale", "lora_rank_activation", "lora_forward",
+           "lora_backward", "lora_forward_rows", "lora_backward_rows", "f64_to_bf16_bits"]

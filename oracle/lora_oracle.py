@@ -41,6 +41,11 @@ def _f64(a: np.ndarray) -> np.ndarray:
     return a.astype(np.float64, copy=False)
 
 
+def lora_rank_activation(X, A) -> np.ndarray:
+    """The rank-r activation U = X A^T of Eq. 1 (the A x term, row-major), [m, r]."""
+    return _f64(X) @ _f64(A).T
+
+
 def lora_forward(X, W, A, B, alpha: float) -> Tuple[np.ndarray, np.ndarray]:
     """Eq. 1 (Section 3): U = X A^T; Y = X W^T + s U B^T, with b0 = 0.
 

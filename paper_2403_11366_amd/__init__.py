@@ -1,0 +1,135 @@
+"""LoRA-adapted linear layer (JORA, arXiv 2403.11366, Eq. 1) for AMD MI355X.
+
+Thin Python binding of the C ABI in include/lora_linear.h.  It only marshals
+arguments: every step of the computation runs in the HIP kernels of
+liblora_linear.so (built in-tree by ``python -m paper_2403_11366_amd.build``).
+Tensors are torch device tensors (torch is used for device memory and
+streams); bf16 matrices are passed as their raw 16-bit patterns.
+
+If the library has not been built, every call raises; there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+__all__ = [
+    "LoraError", "lib_path", "load_library", "lora_linear_fwd", "lora_linear_bwd",
+    "lora_linear_bwd_workspace_size", "lora_status_string", "STATUS",
+]
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_NAME = "liblora_linear.so"
+_lib = None
+
+STATUS = {0: "LORA_OK", 1: "LORA_ERR_NULL", 2: "LORA_ERR_SHAPE", 3: "LORA_ERR_ALIGN",
+          4: "LORA_ERR_UNSUPPORTED", 5: "LORA_ERR_WORKSPACE", 6: "LORA_ERR_ALIAS", 7: "LORA_ERR_HIP"}
+
+
+class LoraError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {STATUS.get(status, status)} ({lora_status_string(status)})")
+
+
+def lib_path() -> str:
+    return os.path.join(_HERE, _LIB_NAME)
+
+
+def load_library() -> ctypes.CDLL:
+    """Load liblora_linear.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    path = lib_path()
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with `python -m paper_2403_11366_amd.build`")
+    lib = ctypes.CDLL(path)
+    p, i64, f32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_float, ctypes.c_size_t
+    lib.lora_linear_fwd.argtypes = [p, p, p, p, p, p, i64, i64, i64, i64, f32, p]
+    lib.lora_linear_fwd.restype = ctypes.c_int
+    lib.lora_linear_bwd_workspace_size.argtypes = [i64, i64, i64, i64]
+    lib.lora_linear_bwd_workspace_size.restype = sz
+    lib.lora_linear_bwd.argtypes = [p, p, p, p, p, p, p, p, p, p, sz, i64, i64, i64, i64, f32, p]
+    lib.lora_linear_bwd.restype = ctypes.c_int
+    lib.lora_status_string.argtypes = [ctypes.c_int]
+    lib.lora_status_string.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+def lora_status_string(status: int) -> str:
+    return load_library().lora_status_string(int(status)).decode()
+
+
+def lora_linear_bwd_workspace_size(m: int, n: int, k: int, r: int) -> int:
+    return int(load_library().lora_linear_bwd_workspace_size(m, n, k, r))
+
+
+def _ptr(t) -> int:
+    return 0 if t is None else int(t.data_ptr())
+
+
+def _stream_handle(stream) -> Optional[int]:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _check(t, name, dtype, shape):
+    import torch
+    if t.dtype != dtype:
+        raise TypeError(f"{name}: expected {dtype}, got {t.dtype}")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name}: expected shape {tuple(shape)}, got {tuple(t.shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name}: must be contiguous (row-major)")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name}: must be a device tensor")
+    return torch
+
+
+def lora_linear_fwd(X, W, A, B, Y, U, alpha: float, stream=None) -> None:
+    """Y = X W^T + (alpha/r) (X A^T) B^T and U = X A^T (see include/lora_linear.h).
+
+    X [m,k], W [n,k], A [r,k], B [n,r], Y [m,n]: torch.bfloat16; U [m,r]: torch.float32."""
+    import torch
+    m, k = X.shape
+    n, r = W.shape[0], A.shape[0]
+    for t, name, dt, shp in ((X, "X", torch.bfloat16, (m, k)), (W, "W", torch.bfloat16, (n, k)),
+                             (A, "A", torch.bfloat16, (r, k)), (B, "B", torch.bfloat16, (n, r)),
+                             (Y, "Y", torch.bfloat16, (m, n)), (U, "U", torch.float32, (m, r))):
+        _check(t, name, dt, shp)
+    st = load_library().lora_linear_fwd(_ptr(X), _ptr(W), _ptr(A), _ptr(B), _ptr(Y), _ptr(U),
+                                        m, n, k, r, float(alpha), _stream_handle(stream))
+    if st != 0:
+        raise LoraError(st, "lora_linear_fwd")
+
+
+def lora_linear_bwd(dY, X, W, A, B, U, dX, dA, dB, workspace, alpha: float, stream=None) -> None:
+    """dX = dY W + dU A, dA = dU^T X, dB = s dY^T U with dU = s dY B, s = alpha/r.
+
+    dY [m,n], X [m,k], W [n,k], A [r,k], B [n,r], dX [m,k]: torch.bfloat16;
+    U [m,r], dA [r,k], dB [n,r]: torch.float32; workspace: a device tensor of at
+    least lora_linear_bwd_workspace_size(m, n, k, r) bytes."""
+    import torch
+    m, n = dY.shape
+    k, r = X.shape[1], A.shape[0]
+    for t, name, dt, shp in ((dY, "dY", torch.bfloat16, (m, n)), (X, "X", torch.bfloat16, (m, k)),
+                             (W, "W", torch.bfloat16, (n, k)), (A, "A", torch.bfloat16, (r, k)),
+                             (B, "B", torch.bfloat16, (n, r)), (U, "U", torch.float32, (m, r)),
+                             (dX, "dX", torch.bfloat16, (m, k)), (dA, "dA", torch.float32, (r, k)),
+                             (dB, "dB", torch.float32, (n, r))):
+        _check(t, name, dt, shp)
+    if workspace.device.type != "cuda" or not workspace.is_contiguous():
+        raise ValueError("workspace: must be a contiguous device tensor")
+    ws_bytes = workspace.numel() * workspace.element_size()
+    st = load_library().lora_linear_bwd(_ptr(dY), _ptr(X), _ptr(W), _ptr(A), _ptr(B), _ptr(U),
+                                        _ptr(dX), _ptr(dA), _ptr(dB), _ptr(workspace), ws_bytes,
+                                        m, n, k, r, float(alpha), _stream_handle(stream))
+    if st != 0:
+        raise LoraError(st, "lora_linear_bwd")

@@ -1,0 +1,121 @@
+// Device-side building blocks shared by the LoRA-linear kernels (gfx950 only).
+//
+// Matrix-core primitive: v_mfma_f32_16x16x32_bf16.  With lane l = 16*g + c
+// (g = l / 16, c = l % 16) the operand and result layouts are:
+//   A operand (16 x 32, M x K): lane holds row c, k = 8g .. 8g+7
+//   B operand (32 x 16, K x N): lane holds column c, k = 8g .. 8g+7
+//   result    (16 x 16):        lane holds column c, rows 4g .. 4g+3
+// Because both operands carry k in the same positions, any matrix stored with
+// k contiguous is read with one 16-byte load per lane.
+//
+// LDS tiles come in two forms:
+//   * k-contiguous tiles: rows of 64 bf16 (128 bytes = 8 chunks of 16 bytes).
+//     Chunk q of row p is stored at chunk position q ^ ((p >> 1) & 7), so the
+//     16 lanes that read one 16-byte chunk from 16 consecutive rows hit
+//     distinct banks.
+//   * mn-contiguous tiles (k is the row index): rows of COLS bf16.  Chunk q of
+//     row p is stored at position q ^ (2 * (p & 3) + 8 * ((p >> 3) & 1)).  They
+//     are read with ds_read_b64_tr_b16, which hands lane i of each 16-lane group
+//     column i of a 4 x 16 block of rows, i.e. one matrix-core operand column
+//     with 4 consecutive k; two such reads give the 8 k of a lane.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace lora {
+
+typedef uint16_t u16;
+typedef short short8 __attribute__((ext_vector_type(8)));
+typedef short short4v __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef int int4v __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) short4v lds_short4v;
+
+// A buffer offset at or beyond every resource size used here: loads at it
+// return zero.  Resource sizes are capped below it.
+constexpr uint32_t kOOB = 0x80000000u;
+constexpr uint32_t kMaxRecords = 0x7FFFFF00u;
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint64_t nbytes) {
+  uint32_t n = nbytes > kMaxRecords ? kMaxRecords : (uint32_t)nbytes;
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)n, 0x00020000);
+}
+
+// 16-byte load through a buffer resource; out-of-range offsets read as zero.
+__device__ __forceinline__ int4v buf_load16(__amdgpu_buffer_rsrc_t rs, uint32_t byte_off) {
+  return __builtin_bit_cast(int4v, __builtin_amdgcn_raw_buffer_load_b128(rs, byte_off, 0, 0));
+}
+
+__device__ __forceinline__ floatx4 mfma16x16x32(short8 a, short8 b, floatx4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16((bf16x8)a, (bf16x8)b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ u16 f32_to_bf16(float f) {  // round to nearest even (v_cvt_pk_bf16_f32)
+  return __builtin_bit_cast(u16, (__bf16)f);
+}
+__device__ __forceinline__ float bf16_to_f32(u16 h) {
+  return __builtin_bit_cast(float, (uint32_t)h << 16);
+}
+
+// ---- k-contiguous LDS tiles (rows of 128 bytes) ----------------------------
+__device__ __forceinline__ int kc_swz(int row) { return (row >> 1) & 7; }
+
+__device__ __forceinline__ uint32_t kc_offset(int row, int chunk) {
+  return (uint32_t)(row * 128 + ((chunk ^ kc_swz(row)) << 4));
+}
+
+__device__ __forceinline__ short8 kc_read(const char* tile, int row, int chunk) {
+  return *reinterpret_cast<const short8*>(tile + kc_offset(row, chunk));
+}
+
+// ---- mn-contiguous LDS tiles (rows of COLS bf16, COLS >= 128) --------------
+__device__ __forceinline__ int mc_swz(int row) { return 2 * (row & 3) + 8 * ((row >> 3) & 1); }
+
+template <int COLS>
+__device__ __forceinline__ uint32_t mc_offset(int row, int chunk) {
+  return (uint32_t)(row * (COLS * 2) + ((chunk ^ mc_swz(row)) << 4));
+}
+
+// Matrix-core operand (A or B layout) of 16 columns x 32 k from an mn-contiguous
+// tile whose rows are k: lane (g, c) receives column col0 + c, k rows
+// krow0 + 8g .. 8g+7.
+template <int COLS>
+__device__ __forceinline__ short8 mc_read_tr(const char* tile, int krow0, int col0, int lane) {
+  const int g = lane >> 4, j = lane & 15;
+  const int e = j >> 2, q = j & 3;            // this lane addresses row e of 4, 4-column piece q
+  const int col = col0 + 4 * q;
+  short4v lo, hi;
+  {
+    const int row = krow0 + 8 * g + e;
+    const char* p = tile + mc_offset<COLS>(row, col >> 3) + (col & 7) * 2;
+    lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4v*)(p));
+  }
+  {
+    const int row = krow0 + 8 * g + 4 + e;
+    const char* p = tile + mc_offset<COLS>(row, col >> 3) + (col & 7) * 2;
+    hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4v*)(p));
+  }
+  return short8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+}
+
+// Block index -> tile coordinates.  Workgroups are dealt to the 8 XCDs round
+// robin (block b runs on XCD b % 8); the first step renumbers blocks so each
+// XCD receives a contiguous range of tile ids, the second walks tiles in
+// groups of `group` tile-rows so neighbours share operand panels in that XCD's L2.
+__device__ __forceinline__ void tile_coords(int tiles_m, int tiles_n, int group, int& tm, int& tn) {
+  const int nb = gridDim.x, b = blockIdx.x;
+  const int xcd = b & 7, idx = b >> 3;
+  const int per = nb >> 3, rem = nb & 7;
+  const int lid = (xcd < rem) ? xcd * (per + 1) + idx : rem * (per + 1) + (xcd - rem) * per + idx;
+  const int gsize = group * tiles_n;
+  const int gi = lid / gsize;
+  const int first_m = gi * group;
+  const int gm = min(tiles_m - first_m, group);
+  const int in = lid - gi * gsize;
+  tm = first_m + in % gm;
+  tn = in / gm;
+}
+
+}  // namespace lora

@@ -1,0 +1,115 @@
+// Internal interface between the C ABI (argument checks, workspace layout) and
+// the kernel launchers.  Shapes here have already been validated.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace lora {
+
+// Rank padded to the matrix-core granularity of 16 (r in 1..64 -> 16..64).
+inline int pad_rank(int64_t r) { return (int)((r + 15) / 16) * 16; }
+
+// Token count padded to the 64-token chunk of the split-K reductions.
+inline int64_t pad_tokens(int64_t m) { return (m + 63) / 64 * 64; }
+
+enum GemmTile { TILE_256x256 = 0, TILE_256x128 = 1, TILE_128x128 = 2 };
+
+// Pick the output tile of the two large GEMMs for an M x N output.  Every
+// workgroup of these kernels fills one compute unit (LDS-limited), so the
+// kernel runs in ceil(tiles / 256) rounds on 256 CUs; the estimate is rounds
+// times the per-tile work divided by a relative per-tile efficiency (larger
+// tiles read less LDS and L2 per flop).
+inline GemmTile choose_gemm_tile(int64_t M, int64_t N) {
+  struct C { GemmTile t; int bm, bn; double eff; };
+  const C cands[3] = {{TILE_256x256, 256, 256, 1.0}, {TILE_256x128, 256, 128, 0.9},
+                      {TILE_128x128, 128, 128, 0.75}};
+  GemmTile best = TILE_256x256;
+  double best_cost = 1e300;
+  for (const C& c : cands) {
+    const int64_t tiles = ((M + c.bm - 1) / c.bm) * ((N + c.bn - 1) / c.bn);
+    const double rounds = (double)((tiles + 255) / 256);
+    const double cost = rounds * c.bm * c.bn / c.eff;
+    if (cost < best_cost) { best_cost = cost; best = c.t; }
+  }
+  return best;
+}
+
+// Split-K plan of a token reduction out[t][c] = sum_i P[t][i] Q[i][c] over
+// `cols` columns: columns in tiles of kRedCols, tokens in `splits` ranges of
+// `span` tokens (a multiple of 64).  Splits are capped so the fp32 partial
+// sums stay at most 1/8 of the bytes of Q.
+constexpr int kRedCols = 128;
+struct RedPlan { int64_t span; int splits; int col_tiles; };
+inline RedPlan plan_reduction(int64_t m, int64_t cols, int rp) {
+  const int64_t mp = pad_tokens(m);
+  const int col_tiles = (int)((cols + kRedCols - 1) / kRedCols);
+  int64_t s = (1024 + col_tiles - 1) / col_tiles;
+  int64_t cap = m / (16 * (int64_t)rp);
+  if (cap < 1) cap = 1;
+  if (s > cap) s = cap;
+  if (s > mp / 64) s = mp / 64;
+  if (s < 1) s = 1;
+  int64_t span = (mp + s - 1) / s;
+  span = (span + 63) / 64 * 64;
+  const int splits = (int)((mp + span - 1) / span);
+  return RedPlan{span, splits, col_tiles};
+}
+
+// Backward workspace, byte offsets of each region (256-byte aligned).
+struct BwdLayout {
+  size_t bt;     // Bt   [RP][n]      bf16: B transposed, zero for t >= r
+  size_t ut2;    // Ut2  [2RP][mp]    bf16: U^T as high part (rows 0..RP) and low part
+  size_t du2;    // dU2  [mp][2RP]    bf16: dU as high part (cols 0..RP) and low part
+  size_t dut2;   // dUt2 [2RP][mp]    bf16: dU^T, high and low parts
+  size_t pb;     // partial dB^T [splits_b][RP][n] fp32
+  size_t pa;     // partial dA   [splits_a][RP][k] fp32
+  size_t total;
+  RedPlan plan_b, plan_a;
+  int rp;
+  int64_t mp;
+};
+
+inline size_t align256(size_t x) { return (x + 255) / 256 * 256; }
+
+inline BwdLayout bwd_layout(int64_t m, int64_t n, int64_t k, int64_t r) {
+  BwdLayout L;
+  L.rp = pad_rank(r);
+  L.mp = pad_tokens(m);
+  L.plan_b = plan_reduction(m, n, L.rp);
+  L.plan_a = plan_reduction(m, k, L.rp);
+  const size_t rp = (size_t)L.rp, mp = (size_t)L.mp;
+  size_t off = 0;
+  L.bt = off;   off = align256(off + rp * (size_t)n * 2);
+  L.ut2 = off;  off = align256(off + 2 * rp * mp * 2);
+  L.du2 = off;  off = align256(off + mp * 2 * rp * 2);
+  L.dut2 = off; off = align256(off + 2 * rp * mp * 2);
+  L.pb = off;   off = align256(off + (size_t)L.plan_b.splits * rp * (size_t)n * 4);
+  L.pa = off;   off = align256(off + (size_t)L.plan_a.splits * rp * (size_t)k * 4);
+  L.total = off;
+  return L;
+}
+
+struct FwdArgs {
+  const uint16_t *X, *W, *A, *B;
+  uint16_t* Y;
+  float* U;
+  int64_t m, n, k, r;
+  float s;
+};
+
+struct BwdArgs {
+  const uint16_t *dY, *X, *W, *A, *B;
+  const float* U;
+  uint16_t* dX;
+  float *dA, *dB;
+  char* ws;
+  int64_t m, n, k, r;
+  float s;
+};
+
+hipError_t launch_fwd(const FwdArgs& a, hipStream_t st);
+hipError_t launch_bwd(const BwdArgs& a, hipStream_t st);
+
+}  // namespace lora

@@ -1,0 +1,177 @@
+"""HIP path vs the fp64 oracle, through the C ABI, on seeded inputs.
+
+Bars: relative Frobenius error <= 5e-3 for Y and dX, <= 1e-2 for dA and dB,
+<= 1e-5 for the fp32 U; bit-exact where the inputs make every partial sum an
+exactly representable integer.  Full-size workloads compare Y and dX on
+sampled token rows (tile edges, the ragged tail, random rows) and U, dA, dB
+whole.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from lora_synth import CONFIGS, Shape, gen_inputs, gen_ternary_inputs
+from gpu_harness import assert_within, compare, f64, rel, run_gpu, sample_rows
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2403_11366_amd as lora
+    lora.load_library()  # raises if the HIP library is missing: no fallback
+
+
+def _shape_id(s: Shape):
+    return f"{s.name}-m{s.m}n{s.n}k{s.k}r{s.r}"
+
+
+def test_tiny_config_full():
+    shape = CONFIGS["tiny"][0]
+    t = gen_inputs(shape)
+    out = run_gpu(t, shape)
+    errs = compare(t, shape, out)
+    print("tiny", errs)
+    assert_within(errs, "tiny")
+
+
+RAGGED = [
+    Shape("ragged", 1, 64, 64, 8, 16.0, 101),
+    Shape("ragged", 7, 64, 64, 1, 2.0, 102),
+    Shape("ragged", 33, 8, 8, 3, 6.0, 103),
+    Shape("ragged", 257, 136, 200, 16, 32.0, 104),
+    Shape("ragged", 300, 520, 264, 40, 80.0, 105),
+    Shape("ragged", 129, 1024, 1032, 64, 128.0, 106),
+    Shape("ragged", 1000, 128, 8, 8, 16.0, 107),
+    Shape("ragged", 2051, 4096, 4096, 8, 16.0, 108),
+    Shape("ragged", 4100, 2048, 1024, 24, 48.0, 109),
+]
+
+
+@pytest.mark.parametrize("shape", RAGGED, ids=_shape_id)
+def test_ragged_shapes(shape):
+    t = gen_inputs(shape, b_std=0.5)
+    out = run_gpu(t, shape)
+    rows = None if shape.m * shape.n * shape.k < 4e9 else sample_rows(shape.m, shape.seed)
+    errs = compare(t, shape, out, rows)
+    print(_shape_id(shape), errs)
+    assert_within(errs, _shape_id(shape))
+
+
+FULL = [s for name in ("llama2_7b_q_proj", "llama2_7b_up_proj", "llama2_7b_down_proj",
+                       "llama2_13b_layer") for s in CONFIGS[name]]
+
+
+@pytest.mark.parametrize("shape", FULL, ids=_shape_id)
+def test_full_size_configs(shape):
+    t = gen_inputs(shape)
+    out = run_gpu(t, shape)
+    for key in out:
+        assert not np.isnan(out[key].astype(np.float64) if out[key].dtype != np.uint16 else f64(out[key])).any(), key
+    errs = compare(t, shape, out, sample_rows(shape.m, shape.seed))
+    print(_shape_id(shape), errs)
+    assert_within(errs, _shape_id(shape))
+
+
+def _mirror_tile(M, N):
+    """Mirror of the library's GEMM tile heuristic (used only to check coverage)."""
+    best, best_cost = None, None
+    for name, bm, bn, eff in (("256x256", 256, 256, 1.0), ("256x128", 256, 128, 0.9),
+                              ("128x128", 128, 128, 0.75)):
+        tiles = -(-M // bm) * -(-N // bn)
+        cost = -(-tiles // 256) * bm * bn / eff
+        if best_cost is None or cost < best_cost:
+            best, best_cost = name, cost
+    return best
+
+
+EXACT = [
+    Shape("exact", 257, 1024, 4096, 8, 16.0, 201),
+    Shape("exact", 2040, 4096, 4096, 16, 32.0, 202),
+    Shape("exact", 2048, 2048, 4104, 64, 128.0, 203),
+    Shape("exact", 4100, 11008, 512, 16, 32.0, 204),
+    Shape("exact", 4096, 512, 11008, 8, 16.0, 205),
+]
+
+
+@pytest.mark.parametrize("shape", EXACT, ids=_shape_id)
+def test_integer_inputs_bit_exact(shape):
+    """Sparse {-1,0,1} inputs and s = 2: every sum is a small integer, exact in
+    bf16 and fp32 whatever the summation order, so GPU == oracle bit for bit."""
+    t = gen_ternary_inputs(shape.m, shape.n, shape.k, shape.r, shape.seed, density=0.01)
+    U, Y = oracle.lora_forward(t["X"], t["W"], t["A"], t["B"], shape.alpha)
+    dU, dX, dA, dB = oracle.lora_backward(t["dY"], t["X"], t["W"], t["A"], t["B"], shape.alpha)
+    for name, v in (("U", U), ("Y", Y), ("dU", dU), ("dX", dX), ("dA", dA), ("dB", dB)):
+        assert np.array_equal(v, np.round(v)), name
+    assert np.abs(Y).max() <= 256 and np.abs(dX).max() <= 256 and np.abs(dU).max() <= 256
+    out = run_gpu(t, shape)
+    assert np.array_equal(out["Y"], oracle.f64_to_bf16_bits(Y))
+    assert np.array_equal(out["dX"], oracle.f64_to_bf16_bits(dX))
+    assert np.array_equal(out["U"].astype(np.float64), U)
+    assert np.array_equal(out["dA"].astype(np.float64), dA)
+    assert np.array_equal(out["dB"].astype(np.float64), dB)
+
+
+def test_hand_example_embedded():
+    """The first hand-worked example of tests/golden, zero-padded to 64 x 64 x 64."""
+    shape = Shape("hand", 64, 64, 64, 1, 2.0, 0)
+    z = lambda r, c: np.zeros((r, c), np.float32)
+    X, W, A, B, dY = z(64, 64), z(64, 64), z(1, 64), z(64, 1), z(64, 64)
+    X[:2, :2] = [[1, 2], [3, 4]]
+    W[:2, :2] = np.eye(2)
+    A[0, :2] = [1, 1]
+    B[:2, 0] = [1, 0]
+    dY[:2, :2] = np.eye(2)
+    from lora_synth import round_to_bf16_bits
+    t = {k: round_to_bf16_bits(v) for k, v in (("X", X), ("W", W), ("A", A), ("B", B), ("dY", dY))}
+    out = run_gpu(t, shape)
+    assert f64(out["Y"])[:2, :2].tolist() == [[7, 2], [17, 4]]
+    assert out["U"][:2, 0].tolist() == [3, 7]
+    assert f64(out["dX"])[:2, :2].tolist() == [[3, 2], [0, 1]]
+    assert out["dB"][:2, 0].tolist() == [6, 14]
+    assert out["dA"][0, :2].tolist() == [2, 4]
+    assert not np.any(f64(out["Y"])[2:]) and not np.any(out["dA"][0, 2:])
+
+
+@pytest.mark.parametrize("shape", [CONFIGS["tiny"][0], Shape("b0", 300, 1024, 520, 16, 32.0, 301)],
+                         ids=_shape_id)
+def test_b_zero_invariants(shape):
+    """The paper's initialisation B = 0: dA == 0 exactly, and Y equals bit for
+    bit the output of the same kernel with A = 0 (both LoRA terms are exact zeros)."""
+    t = gen_inputs(shape, zero_b=True)
+    out = run_gpu(t, shape)
+    assert not np.any(out["dA"])
+    ta = dict(t)
+    ta["A"] = np.zeros_like(t["A"])
+    out_a = run_gpu(ta, shape)
+    assert np.array_equal(out["Y"], out_a["Y"])
+    assert not np.any(out_a["U"]) and not np.any(out_a["dB"])
+    assert_within(compare(t, shape, out), "B=0")
+
+
+def test_deterministic_bitwise():
+    shape = Shape("det", 2051, 4096, 1024, 64, 128.0, 401)
+    t = gen_inputs(shape)
+    a = run_gpu(t, shape)
+    b = run_gpu(t, shape)
+    for key in a:
+        assert np.array_equal(a[key].view(np.uint8), b[key].view(np.uint8)), key
+
+
+@pytest.mark.parametrize("b_std", [1.0, 0.02])
+def test_lora_branch_sensitivity(b_std):
+    """The LoRA term alone: (Y_gpu - X W^T) against s U B^T from the oracle."""
+    shape = CONFIGS["tiny"][0]
+    t = gen_inputs(shape, b_std=b_std)
+    out = run_gpu(t, shape)
+    tb0 = dict(t)
+    tb0["B"] = np.zeros_like(t["B"])
+    _, Y0 = oracle.lora_forward(tb0["X"], tb0["W"], tb0["A"], tb0["B"], shape.alpha)
+    _, Y = oracle.lora_forward(t["X"], t["W"], t["A"], t["B"], shape.alpha)
+    branch_err = rel(f64(out["Y"]) - Y0, Y - Y0)
+    print("branch", b_std, branch_err)
+    assert branch_err <= (2e-2 if b_std >= 1.0 else 5e-2)
+    assert_within(compare(t, shape, out), f"b_std={b_std}")
