@@ -1,0 +1,227 @@
+#!/usr/bin/env python3
+"""LoRA-linear forward + backward throughput on one MI355X.
+
+One step = lora_linear_fwd + lora_linear_bwd (the whole path: fused forward
+GEMM, dU, dB and dA token reductions, dX GEMM, finalize) over one batch of
+synthetic bf16 inputs of a Llama-2 projection shape.  Inputs are resident in
+HBM before timing starts; successive steps rotate over several copies of the
+inputs whose total size exceeds the 256 MB Infinity Cache, so every step reads
+its operands from HBM.
+
+Prints one JSON line: whole-job TFLOP/s (algorithmic flops 4mnk + 6mr(n+k) per
+projection), the fraction of the bf16 dense matrix-core peak, a roofline entry
+for the dominant kernel (the forward GEMM, timed live with HIP events on its
+stream) and the fp64 CPU oracle's throughput on the host as a baseline.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0    # MI355X dense bf16 matrix-core peak
+PEAK_HBM_GBS = 8000.0        # MI355X HBM3E
+MALL_BYTES = 256 << 20       # Infinity Cache
+KERNEL_SOURCES = ["paper_2403_11366_amd/csrc/lora_fwd.hip", "paper_2403_11366_amd/csrc/lora_device.hpp"]
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "lora_fwd_kernel_llama2_7b_q_proj_traffic.json")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per forward-kernel launch from the committed rocprofv3 counter
+    runs, if they were taken on the current kernel source; else None."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("kernel_source_sha") != kernel_source_hash() or rec.get("workload") != workload:
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(shape, seconds: float):
+    """Time the fp64 oracle (as it stands) on this host for `shape`."""
+    import numpy as np
+    import oracle
+    from lora_synth import gen_inputs
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    t = gen_inputs(shape)
+    runs, t0 = 0, time.perf_counter()
+    while True:
+        oracle.lora_forward(t["X"], t["W"], t["A"], t["B"], shape.alpha)
+        oracle.lora_backward(t["dY"], t["X"], t["W"], t["A"], t["B"], shape.alpha)
+        runs += 1
+        el = time.perf_counter() - t0
+        if el >= seconds or runs >= 50:
+            break
+    per = el / runs
+    return {"value": shape.flops_fwd_bwd / per / 1e12, "unit": "TFLOP/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"{runs} full fwd+bwd of {shape.name} (m={shape.m} n={shape.n} k={shape.k} "
+                      f"r={shape.r}) in fp64 numpy/OpenBLAS, {el:.1f} s total, {per:.3f} s each"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--config", default="llama2_7b_q_proj")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(the LoRA linear would shard over tokens with an all-reduce of dA and dB; "
+              "not built here). Run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import paper_2403_11366_amd as lora
+    from lora_synth import CONFIGS
+    from paper_2403_11366_amd.device_io import bits_to_device
+    from lora_synth import gen_inputs
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    lora.load_library()
+    shapes = CONFIGS[args.config]
+    dev = "cuda"
+    stream = torch.cuda.current_stream()
+
+    # ---- inputs resident in HBM, rotated over enough copies to exceed the MALL
+    per_set = sum(2 * (s.m * s.k + s.n * s.k + s.r * s.k + s.n * s.r + s.m * s.n) for s in shapes)
+    nsets = max(1, math.ceil(2 * MALL_BYTES / per_set))
+    log(f"[bench] {args.config}: {len(shapes)} projection(s), {nsets} input set(s) of {per_set / 2**20:.0f} MiB")
+    proj = []
+    for s in shapes:
+        t = gen_inputs(s)
+        base = {key: bits_to_device(v, dev) for key, v in t.items()}
+        sets = [base] + [{key: v.clone() for key, v in base.items()} for _ in range(nsets - 1)]
+        out = {
+            "Y": torch.empty((s.m, s.n), dtype=torch.bfloat16, device=dev),
+            "U": torch.empty((s.m, s.r), dtype=torch.float32, device=dev),
+            "dX": torch.empty((s.m, s.k), dtype=torch.bfloat16, device=dev),
+            "dA": torch.empty((s.r, s.k), dtype=torch.float32, device=dev),
+            "dB": torch.empty((s.n, s.r), dtype=torch.float32, device=dev),
+            "ws": torch.empty(lora.lora_linear_bwd_workspace_size(s.m, s.n, s.k, s.r),
+                              dtype=torch.uint8, device=dev),
+        }
+        proj.append((s, sets, out))
+    torch.cuda.synchronize()
+
+    def fwd(i, s, sets, out):
+        d = sets[i % len(sets)]
+        lora.lora_linear_fwd(d["X"], d["W"], d["A"], d["B"], out["Y"], out["U"], s.alpha, stream=stream)
+
+    def bwd(i, s, sets, out):
+        d = sets[i % len(sets)]
+        lora.lora_linear_bwd(d["dY"], d["X"], d["W"], d["A"], d["B"], out["U"], out["dX"], out["dA"],
+                             out["dB"], out["ws"], s.alpha, stream=stream)
+
+    def step(i):
+        for s, sets, out in proj:
+            fwd(i, s, sets, out)
+            bwd(i, s, sets, out)
+
+    # ---- whole path
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    log(f"[bench] warmup {args.warmup} steps done; timing {args.steps} steps")
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(i)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ms_per_step = elapsed / args.steps * 1e3
+    flops = sum(s.flops_fwd_bwd for s, _, _ in proj)
+    tflops = flops / (ms_per_step / 1e3) / 1e12
+    log(f"[bench] {ms_per_step * 1e3:.1f} us/step, {tflops:.1f} TFLOP/s")
+
+    # ---- dominant kernel: the forward GEMM (one kernel per lora_linear_fwd call),
+    # timed with HIP events recorded on the stream it is launched on.
+    s0, sets0, out0 = proj[0]
+    reps = max(20, args.steps)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    for i in range(5):
+        fwd(i, s0, sets0, out0)
+    ev0.record(stream)
+    for i in range(reps):
+        fwd(i, s0, sets0, out0)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    fwd_us = ev0.elapsed_time(ev1) / reps * 1e3
+    # backward call (several kernels) for context
+    ev0.record(stream)
+    for i in range(reps):
+        bwd(i, s0, sets0, out0)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    bwd_us = ev0.elapsed_time(ev1) / reps * 1e3
+    m, n, k, r = s0.m, s0.n, s0.k, s0.r
+    k1_flops = 2 * m * n * k + 2 * m * k * r + 2 * m * n * r
+    achieved = k1_flops / (fwd_us * 1e-6) / 1e12
+    traffic = measured_traffic(args.config)
+    log(f"[bench] forward kernel {fwd_us:.1f} us ({achieved:.1f} TFLOP/s); backward call {bwd_us:.1f} us")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log(f"[bench] timing the fp64 oracle on the host (~{args.cpu_seconds:.0f} s)")
+        cpu = cpu_baseline(s0, args.cpu_seconds)
+
+    rec = {
+        "metric": "LoRA-linear fwd+bwd TFLOP/s + % bf16 MFMA peak, Llama-2-7B shapes, 1 GPU",
+        "value": round(tflops, 2),
+        "unit": "TFLOP/s",
+        "pct_bf16_mfma_peak": round(100 * tflops / PEAK_BF16_TFLOPS, 2),
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": args.config,
+                   "projections": [{"name": s.name, "m": s.m, "n": s.n, "k": s.k, "r": s.r,
+                                    "alpha": s.alpha} for s in shapes],
+                   "input_sets": nsets, "flops_per_step": flops,
+                   "operands": "bf16 in, fp32 accumulate; Y, dX bf16; U, dA, dB fp32"},
+        "roofline": {"bound": "mfma", "kernel": "lora_fwd_kernel", "achieved": round(achieved, 2),
+                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                     "traffic": traffic, "flops_per_launch": k1_flops, "avg_launch_us": round(fwd_us, 2)},
+        "bwd_call_us": round(bwd_us, 2),
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()
