@@ -22,23 +22,24 @@
 namespace lora {
 
 // ---------------------------------------------------------------------------
+// Index math is 32-bit: validation bounds every index used here below 2^30.
 __global__ __launch_bounds__(256) void lora_bwd_prep_kernel(
     const u16* __restrict__ B, const float* __restrict__ U, u16* __restrict__ Bt,
     u16* __restrict__ Ut2, int m, int n, int r, int rp, int mp) {
-  const int64_t nbt = (int64_t)rp * n;
-  const int64_t nut = (int64_t)2 * rp * mp;
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < nbt + nut; e += stride) {
+  const int nbt = rp * n;
+  const int nut = 2 * rp * mp;
+  const int stride = gridDim.x * blockDim.x;
+  for (int e = blockIdx.x * blockDim.x + threadIdx.x; e < nbt + nut; e += stride) {
     if (e < nbt) {
-      const int t = (int)(e / n);
-      const int j = (int)(e - (int64_t)t * n);
-      Bt[e] = (t < r) ? B[(int64_t)j * r + t] : (u16)0;
+      const int t = e / n;
+      const int j = e - t * n;
+      Bt[e] = (t < r) ? B[(size_t)j * r + t] : (u16)0;
     } else {
-      const int64_t f = e - nbt;
-      const int tt = (int)(f / mp);
-      const int i = (int)(f - (int64_t)tt * mp);
+      const int f = e - nbt;
+      const int tt = f / mp;
+      const int i = f - tt * mp;
       const int t = tt % rp;
-      const float v = (i < m && t < r) ? U[(int64_t)i * r + t] : 0.f;
+      const float v = (i < m && t < r) ? U[(size_t)i * r + t] : 0.f;
       const u16 h = f32_to_bf16(v);
       Ut2[f] = (tt >= rp) ? f32_to_bf16(v - bf16_to_f32(h)) : h;
     }
@@ -46,14 +47,20 @@ __global__ __launch_bounds__(256) void lora_bwd_prep_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// dU for 16 tokens per workgroup; the 4 waves take interleaved 32-wide chunks
-// of n and their partial sums are added in wave order through LDS.
+// dU = s dY B for 16 tokens per workgroup, reducing over all of n.  The 8 waves
+// take interleaved 32-wide chunks of n (four chunks' loads in flight per wave);
+// their sums are added in wave order through LDS, so the result is
+// bit-identical from run to run.  (A split of n over workgroups would need a
+// cross-workgroup reduction, whose device-scope fences write back the
+// per-XCD L2s -- far dearer than the work.)  Writes dU2 (token-major,
+// high | low parts) and dUt2 (its transpose).
 template <int RP>
-__global__ __launch_bounds__(256) void lora_bwd_du_kernel(
+__global__ __launch_bounds__(512) void lora_bwd_du_kernel(
     const u16* __restrict__ dY, const u16* __restrict__ Bt, u16* __restrict__ dU2,
     u16* __restrict__ dUt2, int m, int n, int mp, float s) {
   constexpr int FT = RP / 16;
-  __shared__ floatx4 red[4][FT][64];
+  constexpr int NWV = 8;
+  __shared__ floatx4 red[NWV][FT][64];
   const int i0 = blockIdx.x * 16;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, c16 = lane & 15;
@@ -66,45 +73,50 @@ __global__ __launch_bounds__(256) void lora_bwd_du_kernel(
 #pragma unroll
   for (int ft = 0; ft < FT; ++ft) acc[ft] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  const int nch = (n + 31) / 32;
-#pragma unroll 4
-  for (int c = wave; c < nch; c += 4) {
-    const int j = c * 32 + 8 * g;
-    const bool ok = j < n;
-    const short8 yf = __builtin_bit_cast(short8, buf_load16(rsY, ok ? (uint32_t)c16 * rowbytes + (uint32_t)j * 2 : kOOB));
+  constexpr int UNR = 4;
+  for (int j0 = 32 * wave; j0 < n; j0 += 32 * NWV * UNR) {
+    short8 yf[UNR], bf[UNR][FT];
 #pragma unroll
-    for (int ft = 0; ft < FT; ++ft) {
-      const short8 bf = __builtin_bit_cast(
-          short8, buf_load16(rsB, ok ? (uint32_t)(16 * ft + c16) * rowbytes + (uint32_t)j * 2 : kOOB));
-      acc[ft] = mfma16x16x32(bf, yf, acc[ft]);
+    for (int u = 0; u < UNR; ++u) {
+      const int j = j0 + 32 * NWV * u + 8 * g;
+      const bool ok = j < n;
+      yf[u] = __builtin_bit_cast(short8, buf_load16(rsY, ok ? (uint32_t)c16 * rowbytes + (uint32_t)j * 2 : kOOB));
+#pragma unroll
+      for (int ft = 0; ft < FT; ++ft)
+        bf[u][ft] = __builtin_bit_cast(
+            short8, buf_load16(rsB, ok ? (uint32_t)(16 * ft + c16) * rowbytes + (uint32_t)j * 2 : kOOB));
     }
+#pragma unroll
+    for (int u = 0; u < UNR; ++u)
+#pragma unroll
+      for (int ft = 0; ft < FT; ++ft) acc[ft] = mfma16x16x32(bf[u][ft], yf[u], acc[ft]);
   }
 #pragma unroll
   for (int ft = 0; ft < FT; ++ft) red[wave][ft][lane] = acc[ft];
   __syncthreads();
-  if (wave != 0) return;
+  if (wave >= FT) return;
+  const int ft = wave;  // one wave per 16-row fragment of dU^T
+  floatx4 v = red[0][ft][lane];
+#pragma unroll
+  for (int w = 1; w < NWV; ++w) v += red[w][ft][lane];
   const int i = i0 + c16;  // < mp: the grid covers exactly mp tokens
+  u16 hi[4], lo[4];
 #pragma unroll
-  for (int ft = 0; ft < FT; ++ft) {
-    const floatx4 v = ((red[0][ft][lane] + red[1][ft][lane]) + red[2][ft][lane]) + red[3][ft][lane];
-    u16 hi[4], lo[4];
+  for (int q = 0; q < 4; ++q) {
+    const float d = s * v[q];
+    hi[q] = f32_to_bf16(d);
+    lo[q] = f32_to_bf16(d - bf16_to_f32(hi[q]));
+  }
+  const int t = 16 * ft + 4 * g;
+  u16* row = dU2 + (size_t)i * (2 * RP);
+  *reinterpret_cast<uint2*>(row + t) =
+      uint2{(uint32_t)hi[0] | ((uint32_t)hi[1] << 16), (uint32_t)hi[2] | ((uint32_t)hi[3] << 16)};
+  *reinterpret_cast<uint2*>(row + RP + t) =
+      uint2{(uint32_t)lo[0] | ((uint32_t)lo[1] << 16), (uint32_t)lo[2] | ((uint32_t)lo[3] << 16)};
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const float d = s * v[q];
-      hi[q] = f32_to_bf16(d);
-      lo[q] = f32_to_bf16(d - bf16_to_f32(hi[q]));
-    }
-    const int t = 16 * ft + 4 * g;
-    u16* row = dU2 + (size_t)i * (2 * RP);
-    *reinterpret_cast<uint2*>(row + t) =
-        uint2{(uint32_t)hi[0] | ((uint32_t)hi[1] << 16), (uint32_t)hi[2] | ((uint32_t)hi[3] << 16)};
-    *reinterpret_cast<uint2*>(row + RP + t) =
-        uint2{(uint32_t)lo[0] | ((uint32_t)lo[1] << 16), (uint32_t)lo[2] | ((uint32_t)lo[3] << 16)};
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      dUt2[(size_t)(t + q) * mp + i] = hi[q];
-      dUt2[(size_t)(RP + t + q) * mp + i] = lo[q];
-    }
+  for (int q = 0; q < 4; ++q) {
+    dUt2[(size_t)(t + q) * mp + i] = hi[q];
+    dUt2[(size_t)(RP + t + q) * mp + i] = lo[q];
   }
 }
 
@@ -164,7 +176,7 @@ __global__ __launch_bounds__(64 * NW) void lora_tokred_kernel(
 #pragma unroll
     for (int i = 0; i < LOADS; ++i) {
       const int q = tid + i * NT;
-      *reinterpret_cast<int4v*>(sb + mc_offset<BNC>(q / CPR, q % CPR)) = qregs[i];
+      *reinterpret_cast<int4v*>(sb + mc16_offset<BNC>(q / CPR, q % CPR)) = qregs[i];
     }
   };
 
@@ -187,7 +199,7 @@ __global__ __launch_bounds__(64 * NW) void lora_tokred_kernel(
       for (int ks = 0; ks < 2; ++ks) {
 #pragma unroll
         for (int fc = 0; fc < FC; ++fc) {
-          const short8 qf = mc_read_tr<BNC>(Qs, 32 * ks, wave * WC + 16 * fc, lane);
+          const short8 qf = mc16_read_tr<BNC>(Qs, 32 * ks, wave * WC + 16 * fc, lane);
 #pragma unroll
           for (int f = 0; f < FP; ++f) acc[f][fc] = mfma16x16x32(pcur[ks][f], qf, acc[f][fc]);
         }
@@ -223,17 +235,17 @@ __global__ __launch_bounds__(64 * NW) void lora_tokred_kernel(
 __global__ __launch_bounds__(256) void lora_bwd_finalize_kernel(
     const float* __restrict__ pb, const float* __restrict__ pa, float* __restrict__ dB,
     float* __restrict__ dA, int n, int k, int r, int rp, int sb, int sa, float s) {
-  const int64_t nb = (int64_t)n * r, na = (int64_t)r * k;
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < nb + na; e += stride) {
+  const int nb = n * r, na = r * k;
+  const int stride = gridDim.x * blockDim.x;
+  for (int e = blockIdx.x * blockDim.x + threadIdx.x; e < nb + na; e += stride) {
     if (e < nb) {  // e = t * n + j: partial reads along j are contiguous
-      const int t = (int)(e / n), j = (int)(e - (int64_t)t * n);
+      const int t = e / n, j = e - t * n;
       float v = 0.f;
       for (int p = 0; p < sb; ++p) v += pb[((size_t)p * rp + t) * n + j];
       dB[(size_t)j * r + t] = s * v;
     } else {
-      const int64_t f = e - nb;
-      const int t = (int)(f / k), l = (int)(f - (int64_t)t * k);
+      const int f = e - nb;
+      const int t = f / k, l = f - t * k;
       float v = 0.f;
       for (int p = 0; p < sa; ++p) v += pa[((size_t)p * rp + t) * k + l];
       dA[f] = v;
@@ -242,36 +254,41 @@ __global__ __launch_bounds__(256) void lora_bwd_finalize_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// dX tile of BM tokens x BN input features.  Stages: dY [BM][64] (k = n
-// contiguous) and W [64 rows of n][BN] (mn-contiguous, read transposed); after
-// the n loop, NSLAB stages of the 2RP slab: dU2 [BM][2RP] and A rows repeated
-// for the high and low parts.
+// dX tile of BM tokens x BN input features, formed as dX^T = W^T dY^T with
+// v_mfma_f32_32x32x16_bf16 (W as the A operand, dY as the B operand).  Stages
+// of 64 along n: dY [BM rows][64] (k-contiguous) and W [64 rows of n][BN]
+// (mn-contiguous, read with the transposing LDS read).  After the n stages,
+// NSLAB stages cover the 2 RP wide slab: dU2 [BM][2RP] against A's rows, once
+// for the high and once for the low part.  The next stage is loaded into
+// registers while the current one multiplies and written to the other LDS
+// buffer afterwards (one barrier per stage).
 template <int BM, int BN, int WM, int WN, int RP>
 __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
     const u16* __restrict__ dY, const u16* __restrict__ W, const u16* __restrict__ dU2,
     const u16* __restrict__ A, u16* __restrict__ dX, int m, int n, int k, int r, int mp,
     int tiles_m, int tiles_n) {
-  constexpr int NT = 64 * WM * WN;
-  constexpr int WTM = BM / WM, WTN = BN / WN;
-  constexpr int FI = WTM / 16, FJ = WTN / 16;
-  constexpr int STAGE = (BM + BN) * 128;
-  constexpr int CH_Y = BM * 8;
-  constexpr int CPR = BN / 8;
-  constexpr int CH = CH_Y + 64 * CPR;
-  constexpr int LOADS = (CH + NT - 1) / NT;
+  constexpr int NW = WM * WN;
+  constexpr int NT = 64 * NW;
+  constexpr int WTI = BM / WM, WTJ = BN / WN;
+  constexpr int FI = WTI / 32, FJ = WTJ / 32;
+  constexpr int STAGE = BM * 128 + 64 * BN * 2;
   constexpr int KS2 = 2 * RP;
   constexpr int NSLAB = (KS2 + 63) / 64;
-  static_assert(BM % (16 * WM) == 0 && BN % (16 * WN) == 0, "tile/wave split");
-  static_assert(CH_Y % 64 == 0 && CH % 64 == 0 && BN >= 128, "wave-uniform staging");
+  constexpr int CPR = BN / 8;                       // 16-byte chunks per W tile row
+  constexpr int CY = BM * 8, CW = 64 * CPR;          // chunks per stage
+  constexpr int LY = (CY + NT - 1) / NT, LW = (CW + NT - 1) / NT;
+  static_assert(WTI % 32 == 0 && WTJ % 32 == 0, "32x32 fragments");
+  static_assert(BN == 128 || BN == 256, "W tile rows of 256 or 512 bytes");
   static_assert(2 * STAGE <= 160 * 1024, "LDS budget");
-  __shared__ __attribute__((aligned(16))) char smem[2 * STAGE];
+  __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
 
   int tm, tn;
   tile_coords(tiles_m, tiles_n, 8, tm, tn);
   const int m0 = tm * BM, l0 = tn * BN;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = uniform(tid >> 6);
   const int wm = wave / WN, wn = wave % WN;
-  const int g = lane >> 4, c16 = lane & 15;
+  const int g = lane >> 5, c32 = lane & 31;
   const uint32_t yrow = (uint32_t)n * 2, wrow = (uint32_t)k * 2, urow = (uint32_t)KS2 * 2;
   const __amdgpu_buffer_rsrc_t rsY = make_rsrc(dY + (size_t)m0 * n, (uint64_t)min(BM, m - m0) * yrow);
   const __amdgpu_buffer_rsrc_t rsU = make_rsrc(dU2 + (size_t)m0 * KS2, (uint64_t)min(BM, mp - m0) * urow);
@@ -279,61 +296,81 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
   const int nkb = (n + 63) / 64;
   const int nst = nkb + NSLAB;
 
-  int4v regs[LOADS];
+  int4v gy[LY], gw[LW];
   auto gload = [&](int st) {
     if (st < nkb) {
       const int n0 = st * 64;
       const __amdgpu_buffer_rsrc_t rsW = make_rsrc(W + (size_t)n0 * k, (uint64_t)min(64, n - n0) * wrow);
 #pragma unroll
-      for (int i = 0; i < LOADS; ++i) {
+      for (int i = 0; i < LY; ++i) {
         const int q = tid + i * NT;
-        if (CH % NT != 0 && q >= CH) break;  // wave-uniform
-        if (q < CH_Y) {
-          const int row = q >> 3, nn = n0 + 8 * (q & 7);
-          regs[i] = buf_load16(rsY, nn < n ? (uint32_t)row * yrow + (uint32_t)nn * 2 : kOOB);
-        } else {
-          const int q2 = q - CH_Y, rho = q2 / CPR, ll = l0 + 8 * (q2 % CPR);
-          regs[i] = buf_load16(rsW, ll < k ? (uint32_t)rho * wrow + (uint32_t)ll * 2 : kOOB);
-        }
+        if (CY % NT != 0 && q >= CY) break;
+        const int nn = n0 + 8 * (q & 7);
+        gy[i] = buf_load16(rsY, nn < n ? (uint32_t)(q >> 3) * yrow + (uint32_t)nn * 2 : kOOB);
+      }
+#pragma unroll
+      for (int i = 0; i < LW; ++i) {
+        const int q = tid + i * NT;
+        if (CW % NT != 0 && q >= CW) break;
+        const int ll = l0 + 8 * (q % CPR);
+        gw[i] = buf_load16(rsW, ll < k ? (uint32_t)(q / CPR) * wrow + (uint32_t)ll * 2 : kOOB);
       }
     } else {
       const int kk0 = (st - nkb) * 64;
 #pragma unroll
-      for (int i = 0; i < LOADS; ++i) {
+      for (int i = 0; i < LY; ++i) {
         const int q = tid + i * NT;
-        if (CH % NT != 0 && q >= CH) break;
-        if (q < CH_Y) {
-          const int row = q >> 3, kk = kk0 + 8 * (q & 7);
-          regs[i] = buf_load16(rsU, kk < KS2 ? (uint32_t)row * urow + (uint32_t)kk * 2 : kOOB);
-        } else {
-          const int q2 = q - CH_Y, kk = kk0 + q2 / CPR, ll = l0 + 8 * (q2 % CPR);
-          const int t = kk % RP;
-          const bool ok = kk < KS2 && t < r && ll < k;
-          regs[i] = buf_load16(rsA, ok ? (uint32_t)t * wrow + (uint32_t)ll * 2 : kOOB);
-        }
+        if (CY % NT != 0 && q >= CY) break;
+        const int kk = kk0 + 8 * (q & 7);
+        gy[i] = buf_load16(rsU, kk < KS2 ? (uint32_t)(q >> 3) * urow + (uint32_t)kk * 2 : kOOB);
+      }
+#pragma unroll
+      for (int i = 0; i < LW; ++i) {
+        const int q = tid + i * NT;
+        if (CW % NT != 0 && q >= CW) break;
+        const int kk = kk0 + q / CPR;
+        const int t = kk % RP;
+        const int ll = l0 + 8 * (q % CPR);
+        const bool ok = kk < KS2 && t < r && ll < k;
+        gw[i] = buf_load16(rsA, ok ? (uint32_t)t * wrow + (uint32_t)ll * 2 : kOOB);
       }
     }
   };
   auto swrite = [&](int buf) {
     char* sb = smem + buf * STAGE;
 #pragma unroll
-    for (int i = 0; i < LOADS; ++i) {
+    for (int i = 0; i < LY; ++i) {
       const int q = tid + i * NT;
-      if (CH % NT != 0 && q >= CH) break;
-      if (q < CH_Y) {
-        *reinterpret_cast<int4v*>(sb + kc_offset(q >> 3, q & 7)) = regs[i];
-      } else {
-        const int q2 = q - CH_Y;
-        *reinterpret_cast<int4v*>(sb + BM * 128 + mc_offset<BN>(q2 / CPR, q2 % CPR)) = regs[i];
-      }
+      if (CY % NT != 0 && q >= CY) break;
+      *reinterpret_cast<int4v*>(sb + kc_offset(q >> 3, q & 7)) = gy[i];
+    }
+#pragma unroll
+    for (int i = 0; i < LW; ++i) {
+      const int q = tid + i * NT;
+      if (CW % NT != 0 && q >= CW) break;
+      *reinterpret_cast<int4v*>(sb + BM * 128 + mc32_offset<BN>(q / CPR, q % CPR)) = gw[i];
     }
   };
 
-  floatx4 acc[FJ][FI];
+  floatx16 acc[FJ][FI];
 #pragma unroll
   for (int a = 0; a < FJ; ++a)
 #pragma unroll
-    for (int b = 0; b < FI; ++b) acc[a][b] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int b = 0; b < FI; ++b) acc[a][b] = floatx16{};
+
+  auto substep = [&](const char* sb, int ks) {
+    const char* Ys = sb;
+    const char* Ws = sb + BM * 128;
+    short8 fw[FJ], fy[FI];
+#pragma unroll
+    for (int fj = 0; fj < FJ; ++fj) fw[fj] = mc32_read_tr<BN>(Ws, 16 * ks, wn * WTJ + 32 * fj, lane);
+#pragma unroll
+    for (int fi = 0; fi < FI; ++fi) fy[fi] = kc_read(Ys, wm * WTI + 32 * fi + c32, 2 * ks + g);
+#pragma unroll
+    for (int fi = 0; fi < FI; ++fi)
+#pragma unroll
+      for (int fj = 0; fj < FJ; ++fj) acc[fj][fi] = mfma32x32x16(fw[fj], fy[fi], acc[fj][fi]);
+  };
 
   gload(0);
   swrite(0);
@@ -342,36 +379,28 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
     const bool more = st + 1 < nst;
     if (more) gload(st + 1);
     const char* sb = smem + (st & 1) * STAGE;
-    const char* Ys = sb;
-    const char* Ws = sb + BM * 128;
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      short8 wf[FJ];
-#pragma unroll
-      for (int fj = 0; fj < FJ; ++fj) wf[fj] = mc_read_tr<BN>(Ws, 32 * ks, wn * WTN + 16 * fj, lane);
-#pragma unroll
-      for (int fi = 0; fi < FI; ++fi) {
-        const short8 yf = kc_read(Ys, wm * WTM + 16 * fi + c16, 4 * ks + g);
-#pragma unroll
-        for (int fj = 0; fj < FJ; ++fj) acc[fj][fi] = mfma16x16x32(wf[fj], yf, acc[fj][fi]);
-      }
-    }
+    for (int ks = 0; ks < 4; ++ks) substep(sb, ks);
     if (more) swrite((st + 1) & 1);
     __syncthreads();
   }
 
 #pragma unroll
   for (int fi = 0; fi < FI; ++fi) {
-    const int i = m0 + wm * WTM + 16 * fi + c16;
+    const int i = m0 + wm * WTI + 32 * fi + c32;
     if (i >= m) continue;
+    u16* xrow = dX + (size_t)i * k;
 #pragma unroll
-    for (int fj = 0; fj < FJ; ++fj) {
-      const int l = l0 + wn * WTN + 16 * fj + 4 * g;
-      if (l >= k) continue;
-      const uint32_t lo = (uint32_t)f32_to_bf16(acc[fj][fi][0]) | ((uint32_t)f32_to_bf16(acc[fj][fi][1]) << 16);
-      const uint32_t hi = (uint32_t)f32_to_bf16(acc[fj][fi][2]) | ((uint32_t)f32_to_bf16(acc[fj][fi][3]) << 16);
-      *reinterpret_cast<uint2*>(dX + (size_t)i * k + l) = uint2{lo, hi};
-    }
+    for (int fj = 0; fj < FJ; ++fj)
+#pragma unroll
+      for (int qq = 0; qq < 4; ++qq) {
+        const int l = l0 + wn * WTJ + 32 * fj + 8 * qq + 4 * g;
+        if (l >= k) continue;
+        const floatx16& a = acc[fj][fi];
+        const uint32_t lo = (uint32_t)f32_to_bf16(a[4 * qq]) | ((uint32_t)f32_to_bf16(a[4 * qq + 1]) << 16);
+        const uint32_t hi = (uint32_t)f32_to_bf16(a[4 * qq + 2]) | ((uint32_t)f32_to_bf16(a[4 * qq + 3]) << 16);
+        *reinterpret_cast<uint2*>(xrow + l) = uint2{lo, hi};
+      }
   }
 }
 
@@ -402,7 +431,7 @@ static hipError_t launch_bwd_rp(const BwdArgs& a, const BwdLayout& L, hipStream_
     hipLaunchKernelGGL(lora_bwd_prep_kernel, dim3(blocks), dim3(256), 0, st, a.B, a.U, Bt, Ut2, m, n, r, RP, mp);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
-  hipLaunchKernelGGL((lora_bwd_du_kernel<RP>), dim3(mp / 16), dim3(256), 0, st, a.dY, Bt, dU2, dUt2, m, n, mp, a.s);
+  hipLaunchKernelGGL((lora_bwd_du_kernel<RP>), dim3(mp / 16), dim3(512), 0, st, a.dY, Bt, dU2, dUt2, m, n, mp, a.s);
   if ((e = hipGetLastError()) != hipSuccess) return e;
 
   hipLaunchKernelGGL((lora_tokred_kernel<4, RP>), dim3(L.plan_b.col_tiles, L.plan_b.splits), dim3(256), 0, st,
@@ -411,7 +440,7 @@ static hipError_t launch_bwd_rp(const BwdArgs& a, const BwdLayout& L, hipStream_
 
   switch (choose_gemm_tile(a.m, a.k)) {
     case TILE_256x256: e = launch_dx_cfg<256, 256, 2, 4, RP>(a, L, st); break;
-    case TILE_256x128: e = launch_dx_cfg<256, 128, 4, 2, RP>(a, L, st); break;
+    case TILE_128x256: e = launch_dx_cfg<128, 256, 2, 4, RP>(a, L, st); break;
     default: e = launch_dx_cfg<128, 128, 2, 2, RP>(a, L, st); break;
   }
   if (e != hipSuccess) return e;

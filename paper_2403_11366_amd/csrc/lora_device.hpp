@@ -1,23 +1,29 @@
 // Device-side building blocks shared by the LoRA-linear kernels (gfx950 only).
 //
-// Matrix-core primitive: v_mfma_f32_16x16x32_bf16.  With lane l = 16*g + c
-// (g = l / 16, c = l % 16) the operand and result layouts are:
-//   A operand (16 x 32, M x K): lane holds row c, k = 8g .. 8g+7
-//   B operand (32 x 16, K x N): lane holds column c, k = 8g .. 8g+7
-//   result    (16 x 16):        lane holds column c, rows 4g .. 4g+3
-// Because both operands carry k in the same positions, any matrix stored with
-// k contiguous is read with one 16-byte load per lane.
+// Matrix-core primitives (bf16 in, fp32 accumulate):
+//   v_mfma_f32_32x32x16_bf16 -- the GEMM workhorse.  With lane l, c = l % 32,
+//     g = l / 32:  A operand (32 x 16, M x K): lane holds row c, k = 8g .. 8g+7;
+//     B operand (16 x 32, K x N): lane holds column c, k = 8g .. 8g+7;
+//     result (32 x 32): lane holds column c, rows 8(q/4) + 4g + q%4, q = 0..15.
+//     On gfx950 it issues at the full bf16 rate (1024 flop/clk per SIMD).
+//   v_mfma_f32_16x16x32_bf16 -- used by the small rank-r kernels.  With
+//     c = l % 16, g = l / 16: A holds row c, k = 8g .. 8g+7; B holds column c,
+//     the same k; the result holds column c, rows 4g .. 4g+3.  It issues at
+//     about half the flop rate of the 32x32 form.
+// Both operands carry k in the same positions, so any matrix stored with k
+// contiguous is read with one 16-byte load per lane.
 //
 // LDS tiles come in two forms:
 //   * k-contiguous tiles: rows of 64 bf16 (128 bytes = 8 chunks of 16 bytes).
 //     Chunk q of row p is stored at chunk position q ^ ((p >> 1) & 7), so the
 //     16 lanes that read one 16-byte chunk from 16 consecutive rows hit
 //     distinct banks.
-//   * mn-contiguous tiles (k is the row index): rows of COLS bf16.  Chunk q of
-//     row p is stored at position q ^ (2 * (p & 3) + 8 * ((p >> 3) & 1)).  They
-//     are read with ds_read_b64_tr_b16, which hands lane i of each 16-lane group
-//     column i of a 4 x 16 block of rows, i.e. one matrix-core operand column
-//     with 4 consecutive k; two such reads give the 8 k of a lane.
+//   * mn-contiguous tiles (k is the row index): rows of COLS bf16, read with
+//     ds_read_b64_tr_b16, which hands lane i of each 16-lane group column i of
+//     a 4 x 16 block of rows (4 consecutive k of one operand column); two such
+//     reads give a lane its 8 k.  The chunk swizzle depends on which lanes
+//     share a read cycle: mc16_* for the 16x16x32 operand layout,
+//     mc32_* (chunk q of row p at q ^ 4(p & 3)) for the 32x32x16 one.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -30,6 +36,7 @@ typedef short short8 __attribute__((ext_vector_type(8)));
 typedef short short4v __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef int int4v __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) short4v lds_short4v;
 
@@ -52,6 +59,23 @@ __device__ __forceinline__ floatx4 mfma16x16x32(short8 a, short8 b, floatx4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16((bf16x8)a, (bf16x8)b, c, 0, 0, 0);
 }
 
+__device__ __forceinline__ floatx16 mfma32x32x16(short8 a, short8 b, floatx16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16((bf16x8)a, (bf16x8)b, c, 0, 0, 0);
+}
+
+// Global -> LDS copy of 16 bytes per lane through a buffer resource: lane L's
+// bytes land at lds_base + 16 L (lds_base must be wave-uniform).  Out-of-range
+// offsets write zeros.  Completion is tracked by vmcnt.
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t rs, uint32_t byte_off, void* lds_base) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void*)lds_base, 16, byte_off, 0, 0, 0);
+}
+
+// Wait until this wave's outstanding vector-memory operations (including the
+// global -> LDS copies) have completed; other counters are not waited on.
+__device__ __forceinline__ void wait_vmcnt0() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+__device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
+
 __device__ __forceinline__ u16 f32_to_bf16(float f) {  // round to nearest even (v_cvt_pk_bf16_f32)
   return __builtin_bit_cast(u16, (__bf16)f);
 }
@@ -70,34 +94,75 @@ __device__ __forceinline__ short8 kc_read(const char* tile, int row, int chunk) 
   return *reinterpret_cast<const short8*>(tile + kc_offset(row, chunk));
 }
 
-// ---- mn-contiguous LDS tiles (rows of COLS bf16, COLS >= 128) --------------
-__device__ __forceinline__ int mc_swz(int row) { return 2 * (row & 3) + 8 * ((row >> 3) & 1); }
+// ---- k-contiguous LDS tiles of 32 k (rows of 64 bytes = 4 chunks) ----------
+// Chunk q of row p sits at position q ^ ((p >> 2) & 3): the 16 rows read by 16
+// lanes in one cycle then cover all 64 banks.
+__device__ __forceinline__ int kc32_swz(int row) { return (row >> 2) & 3; }
 
-template <int COLS>
-__device__ __forceinline__ uint32_t mc_offset(int row, int chunk) {
-  return (uint32_t)(row * (COLS * 2) + ((chunk ^ mc_swz(row)) << 4));
+__device__ __forceinline__ uint32_t kc32_offset(int row, int chunk) {
+  return (uint32_t)(row * 64 + ((chunk ^ kc32_swz(row)) << 4));
 }
 
-// Matrix-core operand (A or B layout) of 16 columns x 32 k from an mn-contiguous
-// tile whose rows are k: lane (g, c) receives column col0 + c, k rows
+__device__ __forceinline__ short8 kc32_read(const char* tile, int row, int chunk) {
+  return *reinterpret_cast<const short8*>(tile + kc32_offset(row, chunk));
+}
+
+// s_waitcnt with only the vector-memory count: wait until at most N of this
+// wave's vector-memory operations (global -> LDS copies included) are
+// outstanding.  gfx9 encoding: vmcnt[3:0] in bits 3:0, vmcnt[5:4] in bits 15:14,
+// expcnt (bits 6:4) and lgkmcnt (bits 11:8) left at their maxima.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// ---- mn-contiguous LDS tiles (rows of COLS bf16, COLS >= 128) --------------
+__device__ __forceinline__ int mc16_swz(int row) { return 2 * (row & 3) + 8 * ((row >> 3) & 1); }
+__device__ __forceinline__ int mc32_swz(int row) { return 4 * (row & 3); }
+
+template <int COLS>
+__device__ __forceinline__ uint32_t mc16_offset(int row, int chunk) {
+  return (uint32_t)(row * (COLS * 2) + ((chunk ^ mc16_swz(row)) << 4));
+}
+template <int COLS>
+__device__ __forceinline__ uint32_t mc32_offset(int row, int chunk) {
+  return (uint32_t)(row * (COLS * 2) + ((chunk ^ mc32_swz(row)) << 4));
+}
+
+__device__ __forceinline__ short8 join4(short4v lo, short4v hi) {
+  return short8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+}
+
+// 16x16x32 operand (16 columns x 32 k) from an mn-contiguous tile whose rows
+// are k: lane (g = l/16, c = l%16) receives column col0 + c, k rows
 // krow0 + 8g .. 8g+7.
 template <int COLS>
-__device__ __forceinline__ short8 mc_read_tr(const char* tile, int krow0, int col0, int lane) {
+__device__ __forceinline__ short8 mc16_read_tr(const char* tile, int krow0, int col0, int lane) {
   const int g = lane >> 4, j = lane & 15;
   const int e = j >> 2, q = j & 3;            // this lane addresses row e of 4, 4-column piece q
   const int col = col0 + 4 * q;
-  short4v lo, hi;
-  {
-    const int row = krow0 + 8 * g + e;
-    const char* p = tile + mc_offset<COLS>(row, col >> 3) + (col & 7) * 2;
-    lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4v*)(p));
-  }
-  {
-    const int row = krow0 + 8 * g + 4 + e;
-    const char* p = tile + mc_offset<COLS>(row, col >> 3) + (col & 7) * 2;
-    hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4v*)(p));
-  }
-  return short8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  const int r0 = krow0 + 8 * g + e;
+  const char* p0 = tile + mc16_offset<COLS>(r0, col >> 3) + (col & 7) * 2;
+  const char* p1 = tile + mc16_offset<COLS>(r0 + 4, col >> 3) + (col & 7) * 2;
+  return join4(__builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4v*)p0),
+               __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4v*)p1));
+}
+
+// 32x32x16 operand (32 columns x 16 k) from an mn-contiguous tile whose rows
+// are k: lane (g = l/32, c = l%32) receives column col0 + c, k rows
+// krow0 + 8g .. 8g+7.  Lanes 16h .. 16h+15 of each half-wave cover columns
+// col0 + 16(h%2) .. +15.
+template <int COLS>
+__device__ __forceinline__ short8 mc32_read_tr(const char* tile, int krow0, int col0, int lane) {
+  const int g = lane >> 5, h = (lane >> 4) & 1, j = lane & 15;
+  const int e = j >> 2, q = j & 3;
+  const int col = col0 + 16 * h + 4 * q;
+  const int r0 = krow0 + 8 * g + e;
+  const char* p0 = tile + mc32_offset<COLS>(r0, col >> 3) + (col & 7) * 2;
+  const char* p1 = tile + mc32_offset<COLS>(r0 + 4, col >> 3) + (col & 7) * 2;
+  return join4(__builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4v*)p0),
+               __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4v*)p1));
 }
 
 // Block index -> tile coordinates.  Workgroups are dealt to the 8 XCDs round

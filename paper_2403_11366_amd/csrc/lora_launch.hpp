@@ -14,7 +14,10 @@ inline int pad_rank(int64_t r) { return (int)((r + 15) / 16) * 16; }
 // Token count padded to the 64-token chunk of the split-K reductions.
 inline int64_t pad_tokens(int64_t m) { return (m + 63) / 64 * 64; }
 
-enum GemmTile { TILE_256x256 = 0, TILE_256x128 = 1, TILE_128x128 = 2 };
+// Output tiles of the two large GEMMs (tokens x features): 256x256 and 128x256
+// run 8 waves (two per SIMD) as 2 x 4 waves of 128 x 64 and 64 x 64;
+// 128x128 runs 4 waves of 64 x 64.
+enum GemmTile { TILE_256x256 = 0, TILE_128x256 = 1, TILE_128x128 = 2 };
 
 // Pick the output tile of the two large GEMMs for an M x N output.  Every
 // workgroup of these kernels fills one compute unit (LDS-limited), so the
@@ -23,7 +26,7 @@ enum GemmTile { TILE_256x256 = 0, TILE_256x128 = 1, TILE_128x128 = 2 };
 // tiles read less LDS and L2 per flop).
 inline GemmTile choose_gemm_tile(int64_t M, int64_t N) {
   struct C { GemmTile t; int bm, bn; double eff; };
-  const C cands[3] = {{TILE_256x256, 256, 256, 1.0}, {TILE_256x128, 256, 128, 0.9},
+  const C cands[3] = {{TILE_256x256, 256, 256, 1.0}, {TILE_128x256, 128, 256, 0.9},
                       {TILE_128x128, 128, 128, 0.75}};
   GemmTile best = TILE_256x256;
   double best_cost = 1e300;
