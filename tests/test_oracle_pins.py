@@ -315,3 +315,11 @@ def test_pins_catch_planted_mistake(name, fwd, bwd):
         except AssertionError:
             failed.append(check.__name__)
     assert failed, f"planted mistake {name} passed every pin"
+
+
+def test_f64_to_bf16_bits_rounding():
+    """The oracle's bf16 encoder used by the bit-exact GPU tests: exact for
+    small integers, ties to even (1 + 2^-8 -> 1, 1 + 3*2^-8 -> 1 + 2^-6)."""
+    vals = np.array([0.0, 1.0, -3.0, 256.0, 255.0, 1 + 2 ** -8, 1 + 3 * 2 ** -8], dtype=np.float64)
+    got = oracle.bf16_bits_to_f64(oracle.f64_to_bf16_bits(vals))
+    assert got.tolist() == [0.0, 1.0, -3.0, 256.0, 255.0, 1.0, 1 + 2 ** -6]
