@@ -2,20 +2,22 @@
 // Section 3, for the trainable A and B; W0 is frozen so no dW is formed):
 //   dU = s dY B,   dX = dY W + dU A,   dB = s dY^T U,   dA = dU^T X.
 //
-// Kernels, in stream order:
+// Kernels, in stream order (four launches; each launch costs a few
+// microseconds on its own, so small steps share launches):
 //   prep      Bt = B^T (rank padded to RP with zeros); Ut2 = U^T split into a
 //             bf16 high part and a bf16 low part (tokens padded to mp).
 //   du        dU = s dY B, reducing over n.  Writes dU2 (token-major, high |
 //             low) for the dX GEMM and dUt2 (its transpose) for dA.
-//   tokred    dB^T partials = Ut2 . dY over token ranges (split-K over m).
+//   tokred    one launch, two token reductions split over token ranges:
+//             dB^T partials = Ut2 . dY and dA partials = dUt2 . X.
 //   dx        dX = [dY | dU2] . [W ; A ; A]: one GEMM whose k loop runs over
 //             n and then over the 2 RP wide slab (high and low part of dU
 //             against the same A rows).  W is read through LDS with the
 //             transposing ds_read_b64_tr_b16, since the product contracts
-//             W over its rows.
-//   tokred    dA partials = dUt2 . X over token ranges.
-//   finalize  sums the partials of dB and dA in a fixed order (no atomics, so
-//             results are bit-identical from run to run) and applies s to dB.
+//             W over its rows.  After its tile, each workgroup of this launch
+//             sums a slice of the dB and dA partials in a fixed order (no
+//             atomics, so results are bit-identical from run to run) and
+//             applies s to dB.
 #include "lora_device.hpp"
 #include "lora_launch.hpp"
 
@@ -125,11 +127,24 @@ __global__ __launch_bounds__(512) void lora_bwd_du_kernel(
 // P[t][i] * Q[i][c], t < RP (the high and low rows of P are summed), for a
 // tile of kRedCols columns.  P ([2RP][mp], token-contiguous) is read straight
 // into matrix-core A operands; Q ([m][cols]) is staged in LDS 64 tokens at a
-// time and read transposed.
+// time and read transposed.  One launch serves two such problems (dB^T from
+// Ut2 and dY, dA from dUt2 and X): workgroups [0, nb0) take the first.
+struct RedProblem {
+  const u16* P;
+  const u16* Q;
+  float* part;
+  int ncols, span, col_tiles;
+};
+
 template <int NW, int RP>
-__global__ __launch_bounds__(64 * NW) void lora_tokred_kernel(
-    const u16* __restrict__ P, const u16* __restrict__ Q, float* __restrict__ part,
-    int m, int mp, int ncols, int span) {
+__global__ __launch_bounds__(64 * NW) void lora_tokred_kernel(RedProblem p0, RedProblem p1, int nb0, int m, int mp) {
+  const bool first = (int)blockIdx.x < nb0;
+  const RedProblem& pr = first ? p0 : p1;
+  const int bid = first ? (int)blockIdx.x : (int)blockIdx.x - nb0;
+  const u16* __restrict__ P = pr.P;
+  const u16* __restrict__ Q = pr.Q;
+  float* __restrict__ part = pr.part;
+  const int ncols = pr.ncols, span = pr.span;
   constexpr int BNC = kRedCols;
   constexpr int NT = 64 * NW;
   constexpr int WC = BNC / NW;
@@ -143,8 +158,8 @@ __global__ __launch_bounds__(64 * NW) void lora_tokred_kernel(
   static_assert(CH % NT == 0 && WC % 16 == 0, "shape split");
   __shared__ __attribute__((aligned(16))) char smem[2 * STAGE];
 
-  const int c0 = blockIdx.x * BNC;
-  const int sp = blockIdx.y;
+  const int c0 = (bid % pr.col_tiles) * BNC;
+  const int sp = bid / pr.col_tiles;
   const int tb = sp * span;
   const int te = min(mp, tb + span);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -232,23 +247,32 @@ __global__ __launch_bounds__(64 * NW) void lora_tokred_kernel(
 }
 
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void lora_bwd_finalize_kernel(
-    const float* __restrict__ pb, const float* __restrict__ pa, float* __restrict__ dB,
-    float* __restrict__ dA, int n, int k, int r, int rp, int sb, int sa, float s) {
-  const int nb = n * r, na = r * k;
-  const int stride = gridDim.x * blockDim.x;
-  for (int e = blockIdx.x * blockDim.x + threadIdx.x; e < nb + na; e += stride) {
+// Fixed-order sum of the split partials of dB and dA (s applied to dB), no
+// atomics.  Runs at the end of the dX workgroups, after the token reductions
+// have completed in stream order.
+struct FinalizeArgs {
+  const float* pb;
+  const float* pa;
+  float* dB;
+  float* dA;
+  int n, k, r, rp, sb, sa;
+  float s;
+};
+
+__device__ __forceinline__ void finalize_partials(const FinalizeArgs& f, int first, int stride) {
+  const int nb = f.n * f.r, na = f.r * f.k;
+  for (int e = first; e < nb + na; e += stride) {
     if (e < nb) {  // e = t * n + j: partial reads along j are contiguous
-      const int t = e / n, j = e - t * n;
+      const int t = e / f.n, j = e - t * f.n;
       float v = 0.f;
-      for (int p = 0; p < sb; ++p) v += pb[((size_t)p * rp + t) * n + j];
-      dB[(size_t)j * r + t] = s * v;
+      for (int p = 0; p < f.sb; ++p) v += f.pb[((size_t)p * f.rp + t) * f.n + j];
+      f.dB[(size_t)j * f.r + t] = f.s * v;
     } else {
-      const int f = e - nb;
-      const int t = f / k, l = f - t * k;
+      const int g = e - nb;
+      const int t = g / f.k, l = g - t * f.k;
       float v = 0.f;
-      for (int p = 0; p < sa; ++p) v += pa[((size_t)p * rp + t) * k + l];
-      dA[f] = v;
+      for (int p = 0; p < f.sa; ++p) v += f.pa[((size_t)p * f.rp + t) * f.k + l];
+      f.dA[g] = v;
     }
   }
 }
@@ -266,10 +290,11 @@ template <int BM, int BN, int WM, int WN, int RP>
 __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
     const u16* __restrict__ dY, const u16* __restrict__ W, const u16* __restrict__ dU2,
     const u16* __restrict__ A, u16* __restrict__ dX, int m, int n, int k, int r, int mp,
-    int tiles_m, int tiles_n) {
+    int tiles_m, int tiles_n, FinalizeArgs fin) {
   constexpr int NW = WM * WN;
   constexpr int NT = 64 * NW;
   constexpr int WTI = BM / WM, WTJ = BN / WN;
+
   constexpr int FI = WTI / 32, FJ = WTJ / 32;
   constexpr int STAGE = BM * 128 + 64 * BN * 2;
   constexpr int KS2 = 2 * RP;
@@ -283,7 +308,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
   __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
 
   int tm, tn;
-  tile_coords(tiles_m, tiles_n, 8, tm, tn);
+  tile_coords(tiles_m, tiles_n, 8, (int)blockIdx.x, tm, tn);
   const int m0 = tm * BM, l0 = tn * BN;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = uniform(tid >> 6);
@@ -358,18 +383,22 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
 #pragma unroll
     for (int b = 0; b < FI; ++b) acc[a][b] = floatx16{};
 
-  auto substep = [&](const char* sb, int ks) {
+  // Fragments of the next 16-wide substep are read while the current one
+  // multiplies (two register sets, p = substep parity).
+  short8 fw[2][FJ], fy[2][FI];
+  auto read_frags = [&](const char* sb, int ks, int p) {
     const char* Ys = sb;
     const char* Ws = sb + BM * 128;
-    short8 fw[FJ], fy[FI];
 #pragma unroll
-    for (int fj = 0; fj < FJ; ++fj) fw[fj] = mc32_read_tr<BN>(Ws, 16 * ks, wn * WTJ + 32 * fj, lane);
+    for (int fj = 0; fj < FJ; ++fj) fw[p][fj] = mc32_read_tr<BN>(Ws, 16 * ks, wn * WTJ + 32 * fj, lane);
 #pragma unroll
-    for (int fi = 0; fi < FI; ++fi) fy[fi] = kc_read(Ys, wm * WTI + 32 * fi + c32, 2 * ks + g);
+    for (int fi = 0; fi < FI; ++fi) fy[p][fi] = kc_read(Ys, wm * WTI + 32 * fi + c32, 2 * ks + g);
+  };
+  auto multiply = [&](int p) {
 #pragma unroll
     for (int fi = 0; fi < FI; ++fi)
 #pragma unroll
-      for (int fj = 0; fj < FJ; ++fj) acc[fj][fi] = mfma32x32x16(fw[fj], fy[fi], acc[fj][fi]);
+      for (int fj = 0; fj < FJ; ++fj) acc[fj][fi] = mfma32x32x16(fw[p][fj], fy[p][fi], acc[fj][fi]);
   };
 
   gload(0);
@@ -379,8 +408,12 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
     const bool more = st + 1 < nst;
     if (more) gload(st + 1);
     const char* sb = smem + (st & 1) * STAGE;
+    read_frags(sb, 0, 0);
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) substep(sb, ks);
+    for (int ks = 0; ks < 4; ++ks) {
+      if (ks < 3) read_frags(sb, ks + 1, (ks + 1) & 1);
+      multiply(ks & 1);
+    }
     if (more) swrite((st + 1) & 1);
     __syncthreads();
   }
@@ -402,15 +435,19 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
         *reinterpret_cast<uint2*>(xrow + l) = uint2{lo, hi};
       }
   }
+  // After its tile, every workgroup sums a slice of the dA, dB partials
+  // (complete: the token reductions ran before this launch in stream order).
+  finalize_partials(fin, (int)blockIdx.x * NT + (int)threadIdx.x, (int)gridDim.x * NT);
 }
 
 // ---------------------------------------------------------------------------
 template <int BM, int BN, int WM, int WN, int RP>
-static hipError_t launch_dx_cfg(const BwdArgs& a, const BwdLayout& L, hipStream_t st) {
+static hipError_t launch_dx_cfg(const BwdArgs& a, const BwdLayout& L, const FinalizeArgs& fin, hipStream_t st) {
   const int tiles_m = (int)((a.m + BM - 1) / BM), tiles_n = (int)((a.k + BN - 1) / BN);
-  hipLaunchKernelGGL((lora_bwd_dx_kernel<BM, BN, WM, WN, RP>), dim3(tiles_m * tiles_n), dim3(64 * WM * WN), 0, st,
+  const int nt = 64 * WM * WN;
+  hipLaunchKernelGGL((lora_bwd_dx_kernel<BM, BN, WM, WN, RP>), dim3(tiles_m * tiles_n), dim3(nt), 0, st,
                      a.dY, a.W, reinterpret_cast<const u16*>(a.ws + L.du2), a.A, a.dX, (int)a.m, (int)a.n,
-                     (int)a.k, (int)a.r, (int)L.mp, tiles_m, tiles_n);
+                     (int)a.k, (int)a.r, (int)L.mp, tiles_m, tiles_n, fin);
   return hipGetLastError();
 }
 
@@ -434,28 +471,22 @@ static hipError_t launch_bwd_rp(const BwdArgs& a, const BwdLayout& L, hipStream_
   hipLaunchKernelGGL((lora_bwd_du_kernel<RP>), dim3(mp / 16), dim3(512), 0, st, a.dY, Bt, dU2, dUt2, m, n, mp, a.s);
   if ((e = hipGetLastError()) != hipSuccess) return e;
 
-  hipLaunchKernelGGL((lora_tokred_kernel<4, RP>), dim3(L.plan_b.col_tiles, L.plan_b.splits), dim3(256), 0, st,
-                     Ut2, a.dY, pb, m, mp, n, (int)L.plan_b.span);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
-
-  switch (choose_gemm_tile(a.m, a.k)) {
-    case TILE_256x256: e = launch_dx_cfg<256, 256, 2, 4, RP>(a, L, st); break;
-    case TILE_128x256: e = launch_dx_cfg<128, 256, 2, 4, RP>(a, L, st); break;
-    default: e = launch_dx_cfg<128, 128, 2, 2, RP>(a, L, st); break;
-  }
-  if (e != hipSuccess) return e;
-
-  hipLaunchKernelGGL((lora_tokred_kernel<4, RP>), dim3(L.plan_a.col_tiles, L.plan_a.splits), dim3(256), 0, st,
-                     dUt2, a.X, pa, m, mp, k, (int)L.plan_a.span);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
-
   {
-    const int64_t total = (int64_t)n * r + (int64_t)r * k;
-    const int blocks = (int)std::min<int64_t>((total + 255) / 256, 4096);
-    hipLaunchKernelGGL(lora_bwd_finalize_kernel, dim3(blocks), dim3(256), 0, st, pb, pa, a.dB, a.dA, n, k, r, RP,
-                       L.plan_b.splits, L.plan_a.splits, a.s);
+    const RedProblem pbp{Ut2, a.dY, pb, n, (int)L.plan_b.span, L.plan_b.col_tiles};
+    const RedProblem pap{dUt2, a.X, pa, k, (int)L.plan_a.span, L.plan_a.col_tiles};
+    const int nb0 = L.plan_b.col_tiles * L.plan_b.splits;
+    const int nb1 = L.plan_a.col_tiles * L.plan_a.splits;
+    hipLaunchKernelGGL((lora_tokred_kernel<4, RP>), dim3(nb0 + nb1), dim3(256), 0, st, pbp, pap, nb0, m, mp);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
+
+  const FinalizeArgs fin{pb, pa, a.dB, a.dA, n, k, r, RP, L.plan_b.splits, L.plan_a.splits, a.s};
+  switch (choose_gemm_tile(a.m, a.k)) {
+    case TILE_256x256: e = launch_dx_cfg<256, 256, 2, 4, RP>(a, L, fin, st); break;
+    case TILE_128x256: e = launch_dx_cfg<128, 256, 2, 4, RP>(a, L, fin, st); break;
+    default: e = launch_dx_cfg<128, 128, 2, 2, RP>(a, L, fin, st); break;
+  }
+  if (e != hipSuccess) return e;
   return hipSuccess;
 }
 

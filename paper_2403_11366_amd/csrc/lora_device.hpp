@@ -165,12 +165,12 @@ __device__ __forceinline__ short8 mc32_read_tr(const char* tile, int krow0, int 
                __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4v*)p1));
 }
 
-// Block index -> tile coordinates.  Workgroups are dealt to the 8 XCDs round
-// robin (block b runs on XCD b % 8); the first step renumbers blocks so each
+// Tile workgroup index -> tile coordinates.  Workgroups are dealt to the 8
+// XCDs round robin (block b runs on XCD b % 8); the first step renumbers blocks so each
 // XCD receives a contiguous range of tile ids, the second walks tiles in
 // groups of `group` tile-rows so neighbours share operand panels in that XCD's L2.
-__device__ __forceinline__ void tile_coords(int tiles_m, int tiles_n, int group, int& tm, int& tn) {
-  const int nb = gridDim.x, b = blockIdx.x;
+__device__ __forceinline__ void tile_coords(int tiles_m, int tiles_n, int group, int b, int& tm, int& tn) {
+  const int nb = tiles_m * tiles_n;  // b: this workgroup's index among the tile workgroups
   const int xcd = b & 7, idx = b >> 3;
   const int per = nb >> 3, rem = nb & 7;
   const int lid = (xcd < rem) ? xcd * (per + 1) + idx : rem * (per + 1) + (xcd - rem) * per + idx;

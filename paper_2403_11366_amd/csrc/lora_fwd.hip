@@ -54,7 +54,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
   __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
 
   int tm, tn;
-  tile_coords(tiles_m, tiles_n, 8, tm, tn);
+  tile_coords(tiles_m, tiles_n, 8, (int)blockIdx.x, tm, tn);
   const int m0 = tm * BM, n0 = tn * BN;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = uniform(tid >> 6);
@@ -130,30 +130,33 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
 #pragma unroll
   for (int fu = 0; fu < FUW; ++fu) urow[fu] = wm * WTI + 32 * ((wn + WN * fu) % FI) + c32;
 
-  auto substep = [&](const char* sb, int ks) {
+  // Fragments of the next 16-wide substep are read while the current one
+  // multiplies (two register sets, p = substep parity).
+  short8 fw[2][FJ], fx[2][FI], fa[2][FT], fxu[2][FUW];
+  auto read_frags = [&](const char* sb, int ks, int p) {
     const char* Xs = sb;
     const char* Ws = sb + BM * 128;
     const char* As = sb + (BM + BN) * 128;
     const int ch = 2 * ks + g;
-    short8 fw[FJ], fx[FI];
 #pragma unroll
-    for (int fj = 0; fj < FJ; ++fj) fw[fj] = kc_read(Ws, wn * WTJ + 32 * fj + c32, ch);
+    for (int fj = 0; fj < FJ; ++fj) fw[p][fj] = kc_read(Ws, wn * WTJ + 32 * fj + c32, ch);
 #pragma unroll
-    for (int fi = 0; fi < FI; ++fi) fx[fi] = kc_read(Xs, wm * WTI + 32 * fi + c32, ch);
+    for (int fi = 0; fi < FI; ++fi) fx[p][fi] = kc_read(Xs, wm * WTI + 32 * fi + c32, ch);
+#pragma unroll
+    for (int ft = 0; ft < FT; ++ft) fa[p][ft] = kc_read(As, 32 * ft + c32, ch);
+#pragma unroll
+    for (int fu = 0; fu < FUW; ++fu) fxu[p][fu] = kc_read(Xs, urow[fu], ch);
+  };
+  auto multiply = [&](int p, int ks) {
 #pragma unroll
     for (int fi = 0; fi < FI; ++fi)
 #pragma unroll
-      for (int fj = 0; fj < FJ; ++fj) acc[fj][fi] = mfma32x32x16(fw[fj], fx[fi], acc[fj][fi]);
+      for (int fj = 0; fj < FJ; ++fj) acc[fj][fi] = mfma32x32x16(fw[p][fj], fx[p][fi], acc[fj][fi]);
     if (NDUP == 1 || ks % NDUP == udup) {     // wave-uniform; unconditional when NDUP == 1
-      short8 fa[FT], fxu[FUW];
-#pragma unroll
-      for (int ft = 0; ft < FT; ++ft) fa[ft] = kc_read(As, 32 * ft + c32, ch);
-#pragma unroll
-      for (int fu = 0; fu < FUW; ++fu) fxu[fu] = kc_read(Xs, urow[fu], ch);
 #pragma unroll
       for (int fu = 0; fu < FUW; ++fu)
 #pragma unroll
-        for (int ft = 0; ft < FT; ++ft) uacc[ft][fu] = mfma32x32x16(fa[ft], fxu[fu], uacc[ft][fu]);
+        for (int ft = 0; ft < FT; ++ft) uacc[ft][fu] = mfma32x32x16(fa[p][ft], fxu[p][fu], uacc[ft][fu]);
     }
   };
 
@@ -165,8 +168,12 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
     const bool more = kb + 1 < nkb;
     if (more) gload(kb + 1);
     const char* sb = smem + (kb & 1) * STAGE;
+    read_frags(sb, 0, 0);
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) substep(sb, ks);
+    for (int ks = 0; ks < 4; ++ks) {
+      if (ks < 3) read_frags(sb, ks + 1, (ks + 1) & 1);
+      multiply(ks & 1, ks);
+    }
     if (more) swrite((kb + 1) & 1);
     __syncthreads();
   }
