@@ -58,6 +58,47 @@ def measured_traffic(workload: str):
     return rec.get("hbm_bytes_per_launch")
 
 
+def summarize_traffic(root: str, workload: str, copy_mib: int):
+    """Turn four rocprofv3 --pmc runs into HBM bytes per forward-kernel launch.
+
+    root/{fwd_fetch,fwd_write,copy_fetch,copy_write}/ hold the counter CSVs of
+    `--only fwd` and `--only copy` runs with FETCH_SIZE and WRITE_SIZE (KiB per
+    dispatch).  Each forward reading is scaled by known/measured for a plain
+    copy of copy_mib MiB (which reads and writes exactly that many bytes)."""
+    import csv
+    import glob
+
+    def per_dispatch(sub, counter, name_part):
+        vals = {}
+        for f in glob.glob(os.path.join(root, sub, "**", "*counter_collection.csv"), recursive=True):
+            for r in csv.DictReader(open(f)):
+                if r["Counter_Name"] == counter and name_part in r["Kernel_Name"]:
+                    vals[r["Dispatch_Id"]] = vals.get(r["Dispatch_Id"], 0.0) + float(r["Counter_Value"])
+        if not vals:
+            raise SystemExit(f"no {counter} rows for {name_part} under {root}/{sub}")
+        v = sorted(vals.values())
+        return v[len(v) // 2], len(v)
+
+    f_fwd, nf = per_dispatch("fwd_fetch", "FETCH_SIZE", "lora_fwd_kernel")
+    w_fwd, nw = per_dispatch("fwd_write", "WRITE_SIZE", "lora_fwd_kernel")
+    f_cpy, _ = per_dispatch("copy_fetch", "FETCH_SIZE", "")
+    w_cpy, _ = per_dispatch("copy_write", "WRITE_SIZE", "")
+    known_kib = copy_mib * 1024.0
+    sf, sw = known_kib / f_cpy, known_kib / w_cpy
+    fetch_b = f_fwd * sf * 1024.0
+    write_b = w_fwd * sw * 1024.0
+    rec = {"workload": workload, "kernel": "lora_fwd_kernel", "kernel_source_sha": kernel_source_hash(),
+           "fetch_kib_raw": f_fwd, "write_kib_raw": w_fwd, "copy_mib": copy_mib,
+           "copy_fetch_kib_raw": f_cpy, "copy_write_kib_raw": w_cpy,
+           "fetch_scale": sf, "write_scale": sw,
+           "hbm_fetch_bytes_per_launch": fetch_b, "hbm_write_bytes_per_launch": write_b,
+           "hbm_bytes_per_launch": fetch_b + write_b, "dispatches": [nf, nw]}
+    os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(rec, f, indent=1)
+    print(json.dumps(rec))
+
+
 def cpu_baseline(shape, seconds: float):
     """Time the fp64 oracle (as it stands) on this host for `shape`."""
     import numpy as np
@@ -92,7 +133,16 @@ def main():
     ap.add_argument("--config", default="llama2_7b_q_proj")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--only", choices=["fwd", "copy"], default=None,
+                    help="run only forward launches, or only a plain device copy (for counter runs)")
+    ap.add_argument("--copy-mib", type=int, default=512)
+    ap.add_argument("--summarize-traffic", metavar="DIR", default=None,
+                    help="write the HBM-traffic record from counter runs under DIR and exit")
     args = ap.parse_args()
+
+    if args.summarize_traffic:
+        summarize_traffic(args.summarize_traffic, args.config, args.copy_mib)
+        return
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -110,6 +160,16 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     lora.load_library()
+    if args.only == "copy":
+        n = args.copy_mib << 20
+        src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(args.steps):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"[bench] {args.steps} copies of {args.copy_mib} MiB done")
+        return
     shapes = CONFIGS[args.config]
     dev = "cuda"
     stream = torch.cuda.current_stream()
@@ -148,6 +208,14 @@ def main():
         for s, sets, out in proj:
             fwd(i, s, sets, out)
             bwd(i, s, sets, out)
+
+    if args.only == "fwd":
+        for i in range(args.warmup + args.steps):
+            for s_, sets_, out_ in proj:
+                fwd(i, s_, sets_, out_)
+        torch.cuda.synchronize()
+        log(f"[bench] {args.warmup + args.steps} forward launches done")
+        return
 
     # ---- whole path
     for i in range(args.warmup):
