@@ -5,10 +5,9 @@
 // features) and walks k in stages of 64.  Per stage it stages three
 // k-contiguous tiles in LDS -- X[BM rows], W[BN rows] and the LoRA
 // down-projection A padded to RP rows -- so each X tile is read once and
-// feeds both the W columns and the r extra "U columns".  The next stage's
-// global loads are issued into registers before the current stage is
-// multiplied and written to the other LDS buffer afterwards (one barrier per
-// stage).
+// feeds both the W columns and the r extra "U columns".  Global loads run two
+// stages ahead in registers and are written to the free LDS buffer at the top
+// of the stage before their use (one barrier per stage).
 //
 // Matrix-core products use v_mfma_f32_32x32x16_bf16 and are formed transposed
 // (W and A as the A operand, X as the B operand), so each lane's accumulator
@@ -16,7 +15,7 @@
 //
 // The U columns of a token fragment are accumulated by the waves that share
 // it (each wave owns fixed fragments and k substeps, so the U products are
-// branch-free or behind one wave-uniform branch).  After the k loop the
+// branch-free).  After the k loop the
 // epilogue parks U in LDS, writes it out (tile column 0 only), and adds
 // s U B^T to the accumulators with a short matrix-core pass over t in which
 // s U enters as a bf16 high part and a bf16 low part, then rounds Y to bf16.
@@ -46,6 +45,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
   constexpr int CX = BM * 8, CW = BN * 8, CA = RP * 8;   // 16-byte chunks per region
   constexpr int LX = (CX + NT - 1) / NT, LW = (CW + NT - 1) / NT, LA = (CA + NT - 1) / NT;
   static_assert(WTI % 32 == 0 && WTJ % 32 == 0 && RP % 32 == 0, "32x32 fragments");
+  static_assert(CX % 64 == 0 && CW % 64 == 0 && CA % 64 == 0, "regions end on wave boundaries");
   static_assert(FI >= WN ? FI % WN == 0 : WN % FI == 0, "U fragments split evenly");
   static_assert(4 % NDUP == 0, "U substeps split evenly");
   static_assert(2 * STAGE <= 160 * 1024, "LDS budget");
@@ -67,7 +67,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
   const __amdgpu_buffer_rsrc_t rsW = make_rsrc(W + (size_t)n0 * k, (uint64_t)min(BN, n - n0) * rowbytes);
   const __amdgpu_buffer_rsrc_t rsA = make_rsrc(A, (uint64_t)r * rowbytes);
 
-  // Stage k-block kb+1 in registers while kb multiplies: thread chunk
+  // Register staging of one k-block of the three regions: thread chunk
   // q = tid + i NT of a region is row q/8, k-chunk q%8 (coalesced 128-byte rows).
   int4v gx[LX], gw[LW], ga[LA];
   auto gload = [&](int kb) {
@@ -75,21 +75,21 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
 #pragma unroll
     for (int i = 0; i < LX; ++i) {
       const int q = tid + i * NT;
-      if (CX % NT != 0 && q >= CX) break;
+      if (CX % NT != 0 && wave * 64 + i * NT >= CX) break;   // wave-uniform
       const int kk = k0 + 8 * (q & 7);
       gx[i] = buf_load16(rsX, kk < k ? (uint32_t)(q >> 3) * rowbytes + (uint32_t)kk * 2 : kOOB);
     }
 #pragma unroll
     for (int i = 0; i < LW; ++i) {
       const int q = tid + i * NT;
-      if (CW % NT != 0 && q >= CW) break;
+      if (CW % NT != 0 && wave * 64 + i * NT >= CW) break;   // wave-uniform
       const int kk = k0 + 8 * (q & 7);
       gw[i] = buf_load16(rsW, kk < k ? (uint32_t)(q >> 3) * rowbytes + (uint32_t)kk * 2 : kOOB);
     }
 #pragma unroll
     for (int i = 0; i < LA; ++i) {
       const int q = tid + i * NT;
-      if (CA % NT != 0 && q >= CA) break;
+      if (CA % NT != 0 && wave * 64 + i * NT >= CA) break;   // wave-uniform
       const int kk = k0 + 8 * (q & 7);
       ga[i] = buf_load16(rsA, kk < k ? (uint32_t)(q >> 3) * rowbytes + (uint32_t)kk * 2 : kOOB);
     }
@@ -99,19 +99,19 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
 #pragma unroll
     for (int i = 0; i < LX; ++i) {
       const int q = tid + i * NT;
-      if (CX % NT != 0 && q >= CX) break;
+      if (CX % NT != 0 && wave * 64 + i * NT >= CX) break;   // wave-uniform
       *reinterpret_cast<int4v*>(sb + kc_offset(q >> 3, q & 7)) = gx[i];
     }
 #pragma unroll
     for (int i = 0; i < LW; ++i) {
       const int q = tid + i * NT;
-      if (CW % NT != 0 && q >= CW) break;
+      if (CW % NT != 0 && wave * 64 + i * NT >= CW) break;   // wave-uniform
       *reinterpret_cast<int4v*>(sb + BM * 128 + kc_offset(q >> 3, q & 7)) = gw[i];
     }
 #pragma unroll
     for (int i = 0; i < LA; ++i) {
       const int q = tid + i * NT;
-      if (CA % NT != 0 && q >= CA) break;
+      if (CA % NT != 0 && wave * 64 + i * NT >= CA) break;   // wave-uniform
       *reinterpret_cast<int4v*>(sb + (BM + BN) * 128 + kc_offset(q >> 3, q & 7)) = ga[i];
     }
   };
@@ -131,7 +131,10 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
   for (int fu = 0; fu < FUW; ++fu) urow[fu] = wm * WTI + 32 * ((wn + WN * fu) % FI) + c32;
 
   // Fragments of the next 16-wide substep are read while the current one
-  // multiplies (two register sets, p = substep parity).
+  // multiplies (two register sets, p = substep parity).  The U products of a
+  // shared token fragment run on substeps ks % NDUP == 0 only: there share
+  // udup multiplies the k columns of substep ks + udup, so every wave executes
+  // the same instruction stream.
   short8 fw[2][FJ], fx[2][FI], fa[2][FT], fxu[2][FUW];
   auto read_frags = [&](const char* sb, int ks, int p) {
     const char* Xs = sb;
@@ -142,17 +145,20 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
     for (int fj = 0; fj < FJ; ++fj) fw[p][fj] = kc_read(Ws, wn * WTJ + 32 * fj + c32, ch);
 #pragma unroll
     for (int fi = 0; fi < FI; ++fi) fx[p][fi] = kc_read(Xs, wm * WTI + 32 * fi + c32, ch);
+    if (ks % NDUP == 0) {
+      const int uch = ch + 2 * udup;
 #pragma unroll
-    for (int ft = 0; ft < FT; ++ft) fa[p][ft] = kc_read(As, 32 * ft + c32, ch);
+      for (int ft = 0; ft < FT; ++ft) fa[p][ft] = kc_read(As, 32 * ft + c32, uch);
 #pragma unroll
-    for (int fu = 0; fu < FUW; ++fu) fxu[p][fu] = kc_read(Xs, urow[fu], ch);
+      for (int fu = 0; fu < FUW; ++fu) fxu[p][fu] = kc_read(Xs, urow[fu], uch);
+    }
   };
   auto multiply = [&](int p, int ks) {
 #pragma unroll
     for (int fi = 0; fi < FI; ++fi)
 #pragma unroll
       for (int fj = 0; fj < FJ; ++fj) acc[fj][fi] = mfma32x32x16(fw[p][fj], fx[p][fi], acc[fj][fi]);
-    if (NDUP == 1 || ks % NDUP == udup) {     // wave-uniform; unconditional when NDUP == 1
+    if (ks % NDUP == 0) {
 #pragma unroll
       for (int fu = 0; fu < FUW; ++fu)
 #pragma unroll
@@ -160,23 +166,31 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
     }
   };
 
-  const int nkb = (k + 63) / 64;
-  gload(0);
-  swrite(0);
-  __syncthreads();
-  for (int kb = 0; kb < nkb; ++kb) {
-    const bool more = kb + 1 < nkb;
-    if (more) gload(kb + 1);
+  // Pipeline: at the top of stage kb the registers hold k-block kb+1 (loaded
+  // one stage earlier); they go to the free LDS buffer right after the first
+  // fragment reads of kb, then the loads of kb+2 are issued into them.  The
+  // k loop is peeled so the steady state carries no conditionals.
+  auto stage = [&](int kb, bool write_next, bool load_next) {
     const char* sb = smem + (kb & 1) * STAGE;
     read_frags(sb, 0, 0);
+    if (write_next) swrite((kb + 1) & 1);
+    if (load_next) gload(kb + 2);
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
       if (ks < 3) read_frags(sb, ks + 1, (ks + 1) & 1);
       multiply(ks & 1, ks);
     }
-    if (more) swrite((kb + 1) & 1);
     __syncthreads();
-  }
+  };
+  const int nkb = (k + 63) / 64;
+  gload(0);
+  swrite(0);
+  __syncthreads();
+  if (nkb > 1) gload(1);
+  int kb = 0;
+  for (; kb + 2 < nkb; ++kb) stage(kb, true, true);
+  if (kb + 1 < nkb) stage(kb++, true, false);
+  stage(kb, false, false);
 
   // ---- epilogue ------------------------------------------------------------
   // LDS reuse: Us [NDUP][BM][RP] fp32 partial U (summed in fixed order below),
