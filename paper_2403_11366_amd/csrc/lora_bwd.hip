@@ -283,9 +283,9 @@ __device__ __forceinline__ void finalize_partials(const FinalizeArgs& f, int fir
 // of 64 along n: dY [BM rows][64] (k-contiguous) and W [64 rows of n][BN]
 // (mn-contiguous, read with the transposing LDS read).  After the n stages,
 // NSLAB stages cover the 2 RP wide slab: dU2 [BM][2RP] against A's rows, once
-// for the high and once for the low part.  The next stage is loaded into
-// registers while the current one multiplies and written to the other LDS
-// buffer afterwards (one barrier per stage).
+// for the high and once for the low part.  Global loads run two stages ahead
+// in registers and are written to the free LDS buffer at the top of the stage
+// before their use (one barrier per stage).
 template <int BM, int BN, int WM, int WN, int RP>
 __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
     const u16* __restrict__ dY, const u16* __restrict__ W, const u16* __restrict__ dU2,
@@ -304,6 +304,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
   constexpr int LY = (CY + NT - 1) / NT, LW = (CW + NT - 1) / NT;
   static_assert(WTI % 32 == 0 && WTJ % 32 == 0, "32x32 fragments");
   static_assert(BN == 128 || BN == 256, "W tile rows of 256 or 512 bytes");
+  static_assert(NSLAB == 1 || NSLAB == 2, "slab stages of the unrolled tail");
   static_assert(2 * STAGE <= 160 * 1024, "LDS budget");
   __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
 
@@ -319,46 +320,46 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
   const __amdgpu_buffer_rsrc_t rsU = make_rsrc(dU2 + (size_t)m0 * KS2, (uint64_t)min(BM, mp - m0) * urow);
   const __amdgpu_buffer_rsrc_t rsA = make_rsrc(A, (uint64_t)r * wrow);
   const int nkb = (n + 63) / 64;
-  const int nst = nkb + NSLAB;
 
   int4v gy[LY], gw[LW];
-  auto gload = [&](int st) {
-    if (st < nkb) {
-      const int n0 = st * 64;
-      const __amdgpu_buffer_rsrc_t rsW = make_rsrc(W + (size_t)n0 * k, (uint64_t)min(64, n - n0) * wrow);
+  // Loads of W stage st (dY columns and W rows st*64 ..) and of slab stage sl
+  // (dU2 columns and the matching A rows, high part then low part).
+  auto gload_w = [&](int st) {
+    const int n0 = st * 64;
+    const __amdgpu_buffer_rsrc_t rsW = make_rsrc(W + (size_t)n0 * k, (uint64_t)min(64, n - n0) * wrow);
 #pragma unroll
-      for (int i = 0; i < LY; ++i) {
-        const int q = tid + i * NT;
-        if (CY % NT != 0 && q >= CY) break;
-        const int nn = n0 + 8 * (q & 7);
-        gy[i] = buf_load16(rsY, nn < n ? (uint32_t)(q >> 3) * yrow + (uint32_t)nn * 2 : kOOB);
-      }
+    for (int i = 0; i < LY; ++i) {
+      const int q = tid + i * NT;
+      if (CY % NT != 0 && wave * 64 + i * NT >= CY) break;   // wave-uniform
+      const int nn = n0 + 8 * (q & 7);
+      gy[i] = buf_load16(rsY, nn < n ? (uint32_t)(q >> 3) * yrow + (uint32_t)nn * 2 : kOOB);
+    }
 #pragma unroll
-      for (int i = 0; i < LW; ++i) {
-        const int q = tid + i * NT;
-        if (CW % NT != 0 && q >= CW) break;
-        const int ll = l0 + 8 * (q % CPR);
-        gw[i] = buf_load16(rsW, ll < k ? (uint32_t)(q / CPR) * wrow + (uint32_t)ll * 2 : kOOB);
-      }
-    } else {
-      const int kk0 = (st - nkb) * 64;
+    for (int i = 0; i < LW; ++i) {
+      const int q = tid + i * NT;
+      if (CW % NT != 0 && wave * 64 + i * NT >= CW) break;   // wave-uniform
+      const int ll = l0 + 8 * (q % CPR);
+      gw[i] = buf_load16(rsW, ll < k ? (uint32_t)(q / CPR) * wrow + (uint32_t)ll * 2 : kOOB);
+    }
+  };
+  auto gload_s = [&](int sl) {
+    const int kk0 = sl * 64;
 #pragma unroll
-      for (int i = 0; i < LY; ++i) {
-        const int q = tid + i * NT;
-        if (CY % NT != 0 && q >= CY) break;
-        const int kk = kk0 + 8 * (q & 7);
-        gy[i] = buf_load16(rsU, kk < KS2 ? (uint32_t)(q >> 3) * urow + (uint32_t)kk * 2 : kOOB);
-      }
+    for (int i = 0; i < LY; ++i) {
+      const int q = tid + i * NT;
+      if (CY % NT != 0 && wave * 64 + i * NT >= CY) break;   // wave-uniform
+      const int kk = kk0 + 8 * (q & 7);
+      gy[i] = buf_load16(rsU, kk < KS2 ? (uint32_t)(q >> 3) * urow + (uint32_t)kk * 2 : kOOB);
+    }
 #pragma unroll
-      for (int i = 0; i < LW; ++i) {
-        const int q = tid + i * NT;
-        if (CW % NT != 0 && q >= CW) break;
-        const int kk = kk0 + q / CPR;
-        const int t = kk % RP;
-        const int ll = l0 + 8 * (q % CPR);
-        const bool ok = kk < KS2 && t < r && ll < k;
-        gw[i] = buf_load16(rsA, ok ? (uint32_t)t * wrow + (uint32_t)ll * 2 : kOOB);
-      }
+    for (int i = 0; i < LW; ++i) {
+      const int q = tid + i * NT;
+      if (CW % NT != 0 && wave * 64 + i * NT >= CW) break;   // wave-uniform
+      const int kk = kk0 + q / CPR;
+      const int t = kk % RP;
+      const int ll = l0 + 8 * (q % CPR);
+      const bool ok = kk < KS2 && t < r && ll < k;
+      gw[i] = buf_load16(rsA, ok ? (uint32_t)t * wrow + (uint32_t)ll * 2 : kOOB);
     }
   };
   auto swrite = [&](int buf) {
@@ -366,13 +367,13 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
 #pragma unroll
     for (int i = 0; i < LY; ++i) {
       const int q = tid + i * NT;
-      if (CY % NT != 0 && q >= CY) break;
+      if (CY % NT != 0 && wave * 64 + i * NT >= CY) break;
       *reinterpret_cast<int4v*>(sb + kc_offset(q >> 3, q & 7)) = gy[i];
     }
 #pragma unroll
     for (int i = 0; i < LW; ++i) {
       const int q = tid + i * NT;
-      if (CW % NT != 0 && q >= CW) break;
+      if (CW % NT != 0 && wave * 64 + i * NT >= CW) break;
       *reinterpret_cast<int4v*>(sb + BM * 128 + mc32_offset<BN>(q / CPR, q % CPR)) = gw[i];
     }
   };
@@ -401,22 +402,40 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
       for (int fj = 0; fj < FJ; ++fj) acc[fj][fi] = mfma32x32x16(fw[p][fj], fy[p][fi], acc[fj][fi]);
   };
 
-  gload(0);
-  swrite(0);
-  __syncthreads();
-  for (int st = 0; st < nst; ++st) {
-    const bool more = st + 1 < nst;
-    if (more) gload(st + 1);
+  // Same pipeline as the forward GEMM: registers hold stage st+1 at the top
+  // of stage st, go to the free LDS buffer after the first fragment reads,
+  // then receive the loads of stage st+2.  Stages 0 .. nkb-1 run over n, the
+  // NSLAB (1 or 2) slab stages follow; the tail is unrolled so every load is
+  // of a known kind.
+  enum { LD_NONE, LD_W, LD_S0, LD_S1 };
+  auto stage = [&](int st, bool write_next, int load) {
     const char* sb = smem + (st & 1) * STAGE;
     read_frags(sb, 0, 0);
+    if (write_next) swrite((st + 1) & 1);
+    if (load == LD_W) gload_w(st + 2);
+    if (load == LD_S0) gload_s(0);
+    if (load == LD_S1) gload_s(1);
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
       if (ks < 3) read_frags(sb, ks + 1, (ks + 1) & 1);
       multiply(ks & 1);
     }
-    if (more) swrite((st + 1) & 1);
     __syncthreads();
+  };
+  gload_w(0);
+  swrite(0);
+  __syncthreads();
+  int st = 0;
+  if (nkb >= 2) {
+    gload_w(1);
+    for (; st + 2 < nkb; ++st) stage(st, true, LD_W);
+    stage(st++, true, LD_S0);                       // st = nkb - 2
+  } else {
+    gload_s(0);
   }
+  stage(st++, true, NSLAB > 1 ? LD_S1 : LD_NONE);   // writes slab 0
+  if (NSLAB > 1) stage(st++, true, LD_NONE);        // writes slab 1
+  stage(st, false, LD_NONE);
 
 #pragma unroll
   for (int fi = 0; fi < FI; ++fi) {
