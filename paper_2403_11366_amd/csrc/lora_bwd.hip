@@ -284,8 +284,8 @@ __device__ __forceinline__ void finalize_partials(const FinalizeArgs& f, int fir
 // (mn-contiguous, read with the transposing LDS read).  After the n stages,
 // NSLAB stages cover the 2 RP wide slab: dU2 [BM][2RP] against A's rows, once
 // for the high and once for the low part.  Global loads run two stages ahead
-// in registers and are written to the free LDS buffer at the top of the stage
-// before their use (one barrier per stage).
+// in registers and are stored to the free LDS buffer piece by piece during
+// the stage before their use (one barrier per stage).
 template <int BM, int BN, int WM, int WN, int RP>
 __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
     const u16* __restrict__ dY, const u16* __restrict__ W, const u16* __restrict__ dU2,
@@ -321,60 +321,73 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
   const __amdgpu_buffer_rsrc_t rsA = make_rsrc(A, (uint64_t)r * wrow);
   const int nkb = (n + 63) / 64;
 
+  // Staging registers move in pieces, one per 16-wide substep of the stage
+  // that stores them: 0 = the dY (or dU2) rows, 1 and 2 = the two halves of
+  // the W (or A) rows.
+  constexpr int LW1 = (LW + 1) / 2;
   int4v gy[LY], gw[LW];
   // Loads of W stage st (dY columns and W rows st*64 ..) and of slab stage sl
   // (dU2 columns and the matching A rows, high part then low part).
-  auto gload_w = [&](int st) {
+  auto gload_w = [&](int st, int piece) {
     const int n0 = st * 64;
-    const __amdgpu_buffer_rsrc_t rsW = make_rsrc(W + (size_t)n0 * k, (uint64_t)min(64, n - n0) * wrow);
+    if (piece == 0) {
 #pragma unroll
-    for (int i = 0; i < LY; ++i) {
-      const int q = tid + i * NT;
-      if (CY % NT != 0 && wave * 64 + i * NT >= CY) break;   // wave-uniform
-      const int nn = n0 + 8 * (q & 7);
-      gy[i] = buf_load16(rsY, nn < n ? (uint32_t)(q >> 3) * yrow + (uint32_t)nn * 2 : kOOB);
-    }
+      for (int i = 0; i < LY; ++i) {
+        const int q = tid + i * NT;
+        if (CY % NT != 0 && wave * 64 + i * NT >= CY) break;   // wave-uniform
+        const int nn = n0 + 8 * (q & 7);
+        gy[i] = buf_load16(rsY, nn < n ? (uint32_t)(q >> 3) * yrow + (uint32_t)nn * 2 : kOOB);
+      }
+    } else if (piece <= 2) {
+      const __amdgpu_buffer_rsrc_t rsW = make_rsrc(W + (size_t)n0 * k, (uint64_t)min(64, n - n0) * wrow);
 #pragma unroll
-    for (int i = 0; i < LW; ++i) {
-      const int q = tid + i * NT;
-      if (CW % NT != 0 && wave * 64 + i * NT >= CW) break;   // wave-uniform
-      const int ll = l0 + 8 * (q % CPR);
-      gw[i] = buf_load16(rsW, ll < k ? (uint32_t)(q / CPR) * wrow + (uint32_t)ll * 2 : kOOB);
+      for (int i = piece == 1 ? 0 : LW1; i < (piece == 1 ? LW1 : LW); ++i) {
+        const int q = tid + i * NT;
+        if (CW % NT != 0 && wave * 64 + i * NT >= CW) break;   // wave-uniform
+        const int ll = l0 + 8 * (q % CPR);
+        gw[i] = buf_load16(rsW, ll < k ? (uint32_t)(q / CPR) * wrow + (uint32_t)ll * 2 : kOOB);
+      }
     }
   };
-  auto gload_s = [&](int sl) {
+  auto gload_s = [&](int sl, int piece) {
     const int kk0 = sl * 64;
+    if (piece == 0) {
 #pragma unroll
-    for (int i = 0; i < LY; ++i) {
-      const int q = tid + i * NT;
-      if (CY % NT != 0 && wave * 64 + i * NT >= CY) break;   // wave-uniform
-      const int kk = kk0 + 8 * (q & 7);
-      gy[i] = buf_load16(rsU, kk < KS2 ? (uint32_t)(q >> 3) * urow + (uint32_t)kk * 2 : kOOB);
-    }
+      for (int i = 0; i < LY; ++i) {
+        const int q = tid + i * NT;
+        if (CY % NT != 0 && wave * 64 + i * NT >= CY) break;   // wave-uniform
+        const int kk = kk0 + 8 * (q & 7);
+        gy[i] = buf_load16(rsU, kk < KS2 ? (uint32_t)(q >> 3) * urow + (uint32_t)kk * 2 : kOOB);
+      }
+    } else if (piece <= 2) {
 #pragma unroll
-    for (int i = 0; i < LW; ++i) {
-      const int q = tid + i * NT;
-      if (CW % NT != 0 && wave * 64 + i * NT >= CW) break;   // wave-uniform
-      const int kk = kk0 + q / CPR;
-      const int t = kk % RP;
-      const int ll = l0 + 8 * (q % CPR);
-      const bool ok = kk < KS2 && t < r && ll < k;
-      gw[i] = buf_load16(rsA, ok ? (uint32_t)t * wrow + (uint32_t)ll * 2 : kOOB);
+      for (int i = piece == 1 ? 0 : LW1; i < (piece == 1 ? LW1 : LW); ++i) {
+        const int q = tid + i * NT;
+        if (CW % NT != 0 && wave * 64 + i * NT >= CW) break;   // wave-uniform
+        const int kk = kk0 + q / CPR;
+        const int t = kk % RP;
+        const int ll = l0 + 8 * (q % CPR);
+        const bool ok = kk < KS2 && t < r && ll < k;
+        gw[i] = buf_load16(rsA, ok ? (uint32_t)t * wrow + (uint32_t)ll * 2 : kOOB);
+      }
     }
   };
-  auto swrite = [&](int buf) {
+  auto swrite = [&](int buf, int piece) {
     char* sb = smem + buf * STAGE;
+    if (piece == 0) {
 #pragma unroll
-    for (int i = 0; i < LY; ++i) {
-      const int q = tid + i * NT;
-      if (CY % NT != 0 && wave * 64 + i * NT >= CY) break;
-      *reinterpret_cast<int4v*>(sb + kc_offset(q >> 3, q & 7)) = gy[i];
-    }
+      for (int i = 0; i < LY; ++i) {
+        const int q = tid + i * NT;
+        if (CY % NT != 0 && wave * 64 + i * NT >= CY) break;
+        *reinterpret_cast<int4v*>(sb + kc_offset(q >> 3, q & 7)) = gy[i];
+      }
+    } else if (piece <= 2) {
 #pragma unroll
-    for (int i = 0; i < LW; ++i) {
-      const int q = tid + i * NT;
-      if (CW % NT != 0 && wave * 64 + i * NT >= CW) break;
-      *reinterpret_cast<int4v*>(sb + BM * 128 + mc32_offset<BN>(q / CPR, q % CPR)) = gw[i];
+      for (int i = piece == 1 ? 0 : LW1; i < (piece == 1 ? LW1 : LW); ++i) {
+        const int q = tid + i * NT;
+        if (CW % NT != 0 && wave * 64 + i * NT >= CW) break;
+        *reinterpret_cast<int4v*>(sb + BM * 128 + mc32_offset<BN>(q / CPR, q % CPR)) = gw[i];
+      }
     }
   };
 
@@ -402,40 +415,54 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
       for (int fj = 0; fj < FJ; ++fj) acc[fj][fi] = mfma32x32x16(fw[p][fj], fy[p][fi], acc[fj][fi]);
   };
 
-  // Same pipeline as the forward GEMM: registers hold stage st+1 at the top
-  // of stage st, go to the free LDS buffer after the first fragment reads,
-  // then receive the loads of stage st+2.  Stages 0 .. nkb-1 run over n, the
-  // NSLAB (1 or 2) slab stages follow; the tail is unrolled so every load is
-  // of a known kind.
+  // Same pipeline as the forward GEMM: at the top of stage st the registers
+  // hold stage st+1; piece ks goes to the free LDS buffer at substep ks and
+  // its registers then receive the loads of stage st+2.  With ROT the
+  // products of substep 3 run after the barrier (zero operands before stage
+  // 0).  Stages 0 .. nkb-1 run over n, the NSLAB (1 or 2) slab stages follow;
+  // the tail is unrolled so every load is of a known kind.
+  constexpr bool ROT = BM * BN < 256 * 256;
+  if (ROT) {
+#pragma unroll
+    for (int j = 0; j < FJ; ++j) fw[1][j] = short8{};
+#pragma unroll
+    for (int j = 0; j < FI; ++j) fy[1][j] = short8{};
+  }
   enum { LD_NONE, LD_W, LD_S0, LD_S1 };
   auto stage = [&](int st, bool write_next, int load) {
     const char* sb = smem + (st & 1) * STAGE;
     read_frags(sb, 0, 0);
-    if (write_next) swrite((st + 1) & 1);
-    if (load == LD_W) gload_w(st + 2);
-    if (load == LD_S0) gload_s(0);
-    if (load == LD_S1) gload_s(1);
+    if (ROT) multiply(1);
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
+      if (write_next) swrite((st + 1) & 1, ks);
+      if (load == LD_W) gload_w(st + 2, ks);
+      if (load == LD_S0) gload_s(0, ks);
+      if (load == LD_S1) gload_s(1, ks);
       if (ks < 3) read_frags(sb, ks + 1, (ks + 1) & 1);
-      multiply(ks & 1);
+      if (ks < 3 || !ROT) multiply(ks & 1);
     }
     __syncthreads();
   };
-  gload_w(0);
-  swrite(0);
+#pragma unroll
+  for (int pc = 0; pc < 3; ++pc) gload_w(0, pc);
+#pragma unroll
+  for (int pc = 0; pc < 3; ++pc) swrite(0, pc);
   __syncthreads();
   int st = 0;
   if (nkb >= 2) {
-    gload_w(1);
+#pragma unroll
+    for (int pc = 0; pc < 3; ++pc) gload_w(1, pc);
     for (; st + 2 < nkb; ++st) stage(st, true, LD_W);
     stage(st++, true, LD_S0);                       // st = nkb - 2
   } else {
-    gload_s(0);
+#pragma unroll
+    for (int pc = 0; pc < 3; ++pc) gload_s(0, pc);
   }
   stage(st++, true, NSLAB > 1 ? LD_S1 : LD_NONE);   // writes slab 0
   if (NSLAB > 1) stage(st++, true, LD_NONE);        // writes slab 1
   stage(st, false, LD_NONE);
+  if (ROT) multiply(1);
 
 #pragma unroll
   for (int fi = 0; fi < FI; ++fi) {

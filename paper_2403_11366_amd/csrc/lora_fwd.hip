@@ -6,8 +6,8 @@
 // k-contiguous tiles in LDS -- X[BM rows], W[BN rows] and the LoRA
 // down-projection A padded to RP rows -- so each X tile is read once and
 // feeds both the W columns and the r extra "U columns".  Global loads run two
-// stages ahead in registers and are written to the free LDS buffer at the top
-// of the stage before their use (one barrier per stage).
+// stages ahead in registers and are stored to the free LDS buffer piece by
+// piece during the stage before their use (one barrier per stage).
 //
 // Matrix-core products use v_mfma_f32_32x32x16_bf16 and are formed transposed
 // (W and A as the A operand, X as the B operand), so each lane's accumulator
@@ -68,51 +68,63 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
   const __amdgpu_buffer_rsrc_t rsA = make_rsrc(A, (uint64_t)r * rowbytes);
 
   // Register staging of one k-block of the three regions: thread chunk
-  // q = tid + i NT of a region is row q/8, k-chunk q%8 (coalesced 128-byte rows).
+  // q = tid + i NT of a region is row q/8, k-chunk q%8 (coalesced 128-byte
+  // rows).  The block moves in four pieces, one per 16-wide substep of the
+  // stage that stores it: 0 = X rows, 1 and 2 = the two halves of the W rows,
+  // 3 = A rows.
+  constexpr int LW1 = (LW + 1) / 2;
   int4v gx[LX], gw[LW], ga[LA];
-  auto gload = [&](int kb) {
+  auto gload = [&](int kb, int piece) {
     const int k0 = kb * 64;
+    if (piece == 0) {
 #pragma unroll
-    for (int i = 0; i < LX; ++i) {
-      const int q = tid + i * NT;
-      if (CX % NT != 0 && wave * 64 + i * NT >= CX) break;   // wave-uniform
-      const int kk = k0 + 8 * (q & 7);
-      gx[i] = buf_load16(rsX, kk < k ? (uint32_t)(q >> 3) * rowbytes + (uint32_t)kk * 2 : kOOB);
-    }
+      for (int i = 0; i < LX; ++i) {
+        const int q = tid + i * NT;
+        if (CX % NT != 0 && wave * 64 + i * NT >= CX) break;   // wave-uniform
+        const int kk = k0 + 8 * (q & 7);
+        gx[i] = buf_load16(rsX, kk < k ? (uint32_t)(q >> 3) * rowbytes + (uint32_t)kk * 2 : kOOB);
+      }
+    } else if (piece <= 2) {
 #pragma unroll
-    for (int i = 0; i < LW; ++i) {
-      const int q = tid + i * NT;
-      if (CW % NT != 0 && wave * 64 + i * NT >= CW) break;   // wave-uniform
-      const int kk = k0 + 8 * (q & 7);
-      gw[i] = buf_load16(rsW, kk < k ? (uint32_t)(q >> 3) * rowbytes + (uint32_t)kk * 2 : kOOB);
-    }
+      for (int i = piece == 1 ? 0 : LW1; i < (piece == 1 ? LW1 : LW); ++i) {
+        const int q = tid + i * NT;
+        if (CW % NT != 0 && wave * 64 + i * NT >= CW) break;   // wave-uniform
+        const int kk = k0 + 8 * (q & 7);
+        gw[i] = buf_load16(rsW, kk < k ? (uint32_t)(q >> 3) * rowbytes + (uint32_t)kk * 2 : kOOB);
+      }
+    } else {
 #pragma unroll
-    for (int i = 0; i < LA; ++i) {
-      const int q = tid + i * NT;
-      if (CA % NT != 0 && wave * 64 + i * NT >= CA) break;   // wave-uniform
-      const int kk = k0 + 8 * (q & 7);
-      ga[i] = buf_load16(rsA, kk < k ? (uint32_t)(q >> 3) * rowbytes + (uint32_t)kk * 2 : kOOB);
+      for (int i = 0; i < LA; ++i) {
+        const int q = tid + i * NT;
+        if (CA % NT != 0 && wave * 64 + i * NT >= CA) break;   // wave-uniform
+        const int kk = k0 + 8 * (q & 7);
+        ga[i] = buf_load16(rsA, kk < k ? (uint32_t)(q >> 3) * rowbytes + (uint32_t)kk * 2 : kOOB);
+      }
     }
   };
-  auto swrite = [&](int buf) {
+  auto swrite = [&](int buf, int piece) {
     char* sb = smem + buf * STAGE;
+    if (piece == 0) {
 #pragma unroll
-    for (int i = 0; i < LX; ++i) {
-      const int q = tid + i * NT;
-      if (CX % NT != 0 && wave * 64 + i * NT >= CX) break;   // wave-uniform
-      *reinterpret_cast<int4v*>(sb + kc_offset(q >> 3, q & 7)) = gx[i];
-    }
+      for (int i = 0; i < LX; ++i) {
+        const int q = tid + i * NT;
+        if (CX % NT != 0 && wave * 64 + i * NT >= CX) break;   // wave-uniform
+        *reinterpret_cast<int4v*>(sb + kc_offset(q >> 3, q & 7)) = gx[i];
+      }
+    } else if (piece <= 2) {
 #pragma unroll
-    for (int i = 0; i < LW; ++i) {
-      const int q = tid + i * NT;
-      if (CW % NT != 0 && wave * 64 + i * NT >= CW) break;   // wave-uniform
-      *reinterpret_cast<int4v*>(sb + BM * 128 + kc_offset(q >> 3, q & 7)) = gw[i];
-    }
+      for (int i = piece == 1 ? 0 : LW1; i < (piece == 1 ? LW1 : LW); ++i) {
+        const int q = tid + i * NT;
+        if (CW % NT != 0 && wave * 64 + i * NT >= CW) break;   // wave-uniform
+        *reinterpret_cast<int4v*>(sb + BM * 128 + kc_offset(q >> 3, q & 7)) = gw[i];
+      }
+    } else {
 #pragma unroll
-    for (int i = 0; i < LA; ++i) {
-      const int q = tid + i * NT;
-      if (CA % NT != 0 && wave * 64 + i * NT >= CA) break;   // wave-uniform
-      *reinterpret_cast<int4v*>(sb + (BM + BN) * 128 + kc_offset(q >> 3, q & 7)) = ga[i];
+      for (int i = 0; i < LA; ++i) {
+        const int q = tid + i * NT;
+        if (CA % NT != 0 && wave * 64 + i * NT >= CA) break;   // wave-uniform
+        *reinterpret_cast<int4v*>(sb + (BM + BN) * 128 + kc_offset(q >> 3, q & 7)) = ga[i];
+      }
     }
   };
 
@@ -166,31 +178,53 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
     }
   };
 
-  // Pipeline: at the top of stage kb the registers hold k-block kb+1 (loaded
-  // one stage earlier); they go to the free LDS buffer right after the first
-  // fragment reads of kb, then the loads of kb+2 are issued into them.  The
-  // k loop is peeled so the steady state carries no conditionals.
+  // Pipeline.  At the top of stage kb the staging registers hold k-block
+  // kb+1 (loaded one stage earlier); piece ks of it is stored to the free LDS
+  // buffer at substep ks, and its registers are then reloaded with block kb+2.
+  // With ROT the loop is rotated by one substep: the products of substep 3 of
+  // stage kb-1 are issued after the barrier, while the first fragments of
+  // stage kb are being read (their operands are zeroed for stage 0, adding
+  // exact zeros).  The 256 x 256 tile has no registers to spare for it.  The k
+  // loop is peeled so the steady state carries no conditionals.
+  constexpr bool ROT = BM * BN < 256 * 256;
+  if (ROT) {
+#pragma unroll
+    for (int j = 0; j < FJ; ++j) fw[1][j] = short8{};
+#pragma unroll
+    for (int j = 0; j < FI; ++j) fx[1][j] = short8{};
+#pragma unroll
+    for (int j = 0; j < FT; ++j) fa[1][j] = short8{};
+#pragma unroll
+    for (int j = 0; j < FUW; ++j) fxu[1][j] = short8{};
+  }
   auto stage = [&](int kb, bool write_next, bool load_next) {
     const char* sb = smem + (kb & 1) * STAGE;
     read_frags(sb, 0, 0);
-    if (write_next) swrite((kb + 1) & 1);
-    if (load_next) gload(kb + 2);
+    if (ROT) multiply(1, 3);
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
+      if (write_next) swrite((kb + 1) & 1, ks);
+      if (load_next) gload(kb + 2, ks);
       if (ks < 3) read_frags(sb, ks + 1, (ks + 1) & 1);
-      multiply(ks & 1, ks);
+      if (ks < 3 || !ROT) multiply(ks & 1, ks);
     }
     __syncthreads();
   };
   const int nkb = (k + 63) / 64;
-  gload(0);
-  swrite(0);
+#pragma unroll
+  for (int pc = 0; pc < 4; ++pc) gload(0, pc);
+#pragma unroll
+  for (int pc = 0; pc < 4; ++pc) swrite(0, pc);
   __syncthreads();
-  if (nkb > 1) gload(1);
+  if (nkb > 1) {
+#pragma unroll
+    for (int pc = 0; pc < 4; ++pc) gload(1, pc);
+  }
   int kb = 0;
   for (; kb + 2 < nkb; ++kb) stage(kb, true, true);
   if (kb + 1 < nkb) stage(kb++, true, false);
   stage(kb, false, false);
+  if (ROT) multiply(1, 3);
 
   // ---- epilogue ------------------------------------------------------------
   // LDS reuse: Us [NDUP][BM][RP] fp32 partial U (summed in fixed order below),
