@@ -9,7 +9,8 @@
 //   du        dU = s dY B, reducing over n.  Writes dU2 (token-major, high |
 //             low) for the dX GEMM and dUt2 (its transpose) for dA.
 //   tokred    one launch, two token reductions split over token ranges:
-//             dB^T partials = Ut2 . dY and dA partials = dUt2 . X.
+//             dB^T partials = Ut2 . dY and dA partials = dUt2 . X; the
+//             waves of a workgroup split its tokens.
 //   dx        dX = [dY | dU2] . [W ; A ; A]: one GEMM whose k loop runs over
 //             n and then over the 2 RP wide slab (high and low part of dU
 //             against the same A rows).  W is read through LDS with the
@@ -123,12 +124,19 @@ __global__ __launch_bounds__(512) void lora_bwd_du_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// Token reduction part[sp][t][c] = sum over tokens i of split sp of
-// P[t][i] * Q[i][c], t < RP (the high and low rows of P are summed), for a
-// tile of kRedCols columns.  P ([2RP][mp], token-contiguous) is read straight
-// into matrix-core A operands; Q ([m][cols]) is staged in LDS 64 tokens at a
-// time and read transposed.  One launch serves two such problems (dB^T from
-// Ut2 and dY, dA from dUt2 and X): workgroups [0, nb0) take the first.
+// Token reduction part[sp][t][c] = sum over the tokens i of split sp of
+// P[t][i] * Q[i][c], t < RP (the high rows t and low rows RP + t of P are
+// summed), for a tile of kRedCols = 128 columns.  One launch serves two such
+// problems (dB^T from Ut2 and dY, dA from dUt2 and X): workgroups [0, nb0)
+// take the first.
+//
+// The four waves of a workgroup take interleaved 32-token slices of the
+// split.  Each reads its P fragments straight from the token-contiguous P
+// ([2RP][mp]) into matrix-core A operands and stages its 32 x 128 slice of Q
+// ([m][cols]) in a private LDS region that it reads back transposed, so the
+// token loop has no barriers; the next slice is loaded while the current one
+// multiplies.  At the end the four waves' sums are added in wave order
+// through LDS (bit-identical from run to run).
 struct RedProblem {
   const u16* P;
   const u16* Q;
@@ -136,64 +144,34 @@ struct RedProblem {
   int ncols, span, col_tiles;
 };
 
-template <int NW, int RP>
-__global__ __launch_bounds__(64 * NW) void lora_tokred_kernel(RedProblem p0, RedProblem p1, int nb0, int m, int mp) {
+template <int RP>
+__global__ __launch_bounds__(256) void lora_tokred_kernel(RedProblem p0, RedProblem p1, int nb0, int m, int mp) {
+  constexpr int CB = kRedCols;                // columns per workgroup
+  constexpr int FC = CB / 16;                 // column fragments
+  constexpr int FH = RP / 16, FP = 2 * FH;    // high-part row fragments; low part follows
+  constexpr int CPR = CB / 8;                 // 16-byte chunks per Q row
+  constexpr int QL = 32 * CPR / 64;           // Q loads per lane per slice
+  constexpr int REG = 32 * CB * 2;            // bytes of one staged Q slice
+  constexpr int FCP = 16 / FP > FC ? FC : (16 / FP > 0 ? 16 / FP : 1);   // fragments per reduction pass
+  static_assert(CB == 128 && QL * 64 == 32 * CPR, "slice shape");
+  static_assert(4 * FP * FCP * 64 * 16 <= 4 * 2 * REG, "reduction fits the staging LDS");
+  __shared__ __attribute__((aligned(1024))) char smem[4 * 2 * REG];
+
   const bool first = (int)blockIdx.x < nb0;
   const RedProblem& pr = first ? p0 : p1;
   const int bid = first ? (int)blockIdx.x : (int)blockIdx.x - nb0;
   const u16* __restrict__ P = pr.P;
   const u16* __restrict__ Q = pr.Q;
-  float* __restrict__ part = pr.part;
-  const int ncols = pr.ncols, span = pr.span;
-  constexpr int BNC = kRedCols;
-  constexpr int NT = 64 * NW;
-  constexpr int WC = BNC / NW;
-  constexpr int FC = WC / 16;
-  constexpr int FH = RP / 16;     // high-part row fragments; low part follows
-  constexpr int FP = 2 * FH;
-  constexpr int CPR = BNC / 8;    // 16-byte chunks per Q row
-  constexpr int STAGE = 64 * BNC * 2;
-  constexpr int CH = 64 * CPR;
-  constexpr int LOADS = CH / NT;
-  static_assert(CH % NT == 0 && WC % 16 == 0, "shape split");
-  __shared__ __attribute__((aligned(16))) char smem[2 * STAGE];
-
-  const int c0 = (bid % pr.col_tiles) * BNC;
+  const int ncols = pr.ncols;
+  const int c0 = (bid % pr.col_tiles) * CB;
   const int sp = bid / pr.col_tiles;
-  const int tb = sp * span;
-  const int te = min(mp, tb + span);
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tb = sp * pr.span;
+  const int te = min(mp, tb + pr.span);
+  const int tid = threadIdx.x, lane = tid & 63, wave = uniform(tid >> 6);
   const int g = lane >> 4, c16 = lane & 15;
   const uint32_t qrow = (uint32_t)ncols * 2;
   const __amdgpu_buffer_rsrc_t rsP = make_rsrc(P, (uint64_t)2 * RP * mp * 2);
-
-  int4v qregs[LOADS];
-  short8 pcur[2][FP], pnext[2][FP];
-  auto gload = [&](int tc, short8 (&pf)[2][FP]) {
-    const int rows = max(0, min(64, m - tc));
-    const __amdgpu_buffer_rsrc_t rsQ = make_rsrc(Q + (size_t)tc * ncols, (uint64_t)rows * qrow);
-#pragma unroll
-    for (int i = 0; i < LOADS; ++i) {
-      const int q = tid + i * NT;
-      const int rho = q / CPR, c = q % CPR;
-      const int cc = c0 + 8 * c;
-      qregs[i] = buf_load16(rsQ, cc < ncols ? (uint32_t)rho * qrow + (uint32_t)cc * 2 : kOOB);
-    }
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks)
-#pragma unroll
-      for (int f = 0; f < FP; ++f)
-        pf[ks][f] = __builtin_bit_cast(
-            short8, buf_load16(rsP, ((uint32_t)(16 * f + c16) * (uint32_t)mp + (uint32_t)(tc + 32 * ks + 8 * g)) * 2));
-  };
-  auto swrite = [&](int buf) {
-    char* sb = smem + buf * STAGE;
-#pragma unroll
-    for (int i = 0; i < LOADS; ++i) {
-      const int q = tid + i * NT;
-      *reinterpret_cast<int4v*>(sb + mc16_offset<BNC>(q / CPR, q % CPR)) = qregs[i];
-    }
-  };
+  char* wreg = smem + wave * 2 * REG;
 
   floatx4 acc[FP][FC];
 #pragma unroll
@@ -201,48 +179,78 @@ __global__ __launch_bounds__(64 * NW) void lora_tokred_kernel(RedProblem p0, Red
 #pragma unroll
     for (int fc = 0; fc < FC; ++fc) acc[f][fc] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  if (tb < te) {
-    gload(tb, pcur);
-    swrite(0);
-    __syncthreads();
-    int buf = 0;
-    for (int tc = tb; tc < te; tc += 64) {
-      const bool more = tc + 64 < te;
-      if (more) gload(tc + 64, pnext);
-      const char* Qs = smem + buf * STAGE;
+  // Slice loads: Q chunk u of this lane is row (lane + 64u) / CPR, chunk
+  // (lane + 64u) % CPR; P fragment f is row 16f + c16, tokens ts + 8g .. +7.
+  int4v qv[2][QL];
+  short8 pv[2][FP];
+  auto load = [&](int ts, int b) {
+    const int rows = uniform(max(0, min(32, m - ts)));   // keeps the resource in scalar registers
+    const __amdgpu_buffer_rsrc_t rsQ = make_rsrc(Q + (size_t)ts * ncols, (uint64_t)rows * qrow);
 #pragma unroll
-      for (int ks = 0; ks < 2; ++ks) {
-#pragma unroll
-        for (int fc = 0; fc < FC; ++fc) {
-          const short8 qf = mc16_read_tr<BNC>(Qs, 32 * ks, wave * WC + 16 * fc, lane);
-#pragma unroll
-          for (int f = 0; f < FP; ++f) acc[f][fc] = mfma16x16x32(pcur[ks][f], qf, acc[f][fc]);
-        }
-      }
-      if (more) {
-        swrite(buf ^ 1);
-#pragma unroll
-        for (int ks = 0; ks < 2; ++ks)
-#pragma unroll
-          for (int f = 0; f < FP; ++f) pcur[ks][f] = pnext[ks][f];
-      }
-      __syncthreads();
-      buf ^= 1;
+    for (int u = 0; u < QL; ++u) {
+      const int q = lane + 64 * u;
+      const int cc = c0 + 8 * (q % CPR);
+      qv[b][u] = buf_load16(rsQ, cc < ncols ? (uint32_t)(q / CPR) * qrow + (uint32_t)cc * 2 : kOOB);
     }
-  }
+#pragma unroll
+    for (int f = 0; f < FP; ++f)
+      pv[b][f] = __builtin_bit_cast(
+          short8, buf_load16(rsP, ((uint32_t)(16 * f + c16) * (uint32_t)mp + (uint32_t)(ts + 8 * g)) * 2));
+  };
+  auto step = [&](int b) {
+    char* qs = wreg + b * REG;
+#pragma unroll
+    for (int u = 0; u < QL; ++u) {
+      const int q = lane + 64 * u;
+      *reinterpret_cast<int4v*>(qs + mc16_offset<CB>(q / CPR, q % CPR)) = qv[b][u];
+    }
+#pragma unroll
+    for (int fc = 0; fc < FC; ++fc) {
+      const short8 qf = mc16_read_tr<CB>(qs, 0, 16 * fc, lane);
+#pragma unroll
+      for (int f = 0; f < FP; ++f) acc[f][fc] = mfma16x16x32(pv[b][f], qf, acc[f][fc]);
+    }
+  };
 
-  // lane holds column c16 of fragment fc, rows 4g..4g+3 of fragment f
+  // Slices of this wave: ts0 + 128 j < te, ts0 = tb + 32 wave (te - tb is a
+  // multiple of 64, so slices never straddle te).
+  const int ts0 = tb + 32 * wave;
+  const int ns = ts0 < te ? (te - ts0 + 127) / 128 : 0;
+  if (ns > 0) load(ts0, 0);
+  int j = 0;
+  for (; j + 2 <= ns; j += 2) {
+    load(ts0 + 128 * (j + 1), 1);
+    step(0);
+    if (j + 2 < ns) load(ts0 + 128 * (j + 2), 0);
+    step(1);
+  }
+  if (j < ns) step(0);
+
+  // Cross-wave sum in wave order, FCP column fragments per pass; lane holds
+  // column c16 of fragment fc, rows 4g .. 4g+3 of fragment f.
+  floatx4* red = reinterpret_cast<floatx4*>(smem);   // [4 waves][FP][FCP][64]
+  float* part = pr.part;
 #pragma unroll
-  for (int fc = 0; fc < FC; ++fc) {
-    const int col = c0 + wave * WC + 16 * fc + c16;
-    if (col >= ncols) continue;
+  for (int f0 = 0; f0 < FC; f0 += FCP) {
+    __syncthreads();
 #pragma unroll
-    for (int f = 0; f < FH; ++f)
+    for (int f = 0; f < FP; ++f)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int t = 16 * f + 4 * g + q;
-        part[((size_t)sp * RP + t) * ncols + col] = acc[f][fc][q] + acc[f + FH][fc][q];
+      for (int j = 0; j < FCP; ++j) red[((wave * FP + f) * FCP + j) * 64 + lane] = acc[f][f0 + j];
+    __syncthreads();
+    for (int e = wave; e < FH * FCP; e += 4) {
+      const int fh = e / FCP, j = e - fh * FCP;
+      floatx4 v = red[((0 * FP + fh) * FCP + j) * 64 + lane];
+#pragma unroll
+      for (int w = 1; w < 4; ++w) v += red[((w * FP + fh) * FCP + j) * 64 + lane];
+#pragma unroll
+      for (int w = 0; w < 4; ++w) v += red[((w * FP + FH + fh) * FCP + j) * 64 + lane];
+      const int col = c0 + 16 * (f0 + j) + c16;
+      if (col < ncols) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) part[((size_t)sp * RP + 16 * fh + 4 * g + q) * ncols + col] = v[q];
       }
+    }
   }
 }
 
@@ -522,7 +530,7 @@ static hipError_t launch_bwd_rp(const BwdArgs& a, const BwdLayout& L, hipStream_
     const RedProblem pap{dUt2, a.X, pa, k, (int)L.plan_a.span, L.plan_a.col_tiles};
     const int nb0 = L.plan_b.col_tiles * L.plan_b.splits;
     const int nb1 = L.plan_a.col_tiles * L.plan_a.splits;
-    hipLaunchKernelGGL((lora_tokred_kernel<4, RP>), dim3(nb0 + nb1), dim3(256), 0, st, pbp, pap, nb0, m, mp);
+    hipLaunchKernelGGL((lora_tokred_kernel<RP>), dim3(nb0 + nb1), dim3(256), 0, st, pbp, pap, nb0, m, mp);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
 
