@@ -267,20 +267,32 @@ struct FinalizeArgs {
   float s;
 };
 
+// Sum of `count` partials spaced `step` floats apart, in index order; the
+// loads of each group of eight are all issued before the first add.
+__device__ __forceinline__ float sum_partials(const float* p, size_t step, int count) {
+  float v = 0.f;
+  for (int p0 = 0; p0 < count; p0 += 8) {
+    float x[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) x[u] = p0 + u < count ? p[(size_t)(p0 + u) * step] : 0.f;
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (p0 + u < count) v += x[u];
+  }
+  return v;
+}
+
 __device__ __forceinline__ void finalize_partials(const FinalizeArgs& f, int first, int stride) {
   const int nb = f.n * f.r, na = f.r * f.k;
   for (int e = first; e < nb + na; e += stride) {
     if (e < nb) {  // e = t * n + j: partial reads along j are contiguous
       const int t = e / f.n, j = e - t * f.n;
-      float v = 0.f;
-      for (int p = 0; p < f.sb; ++p) v += f.pb[((size_t)p * f.rp + t) * f.n + j];
+      const float v = sum_partials(f.pb + (size_t)t * f.n + j, (size_t)f.rp * f.n, f.sb);
       f.dB[(size_t)j * f.r + t] = f.s * v;
     } else {
       const int g = e - nb;
       const int t = g / f.k, l = g - t * f.k;
-      float v = 0.f;
-      for (int p = 0; p < f.sa; ++p) v += f.pa[((size_t)p * f.rp + t) * f.k + l];
-      f.dA[g] = v;
+      f.dA[g] = sum_partials(f.pa + (size_t)t * f.k + l, (size_t)f.rp * f.k, f.sa);
     }
   }
 }

@@ -228,9 +228,21 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
 
   // ---- epilogue ------------------------------------------------------------
   // LDS reuse: Us [NDUP][BM][RP] fp32 partial U (summed in fixed order below),
-  // then Bs [BN][RP] bf16 (B rows of this tile, zero beyond r and n).
+  // then Bs [BN][RP] bf16 (B rows of this tile, zero beyond r and n).  Rows
+  // n0 .. n0+jn-1 of B are contiguous, so they are fetched as 16-byte chunks
+  // of 8 elements, all issued before the first wait, and scattered into Bs.
   float* Us = reinterpret_cast<float*>(smem);
   u16* Bs = reinterpret_cast<u16*>(smem + NDUP * BM * RP * 4);
+  constexpr int BCH = (BN * RP / 8 + NT - 1) / NT;   // chunks per thread (r <= RP)
+  const int jn = min(BN, n - n0);
+  const int nch = jn * r / 8;                       // exact: n and n0 are multiples of 8
+  const __amdgpu_buffer_rsrc_t rsB = make_rsrc(B + (size_t)n0 * r, (uint64_t)nch * 16);
+  int4v bv[BCH];
+#pragma unroll
+  for (int i = 0; i < BCH; ++i) {
+    const int q = tid + i * NT;
+    bv[i] = buf_load16(rsB, q < nch ? (uint32_t)q * 16 : kOOB);
+  }
 #pragma unroll
   for (int fu = 0; fu < FUW; ++fu) {
     const int il = urow[fu];
@@ -242,11 +254,26 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
         Us[(udup * BM + il) * RP + t] = uacc[ft][fu][q];
       }
   }
-  for (int e = tid; e < BN * RP; e += NT) {
-    const int j = e / RP, t = e - j * RP;
-    Bs[e] = (n0 + j < n && t < r) ? B[(size_t)(n0 + j) * r + t] : (u16)0;
-  }
+  for (int e = tid; e < BN * RP / 8; e += NT) reinterpret_cast<int4v*>(Bs)[e] = int4v{0, 0, 0, 0};
   __syncthreads();
+  {
+    // element idx of the chunks is B row idx / r, column idx % r; the quotient
+    // comes from a float product that stays at least 0.5/r away from an integer
+    const float rinv = 1.0f / (float)r;
+#pragma unroll
+    for (int i = 0; i < BCH; ++i) {
+      const int q = tid + i * NT;
+      if (q < nch) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int idx = 8 * q + e;
+          const int j = (int)(((float)idx + 0.5f) * rinv);
+          const int t = idx - j * r;
+          Bs[j * RP + t] = (u16)((uint32_t)bv[i][e >> 1] >> (16 * (e & 1)));
+        }
+      }
+    }
+  }
   if (NDUP > 1) {  // fold the partial U sums into copy 0 (fixed order)
     for (int e = tid; e < BM * RP; e += NT) {
       float v = Us[e];
@@ -254,8 +281,8 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
       for (int d = 1; d < NDUP; ++d) v += Us[d * BM * RP + e];
       Us[e] = v;
     }
-    __syncthreads();
   }
+  __syncthreads();
   if (tn == 0) {   // U output: one tile column writes it
     for (int e = tid; e < BM * RP; e += NT) {
       const int il = e / RP, t = e - il * RP;
