@@ -2,12 +2,12 @@
 // Section 3, for the trainable A and B; W0 is frozen so no dW is formed):
 //   dU = s dY B,   dX = dY W + dU A,   dB = s dY^T U,   dA = dU^T X.
 //
-// Kernels, in stream order (four launches; each launch costs a few
+// Kernels, in stream order (three launches; each launch costs a few
 // microseconds on its own, so small steps share launches):
-//   prep      Bt = B^T (rank padded to RP with zeros); Ut2 = U^T split into a
-//             bf16 high part and a bf16 low part (tokens padded to mp).
 //   du        dU = s dY B, reducing over n.  Writes dU2 (token-major, high |
-//             low) for the dX GEMM and dUt2 (its transpose) for dA.
+//             low) for the dX GEMM and dUt2 (its transpose) for dA, and Ut2
+//             = U^T split into a bf16 high part and a bf16 low part (tokens
+//             padded to mp) for dB.
 //   tokred    one launch, two token reductions split over token ranges:
 //             dB^T partials = Ut2 . dY and dA partials = dUt2 . X; the
 //             waves of a workgroup split its tokens.
@@ -25,83 +25,132 @@
 namespace lora {
 
 // ---------------------------------------------------------------------------
-// Index math is 32-bit: validation bounds every index used here below 2^30.
-__global__ __launch_bounds__(256) void lora_bwd_prep_kernel(
-    const u16* __restrict__ B, const float* __restrict__ U, u16* __restrict__ Bt,
-    u16* __restrict__ Ut2, int m, int n, int r, int rp, int mp) {
-  const int nbt = rp * n;
-  const int nut = 2 * rp * mp;
-  const int stride = gridDim.x * blockDim.x;
-  for (int e = blockIdx.x * blockDim.x + threadIdx.x; e < nbt + nut; e += stride) {
-    if (e < nbt) {
-      const int t = e / n;
-      const int j = e - t * n;
-      Bt[e] = (t < r) ? B[(size_t)j * r + t] : (u16)0;
-    } else {
-      const int f = e - nbt;
-      const int tt = f / mp;
-      const int i = f - tt * mp;
-      const int t = tt % rp;
-      const float v = (i < m && t < r) ? U[(size_t)i * r + t] : 0.f;
-      const u16 h = f32_to_bf16(v);
-      Ut2[f] = (tt >= rp) ? f32_to_bf16(v - bf16_to_f32(h)) : h;
-    }
-  }
+// 16x16x32 A operand (16 columns x 32 k) from a small row-major LDS tile
+// whose rows are k (no swizzle, `pitch` bytes per row): lane (g = l/16,
+// c = l%16) receives column col0 + c, k rows 8g .. 8g+7.
+__device__ __forceinline__ short8 tr16_read(const char* tile, int pitch, int col0, int lane) {
+  const int g = lane >> 4, j = lane & 15;
+  const int e = j >> 2, q = j & 3;
+  const char* p0 = tile + (8 * g + e) * pitch + (col0 + 4 * q) * 2;
+  return join4(__builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4v*)p0),
+               __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4v*)(p0 + 4 * pitch)));
 }
 
 // ---------------------------------------------------------------------------
-// dU = s dY B for 16 tokens per workgroup, reducing over all of n.  The 8 waves
-// take interleaved 32-wide chunks of n (four chunks' loads in flight per wave);
-// their sums are added in wave order through LDS, so the result is
-// bit-identical from run to run.  (A split of n over workgroups would need a
-// cross-workgroup reduction, whose device-scope fences write back the
-// per-XCD L2s -- far dearer than the work.)  Writes dU2 (token-major,
-// high | low parts) and dUt2 (its transpose).
+// dU = s dY B for 16 tokens per workgroup, reducing over all of n, plus the
+// U^T high/low split of the same tokens.  The 8 waves take interleaved
+// 32-wide chunks of n, UNR chunks per batch with all of a batch's loads
+// issued together.  A chunk's B rows (32 x r, contiguous in B) are staged in a
+// wave-private LDS slot as [32][RP] (columns t >= r stay zero) and read back
+// transposed into matrix-core A operands; dY rows go straight into B
+// operands.  The waves' sums are added in wave order through LDS, so the
+// result is bit-identical from run to run.  (A split of n over workgroups
+// would need a cross-workgroup reduction, whose device-scope fences write
+// back the per-XCD L2s -- far dearer than the work.)  Writes dU2 (token-major,
+// high | low parts), dUt2 (its transpose) and Ut2 (U^T, high rows then low
+// rows).  Index math is 32-bit: validation bounds every index below 2^30.
 template <int RP>
 __global__ __launch_bounds__(512) void lora_bwd_du_kernel(
-    const u16* __restrict__ dY, const u16* __restrict__ Bt, u16* __restrict__ dU2,
-    u16* __restrict__ dUt2, int m, int n, int mp, float s) {
+    const u16* __restrict__ dY, const u16* __restrict__ B, const float* __restrict__ U,
+    u16* __restrict__ dU2, u16* __restrict__ dUt2, u16* __restrict__ Ut2,
+    int m, int n, int r, int mp, float s) {
   constexpr int FT = RP / 16;
   constexpr int NWV = 8;
-  __shared__ floatx4 red[NWV][FT][64];
+  constexpr int UNR = RP <= 16 ? 8 : (RP <= 32 ? 4 : 2);
+  constexpr int SLOT = 32 * RP * 2;                 // bytes of one staged chunk of B
+  constexpr int BL = RP / 16;                       // 16-byte B loads per lane per chunk (4r <= 4 RP)
+  static_assert(NWV * FT * 64 * 16 <= NWV * UNR * SLOT, "reduction fits the staging LDS");
+  __shared__ __attribute__((aligned(1024))) char sm[NWV * UNR * SLOT];
   const int i0 = blockIdx.x * 16;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = uniform(tid >> 6);
   const int g = lane >> 4, c16 = lane & 15;
   const uint32_t rowbytes = (uint32_t)n * 2;
-  const int rows = max(0, min(16, m - i0));
+  const int rows = uniform(max(0, min(16, m - i0)));
   const __amdgpu_buffer_rsrc_t rsY = make_rsrc(dY + (size_t)i0 * n, (uint64_t)rows * rowbytes);
-  const __amdgpu_buffer_rsrc_t rsB = make_rsrc(Bt, (uint64_t)RP * rowbytes);
+  const __amdgpu_buffer_rsrc_t rsB = make_rsrc(B, (uint64_t)n * r * 2);
+  char* slots = sm + wave * UNR * SLOT;
+
+  for (int e = lane; e < UNR * SLOT / 16; e += 64) reinterpret_cast<int4v*>(slots)[e] = int4v{0, 0, 0, 0};
 
   floatx4 acc[FT];
 #pragma unroll
   for (int ft = 0; ft < FT; ++ft) acc[ft] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  constexpr int UNR = 4;
-  for (int j0 = 32 * wave; j0 < n; j0 += 32 * NWV * UNR) {
-    short8 yf[UNR], bf[UNR][FT];
+  const int nbch = 4 * r;                           // 16-byte chunks in 32 rows of B
+  const bool fast = (r & 7) == 0;                   // a chunk then lies inside one row of B
+  const float rinv = 1.0f / (float)r;
+  // Batch b of this wave covers chunks j = 32 wave + 32 NWV (UNR b + u); the
+  // loads of batch b+1 are in flight while batch b multiplies.
+  short8 yf[2][UNR];
+  int4v bq[2][UNR][BL];
+  auto load = [&](int bt, int p) {
 #pragma unroll
     for (int u = 0; u < UNR; ++u) {
-      const int j = j0 + 32 * NWV * u + 8 * g;
-      const bool ok = j < n;
-      yf[u] = __builtin_bit_cast(short8, buf_load16(rsY, ok ? (uint32_t)c16 * rowbytes + (uint32_t)j * 2 : kOOB));
+      const int j = 32 * wave + 32 * NWV * (UNR * bt + u);
+      const int jy = j + 8 * g;
+      yf[p][u] = __builtin_bit_cast(short8, buf_load16(rsY, jy < n ? (uint32_t)c16 * rowbytes + (uint32_t)jy * 2 : kOOB));
 #pragma unroll
-      for (int ft = 0; ft < FT; ++ft)
-        bf[u][ft] = __builtin_bit_cast(
-            short8, buf_load16(rsB, ok ? (uint32_t)(16 * ft + c16) * rowbytes + (uint32_t)j * 2 : kOOB));
+      for (int v = 0; v < BL; ++v) {
+        const int c = lane + 64 * v;
+        bq[p][u][v] = buf_load16(rsB, (j < n && c < nbch) ? (uint32_t)j * r * 2 + (uint32_t)c * 16 : kOOB);
+      }
     }
+  };
+  auto process = [&](int p) {
 #pragma unroll
-    for (int u = 0; u < UNR; ++u)
+    for (int u = 0; u < UNR; ++u) {
+      char* slot = slots + u * SLOT;
 #pragma unroll
-      for (int ft = 0; ft < FT; ++ft) acc[ft] = mfma16x16x32(bf[u][ft], yf[u], acc[ft]);
+      for (int v = 0; v < BL; ++v) {
+        const int c = lane + 64 * v;
+        if (c < nbch) {
+          if (fast) {
+            const int e0 = 8 * c, jj = e0 / r;
+            *reinterpret_cast<int4v*>(slot + (jj * RP + e0 - jj * r) * 2) = bq[p][u][v];
+          } else {
+#pragma unroll
+            for (int x = 0; x < 8; ++x) {   // quotient from a float product at least 0.5/r from an integer
+              const int e = 8 * c + x;
+              const int jj = (int)(((float)e + 0.5f) * rinv);
+              *reinterpret_cast<u16*>(slot + (jj * RP + e - jj * r) * 2) =
+                  (u16)((uint32_t)bq[p][u][v][x >> 1] >> (16 * (x & 1)));
+            }
+          }
+        }
+      }
+#pragma unroll
+      for (int ft = 0; ft < FT; ++ft) acc[ft] = mfma16x16x32(tr16_read(slot, RP * 2, 16 * ft, lane), yf[p][u], acc[ft]);
+    }
+  };
+  const int nbt = uniform(32 * wave < n ? (n - 32 * wave + 32 * NWV * UNR - 1) / (32 * NWV * UNR) : 0);
+  if (nbt > 0) load(0, 0);
+  for (int bt = 0; bt < nbt; bt += 2) {
+    if (bt + 1 < nbt) load(bt + 1, 1);
+    process(0);
+    if (bt + 1 >= nbt) break;
+    if (bt + 2 < nbt) load(bt + 2, 0);
+    process(1);
   }
+
+  // U^T high/low split of this workgroup's tokens (tokens >= m are zero).
+  for (int e = tid; e < 2 * RP * 16; e += 64 * NWV) {
+    const int tt = e >> 4, i = i0 + (e & 15);
+    const int t = tt < RP ? tt : tt - RP;
+    const float v = (i < m && t < r) ? U[(size_t)i * r + t] : 0.f;
+    const u16 h = f32_to_bf16(v);
+    Ut2[(size_t)tt * mp + i] = tt < RP ? h : f32_to_bf16(v - bf16_to_f32(h));
+  }
+
+  __syncthreads();
+  floatx4* red = reinterpret_cast<floatx4*>(sm);   // [NWV][FT][64]
 #pragma unroll
-  for (int ft = 0; ft < FT; ++ft) red[wave][ft][lane] = acc[ft];
+  for (int ft = 0; ft < FT; ++ft) red[(wave * FT + ft) * 64 + lane] = acc[ft];
   __syncthreads();
   if (wave >= FT) return;
   const int ft = wave;  // one wave per 16-row fragment of dU^T
-  floatx4 v = red[0][ft][lane];
+  floatx4 v = red[ft * 64 + lane];
 #pragma unroll
-  for (int w = 1; w < NWV; ++w) v += red[w][ft][lane];
+  for (int w = 1; w < NWV; ++w) v += red[(w * FT + ft) * 64 + lane];
   const int i = i0 + c16;  // < mp: the grid covers exactly mp tokens
   u16 hi[4], lo[4];
 #pragma unroll
@@ -520,7 +569,6 @@ static hipError_t launch_dx_cfg(const BwdArgs& a, const BwdLayout& L, const Fina
 template <int RP>
 static hipError_t launch_bwd_rp(const BwdArgs& a, const BwdLayout& L, hipStream_t st) {
   const int m = (int)a.m, n = (int)a.n, k = (int)a.k, r = (int)a.r, mp = (int)L.mp;
-  u16* Bt = reinterpret_cast<u16*>(a.ws + L.bt);
   u16* Ut2 = reinterpret_cast<u16*>(a.ws + L.ut2);
   u16* dU2 = reinterpret_cast<u16*>(a.ws + L.du2);
   u16* dUt2 = reinterpret_cast<u16*>(a.ws + L.dut2);
@@ -528,13 +576,8 @@ static hipError_t launch_bwd_rp(const BwdArgs& a, const BwdLayout& L, hipStream_
   float* pa = reinterpret_cast<float*>(a.ws + L.pa);
   hipError_t e;
 
-  {
-    const int64_t total = (int64_t)RP * n + (int64_t)2 * RP * mp;
-    const int blocks = (int)std::min<int64_t>((total + 255) / 256, 4096);
-    hipLaunchKernelGGL(lora_bwd_prep_kernel, dim3(blocks), dim3(256), 0, st, a.B, a.U, Bt, Ut2, m, n, r, RP, mp);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-  }
-  hipLaunchKernelGGL((lora_bwd_du_kernel<RP>), dim3(mp / 16), dim3(512), 0, st, a.dY, Bt, dU2, dUt2, m, n, mp, a.s);
+  hipLaunchKernelGGL((lora_bwd_du_kernel<RP>), dim3(mp / 16), dim3(512), 0, st, a.dY, a.B, a.U, dU2, dUt2, Ut2, m, n, r,
+                     mp, a.s);
   if ((e = hipGetLastError()) != hipSuccess) return e;
 
   {

@@ -62,7 +62,6 @@ inline RedPlan plan_reduction(int64_t m, int64_t cols, int rp) {
 
 // Backward workspace, byte offsets of each region (256-byte aligned).
 struct BwdLayout {
-  size_t bt;     // Bt   [RP][n]      bf16: B transposed, zero for t >= r
   size_t ut2;    // Ut2  [2RP][mp]    bf16: U^T as high part (rows 0..RP) and low part
   size_t du2;    // dU2  [mp][2RP]    bf16: dU as high part (cols 0..RP) and low part
   size_t dut2;   // dUt2 [2RP][mp]    bf16: dU^T, high and low parts
@@ -84,7 +83,6 @@ inline BwdLayout bwd_layout(int64_t m, int64_t n, int64_t k, int64_t r) {
   L.plan_a = plan_reduction(m, k, L.rp);
   const size_t rp = (size_t)L.rp, mp = (size_t)L.mp;
   size_t off = 0;
-  L.bt = off;   off = align256(off + rp * (size_t)n * 2);
   L.ut2 = off;  off = align256(off + 2 * rp * mp * 2);
   L.du2 = off;  off = align256(off + mp * 2 * rp * 2);
   L.dut2 = off; off = align256(off + 2 * rp * mp * 2);
