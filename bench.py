@@ -125,6 +125,86 @@ def cpu_baseline(shape, seconds: float):
                       f"r={shape.r}) in fp64 numpy/OpenBLAS, {el:.1f} s total, {per:.3f} s each"}
 
 
+def cpu_baseline_merge(shape, seconds: float):
+    """Time the fp64 oracle's merge (as it stands) on this host for `shape`."""
+    import oracle
+    from lora_synth import gen_inputs
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    t = gen_inputs(shape)
+    runs, t0 = 0, time.perf_counter()
+    while True:
+        oracle.lora_merge_bf16(t["W"], t["A"], t["B"], shape.alpha, 1)
+        runs += 1
+        el = time.perf_counter() - t0
+        if el >= seconds or runs >= 50:
+            break
+    per = el / runs
+    nbytes = 2 * 2 * shape.n * shape.k + 2 * shape.r * (shape.n + shape.k)
+    return {"value": nbytes / per / 1e9, "unit": "GB/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{runs} merges of {shape.name} (n={shape.n} k={shape.k} r={shape.r}) in fp64 "
+                      f"numpy/OpenBLAS with exact bf16 rounding, {el:.1f} s total, {per:.3f} s each"}
+
+
+def bench_merge(args, shapes, stream):
+    """Merge throughput: W_out = W + s B A for every projection of the workload,
+    out of place, over rotating copies of W past the Infinity Cache.  Bytes are
+    the algorithmic ones: W read, W_out written, A and B read."""
+    import torch
+    import paper_2403_11366_amd as lora
+    from paper_2403_11366_amd.device_io import bits_to_device
+    from lora_synth import gen_inputs
+    dev = "cuda"
+    per_set = sum(2 * 2 * s.n * s.k for s in shapes)
+    nsets = max(2, math.ceil(2 * MALL_BYTES / per_set))
+    proj = []
+    for s in shapes:
+        t = gen_inputs(s)
+        W = bits_to_device(t["W"], dev)
+        A, B = bits_to_device(t["A"], dev), bits_to_device(t["B"], dev)
+        Ws = [W] + [W.clone() for _ in range(nsets - 1)]
+        Os = [torch.empty_like(W) for _ in range(nsets)]
+        proj.append((s, Ws, Os, A, B))
+    torch.cuda.synchronize()
+
+    def run(i):
+        for s, Ws, Os, A, B in proj:
+            lora.lora_linear_merge(Ws[i % nsets], A, B, Os[i % nsets], s.alpha, 1, stream=stream)
+
+    for i in range(args.warmup):
+        run(i)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record(stream)
+    for i in range(args.steps):
+        run(i)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    us = ev0.elapsed_time(ev1) / args.steps * 1e3
+    nbytes = sum(2 * 2 * s.n * s.k + 2 * s.r * (s.n + s.k) for s in shapes)
+    gbs = nbytes / (us * 1e-6) / 1e9
+    log(f"[bench] merge {us:.1f} us per step, {gbs:.0f} GB/s")
+    cpu = None if args.no_cpu_baseline else cpu_baseline_merge(shapes[0], args.cpu_seconds)
+    rec = {
+        "metric": "LoRA merge W + s B A GB/s (HBM), Llama-2 projection shapes, 1 GPU",
+        "value": round(gbs, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(us / 1e3, 4), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": args.config, "op": "merge",
+                   "projections": [{"name": s.name, "n": s.n, "k": s.k, "r": s.r, "alpha": s.alpha}
+                                   for s in shapes],
+                   "input_sets": nsets, "bytes_per_step": nbytes},
+        "roofline": {"bound": "hbm", "kernel": "lora_merge_kernel", "achieved": round(gbs, 1),
+                     "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
+                     "traffic": None, "bytes_per_launch": nbytes // len(shapes) if len(shapes) == 1 else None,
+                     "avg_launch_us": round(us / len(shapes), 2)},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(rec), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -136,6 +216,9 @@ def main():
     ap.add_argument("--only", choices=["fwd", "copy"], default=None,
                     help="run only forward launches, or only a plain device copy (for counter runs)")
     ap.add_argument("--copy-mib", type=int, default=512)
+    ap.add_argument("--op", choices=["train", "merge"], default="train",
+                    help="train: forward + backward (the default measurement); merge: the "
+                         "merge W + s B A of each projection's adapter into its weight")
     ap.add_argument("--summarize-traffic", metavar="DIR", default=None,
                     help="write the HBM-traffic record from counter runs under DIR and exit")
     args = ap.parse_args()
@@ -173,6 +256,9 @@ def main():
     shapes = CONFIGS[args.config]
     dev = "cuda"
     stream = torch.cuda.current_stream()
+    if args.op == "merge":
+        bench_merge(args, shapes, stream)
+        return
 
     # ---- inputs resident in HBM, rotated over enough copies to exceed the MALL
     per_set = sum(2 * (s.m * s.k + s.n * s.k + s.r * s.k + s.n * s.r + s.m * s.n) for s in shapes)

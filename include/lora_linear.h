@@ -51,7 +51,7 @@ typedef uint16_t lora_bf16;
 typedef enum {
   LORA_OK = 0,
   LORA_ERR_NULL = 1,        /* a required pointer is NULL */
-  LORA_ERR_SHAPE = 2,       /* m < 1, n or k < 8 or not a multiple of 8, r < 1, or size overflow */
+  LORA_ERR_SHAPE = 2,       /* m < 1, n or k < 8 or not a multiple of 8, r < 1, merge sign not +-1 */
   LORA_ERR_ALIGN = 3,       /* a matrix pointer is not 16-byte aligned */
   LORA_ERR_UNSUPPORTED = 4, /* r > 64, or a dimension beyond the supported range */
   LORA_ERR_WORKSPACE = 5,   /* workspace missing or smaller than lora_linear_bwd_workspace_size() */
@@ -107,6 +107,28 @@ lora_status lora_linear_bwd(const lora_bf16* dY, const lora_bf16* X, const lora_
                             void* workspace, size_t workspace_bytes,
                             int64_t m, int64_t n, int64_t k, int64_t r, float alpha,
                             void* stream);
+
+/*
+ * Merge (sign = +1) or unmerge (sign = -1) of the adapter into the frozen
+ * weight, following the second form of Eq. 1 (Section 3): W0 x + B A x =
+ * (W0 + B A) x.  With the scale s = alpha / r:
+ *
+ *     W_out = W + sign * s * B A            [n, k]
+ *
+ *   W      [n, k]  frozen weight (bf16), read only
+ *   A      [r, k]  LoRA down projection (bf16), read only
+ *   B      [n, r]  LoRA up projection (bf16), read only
+ *   W_out  [n, k]  output (bf16), written; it may be W itself (in-place merge),
+ *                  but any other overlap with an input is LORA_ERR_ALIAS
+ *   sign   +1 or -1 (anything else is LORA_ERR_SHAPE)
+ *
+ * The rank-r product runs on the matrix cores with fp32 accumulation; the sum
+ * with W is formed in fp32 and rounded once to bf16 (nearest-even).  Because
+ * of that rounding, unmerging a merged weight returns W only up to bf16
+ * rounding.  The shape rules are those above with no m.
+ */
+lora_status lora_linear_merge(const lora_bf16* W, const lora_bf16* A, const lora_bf16* B, lora_bf16* W_out,
+                              int64_t n, int64_t k, int64_t r, float alpha, int sign, void* stream);
 
 /* Static, human-readable name of a status code. */
 const char* lora_status_string(lora_status s);

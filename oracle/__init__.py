@@ -23,6 +23,10 @@ on the exact decoded bfloat16 inputs:
       dB = s dY^T U                    [n, r]
       dA = dU^T X                      [r, k]
 
+The merge of the adapter into the frozen weight (Eq. 1's second form,
+W0 x + B A x = (W0 + B A) x) is W + sign s B A, rounded once to bfloat16
+(nearest-even) for the stored result.
+
 Each step is one numpy float64 matrix product; there is no blocking, fusion or
 reordering beyond the definition.  Pins that tie this to the paper and to the
 mathematics (merge identity, B = 0 and A = 0 invariants, finite differences,
@@ -30,7 +34,9 @@ a hand-worked example, brute-force loops, closed forms) live in
 tests/test_oracle_pins.py.
 """
 from .lora_oracle import (bf16_bits_to_f64, lora_scale, lora_rank_activation, lora_forward,
-                          lora_backward, lora_forward_rows, lora_backward_rows, f64_to_bf16_bits)
+                          lora_backward, lora_forward_rows, lora_backward_rows, f64_to_bf16_bits,
+                          f64_to_bf16_rne, lora_merged_weight, lora_merge_bf16)
 
 __all__ = ["bf16_bits_to_f64", "lora_scale", "lora_rank_activation", "lora_forward",
-           "lora_backward", "lora_forward_rows", "lora_backward_rows", "f64_to_bf16_bits"]
+           "lora_backward", "lora_forward_rows", "lora_backward_rows", "f64_to_bf16_bits",
+           "f64_to_bf16_rne", "lora_merged_weight", "lora_merge_bf16"]

@@ -27,6 +27,25 @@ def f64_to_bf16_bits(x: np.ndarray) -> np.ndarray:
     return ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
 
 
+def f64_to_bf16_rne(x: np.ndarray) -> np.ndarray:
+    """Round float64 values to bfloat16 bit patterns, nearest with ties to even,
+    in one rounding step (no intermediate float32).
+
+    A finite x = m 2^e with 0.5 <= |m| < 1 has bfloat16 neighbours spaced
+    2^(e-8) apart (8 significant bits); below the smallest normal (2^-126) the
+    spacing stays 2^-133.  x / spacing is an exact power-of-two scaling, so
+    rounding it to an integer with ties to even (numpy.rint) and scaling back
+    gives the bfloat16 value exactly; that value is exact in float32, whose top
+    16 bits are the pattern.  NaN and infinity are not handled (the data here
+    has none)."""
+    x = np.asarray(x, dtype=np.float64)
+    _, e = np.frexp(x)
+    e = np.maximum(e, -125)
+    q = np.ldexp(1.0, e - 8)
+    y = np.rint(x / q) * q
+    return (y.astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+
+
 def lora_scale(alpha: float, r: int) -> float:
     """LoRA scale s = alpha / r.  The paper's Eq. 1 shows no scale; its config
     (Listing 3) carries LORA_ALPHA and LORA_R, whose defaults (16, 16) give s = 1,
@@ -72,6 +91,20 @@ def lora_backward(dY, X, W, A, B, alpha: float
     dB = s * (dY.T @ U)
     dA = dU.T @ X
     return dU, dX, dA, dB
+
+
+def lora_merged_weight(W, A, B, alpha: float, sign: int = 1) -> np.ndarray:
+    """The merged weight of Eq. 1's second form, W0 x + B A x = (W0 + B A) x,
+    with the LoRA scale: W + sign s B A (sign = -1 unmerges).  [n, k], float64."""
+    W, A, B = _f64(W), _f64(A), _f64(B)
+    s = lora_scale(alpha, A.shape[0])
+    return W + float(sign) * s * (B @ A)
+
+
+def lora_merge_bf16(W, A, B, alpha: float, sign: int = 1) -> np.ndarray:
+    """lora_merged_weight rounded once to bfloat16 (nearest-even): the stored
+    result of a merge or unmerge.  Returns uint16 bit patterns [n, k]."""
+    return f64_to_bf16_rne(lora_merged_weight(W, A, B, alpha, sign))
 
 
 def lora_forward_rows(X, W, A, B, alpha: float, rows: Sequence[int]

@@ -16,7 +16,7 @@ from typing import Optional
 
 __all__ = [
     "LoraError", "lib_path", "load_library", "lora_linear_fwd", "lora_linear_bwd",
-    "lora_linear_bwd_workspace_size", "lora_status_string", "STATUS",
+    "lora_linear_bwd_workspace_size", "lora_linear_merge", "lora_status_string", "STATUS",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -53,6 +53,8 @@ def load_library() -> ctypes.CDLL:
     lib.lora_linear_bwd_workspace_size.restype = sz
     lib.lora_linear_bwd.argtypes = [p, p, p, p, p, p, p, p, p, p, sz, i64, i64, i64, i64, f32, p]
     lib.lora_linear_bwd.restype = ctypes.c_int
+    lib.lora_linear_merge.argtypes = [p, p, p, p, i64, i64, i64, f32, ctypes.c_int, p]
+    lib.lora_linear_merge.restype = ctypes.c_int
     lib.lora_status_string.argtypes = [ctypes.c_int]
     lib.lora_status_string.restype = ctypes.c_char_p
     _lib = lib
@@ -133,3 +135,19 @@ def lora_linear_bwd(dY, X, W, A, B, U, dX, dA, dB, workspace, alpha: float, stre
                                         m, n, k, r, float(alpha), _stream_handle(stream))
     if st != 0:
         raise LoraError(st, "lora_linear_bwd")
+
+
+def lora_linear_merge(W, A, B, W_out, alpha: float, sign: int = 1, stream=None) -> None:
+    """W_out = W + sign (alpha/r) B A, rounded to bf16 (sign +1 merges, -1 unmerges).
+
+    W, W_out [n,k], A [r,k], B [n,r]: torch.bfloat16.  W_out may be W itself."""
+    import torch
+    n, k = W.shape
+    r = A.shape[0]
+    for t, name, dt, shp in ((W, "W", torch.bfloat16, (n, k)), (A, "A", torch.bfloat16, (r, k)),
+                             (B, "B", torch.bfloat16, (n, r)), (W_out, "W_out", torch.bfloat16, (n, k))):
+        _check(t, name, dt, shp)
+    st = load_library().lora_linear_merge(_ptr(W), _ptr(A), _ptr(B), _ptr(W_out), n, k, r, float(alpha),
+                                          int(sign), _stream_handle(stream))
+    if st != 0:
+        raise LoraError(st, "lora_linear_merge")

@@ -43,7 +43,7 @@ const char* lora_status_string(lora_status s) {
   switch (s) {
     case LORA_OK: return "ok";
     case LORA_ERR_NULL: return "null pointer argument";
-    case LORA_ERR_SHAPE: return "invalid shape (need m >= 1, n and k >= 8 and multiples of 8, r >= 1)";
+    case LORA_ERR_SHAPE: return "invalid shape (need m >= 1, n and k >= 8 and multiples of 8, r >= 1; merge sign +1 or -1)";
     case LORA_ERR_ALIGN: return "matrix pointer not 16-byte aligned";
     case LORA_ERR_UNSUPPORTED: return "unsupported size (r > 64, a dimension > 2^22, or a matrix > 2^30 elements)";
     case LORA_ERR_WORKSPACE: return "workspace missing or too small";
@@ -109,6 +109,22 @@ lora_status lora_linear_bwd(const lora_bf16* dY, const lora_bf16* X, const lora_
   lora::BwdArgs a{dY, X, W, A, B, U, dX, dA, dB, static_cast<char*>(workspace),
                   m, n, k, r, (float)alpha / (float)r};
   hipError_t e = lora::launch_bwd(a, reinterpret_cast<hipStream_t>(stream));
+  return e == hipSuccess ? LORA_OK : LORA_ERR_HIP;
+}
+
+lora_status lora_linear_merge(const lora_bf16* W, const lora_bf16* A, const lora_bf16* B, lora_bf16* W_out,
+                              int64_t n, int64_t k, int64_t r, float alpha, int sign, void* stream) {
+  if (!W || !A || !B || !W_out) return LORA_ERR_NULL;
+  lora_status st = check_shape(1, n, k, r);
+  if (st != LORA_OK) return st;
+  if (sign != 1 && sign != -1) return LORA_ERR_SHAPE;
+  if (!aligned16(W) || !aligned16(A) || !aligned16(B) || !aligned16(W_out)) return LORA_ERR_ALIGN;
+  const Range rw = span(W, n, k, 2), ro = span(W_out, n, k, 2);
+  if (overlap(ro, span(A, r, k, 2)) || overlap(ro, span(B, n, r, 2))) return LORA_ERR_ALIAS;
+  if (overlap(ro, rw) && W_out != W) return LORA_ERR_ALIAS;   // in place is allowed, a shifted overlap is not
+
+  lora::MergeArgs a{W, A, B, W_out, n, k, r, (float)sign * ((float)alpha / (float)r)};
+  hipError_t e = lora::launch_merge(a, reinterpret_cast<hipStream_t>(stream));
   return e == hipSuccess ? LORA_OK : LORA_ERR_HIP;
 }
 

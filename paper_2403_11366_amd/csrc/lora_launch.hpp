@@ -110,7 +110,16 @@ struct BwdArgs {
   float s;
 };
 
+struct MergeArgs {
+  const uint16_t* W;       // [n, k]
+  const uint16_t *A, *B;   // [r, k], [n, r]
+  uint16_t* Wout;          // [n, k], may equal W
+  int64_t n, k, r;
+  float ss;                // sign * alpha / r
+};
+
 hipError_t launch_fwd(const FwdArgs& a, hipStream_t st);
+hipError_t launch_merge(const MergeArgs& a, hipStream_t st);
 hipError_t launch_bwd(const BwdArgs& a, hipStream_t st);
 
 }  // namespace lora

@@ -131,3 +131,36 @@ def test_bwd_misaligned_and_alias(lib):
 @pytest.mark.parametrize("m,n,k,r,code", [(0, 64, 64, 8, 2), (64, 64, 64, 65, 4), (64, 8, 7, 8, 2)])
 def test_bwd_bad_shapes(lib, m, n, k, r, code):
     assert bwd(lib, ws_bytes=1 << 30, m=m, n=n, k=k, r=r) == code
+
+
+def merge(lib, ptrs=None, n=64, k=64, r=8, alpha=16.0, sign=1):
+    p = [addr(i) for i in range(4)] if ptrs is None else ptrs
+    return lib.lora_linear_merge(*p, n, k, r, alpha, sign, None)
+
+
+def test_merge_null_and_sign(lib):
+    for i in range(4):
+        p = [addr(j) for j in range(4)]
+        p[i] = None
+        assert merge(lib, p) == 1
+    for sign in (0, 2, -2):
+        assert merge(lib, sign=sign) == 2
+
+
+@pytest.mark.parametrize("n,k,r,code", [(0, 64, 8, 2), (64, 60, 8, 2), (64, 64, 0, 2), (64, 64, 65, 4),
+                                        (1 << 23, 64, 8, 4)])
+def test_merge_bad_shapes(lib, n, k, r, code):
+    assert merge(lib, n=n, k=k, r=r) == code
+
+
+def test_merge_misaligned_and_alias(lib):
+    for i in range(4):
+        p = [addr(j) for j in range(4)]
+        p[i] += 2
+        assert merge(lib, p) == 3
+    p = [addr(j) for j in range(4)]
+    p[3] = p[0] + 16          # W_out shifted inside W (in place means exactly W)
+    assert merge(lib, p) == 6
+    p = [addr(j) for j in range(4)]
+    p[3] = p[2]               # W_out on top of B
+    assert merge(lib, p) == 6
