@@ -34,19 +34,26 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
   constexpr int WTI = BM / WM, WTJ = BN / WN;   // tokens, features per wave
   constexpr int FI = WTI / 32;                   // token fragments (B operand)
   constexpr int FJ = WTJ / 32;                   // feature fragments (A operand)
-  constexpr int FT = RP / 32;                    // U row fragments (A operand)
-  // U work: the FI token fragments of a wave row are shared by its WN waves.
-  // With FI >= WN each wave owns FUW fragments; with FI < WN, NDUP waves share a
-  // fragment and split its k substeps (partial sums added in the epilogue).
-  constexpr int FUW = FI >= WN ? FI / WN : 1;
-  constexpr int NDUP = FI >= WN ? 1 : WN / FI;
+  // U work.  For RP = 16 (rank <= 16) U runs on v_mfma_f32_16x16x32_bf16: a
+  // wave row's WTI tokens form WTI/16 groups of 16, GPW per wave, each over
+  // the 32-wide halves of the stage (substeps 0-1 and 2-3).  For RP >= 32 it
+  // runs on the 32x32x16 form: the FI token fragments of a wave row are shared
+  // by its WN waves; with FI >= WN each wave owns FUW fragments, with FI < WN
+  // NDUP waves share a fragment and split its k substeps (partial sums added in
+  // the epilogue).
+  constexpr bool U16 = RP == 16;
+  constexpr int FT = U16 ? 1 : RP / 32;          // U row fragments (A operand)
+  constexpr int FUW = U16 ? 1 : (FI >= WN ? FI / WN : 1);
+  constexpr int NDUP = U16 ? 1 : (FI >= WN ? 1 : WN / FI);
+  constexpr int GPW = U16 ? (WTI / 16) / WN : 1;
   constexpr int ROWS = BM + BN + RP;             // 128-byte rows per 64-wide stage
   constexpr int STAGE = ROWS * 128;
   constexpr int CX = BM * 8, CW = BN * 8, CA = RP * 8;   // 16-byte chunks per region
   constexpr int LX = (CX + NT - 1) / NT, LW = (CW + NT - 1) / NT, LA = (CA + NT - 1) / NT;
-  static_assert(WTI % 32 == 0 && WTJ % 32 == 0 && RP % 32 == 0, "32x32 fragments");
+  static_assert(WTI % 32 == 0 && WTJ % 32 == 0 && (U16 || RP % 32 == 0), "32x32 fragments");
+  static_assert(!U16 || ((WTI / 16) % WN == 0 && GPW >= 1), "U groups split evenly");
   static_assert(CX % 64 == 0 && CW % 64 == 0 && CA % 64 == 0, "regions end on wave boundaries");
-  static_assert(FI >= WN ? FI % WN == 0 : WN % FI == 0, "U fragments split evenly");
+  static_assert(U16 || (FI >= WN ? FI % WN == 0 : WN % FI == 0), "U fragments split evenly");
   static_assert(4 % NDUP == 0, "U substeps split evenly");
   static_assert(2 * STAGE <= 160 * 1024, "LDS budget");
   static_assert(NDUP * BM * RP * 4 + BN * RP * 2 <= 2 * STAGE, "epilogue LDS reuse");
@@ -60,6 +67,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
   const int wave = uniform(tid >> 6);
   const int wm = wave / WN, wn = wave % WN;
   const int g = lane >> 5, c32 = lane & 31;
+  const int g16 = lane >> 4, c16 = lane & 15;
   const int udup = NDUP > 1 ? wn / FI : 0;       // which share of the U substeps
 
   const uint32_t rowbytes = (uint32_t)k * 2;
@@ -129,7 +137,10 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
   };
 
   floatx16 acc[FJ][FI];
-  floatx16 uacc[FT][FUW];
+  floatx16 uacc[FT][FUW];      // U on the 32x32x16 form (RP >= 32)
+  floatx4 uacc16[GPW];         // U on the 16x16x32 form (RP = 16)
+#pragma unroll
+  for (int a = 0; a < GPW; ++a) uacc16[a] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int a = 0; a < FJ; ++a)
 #pragma unroll
@@ -141,6 +152,9 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
   int urow[FUW];
 #pragma unroll
   for (int fu = 0; fu < FUW; ++fu) urow[fu] = wm * WTI + 32 * ((wn + WN * fu) % FI) + c32;
+  int urow16[GPW];
+#pragma unroll
+  for (int gg = 0; gg < GPW; ++gg) urow16[gg] = wm * WTI + 16 * (wn * GPW + gg) + c16;
 
   // Fragments of the next 16-wide substep are read while the current one
   // multiplies (two register sets, p = substep parity).  The U products of a
@@ -148,6 +162,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
   // udup multiplies the k columns of substep ks + udup, so every wave executes
   // the same instruction stream.
   short8 fw[2][FJ], fx[2][FI], fa[2][FT], fxu[2][FUW];
+  short8 fa16[2], fxu16[2][GPW];
   auto read_frags = [&](const char* sb, int ks, int p) {
     const char* Xs = sb;
     const char* Ws = sb + BM * 128;
@@ -157,7 +172,13 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
     for (int fj = 0; fj < FJ; ++fj) fw[p][fj] = kc_read(Ws, wn * WTJ + 32 * fj + c32, ch);
 #pragma unroll
     for (int fi = 0; fi < FI; ++fi) fx[p][fi] = kc_read(Xs, wm * WTI + 32 * fi + c32, ch);
-    if (ks % NDUP == 0) {
+    if (U16) {
+      if (ks % 2 == 0) {   // the 32-wide half starting at substep ks: chunks 2 ks + g16
+        fa16[p] = kc_read(As, c16, 2 * ks + g16);
+#pragma unroll
+        for (int gg = 0; gg < GPW; ++gg) fxu16[p][gg] = kc_read(Xs, urow16[gg], 2 * ks + g16);
+      }
+    } else if (ks % NDUP == 0) {
       const int uch = ch + 2 * udup;
 #pragma unroll
       for (int ft = 0; ft < FT; ++ft) fa[p][ft] = kc_read(As, 32 * ft + c32, uch);
@@ -170,7 +191,12 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
     for (int fi = 0; fi < FI; ++fi)
 #pragma unroll
       for (int fj = 0; fj < FJ; ++fj) acc[fj][fi] = mfma32x32x16(fw[p][fj], fx[p][fi], acc[fj][fi]);
-    if (ks % NDUP == 0) {
+    if (U16) {
+      if (ks % 2 == 0) {
+#pragma unroll
+        for (int gg = 0; gg < GPW; ++gg) uacc16[gg] = mfma16x16x32(fa16[p], fxu16[p][gg], uacc16[gg]);
+      }
+    } else if (ks % NDUP == 0) {
 #pragma unroll
       for (int fu = 0; fu < FUW; ++fu)
 #pragma unroll
@@ -196,6 +222,9 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
     for (int j = 0; j < FT; ++j) fa[1][j] = short8{};
 #pragma unroll
     for (int j = 0; j < FUW; ++j) fxu[1][j] = short8{};
+    fa16[1] = short8{};
+#pragma unroll
+    for (int j = 0; j < GPW; ++j) fxu16[1][j] = short8{};
   }
   auto stage = [&](int kb, bool write_next, bool load_next) {
     const char* sb = smem + (kb & 1) * STAGE;
@@ -243,16 +272,23 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
     const int q = tid + i * NT;
     bv[i] = buf_load16(rsB, q < nch ? (uint32_t)q * 16 : kOOB);
   }
+  if (U16) {   // lane holds token column c16 of its group, U rows t = 4 g16 .. +3
 #pragma unroll
-  for (int fu = 0; fu < FUW; ++fu) {
-    const int il = urow[fu];
+    for (int gg = 0; gg < GPW; ++gg)
 #pragma unroll
-    for (int ft = 0; ft < FT; ++ft)
+      for (int q = 0; q < 4; ++q) Us[urow16[gg] * RP + 4 * g16 + q] = uacc16[gg][q];
+  } else {
 #pragma unroll
-      for (int q = 0; q < 16; ++q) {
-        const int t = 32 * ft + 8 * (q >> 2) + 4 * g + (q & 3);
-        Us[(udup * BM + il) * RP + t] = uacc[ft][fu][q];
-      }
+    for (int fu = 0; fu < FUW; ++fu) {
+      const int il = urow[fu];
+#pragma unroll
+      for (int ft = 0; ft < FT; ++ft)
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+          const int t = 32 * ft + 8 * (q >> 2) + 4 * g + (q & 3);
+          Us[(udup * BM + il) * RP + t] = uacc[ft][fu][q];
+        }
+    }
   }
   for (int e = tid; e < BN * RP / 8; e += NT) reinterpret_cast<int4v*>(Bs)[e] = int4v{0, 0, 0, 0};
   __syncthreads();
@@ -353,6 +389,7 @@ static hipError_t launch_fwd_cfg(const FwdArgs& a, hipStream_t st) {
 
 template <int BM, int BN, int WM, int WN>
 static hipError_t launch_fwd_rp(const FwdArgs& a, hipStream_t st) {
+  if (a.r <= 16) return launch_fwd_cfg<BM, BN, WM, WN, 16>(a, st);
   if (a.r <= 32) return launch_fwd_cfg<BM, BN, WM, WN, 32>(a, st);
   return launch_fwd_cfg<BM, BN, WM, WN, 64>(a, st);
 }
