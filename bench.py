@@ -99,21 +99,27 @@ def summarize_traffic(root: str, workload: str, copy_mib: int):
     print(json.dumps(rec))
 
 
-def cpu_baseline(shape, seconds: float):
-    """Time the fp64 oracle (as it stands) on this host for `shape`."""
+def cpu_baseline(shape, seconds: float, drop=None):
+    """Time the fp64 oracle (as it stands) on this host for `shape` (with LoRA
+    dropout at rate `drop` when given)."""
     import numpy as np
     import oracle
-    from lora_synth import gen_inputs
+    from lora_synth import gen_inputs, gen_keep_mask
     try:
         from threadpoolctl import threadpool_info
         threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
     except Exception:
         threads = os.cpu_count() or 1
     t = gen_inputs(shape)
+    keep = None if drop is None else gen_keep_mask(shape.m, shape.k, drop, shape.seed + 1)
     runs, t0 = 0, time.perf_counter()
     while True:
-        oracle.lora_forward(t["X"], t["W"], t["A"], t["B"], shape.alpha)
-        oracle.lora_backward(t["dY"], t["X"], t["W"], t["A"], t["B"], shape.alpha)
+        if keep is None:
+            oracle.lora_forward(t["X"], t["W"], t["A"], t["B"], shape.alpha)
+            oracle.lora_backward(t["dY"], t["X"], t["W"], t["A"], t["B"], shape.alpha)
+        else:
+            oracle.lora_forward_dropout(t["X"], t["W"], t["A"], t["B"], keep, drop, shape.alpha)
+            oracle.lora_backward_dropout(t["dY"], t["X"], t["W"], t["A"], t["B"], keep, drop, shape.alpha)
         runs += 1
         el = time.perf_counter() - t0
         if el >= seconds or runs >= 50:
@@ -219,6 +225,9 @@ def main():
     ap.add_argument("--op", choices=["train", "merge"], default="train",
                     help="train: forward + backward (the default measurement); merge: the "
                          "merge W + s B A of each projection's adapter into its weight")
+    ap.add_argument("--dropout", type=float, default=None, metavar="P",
+                    help="train with LoRA dropout at rate P on the adapter input (the *_dropout "
+                         "entry points, a seeded keep mask per input set)")
     ap.add_argument("--summarize-traffic", metavar="DIR", default=None,
                     help="write the HBM-traffic record from counter runs under DIR and exit")
     args = ap.parse_args()
@@ -239,7 +248,7 @@ def main():
     import paper_2403_11366_amd as lora
     from lora_synth import CONFIGS
     from paper_2403_11366_amd.device_io import bits_to_device
-    from lora_synth import gen_inputs
+    from lora_synth import gen_inputs, gen_keep_mask
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     lora.load_library()
@@ -261,13 +270,17 @@ def main():
         return
 
     # ---- inputs resident in HBM, rotated over enough copies to exceed the MALL
-    per_set = sum(2 * (s.m * s.k + s.n * s.k + s.r * s.k + s.n * s.r + s.m * s.n) for s in shapes)
+    drop = args.dropout
+    per_set = sum(2 * (s.m * s.k + s.n * s.k + s.r * s.k + s.n * s.r + s.m * s.n)
+                  + (s.m * s.k // 8 if drop is not None else 0) for s in shapes)
     nsets = max(1, math.ceil(2 * MALL_BYTES / per_set))
     log(f"[bench] {args.config}: {len(shapes)} projection(s), {nsets} input set(s) of {per_set / 2**20:.0f} MiB")
     proj = []
     for s in shapes:
         t = gen_inputs(s)
         base = {key: bits_to_device(v, dev) for key, v in t.items()}
+        if drop is not None:
+            base["keep"] = torch.from_numpy(gen_keep_mask(s.m, s.k, drop, s.seed + 1)).to(dev)
         sets = [base] + [{key: v.clone() for key, v in base.items()} for _ in range(nsets - 1)]
         out = {
             "Y": torch.empty((s.m, s.n), dtype=torch.bfloat16, device=dev),
@@ -283,10 +296,18 @@ def main():
 
     def fwd(i, s, sets, out):
         d = sets[i % len(sets)]
+        if drop is not None:
+            lora.lora_linear_fwd_dropout(d["X"], d["W"], d["A"], d["B"], d["keep"], drop, out["Y"], out["U"],
+                                         s.alpha, stream=stream)
+            return
         lora.lora_linear_fwd(d["X"], d["W"], d["A"], d["B"], out["Y"], out["U"], s.alpha, stream=stream)
 
     def bwd(i, s, sets, out):
         d = sets[i % len(sets)]
+        if drop is not None:
+            lora.lora_linear_bwd_dropout(d["dY"], d["X"], d["W"], d["A"], d["B"], out["U"], d["keep"], drop,
+                                         out["dX"], out["dA"], out["dB"], out["ws"], s.alpha, stream=stream)
+            return
         lora.lora_linear_bwd(d["dY"], d["X"], d["W"], d["A"], d["B"], out["U"], out["dX"], out["dA"],
                              out["dB"], out["ws"], s.alpha, stream=stream)
 
@@ -341,16 +362,17 @@ def main():
     m, n, k, r = s0.m, s0.n, s0.k, s0.r
     k1_flops = 2 * m * n * k + 2 * m * k * r + 2 * m * n * r
     achieved = k1_flops / (fwd_us * 1e-6) / 1e12
-    traffic = measured_traffic(args.config)
+    traffic = measured_traffic(args.config) if drop is None else None
     log(f"[bench] forward kernel {fwd_us:.1f} us ({achieved:.1f} TFLOP/s); backward call {bwd_us:.1f} us")
 
     cpu = None
     if not args.no_cpu_baseline:
         log(f"[bench] timing the fp64 oracle on the host (~{args.cpu_seconds:.0f} s)")
-        cpu = cpu_baseline(s0, args.cpu_seconds)
+        cpu = cpu_baseline(s0, args.cpu_seconds, drop)
 
     rec = {
-        "metric": "LoRA-linear fwd+bwd TFLOP/s + % bf16 MFMA peak, Llama-2-7B shapes, 1 GPU",
+        "metric": "LoRA-linear fwd+bwd TFLOP/s + % bf16 MFMA peak, Llama-2-7B shapes, 1 GPU"
+                  + ("" if drop is None else f", LoRA dropout p={drop}"),
         "value": round(tflops, 2),
         "unit": "TFLOP/s",
         "pct_bf16_mfma_peak": round(100 * tflops / PEAK_BF16_TFLOPS, 2),
@@ -366,7 +388,7 @@ def main():
         "config": {"workload": args.config,
                    "projections": [{"name": s.name, "m": s.m, "n": s.n, "k": s.k, "r": s.r,
                                     "alpha": s.alpha} for s in shapes],
-                   "input_sets": nsets, "flops_per_step": flops,
+                   "input_sets": nsets, "flops_per_step": flops, "lora_dropout": drop,
                    "operands": "bf16 in, fp32 accumulate; Y, dX bf16; U, dA, dB fp32"},
         "roofline": {"bound": "mfma", "kernel": "lora_fwd_kernel", "achieved": round(achieved, 2),
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),

@@ -80,6 +80,27 @@ lora_status lora_linear_fwd(const lora_bf16* X, const lora_bf16* W, const lora_b
                             void* stream);
 
 /*
+ * Forward with LoRA dropout on the adapter input (the configuration of
+ * Listing 3 carries LORA_DROPOUT = 0.05; the dropout acts on the input of A,
+ * while the frozen W0 sees x unchanged):
+ *
+ *     D = keep * X / (1 - p),   U = D A^T,   Y = X W^T + (alpha/r) U B^T
+ *
+ *   keep  [m, k/8] bytes, device: bit (l % 8) of byte (i, l / 8) set keeps
+ *         X[i][l] in D.  The mask is an input (the caller draws it, for
+ *         instance from a Bernoulli(1 - p) source); the backward must be given
+ *         the same mask.  16-byte aligned, read only.
+ *   p     dropout rate, 0 <= p < 1 (else LORA_ERR_SHAPE)
+ *   other arguments as in lora_linear_fwd; U is the dropped U = D A^T.
+ * Requires k % 64 == 0 (LORA_ERR_SHAPE otherwise).  The mask zeroes X
+ * elements of the U operand on the matrix cores; 1 / (1 - p) is applied to U
+ * in fp32.
+ */
+lora_status lora_linear_fwd_dropout(const lora_bf16* X, const lora_bf16* W, const lora_bf16* A,
+                                    const lora_bf16* B, const uint8_t* keep, float p, lora_bf16* Y, float* U,
+                                    int64_t m, int64_t n, int64_t k, int64_t r, float alpha, void* stream);
+
+/*
  * Bytes of device workspace lora_linear_bwd needs for this shape (0 on an
  * invalid shape).  The workspace holds transposed and split copies of the
  * rank-r operands and the fixed-order split-K partial sums of dA and dB.
@@ -107,6 +128,22 @@ lora_status lora_linear_bwd(const lora_bf16* dY, const lora_bf16* X, const lora_
                             void* workspace, size_t workspace_bytes,
                             int64_t m, int64_t n, int64_t k, int64_t r, float alpha,
                             void* stream);
+
+/*
+ * Backward of lora_linear_fwd_dropout for the same keep mask and rate:
+ *
+ *     dU = s dY B,  dX = dY W + keep * (dU A) / (1 - p),
+ *     dB = s dY^T U,  dA = dU^T D  with  D = keep * X / (1 - p)
+ *
+ * Arguments as in lora_linear_bwd plus keep and p as in
+ * lora_linear_fwd_dropout (U must be that forward's U).  The workspace size is
+ * lora_linear_bwd_workspace_size(m, n, k, r).  Requires k % 64 == 0.
+ */
+lora_status lora_linear_bwd_dropout(const lora_bf16* dY, const lora_bf16* X, const lora_bf16* W,
+                                    const lora_bf16* A, const lora_bf16* B, const float* U, const uint8_t* keep,
+                                    float p, lora_bf16* dX, float* dA, float* dB, void* workspace,
+                                    size_t workspace_bytes, int64_t m, int64_t n, int64_t k, int64_t r, float alpha,
+                                    void* stream);
 
 /*
  * Merge (sign = +1) or unmerge (sign = -1) of the adapter into the frozen

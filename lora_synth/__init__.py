@@ -29,7 +29,7 @@ import numpy as np
 
 __all__ = [
     "Shape", "CONFIGS", "config_shapes", "round_to_bf16_bits", "bf16_bits_to_f32",
-    "gen_inputs", "gen_ternary_inputs",
+    "gen_inputs", "gen_ternary_inputs", "gen_keep_mask",
 ]
 
 
@@ -131,3 +131,14 @@ def gen_ternary_inputs(m: int, n: int, k: int, r: int, seed: int,
     return {"X": tern((m, k), density), "W": tern((n, k), density),
             "A": tern((r, k), density), "B": tern((n, r), 4 * density),
             "dY": tern((m, n), density)}
+
+
+def gen_keep_mask(m: int, k: int, p: float, seed: int) -> np.ndarray:
+    """Seeded dropout keep mask for the adapter input, packed as the library
+    takes it: [m, k / 8] bytes, bit (l % 8) of byte l // 8 of row i set when
+    element (i, l) is kept.  Each element is kept independently with
+    probability 1 - p (numpy PCG64, float64 uniforms compared with p)."""
+    assert k % 8 == 0
+    rng = np.random.default_rng(seed)
+    keep = rng.random((m, k)) >= p
+    return np.packbits(keep, axis=1, bitorder="little")

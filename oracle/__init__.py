@@ -23,6 +23,10 @@ on the exact decoded bfloat16 inputs:
       dB = s dY^T U                    [n, r]
       dA = dU^T X                      [r, k]
 
+LoRA dropout (Listing 3's LORA_DROPOUT) acts on the adapter's input only:
+with a keep mask and rate p, D = keep * X / (1 - p), U = D A^T, and the
+backward carries the mask into dX's LoRA term and into dA = dU^T D.
+
 The merge of the adapter into the frozen weight (Eq. 1's second form,
 W0 x + B A x = (W0 + B A) x) is W + sign s B A, rounded once to bfloat16
 (nearest-even) for the stored result.
@@ -35,8 +39,10 @@ tests/test_oracle_pins.py.
 """
 from .lora_oracle import (bf16_bits_to_f64, lora_scale, lora_rank_activation, lora_forward,
                           lora_backward, lora_forward_rows, lora_backward_rows, f64_to_bf16_bits,
-                          f64_to_bf16_rne, lora_merged_weight, lora_merge_bf16)
+                          f64_to_bf16_rne, lora_merged_weight, lora_merge_bf16, dropout_keep,
+                          dropped_input, lora_forward_dropout, lora_backward_dropout)
 
 __all__ = ["bf16_bits_to_f64", "lora_scale", "lora_rank_activation", "lora_forward",
            "lora_backward", "lora_forward_rows", "lora_backward_rows", "f64_to_bf16_bits",
-           "f64_to_bf16_rne", "lora_merged_weight", "lora_merge_bf16"]
+           "f64_to_bf16_rne", "lora_merged_weight", "lora_merge_bf16", "dropout_keep",
+           "dropped_input", "lora_forward_dropout", "lora_backward_dropout"]

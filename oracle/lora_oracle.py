@@ -107,6 +107,50 @@ def lora_merge_bf16(W, A, B, alpha: float, sign: int = 1) -> np.ndarray:
     return f64_to_bf16_rne(lora_merged_weight(W, A, B, alpha, sign))
 
 
+def dropout_keep(keep_bits, k: int) -> np.ndarray:
+    """Decode a packed keep mask ([m, k/8] bytes, bit l % 8 of byte l // 8 of
+    row i keeps element (i, l)) into a float64 0/1 matrix [m, k]."""
+    b = np.asarray(keep_bits, dtype=np.uint8)
+    return np.unpackbits(b, axis=1, bitorder="little")[:, :k].astype(np.float64)
+
+
+def dropped_input(X, keep_bits, p: float) -> np.ndarray:
+    """The adapter's input under LoRA dropout (Listing 3's LORA_DROPOUT; the
+    dropout acts on the input of A only, the frozen W0 sees x unchanged):
+    D = keep * X / (1 - p), the usual inverted-dropout scaling during training."""
+    X = _f64(X)
+    return dropout_keep(keep_bits, X.shape[1]) * X / (1.0 - float(p))
+
+
+def lora_forward_dropout(X, W, A, B, keep_bits, p: float, alpha: float
+                         ) -> Tuple[np.ndarray, np.ndarray]:
+    """Eq. 1 with dropout on the adapter input: U = D A^T, Y = X W^T + s U B^T,
+    D = dropped_input(X).  Returns (U [m,r], Y [m,n]) in float64."""
+    X, W, A, B = _f64(X), _f64(W), _f64(A), _f64(B)
+    s = lora_scale(alpha, A.shape[0])
+    D = dropped_input(X, keep_bits, p)
+    U = D @ A.T
+    Y = X @ W.T + s * (U @ B.T)
+    return U, Y
+
+
+def lora_backward_dropout(dY, X, W, A, B, keep_bits, p: float, alpha: float
+                          ) -> Tuple[np.ndarray, np.ndarray, np.ndarray, np.ndarray]:
+    """Chain rule through lora_forward_dropout for a fixed mask: with
+    dU = s dY B,  dX = dY W + keep * (dU A) / (1 - p),  dB = s dY^T U,
+    dA = dU^T D.  Returns (dU, dX, dA, dB) in float64."""
+    dY, X, W, A, B = _f64(dY), _f64(X), _f64(W), _f64(A), _f64(B)
+    s = lora_scale(alpha, A.shape[0])
+    keep = dropout_keep(keep_bits, X.shape[1])
+    D = keep * X / (1.0 - float(p))
+    U = D @ A.T
+    dU = s * (dY @ B)
+    dX = dY @ W + keep * (dU @ A) / (1.0 - float(p))
+    dB = s * (dY.T @ U)
+    dA = dU.T @ D
+    return dU, dX, dA, dB
+
+
 def lora_forward_rows(X, W, A, B, alpha: float, rows: Sequence[int]
                       ) -> Tuple[np.ndarray, np.ndarray]:
     """The forward restricted to the token rows `rows` (each output row of Eq. 1

@@ -16,7 +16,8 @@ from typing import Optional
 
 __all__ = [
     "LoraError", "lib_path", "load_library", "lora_linear_fwd", "lora_linear_bwd",
-    "lora_linear_bwd_workspace_size", "lora_linear_merge", "lora_status_string", "STATUS",
+    "lora_linear_bwd_workspace_size", "lora_linear_merge", "lora_linear_fwd_dropout", "lora_linear_bwd_dropout",
+    "lora_status_string", "STATUS",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -53,6 +54,10 @@ def load_library() -> ctypes.CDLL:
     lib.lora_linear_bwd_workspace_size.restype = sz
     lib.lora_linear_bwd.argtypes = [p, p, p, p, p, p, p, p, p, p, sz, i64, i64, i64, i64, f32, p]
     lib.lora_linear_bwd.restype = ctypes.c_int
+    lib.lora_linear_fwd_dropout.argtypes = [p, p, p, p, p, f32, p, p, i64, i64, i64, i64, f32, p]
+    lib.lora_linear_fwd_dropout.restype = ctypes.c_int
+    lib.lora_linear_bwd_dropout.argtypes = [p, p, p, p, p, p, p, f32, p, p, p, p, sz, i64, i64, i64, i64, f32, p]
+    lib.lora_linear_bwd_dropout.restype = ctypes.c_int
     lib.lora_linear_merge.argtypes = [p, p, p, p, i64, i64, i64, f32, ctypes.c_int, p]
     lib.lora_linear_merge.restype = ctypes.c_int
     lib.lora_status_string.argtypes = [ctypes.c_int]
@@ -151,3 +156,51 @@ def lora_linear_merge(W, A, B, W_out, alpha: float, sign: int = 1, stream=None) 
                                           int(sign), _stream_handle(stream))
     if st != 0:
         raise LoraError(st, "lora_linear_merge")
+
+
+def _check_keep(keep, m, k):
+    import torch
+    if keep.dtype != torch.uint8 or tuple(keep.shape) != (m, k // 8) or not keep.is_contiguous() \
+            or keep.device.type != "cuda":
+        raise ValueError(f"keep: expected a contiguous uint8 device tensor of shape {(m, k // 8)}")
+
+
+def lora_linear_fwd_dropout(X, W, A, B, keep, p: float, Y, U, alpha: float, stream=None) -> None:
+    """Forward with dropout on the adapter input: D = keep * X / (1 - p),
+    U = D A^T, Y = X W^T + (alpha/r) U B^T.  keep: uint8 [m, k/8] packed bits
+    (bit l % 8 of byte l // 8 keeps element l)."""
+    import torch
+    m, k = X.shape
+    n, r = W.shape[0], A.shape[0]
+    for t, name, dt, shp in ((X, "X", torch.bfloat16, (m, k)), (W, "W", torch.bfloat16, (n, k)),
+                             (A, "A", torch.bfloat16, (r, k)), (B, "B", torch.bfloat16, (n, r)),
+                             (Y, "Y", torch.bfloat16, (m, n)), (U, "U", torch.float32, (m, r))):
+        _check(t, name, dt, shp)
+    _check_keep(keep, m, k)
+    st = load_library().lora_linear_fwd_dropout(_ptr(X), _ptr(W), _ptr(A), _ptr(B), _ptr(keep), float(p), _ptr(Y),
+                                                _ptr(U), m, n, k, r, float(alpha), _stream_handle(stream))
+    if st != 0:
+        raise LoraError(st, "lora_linear_fwd_dropout")
+
+
+def lora_linear_bwd_dropout(dY, X, W, A, B, U, keep, p: float, dX, dA, dB, workspace, alpha: float,
+                            stream=None) -> None:
+    """Backward of lora_linear_fwd_dropout for the same keep mask and rate p."""
+    import torch
+    m, n = dY.shape
+    k, r = X.shape[1], A.shape[0]
+    for t, name, dt, shp in ((dY, "dY", torch.bfloat16, (m, n)), (X, "X", torch.bfloat16, (m, k)),
+                             (W, "W", torch.bfloat16, (n, k)), (A, "A", torch.bfloat16, (r, k)),
+                             (B, "B", torch.bfloat16, (n, r)), (U, "U", torch.float32, (m, r)),
+                             (dX, "dX", torch.bfloat16, (m, k)), (dA, "dA", torch.float32, (r, k)),
+                             (dB, "dB", torch.float32, (n, r))):
+        _check(t, name, dt, shp)
+    _check_keep(keep, m, k)
+    if workspace.device.type != "cuda" or not workspace.is_contiguous():
+        raise ValueError("workspace: must be a contiguous device tensor")
+    ws_bytes = workspace.numel() * workspace.element_size()
+    st = load_library().lora_linear_bwd_dropout(_ptr(dY), _ptr(X), _ptr(W), _ptr(A), _ptr(B), _ptr(U), _ptr(keep),
+                                                float(p), _ptr(dX), _ptr(dA), _ptr(dB), _ptr(workspace), ws_bytes,
+                                                m, n, k, r, float(alpha), _stream_handle(stream))
+    if st != 0:
+        raise LoraError(st, "lora_linear_bwd_dropout")

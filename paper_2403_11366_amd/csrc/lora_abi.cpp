@@ -73,6 +73,28 @@ lora_status lora_linear_fwd(const lora_bf16* X, const lora_bf16* W, const lora_b
   return e == hipSuccess ? LORA_OK : LORA_ERR_HIP;
 }
 
+lora_status lora_linear_fwd_dropout(const lora_bf16* X, const lora_bf16* W, const lora_bf16* A,
+                                    const lora_bf16* B, const uint8_t* keep, float p, lora_bf16* Y, float* U,
+                                    int64_t m, int64_t n, int64_t k, int64_t r, float alpha, void* stream) {
+  if (!X || !W || !A || !B || !keep || !Y || !U) return LORA_ERR_NULL;
+  lora_status st = check_shape(m, n, k, r);
+  if (st != LORA_OK) return st;
+  if (k % 64 != 0 || !(p >= 0.0f && p < 1.0f)) return LORA_ERR_SHAPE;
+  if (!aligned16(X) || !aligned16(W) || !aligned16(A) || !aligned16(B) || !aligned16(keep) || !aligned16(Y) ||
+      !aligned16(U))
+    return LORA_ERR_ALIGN;
+  const Range in[5] = {span(X, m, k, 2), span(W, n, k, 2), span(A, r, k, 2), span(B, n, r, 2),
+                       span(keep, m, k / 8, 1)};
+  const Range ry = span(Y, m, n, 2), ru = span(U, m, r, 4);
+  for (const Range& x : in)
+    if (overlap(ry, x) || overlap(ru, x)) return LORA_ERR_ALIAS;
+  if (overlap(ry, ru)) return LORA_ERR_ALIAS;
+
+  lora::FwdArgs a{X, W, A, B, Y, U, m, n, k, r, (float)alpha / (float)r, keep, 1.0f / (1.0f - p)};
+  hipError_t e = lora::launch_fwd(a, reinterpret_cast<hipStream_t>(stream));
+  return e == hipSuccess ? LORA_OK : LORA_ERR_HIP;
+}
+
 size_t lora_linear_bwd_workspace_size(int64_t m, int64_t n, int64_t k, int64_t r) {
   if (check_shape(m, n, k, r) != LORA_OK) return 0;
   return lora::bwd_layout(m, n, k, r).total;
@@ -108,6 +130,40 @@ lora_status lora_linear_bwd(const lora_bf16* dY, const lora_bf16* X, const lora_
 
   lora::BwdArgs a{dY, X, W, A, B, U, dX, dA, dB, static_cast<char*>(workspace),
                   m, n, k, r, (float)alpha / (float)r};
+  hipError_t e = lora::launch_bwd(a, reinterpret_cast<hipStream_t>(stream));
+  return e == hipSuccess ? LORA_OK : LORA_ERR_HIP;
+}
+
+lora_status lora_linear_bwd_dropout(const lora_bf16* dY, const lora_bf16* X, const lora_bf16* W,
+                                    const lora_bf16* A, const lora_bf16* B, const float* U, const uint8_t* keep,
+                                    float p, lora_bf16* dX, float* dA, float* dB, void* workspace,
+                                    size_t workspace_bytes, int64_t m, int64_t n, int64_t k, int64_t r, float alpha,
+                                    void* stream) {
+  if (!dY || !X || !W || !A || !B || !U || !keep || !dX || !dA || !dB) return LORA_ERR_NULL;
+  lora_status st = check_shape(m, n, k, r);
+  if (st != LORA_OK) return st;
+  if (k % 64 != 0 || !(p >= 0.0f && p < 1.0f)) return LORA_ERR_SHAPE;
+  if (!aligned16(dY) || !aligned16(X) || !aligned16(W) || !aligned16(A) || !aligned16(B) ||
+      !aligned16(U) || !aligned16(keep) || !aligned16(dX) || !aligned16(dA) || !aligned16(dB))
+    return LORA_ERR_ALIGN;
+  const size_t need = lora::bwd_layout(m, n, k, r).total;
+  if (!workspace || workspace_bytes < need) return LORA_ERR_WORKSPACE;
+  if (!aligned16(workspace)) return LORA_ERR_ALIGN;
+
+  const Range in[7] = {span(dY, m, n, 2), span(X, m, k, 2), span(W, n, k, 2), span(A, r, k, 2),
+                       span(B, n, r, 2),  span(U, m, r, 4), span(keep, m, k / 8, 1)};
+  const Range out[4] = {span(dX, m, k, 2), span(dA, r, k, 4), span(dB, n, r, 4),
+                        Range{reinterpret_cast<uintptr_t>(workspace),
+                              reinterpret_cast<uintptr_t>(workspace) + need}};
+  for (int i = 0; i < 4; ++i) {
+    for (const Range& x : in)
+      if (overlap(out[i], x)) return LORA_ERR_ALIAS;
+    for (int j = i + 1; j < 4; ++j)
+      if (overlap(out[i], out[j])) return LORA_ERR_ALIAS;
+  }
+
+  lora::BwdArgs a{dY, X, W, A, B, U, dX, dA, dB, static_cast<char*>(workspace),
+                  m, n, k, r, (float)alpha / (float)r, keep, 1.0f / (1.0f - p)};
   hipError_t e = lora::launch_bwd(a, reinterpret_cast<hipStream_t>(stream));
   return e == hipSuccess ? LORA_OK : LORA_ERR_HIP;
 }

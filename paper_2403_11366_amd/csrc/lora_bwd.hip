@@ -191,6 +191,7 @@ struct RedProblem {
   const u16* Q;
   float* part;
   int ncols, span, col_tiles;
+  const uint8_t* keep;   // dropout keep bits of Q ([m][ncols/8]) or null: masked Q elements count as 0
 };
 
 template <int RP>
@@ -231,7 +232,10 @@ __global__ __launch_bounds__(256) void lora_tokred_kernel(RedProblem p0, RedProb
   // Slice loads: Q chunk u of this lane is row (lane + 64u) / CPR, chunk
   // (lane + 64u) % CPR; P fragment f is row 16f + c16, tokens ts + 8g .. +7.
   int4v qv[2][QL];
+  uint32_t kq[2][QL];          // keep byte of each Q chunk (dropout)
   short8 pv[2][FP];
+  const uint8_t* keep = pr.keep;
+  const uint32_t kb8 = (uint32_t)ncols / 8;
   auto load = [&](int ts, int b) {
     const int rows = uniform(max(0, min(32, m - ts)));   // keeps the resource in scalar registers
     const __amdgpu_buffer_rsrc_t rsQ = make_rsrc(Q + (size_t)ts * ncols, (uint64_t)rows * qrow);
@@ -240,6 +244,15 @@ __global__ __launch_bounds__(256) void lora_tokred_kernel(RedProblem p0, RedProb
       const int q = lane + 64 * u;
       const int cc = c0 + 8 * (q % CPR);
       qv[b][u] = buf_load16(rsQ, cc < ncols ? (uint32_t)(q / CPR) * qrow + (uint32_t)cc * 2 : kOOB);
+    }
+    if (keep) {   // workgroup-uniform
+      const __amdgpu_buffer_rsrc_t rsK = make_rsrc(keep + (size_t)ts * kb8, (uint64_t)rows * kb8);
+#pragma unroll
+      for (int u = 0; u < QL; ++u) {
+        const int q = lane + 64 * u;
+        const int cc = c0 + 8 * (q % CPR);
+        kq[b][u] = buf_load_u8(rsK, cc < ncols ? (uint32_t)(q / CPR) * kb8 + (uint32_t)cc / 8 : kOOB);
+      }
     }
 #pragma unroll
     for (int f = 0; f < FP; ++f)
@@ -251,7 +264,9 @@ __global__ __launch_bounds__(256) void lora_tokred_kernel(RedProblem p0, RedProb
 #pragma unroll
     for (int u = 0; u < QL; ++u) {
       const int q = lane + 64 * u;
-      *reinterpret_cast<int4v*>(qs + mc16_offset<CB>(q / CPR, q % CPR)) = qv[b][u];
+      int4v v = qv[b][u];
+      if (keep) v = __builtin_bit_cast(int4v, keep_mask8(__builtin_bit_cast(short8, v), kq[b][u]));
+      *reinterpret_cast<int4v*>(qs + mc16_offset<CB>(q / CPR, q % CPR)) = v;
     }
 #pragma unroll
     for (int fc = 0; fc < FC; ++fc) {
@@ -314,6 +329,7 @@ struct FinalizeArgs {
   float* dA;
   int n, k, r, rp, sb, sa;
   float s;
+  float sa_scale;   // 1, or 1 / (1 - p) with dropout (dA = dU^T keep X / (1 - p))
 };
 
 // Sum of `count` partials spaced `step` floats apart, in index order; the
@@ -341,7 +357,7 @@ __device__ __forceinline__ void finalize_partials(const FinalizeArgs& f, int fir
     } else {
       const int g = e - nb;
       const int t = g / f.k, l = g - t * f.k;
-      f.dA[g] = sum_partials(f.pa + (size_t)t * f.k + l, (size_t)f.rp * f.k, f.sa);
+      f.dA[g] = f.sa_scale * sum_partials(f.pa + (size_t)t * f.k + l, (size_t)f.rp * f.k, f.sa);
     }
   }
 }
@@ -355,11 +371,17 @@ __device__ __forceinline__ void finalize_partials(const FinalizeArgs& f, int fir
 // for the high and once for the low part.  Global loads run two stages ahead
 // in registers and are stored to the free LDS buffer piece by piece during
 // the stage before their use (one barrier per stage).
-template <int BM, int BN, int WM, int WN, int RP>
+//
+// With dropout (DROP) the LoRA term is keep * (dU A) / (1 - p): the mask acts
+// after the rank-r product, so it cannot ride in the k loop.  The slab stages
+// are skipped; after the n stages the tile's dU2 rows, A columns and keep bits
+// are staged in LDS, dU A is formed per fragment into a temporary
+// accumulator, and added under the mask with the 1 / (1 - p) scale.
+template <int BM, int BN, int WM, int WN, int RP, bool DROP>
 __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
     const u16* __restrict__ dY, const u16* __restrict__ W, const u16* __restrict__ dU2,
-    const u16* __restrict__ A, u16* __restrict__ dX, int m, int n, int k, int r, int mp,
-    int tiles_m, int tiles_n, FinalizeArgs fin) {
+    const u16* __restrict__ A, const uint8_t* __restrict__ keep, u16* __restrict__ dX, int m, int n, int k,
+    int r, int mp, float inv_keep, int tiles_m, int tiles_n, FinalizeArgs fin) {
   constexpr int NW = WM * WN;
   constexpr int NT = 64 * NW;
   constexpr int WTI = BM / WM, WTJ = BN / WN;
@@ -518,20 +540,85 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
 #pragma unroll
   for (int pc = 0; pc < 3; ++pc) swrite(0, pc);
   __syncthreads();
+  constexpr int NSL = DROP ? 0 : NSLAB;   // slab stages in the k loop
   int st = 0;
   if (nkb >= 2) {
 #pragma unroll
     for (int pc = 0; pc < 3; ++pc) gload_w(1, pc);
     for (; st + 2 < nkb; ++st) stage(st, true, LD_W);
-    stage(st++, true, LD_S0);                       // st = nkb - 2
-  } else {
+    stage(st++, true, NSL > 0 ? LD_S0 : LD_NONE);   // st = nkb - 2
+  } else if (NSL > 0) {
 #pragma unroll
     for (int pc = 0; pc < 3; ++pc) gload_s(0, pc);
   }
-  stage(st++, true, NSLAB > 1 ? LD_S1 : LD_NONE);   // writes slab 0
-  if (NSLAB > 1) stage(st++, true, LD_NONE);        // writes slab 1
+  if (NSL > 0) stage(st++, true, NSL > 1 ? LD_S1 : LD_NONE);   // writes slab 0
+  if (NSL > 1) stage(st++, true, LD_NONE);                     // writes slab 1
   stage(st, false, LD_NONE);
   if (ROT) multiply(1);
+
+  if (DROP) {
+    // LDS after the k loop: Us2 [BM][UP] bf16 (dU high | low of the tile's
+    // tokens), As2 [RP][BN] bf16 mn-contiguous (A rows, zero beyond r and k),
+    // Kb [BM][BN/8] keep bytes of the tile.
+    constexpr int UP = 2 * RP + 8;                  // Us2 row pitch in elements (16-byte multiple)
+    constexpr int US_BYTES = BM * UP * 2, AS_BYTES = RP * BN * 2;
+    static_assert(US_BYTES + AS_BYTES + BM * BN / 8 <= 2 * STAGE, "dropout epilogue fits the stage LDS");
+    u16* Us2 = reinterpret_cast<u16*>(smem);
+    char* As2 = smem + US_BYTES;
+    uint8_t* Kb = reinterpret_cast<uint8_t*>(smem + US_BYTES + AS_BYTES);
+    const uint32_t kb8 = (uint32_t)k / 8;
+    {
+      constexpr int UCH = BM * (RP / 4);            // 16-byte chunks of the dU2 rows
+      const __amdgpu_buffer_rsrc_t rsU2 = make_rsrc(dU2 + (size_t)m0 * KS2, (uint64_t)min(BM, mp - m0) * urow);
+      for (int q = tid; q < UCH; q += NT) {
+        const int i = q / (RP / 4), c = q % (RP / 4);
+        *reinterpret_cast<int4v*>(Us2 + i * UP + 8 * c) = buf_load16(rsU2, (uint32_t)i * urow + (uint32_t)c * 16);
+      }
+      constexpr int ACH = RP * (BN / 8);
+      for (int q = tid; q < ACH; q += NT) {
+        const int t = q / (BN / 8), c = q % (BN / 8);
+        const int ll = l0 + 8 * c;
+        *reinterpret_cast<int4v*>(As2 + mc32_offset<BN>(t, c)) =
+            buf_load16(rsA, (t < r && ll < k) ? (uint32_t)t * wrow + (uint32_t)ll * 2 : kOOB);
+      }
+      constexpr int KCH = BM * (BN / 64);           // 8-byte chunks of keep bits
+      const __amdgpu_buffer_rsrc_t rsK = make_rsrc(keep + (size_t)m0 * kb8, (uint64_t)min(BM, m - m0) * kb8);
+      for (int q = tid; q < KCH; q += NT) {
+        const int i = q / (BN / 64), c = q % (BN / 64);
+        *reinterpret_cast<uint2*>(Kb + i * (BN / 8) + 8 * c) =
+            buf_load8(rsK, (uint32_t)i * kb8 + (uint32_t)l0 / 8 + 8 * c);
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int fj = 0; fj < FJ; ++fj) {
+      floatx16 tmp[FI];
+#pragma unroll
+      for (int fi = 0; fi < FI; ++fi) tmp[fi] = floatx16{};
+#pragma unroll
+      for (int kk = 0; kk < KS2 / 16; ++kk) {        // k = t of [dU_hi | dU_lo] against [A; A]
+        const short8 af = mc32_read_tr<BN>(As2, (16 * kk) % RP, wn * WTJ + 32 * fj, lane);
+#pragma unroll
+        for (int fi = 0; fi < FI; ++fi) {
+          const short8 bf = *reinterpret_cast<const short8*>(Us2 + (wm * WTI + 32 * fi + c32) * UP + 16 * kk + 8 * g);
+          tmp[fi] = mfma32x32x16(af, bf, tmp[fi]);
+        }
+      }
+      // lane: token column c32 of fragment fi, features 8 qq + 4 g + q4 of
+      // fragment fj -> keep byte (wn WTJ + 32 fj) / 8 + qq, bit 4 g + q4
+#pragma unroll
+      for (int fi = 0; fi < FI; ++fi) {
+        const uint8_t* kr = Kb + (wm * WTI + 32 * fi + c32) * (BN / 8) + (wn * WTJ + 32 * fj) / 8;
+#pragma unroll
+        for (int qq = 0; qq < 4; ++qq) {
+          const uint32_t byte = kr[qq];
+#pragma unroll
+          for (int q4 = 0; q4 < 4; ++q4)
+            if ((byte >> (4 * g + q4)) & 1u) acc[fj][fi][4 * qq + q4] += inv_keep * tmp[fi][4 * qq + q4];
+        }
+      }
+    }
+  }
 
 #pragma unroll
   for (int fi = 0; fi < FI; ++fi) {
@@ -556,13 +643,13 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
 }
 
 // ---------------------------------------------------------------------------
-template <int BM, int BN, int WM, int WN, int RP>
+template <int BM, int BN, int WM, int WN, int RP, bool DROP>
 static hipError_t launch_dx_cfg(const BwdArgs& a, const BwdLayout& L, const FinalizeArgs& fin, hipStream_t st) {
   const int tiles_m = (int)((a.m + BM - 1) / BM), tiles_n = (int)((a.k + BN - 1) / BN);
   const int nt = 64 * WM * WN;
-  hipLaunchKernelGGL((lora_bwd_dx_kernel<BM, BN, WM, WN, RP>), dim3(tiles_m * tiles_n), dim3(nt), 0, st,
-                     a.dY, a.W, reinterpret_cast<const u16*>(a.ws + L.du2), a.A, a.dX, (int)a.m, (int)a.n,
-                     (int)a.k, (int)a.r, (int)L.mp, tiles_m, tiles_n, fin);
+  hipLaunchKernelGGL((lora_bwd_dx_kernel<BM, BN, WM, WN, RP, DROP>), dim3(tiles_m * tiles_n), dim3(nt), 0, st,
+                     a.dY, a.W, reinterpret_cast<const u16*>(a.ws + L.du2), a.A, a.keep, a.dX, (int)a.m, (int)a.n,
+                     (int)a.k, (int)a.r, (int)L.mp, a.inv_keep, tiles_m, tiles_n, fin);
   return hipGetLastError();
 }
 
@@ -581,19 +668,26 @@ static hipError_t launch_bwd_rp(const BwdArgs& a, const BwdLayout& L, hipStream_
   if ((e = hipGetLastError()) != hipSuccess) return e;
 
   {
-    const RedProblem pbp{Ut2, a.dY, pb, n, (int)L.plan_b.span, L.plan_b.col_tiles};
-    const RedProblem pap{dUt2, a.X, pa, k, (int)L.plan_a.span, L.plan_a.col_tiles};
+    const RedProblem pbp{Ut2, a.dY, pb, n, (int)L.plan_b.span, L.plan_b.col_tiles, nullptr};
+    const RedProblem pap{dUt2, a.X, pa, k, (int)L.plan_a.span, L.plan_a.col_tiles, a.keep};
     const int nb0 = L.plan_b.col_tiles * L.plan_b.splits;
     const int nb1 = L.plan_a.col_tiles * L.plan_a.splits;
     hipLaunchKernelGGL((lora_tokred_kernel<RP>), dim3(nb0 + nb1), dim3(256), 0, st, pbp, pap, nb0, m, mp);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
 
-  const FinalizeArgs fin{pb, pa, a.dB, a.dA, n, k, r, RP, L.plan_b.splits, L.plan_a.splits, a.s};
-  switch (choose_gemm_tile(a.m, a.k)) {
-    case TILE_256x256: e = launch_dx_cfg<256, 256, 2, 4, RP>(a, L, fin, st); break;
-    case TILE_128x256: e = launch_dx_cfg<128, 256, 2, 4, RP>(a, L, fin, st); break;
-    default: e = launch_dx_cfg<128, 128, 2, 2, RP>(a, L, fin, st); break;
+  const FinalizeArgs fin{pb, pa, a.dB, a.dA, n, k, r, RP, L.plan_b.splits, L.plan_a.splits, a.s,
+                         a.keep ? a.inv_keep : 1.0f};
+  const GemmTile t = choose_gemm_tile(a.m, a.k);
+  if (a.keep) {   // the 256 x 256 tile has no registers left for the dropout epilogue
+    if (t == TILE_128x128) e = launch_dx_cfg<128, 128, 2, 2, RP, true>(a, L, fin, st);
+    else e = launch_dx_cfg<128, 256, 2, 4, RP, true>(a, L, fin, st);
+  } else {
+    switch (t) {
+      case TILE_256x256: e = launch_dx_cfg<256, 256, 2, 4, RP, false>(a, L, fin, st); break;
+      case TILE_128x256: e = launch_dx_cfg<128, 256, 2, 4, RP, false>(a, L, fin, st); break;
+      default: e = launch_dx_cfg<128, 128, 2, 2, RP, false>(a, L, fin, st); break;
+    }
   }
   if (e != hipSuccess) return e;
   return hipSuccess;

@@ -76,6 +76,29 @@ __device__ __forceinline__ void wait_vmcnt0() { __builtin_amdgcn_s_waitcnt(0x0F7
 
 __device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
 
+// 8-byte load through a buffer resource (byte_off a multiple of 8).
+__device__ __forceinline__ uint2 buf_load8(__amdgpu_buffer_rsrc_t rs, uint32_t byte_off) {
+  const auto v = __builtin_amdgcn_raw_buffer_load_b64(rs, byte_off, 0, 0);
+  return uint2{(uint32_t)v[0], (uint32_t)v[1]};
+}
+
+// 1-byte load through a buffer resource; out-of-range offsets read as zero.
+__device__ __forceinline__ uint32_t buf_load_u8(__amdgpu_buffer_rsrc_t rs, uint32_t byte_off) {
+  return (uint32_t)__builtin_amdgcn_raw_buffer_load_b8(rs, byte_off, 0, 0);
+}
+
+// Dropout on an operand fragment: element e of the 8 bf16 values in v is kept
+// when bit e of `bits` is set and zeroed otherwise.
+__device__ __forceinline__ short8 keep_mask8(short8 v, uint32_t bits) {
+  int4v w = __builtin_bit_cast(int4v, v);
+#pragma unroll
+  for (int h = 0; h < 4; ++h) {
+    const uint32_t lo = 0u - ((bits >> (2 * h)) & 1u), hi = 0u - ((bits >> (2 * h + 1)) & 1u);
+    w[h] &= (int)((lo & 0xFFFFu) | (hi << 16));
+  }
+  return __builtin_bit_cast(short8, w);
+}
+
 __device__ __forceinline__ u16 f32_to_bf16(float f) {  // round to nearest even (v_cvt_pk_bf16_f32)
   return __builtin_bit_cast(u16, (__bf16)f);
 }

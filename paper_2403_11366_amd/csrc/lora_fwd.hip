@@ -24,11 +24,11 @@
 
 namespace lora {
 
-template <int BM, int BN, int WM, int WN, int RP>
+template <int BM, int BN, int WM, int WN, int RP, bool DROP>
 __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
     const u16* __restrict__ X, const u16* __restrict__ W, const u16* __restrict__ A,
-    const u16* __restrict__ B, u16* __restrict__ Y, float* __restrict__ U,
-    int m, int n, int k, int r, float s, int tiles_m, int tiles_n) {
+    const u16* __restrict__ B, const uint8_t* __restrict__ keep, u16* __restrict__ Y,
+    float* __restrict__ U, int m, int n, int k, int r, float s, float inv_keep, int tiles_m, int tiles_n) {
   constexpr int NW = WM * WN;
   constexpr int NT = 64 * NW;
   constexpr int WTI = BM / WM, WTJ = BN / WN;   // tokens, features per wave
@@ -47,7 +47,10 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
   constexpr int NDUP = U16 ? 1 : (FI >= WN ? 1 : WN / FI);
   constexpr int GPW = U16 ? (WTI / 16) / WN : 1;
   constexpr int ROWS = BM + BN + RP;             // 128-byte rows per 64-wide stage
-  constexpr int STAGE = ROWS * 128;
+  // With dropout the stage also holds the keep bits of its X rows: 8 bytes
+  // (64 k) per row.
+  constexpr int KS_OFF = ROWS * 128;
+  constexpr int STAGE = KS_OFF + (DROP ? BM * 8 : 0);
   constexpr int CX = BM * 8, CW = BN * 8, CA = RP * 8;   // 16-byte chunks per region
   constexpr int LX = (CX + NT - 1) / NT, LW = (CW + NT - 1) / NT, LA = (CA + NT - 1) / NT;
   static_assert(WTI % 32 == 0 && WTJ % 32 == 0 && (U16 || RP % 32 == 0), "32x32 fragments");
@@ -74,6 +77,9 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
   const __amdgpu_buffer_rsrc_t rsX = make_rsrc(X + (size_t)m0 * k, (uint64_t)min(BM, m - m0) * rowbytes);
   const __amdgpu_buffer_rsrc_t rsW = make_rsrc(W + (size_t)n0 * k, (uint64_t)min(BN, n - n0) * rowbytes);
   const __amdgpu_buffer_rsrc_t rsA = make_rsrc(A, (uint64_t)r * rowbytes);
+  const uint32_t kb8 = (uint32_t)k / 8;          // keep-mask bytes per row (k % 64 == 0 with dropout)
+  const __amdgpu_buffer_rsrc_t rsK = make_rsrc(DROP ? (const void*)(keep + (size_t)m0 * kb8) : (const void*)X,
+                                                DROP ? (uint64_t)min(BM, m - m0) * kb8 : 0);
 
   // Register staging of one k-block of the three regions: thread chunk
   // q = tid + i NT of a region is row q/8, k-chunk q%8 (coalesced 128-byte
@@ -82,8 +88,10 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
   // 3 = A rows.
   constexpr int LW1 = (LW + 1) / 2;
   int4v gx[LX], gw[LW], ga[LA];
+  uint2 gk = uint2{0u, 0u};   // keep bits of row tid for this k-block (dropout; tid < BM)
   auto gload = [&](int kb, int piece) {
     const int k0 = kb * 64;
+    if (DROP && piece == 0 && wave * 64 < BM) gk = buf_load8(rsK, (uint32_t)tid * kb8 + (uint32_t)kb * 8);
     if (piece == 0) {
 #pragma unroll
       for (int i = 0; i < LX; ++i) {
@@ -112,6 +120,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
   };
   auto swrite = [&](int buf, int piece) {
     char* sb = smem + buf * STAGE;
+    if (DROP && piece == 0 && wave * 64 < BM) *reinterpret_cast<uint2*>(sb + KS_OFF + tid * 8) = gk;
     if (piece == 0) {
 #pragma unroll
       for (int i = 0; i < LX; ++i) {
@@ -172,18 +181,27 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
     for (int fj = 0; fj < FJ; ++fj) fw[p][fj] = kc_read(Ws, wn * WTJ + 32 * fj + c32, ch);
 #pragma unroll
     for (int fi = 0; fi < FI; ++fi) fx[p][fi] = kc_read(Xs, wm * WTI + 32 * fi + c32, ch);
+    // Dropout acts on the U operand only (the W path reads X unmasked): each
+    // 8-k chunk of a row has one keep byte in the stage.
+    const uint8_t* Ks = reinterpret_cast<const uint8_t*>(sb + KS_OFF);
     if (U16) {
       if (ks % 2 == 0) {   // the 32-wide half starting at substep ks: chunks 2 ks + g16
         fa16[p] = kc_read(As, c16, 2 * ks + g16);
 #pragma unroll
-        for (int gg = 0; gg < GPW; ++gg) fxu16[p][gg] = kc_read(Xs, urow16[gg], 2 * ks + g16);
+        for (int gg = 0; gg < GPW; ++gg) {
+          fxu16[p][gg] = kc_read(Xs, urow16[gg], 2 * ks + g16);
+          if (DROP) fxu16[p][gg] = keep_mask8(fxu16[p][gg], Ks[urow16[gg] * 8 + 2 * ks + g16]);
+        }
       }
     } else if (ks % NDUP == 0) {
       const int uch = ch + 2 * udup;
 #pragma unroll
       for (int ft = 0; ft < FT; ++ft) fa[p][ft] = kc_read(As, 32 * ft + c32, uch);
 #pragma unroll
-      for (int fu = 0; fu < FUW; ++fu) fxu[p][fu] = kc_read(Xs, urow[fu], uch);
+      for (int fu = 0; fu < FUW; ++fu) {
+        fxu[p][fu] = kc_read(Xs, urow[fu], uch);
+        if (DROP) fxu[p][fu] = keep_mask8(fxu[p][fu], Ks[urow[fu] * 8 + uch]);
+      }
     }
   };
   auto multiply = [&](int p, int ks) {
@@ -272,11 +290,13 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
     const int q = tid + i * NT;
     bv[i] = buf_load16(rsB, q < nch ? (uint32_t)q * 16 : kOOB);
   }
+  // (with dropout the accumulated products are scaled by 1 / (1 - p) here)
+  const float uscale = DROP ? inv_keep : 1.0f;
   if (U16) {   // lane holds token column c16 of its group, U rows t = 4 g16 .. +3
 #pragma unroll
     for (int gg = 0; gg < GPW; ++gg)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) Us[urow16[gg] * RP + 4 * g16 + q] = uacc16[gg][q];
+      for (int q = 0; q < 4; ++q) Us[urow16[gg] * RP + 4 * g16 + q] = uscale * uacc16[gg][q];
   } else {
 #pragma unroll
     for (int fu = 0; fu < FUW; ++fu) {
@@ -286,7 +306,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
 #pragma unroll
         for (int q = 0; q < 16; ++q) {
           const int t = 32 * ft + 8 * (q >> 2) + 4 * g + (q & 3);
-          Us[(udup * BM + il) * RP + t] = uacc[ft][fu][q];
+          Us[(udup * BM + il) * RP + t] = uscale * uacc[ft][fu][q];
         }
     }
   }
@@ -378,27 +398,33 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
   }
 }
 
-template <int BM, int BN, int WM, int WN, int RP>
+template <int BM, int BN, int WM, int WN, int RP, bool DROP>
 static hipError_t launch_fwd_cfg(const FwdArgs& a, hipStream_t st) {
   const int tiles_m = (int)((a.m + BM - 1) / BM), tiles_n = (int)((a.n + BN - 1) / BN);
-  hipLaunchKernelGGL((lora_fwd_kernel<BM, BN, WM, WN, RP>), dim3(tiles_m * tiles_n), dim3(64 * WM * WN), 0, st,
-                     a.X, a.W, a.A, a.B, a.Y, a.U, (int)a.m, (int)a.n, (int)a.k, (int)a.r, a.s,
-                     tiles_m, tiles_n);
+  hipLaunchKernelGGL((lora_fwd_kernel<BM, BN, WM, WN, RP, DROP>), dim3(tiles_m * tiles_n), dim3(64 * WM * WN), 0,
+                     st, a.X, a.W, a.A, a.B, a.keep, a.Y, a.U, (int)a.m, (int)a.n, (int)a.k, (int)a.r, a.s,
+                     a.inv_keep, tiles_m, tiles_n);
   return hipGetLastError();
 }
 
-template <int BM, int BN, int WM, int WN>
+template <int BM, int BN, int WM, int WN, bool DROP>
 static hipError_t launch_fwd_rp(const FwdArgs& a, hipStream_t st) {
-  if (a.r <= 16) return launch_fwd_cfg<BM, BN, WM, WN, 16>(a, st);
-  if (a.r <= 32) return launch_fwd_cfg<BM, BN, WM, WN, 32>(a, st);
-  return launch_fwd_cfg<BM, BN, WM, WN, 64>(a, st);
+  if (a.r <= 16) return launch_fwd_cfg<BM, BN, WM, WN, 16, DROP>(a, st);
+  if (a.r <= 32) return launch_fwd_cfg<BM, BN, WM, WN, 32, DROP>(a, st);
+  return launch_fwd_cfg<BM, BN, WM, WN, 64, DROP>(a, st);
 }
 
+// With dropout the 256 x 256 tile is not used: its registers are already full.
 hipError_t launch_fwd(const FwdArgs& a, hipStream_t st) {
-  switch (choose_gemm_tile(a.m, a.n)) {
-    case TILE_256x256: return launch_fwd_rp<256, 256, 2, 4>(a, st);
-    case TILE_128x256: return launch_fwd_rp<128, 256, 2, 4>(a, st);
-    default: return launch_fwd_rp<128, 128, 2, 2>(a, st);
+  const GemmTile t = choose_gemm_tile(a.m, a.n);
+  if (a.keep) {
+    if (t == TILE_128x128) return launch_fwd_rp<128, 128, 2, 2, true>(a, st);
+    return launch_fwd_rp<128, 256, 2, 4, true>(a, st);
+  }
+  switch (t) {
+    case TILE_256x256: return launch_fwd_rp<256, 256, 2, 4, false>(a, st);
+    case TILE_128x256: return launch_fwd_rp<128, 256, 2, 4, false>(a, st);
+    default: return launch_fwd_rp<128, 128, 2, 2, false>(a, st);
   }
 }
 

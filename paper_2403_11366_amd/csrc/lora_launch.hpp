@@ -98,6 +98,8 @@ struct FwdArgs {
   float* U;
   int64_t m, n, k, r;
   float s;
+  const uint8_t* keep = nullptr;   // dropout keep bits [m][k/8], or none
+  float inv_keep = 1.0f;           // 1 / (1 - p)
 };
 
 struct BwdArgs {
@@ -108,6 +110,8 @@ struct BwdArgs {
   char* ws;
   int64_t m, n, k, r;
   float s;
+  const uint8_t* keep = nullptr;   // dropout keep bits [m][k/8], or none
+  float inv_keep = 1.0f;           // 1 / (1 - p)
 };
 
 struct MergeArgs {

@@ -164,3 +164,40 @@ def test_merge_misaligned_and_alias(lib):
     p = [addr(j) for j in range(4)]
     p[3] = p[2]               # W_out on top of B
     assert merge(lib, p) == 6
+
+
+def fwd_drop(lib, ptrs=None, p=0.05, m=64, n=64, k=64, r=8, alpha=16.0):
+    q = [addr(i) for i in range(7)] if ptrs is None else ptrs
+    return lib.lora_linear_fwd_dropout(q[0], q[1], q[2], q[3], q[4], p, q[5], q[6], m, n, k, r, alpha, None)
+
+
+def bwd_drop(lib, ptrs=None, p=0.05, m=64, n=64, k=64, r=8, alpha=16.0, ws_bytes=None):
+    q = [addr(i) for i in range(11)] if ptrs is None else ptrs
+    if ws_bytes is None:
+        ws_bytes = lora.lora_linear_bwd_workspace_size(m, n, k, r)
+    return lib.lora_linear_bwd_dropout(q[0], q[1], q[2], q[3], q[4], q[5], q[6], p, q[7], q[8], q[9], q[10],
+                                       ws_bytes, m, n, k, r, alpha, None)
+
+
+def test_dropout_validation(lib):
+    for i in range(7):
+        q = [addr(j) for j in range(7)]
+        q[i] = None
+        assert fwd_drop(lib, q) == 1
+    for p in (-0.1, 1.0, 2.0, float("nan")):
+        assert fwd_drop(lib, p=p) == 2
+        assert bwd_drop(lib, p=p) == 2
+    assert fwd_drop(lib, k=72) == 2          # k must be a multiple of 64 with dropout
+    assert bwd_drop(lib, k=72, ws_bytes=1 << 30) == 2
+    q = [addr(j) for j in range(7)]
+    q[4] += 8                                 # keep mask misaligned
+    assert fwd_drop(lib, q) == 3
+    q = [addr(j) for j in range(7)]
+    q[5] = q[4] + 64                          # Y on top of the keep mask
+    assert fwd_drop(lib, q) == 6
+    q = [addr(j) for j in range(11)]
+    q[6] = None
+    assert bwd_drop(lib, q) == 1
+    q = [addr(j) for j in range(11)]
+    q[7] = q[6]                               # dX on top of the keep mask
+    assert bwd_drop(lib, q) == 6

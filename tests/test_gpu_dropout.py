@@ -1,0 +1,87 @@
+"""GPU parity of the LoRA-dropout entry points (through the C ABI) against the
+fp64 oracle, with the keep mask drawn by the seeded input generator.
+
+Tolerances are those of the plain path (Y, dX 5e-3; dA, dB 1e-2; U 1e-5).
+Edge cases: every element kept with p = 0 (the forward and dA, dB then match
+the plain entry points bit for bit), nothing kept (U, dA and dB exactly zero,
+Y and dX the frozen path alone), ragged shapes and every padded rank.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from lora_synth import Shape, gen_inputs, gen_keep_mask
+from gpu_harness import TOL_DA, TOL_DB, TOL_DX, TOL_U, TOL_Y, f64, rel, run_gpu
+
+pytestmark = pytest.mark.gpu
+
+
+def run_dropout(t, shape, keep, p):
+    import torch
+    import paper_2403_11366_amd as lora
+    from paper_2403_11366_amd.device_io import bits_to_device, device_to_bits
+    m, n, k, r = shape.m, shape.n, shape.k, shape.r
+    d = {key: bits_to_device(v) for key, v in t.items()}
+    kd = torch.from_numpy(np.ascontiguousarray(keep)).cuda()
+    Y = torch.full((m, n), float("nan"), dtype=torch.bfloat16, device="cuda")
+    U = torch.full((m, r), float("nan"), dtype=torch.float32, device="cuda")
+    dX = torch.full((m, k), float("nan"), dtype=torch.bfloat16, device="cuda")
+    dA = torch.full((r, k), float("nan"), dtype=torch.float32, device="cuda")
+    dB = torch.full((n, r), float("nan"), dtype=torch.float32, device="cuda")
+    ws = torch.full((lora.lora_linear_bwd_workspace_size(m, n, k, r),), 0xFF, dtype=torch.uint8, device="cuda")
+    lora.lora_linear_fwd_dropout(d["X"], d["W"], d["A"], d["B"], kd, p, Y, U, shape.alpha)
+    lora.lora_linear_bwd_dropout(d["dY"], d["X"], d["W"], d["A"], d["B"], U, kd, p, dX, dA, dB, ws, shape.alpha)
+    torch.cuda.synchronize()
+    return {"Y": device_to_bits(Y), "U": U.cpu().numpy(), "dX": device_to_bits(dX),
+            "dA": dA.cpu().numpy(), "dB": dB.cpu().numpy()}
+
+
+def check(t, shape, keep, p, out):
+    U, Y = oracle.lora_forward_dropout(t["X"], t["W"], t["A"], t["B"], keep, p, shape.alpha)
+    _, dX, dA, dB = oracle.lora_backward_dropout(t["dY"], t["X"], t["W"], t["A"], t["B"], keep, p, shape.alpha)
+    e = {"Y": rel(f64(out["Y"]), Y), "U": rel(out["U"], U), "dX": rel(f64(out["dX"]), dX),
+         "dA": rel(out["dA"], dA), "dB": rel(out["dB"], dB)}
+    print(shape, p, {x: f"{v:.2e}" for x, v in e.items()}, flush=True)
+    assert e["Y"] <= TOL_Y and e["dX"] <= TOL_DX and e["dA"] <= TOL_DA and e["dB"] <= TOL_DB and e["U"] <= TOL_U
+    return e
+
+
+SHAPES = [Shape("drop_tiny", 256, 512, 512, 8, 16.0, 21), Shape("drop_ragged", 200, 264, 320, 5, 10.0, 22),
+          Shape("drop_r33", 130, 136, 192, 33, 66.0, 23), Shape("drop_r64", 264, 392, 448, 64, 128.0, 24),
+          Shape("drop_r16", 520, 1032, 640, 16, 32.0, 25)]
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: s.name)
+@pytest.mark.parametrize("p", [0.05, 0.5])
+def test_dropout_parity(shape, p):
+    t = gen_inputs(shape, b_std=0.3)
+    keep = gen_keep_mask(shape.m, shape.k, p, shape.seed + 7)
+    check(t, shape, keep, p, run_dropout(t, shape, keep, p))
+
+
+def test_dropout_full_size_q_proj():
+    shape = Shape("llama2_7b_q_proj", 2048, 4096, 4096, 8, 16.0, 1000)
+    t = gen_inputs(shape)
+    keep = gen_keep_mask(shape.m, shape.k, 0.05, 31)
+    check(t, shape, keep, 0.05, run_dropout(t, shape, keep, 0.05))
+
+
+def test_dropout_keep_all_matches_plain_path():
+    shape = Shape("drop_all_kept", 192, 256, 320, 12, 24.0, 26)
+    t = gen_inputs(shape, b_std=0.3)
+    keep = np.full((shape.m, shape.k // 8), 0xFF, dtype=np.uint8)
+    got = run_dropout(t, shape, keep, 0.0)
+    plain = run_gpu(t, shape)
+    for x in ("Y", "U", "dA", "dB"):
+        assert np.array_equal(got[x], plain[x]), x
+    assert rel(f64(got["dX"]), f64(plain["dX"])) <= 1e-3
+    check(t, shape, keep, 0.0, got)
+
+
+def test_dropout_keep_none():
+    shape = Shape("drop_none_kept", 136, 200, 256, 8, 16.0, 27)
+    t = gen_inputs(shape, b_std=0.3)
+    keep = np.zeros((shape.m, shape.k // 8), dtype=np.uint8)
+    out = run_dropout(t, shape, keep, 0.3)
+    assert not out["U"].any() and not out["dA"].any() and not out["dB"].any()
+    check(t, shape, keep, 0.3, out)
