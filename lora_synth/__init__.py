@@ -29,7 +29,7 @@ import numpy as np
 
 __all__ = [
     "Shape", "CONFIGS", "config_shapes", "round_to_bf16_bits", "bf16_bits_to_f32",
-    "gen_inputs", "gen_ternary_inputs", "gen_keep_mask",
+    "gen_inputs", "gen_ternary_inputs", "gen_keep_mask", "LAYER_GROUPS", "gen_group_inputs",
 ]
 
 
@@ -142,3 +142,20 @@ def gen_keep_mask(m: int, k: int, p: float, seed: int) -> np.ndarray:
     rng = np.random.default_rng(seed)
     keep = rng.random((m, k)) >= p
     return np.packbits(keep, axis=1, bitorder="little")
+
+
+# Projections of one decoder layer that read the same input: q, k, v (the
+# attention input) and gate, up (the MLP input); o and down stand alone.
+LAYER_GROUPS: Dict[str, List[List[int]]] = {"llama2_13b_layer": [[0, 1, 2], [3], [4, 5], [6]]}
+
+
+def gen_group_inputs(shapes: List[Shape], b_std: float = 0.02) -> Dict[str, object]:
+    """Inputs of projections that share one layer input: X is the first
+    projection's draw; W, A, B and dY of each projection come from its own
+    seeded draw (gen_inputs), so they equal the per-projection inputs.
+    Returns {"X": X, "W": [..], "A": [..], "B": [..], "dY": [..]}."""
+    s0 = shapes[0]
+    assert all(s.m == s0.m and s.k == s0.k and s.r == s0.r and s.alpha == s0.alpha for s in shapes)
+    per = [gen_inputs(s, b_std=b_std) for s in shapes]
+    return {"X": per[0]["X"], "W": [t["W"] for t in per], "A": [t["A"] for t in per],
+            "B": [t["B"] for t in per], "dY": [t["dY"] for t in per]}

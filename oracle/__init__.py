@@ -27,6 +27,10 @@ LoRA dropout (Listing 3's LORA_DROPOUT) acts on the adapter's input only:
 with a keep mask and rate p, D = keep * X / (1 - p), U = D A^T, and the
 backward carries the mask into dX's LoRA term and into dA = dU^T D.
 
+Grouped projections share one input X (query, key and value of an attention
+block): each has its own W_g, A_g, B_g and output Y_g, and the input gradient is
+the sum dX = sum_g (dY_g W_g + dU_g A_g).
+
 The merge of the adapter into the frozen weight (Eq. 1's second form,
 W0 x + B A x = (W0 + B A) x) is W + sign s B A, rounded once to bfloat16
 (nearest-even) for the stored result.
@@ -40,9 +44,11 @@ tests/test_oracle_pins.py.
 from .lora_oracle import (bf16_bits_to_f64, lora_scale, lora_rank_activation, lora_forward,
                           lora_backward, lora_forward_rows, lora_backward_rows, f64_to_bf16_bits,
                           f64_to_bf16_rne, lora_merged_weight, lora_merge_bf16, dropout_keep,
-                          dropped_input, lora_forward_dropout, lora_backward_dropout)
+                          dropped_input, lora_forward_dropout, lora_backward_dropout,
+                          lora_group_forward, lora_group_backward)
 
 __all__ = ["bf16_bits_to_f64", "lora_scale", "lora_rank_activation", "lora_forward",
            "lora_backward", "lora_forward_rows", "lora_backward_rows", "f64_to_bf16_bits",
            "f64_to_bf16_rne", "lora_merged_weight", "lora_merge_bf16", "dropout_keep",
-           "dropped_input", "lora_forward_dropout", "lora_backward_dropout"]
+           "dropped_input", "lora_forward_dropout", "lora_backward_dropout",
+           "lora_group_forward", "lora_group_backward"]

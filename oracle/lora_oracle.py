@@ -174,3 +174,35 @@ def lora_backward_rows(dY, X, W, A, B, alpha: float, rows: Optional[Sequence[int
     dB = s * (dY64.T @ U)
     dA = dU.T @ X64
     return dU, dX, dA, dB
+
+
+def lora_group_forward(X, Ws: Sequence, As: Sequence, Bs: Sequence, alpha: float
+                       ) -> Tuple[list, list]:
+    """G adapted projections that read one input X (the query, key and value
+    projections of an attention block; Section 3 adapts the query and value
+    projections): for each g, Eq. 1 with its own W_g, A_g, B_g and the shared
+    rank and alpha.  Returns ([U_g], [Y_g]) in float64."""
+    X = _f64(X)
+    outs = [lora_forward(X, W, A, B, alpha) for W, A, B in zip(Ws, As, Bs)]
+    return [u for u, _ in outs], [y for _, y in outs]
+
+
+def lora_group_backward(dYs: Sequence, X, Ws: Sequence, As: Sequence, Bs: Sequence, alpha: float,
+                        rows: Optional[Sequence[int]] = None) -> Tuple[list, np.ndarray, list, list]:
+    """Chain rule through lora_group_forward.  X feeds every projection, so its
+    gradient is the sum of the projections' contributions:
+        dX = sum_g (dY_g W_g + dU_g A_g),   dU_g = s dY_g B_g,
+        dB_g = s dY_g^T U_g,   dA_g = dU_g^T X.
+    With `rows`, dX is evaluated only at those token rows.  Returns
+    ([dU_g], dX, [dA_g], [dB_g]) in float64."""
+    X = _f64(X)
+    idx = np.arange(X.shape[0]) if rows is None else np.asarray(rows, dtype=np.int64)
+    dUs, dAs, dBs = [], [], []
+    dX = np.zeros((len(idx), X.shape[1]))
+    for dY, W, A, B in zip(dYs, Ws, As, Bs):
+        dU, dXg, dA, dB = lora_backward_rows(dY, X, W, A, B, alpha, idx)
+        dUs.append(dU)
+        dAs.append(dA)
+        dBs.append(dB)
+        dX = dX + dXg
+    return dUs, dX, dAs, dBs
