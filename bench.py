@@ -211,6 +211,95 @@ def bench_merge(args, shapes, stream):
     print(json.dumps(rec), flush=True)
 
 
+def bench_grouped(args, shapes, groups, stream):
+    """Train step of a decoder layer whose projections that read one input run
+    as a group (q, k, v and gate, up: lora_linear_group_fwd / _bwd, one forward
+    launch and one dX launch per group); the others run alone.  Same
+    algorithmic flops as the per-projection step."""
+    import torch
+    import paper_2403_11366_amd as lora
+    from paper_2403_11366_amd.device_io import bits_to_device
+    from lora_synth import gen_group_inputs
+    dev = "cuda"
+    per_set = sum(2 * (s.m * s.k + s.n * s.k + s.r * s.k + s.n * s.r + s.m * s.n) for s in shapes)
+    nsets = max(1, math.ceil(2 * MALL_BYTES / per_set))
+    log(f"[bench] {args.config} grouped {groups}: {nsets} input set(s)")
+    work = []
+    for members in groups:
+        gs = [shapes[i] for i in members]
+        s0 = gs[0]
+        t = gen_group_inputs(gs)
+        base = {"X": bits_to_device(t["X"], dev)}
+        for key in ("W", "A", "B", "dY"):
+            base[key] = [bits_to_device(v, dev) for v in t[key]]
+        sets = [base] + [{key: (v.clone() if key == "X" else [x.clone() for x in v]) for key, v in base.items()}
+                         for _ in range(nsets - 1)]
+        ns = [s.n for s in gs]
+        out = {"Y": [torch.empty((s0.m, n), dtype=torch.bfloat16, device=dev) for n in ns],
+               "U": [torch.empty((s0.m, s0.r), dtype=torch.float32, device=dev) for _ in ns],
+               "dX": torch.empty((s0.m, s0.k), dtype=torch.bfloat16, device=dev),
+               "dA": [torch.empty((s0.r, s0.k), dtype=torch.float32, device=dev) for _ in ns],
+               "dB": [torch.empty((n, s0.r), dtype=torch.float32, device=dev) for n in ns],
+               "ws": torch.empty(lora.lora_linear_group_bwd_workspace_size(ns, s0.m, s0.k, s0.r),
+                                 dtype=torch.uint8, device=dev)}
+        work.append((gs, sets, out))
+    torch.cuda.synchronize()
+
+    def fwd(i, gs, sets, out):
+        d = sets[i % len(sets)]
+        lora.lora_linear_group_fwd(d["X"], d["W"], d["A"], d["B"], out["Y"], out["U"], gs[0].alpha, stream=stream)
+
+    def bwd(i, gs, sets, out):
+        d = sets[i % len(sets)]
+        lora.lora_linear_group_bwd(d["dY"], d["X"], d["W"], d["A"], d["B"], out["U"], out["dX"], out["dA"],
+                                   out["dB"], out["ws"], gs[0].alpha, stream=stream)
+
+    def step(i):
+        for gs, sets, out in work:
+            fwd(i, gs, sets, out)
+            bwd(i, gs, sets, out)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(i)
+    torch.cuda.synchronize()
+    ms_per_step = (time.perf_counter() - t0) / args.steps * 1e3
+    flops = sum(s.flops_fwd_bwd for s in shapes)
+    tflops = flops / (ms_per_step / 1e3) / 1e12
+    log(f"[bench] grouped {ms_per_step * 1e3:.1f} us/step, {tflops:.1f} TFLOP/s")
+    # dominant kernel: the forward launch of the largest group, HIP events on its stream
+    gi = max(range(len(work)), key=lambda j: sum(s.n for s in work[j][0]))
+    gs, sets, out = work[gi]
+    reps = max(20, args.steps)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record(stream)
+    for i in range(reps):
+        fwd(i, gs, sets, out)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    fwd_us = ev0.elapsed_time(ev1) / reps * 1e3
+    m, k, r = gs[0].m, gs[0].k, gs[0].r
+    k1 = sum(2 * m * s.n * k + 2 * m * k * r + 2 * m * s.n * r for s in gs)
+    achieved = k1 / (fwd_us * 1e-6) / 1e12
+    rec = {
+        "metric": "LoRA-linear fwd+bwd TFLOP/s + % bf16 MFMA peak, Llama-2 layer with grouped projections, 1 GPU",
+        "value": round(tflops, 2), "unit": "TFLOP/s", "pct_bf16_mfma_peak": round(100 * tflops / PEAK_BF16_TFLOPS, 2),
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": args.config, "groups": [[shapes[i].name for i in g] for g in groups],
+                   "input_sets": nsets, "flops_per_step": flops},
+        "roofline": {"bound": "mfma", "kernel": "lora_fwd_kernel (group " + "+".join(s.name for s in gs) + ")",
+                     "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None, "flops_per_launch": k1,
+                     "avg_launch_us": round(fwd_us, 2)},
+        "cpu_baseline": None,
+    }
+    print(json.dumps(rec), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -228,6 +317,9 @@ def main():
     ap.add_argument("--dropout", type=float, default=None, metavar="P",
                     help="train with LoRA dropout at rate P on the adapter input (the *_dropout "
                          "entry points, a seeded keep mask per input set)")
+    ap.add_argument("--grouped", action="store_true",
+                    help="run the projections that read one input (q, k, v; gate, up) as groups "
+                         "(workloads with a layer grouping only)")
     ap.add_argument("--summarize-traffic", metavar="DIR", default=None,
                     help="write the HBM-traffic record from counter runs under DIR and exit")
     args = ap.parse_args()
@@ -267,6 +359,12 @@ def main():
     stream = torch.cuda.current_stream()
     if args.op == "merge":
         bench_merge(args, shapes, stream)
+        return
+    if args.grouped:
+        from lora_synth import LAYER_GROUPS
+        if args.config not in LAYER_GROUPS or args.dropout is not None:
+            sys.exit(f"--grouped needs a layer workload ({', '.join(LAYER_GROUPS)}) and no dropout")
+        bench_grouped(args, shapes, LAYER_GROUPS[args.config], stream)
         return
 
     # ---- inputs resident in HBM, rotated over enough copies to exceed the MALL

@@ -167,6 +167,64 @@ lora_status lora_linear_bwd_dropout(const lora_bf16* dY, const lora_bf16* X, con
 lora_status lora_linear_merge(const lora_bf16* W, const lora_bf16* A, const lora_bf16* B, lora_bf16* W_out,
                               int64_t n, int64_t k, int64_t r, float alpha, int sign, void* stream);
 
+/*
+ * Grouped forward of projections that read one input (the query, key and value
+ * projections of an attention block, or gate and up of an MLP; Section 3
+ * adapts the query and value projections): for g = 0 .. group-1,
+ *
+ *     U_g = X A_g^T,   Y_g = X W_g^T + (alpha/r) U_g B_g^T
+ *
+ *   X       [m, k] device, shared input (bf16), read only
+ *   group   number of projections, 1 .. 8 (0 or less: LORA_ERR_SHAPE; more than
+ *           8: LORA_ERR_UNSUPPORTED)
+ *   n       HOST array [group]: output features n_g of each projection (the
+ *           shape rules above apply to each; their sum is at most 2^22)
+ *   W, A, B HOST arrays [group] of device pointers: W_g [n_g, k], A_g [r, k],
+ *           B_g [n_g, r] (bf16), read only
+ *   Y, U    HOST arrays [group] of device pointers: Y_g [m, n_g] (bf16) and
+ *           U_g [m, r] (fp32), written
+ *   r, alpha  one rank and alpha for the group
+ * One kernel launch: the output tiles of all projections form one grid, so the
+ * group fills the chip as one problem of m x (sum of n_g) outputs.  Each Y_g,
+ * U_g equals what lora_linear_fwd computes for projection g.  No output may
+ * overlap any input or another output.
+ */
+lora_status lora_linear_group_fwd(const lora_bf16* X, int64_t group, const int64_t* n,
+                                  const lora_bf16* const* W, const lora_bf16* const* A,
+                                  const lora_bf16* const* B, lora_bf16* const* Y, float* const* U,
+                                  int64_t m, int64_t k, int64_t r, float alpha, void* stream);
+
+/*
+ * Bytes of device workspace lora_linear_group_bwd needs (0 on invalid
+ * arguments): the sum over the group of each projection's backward workspace.
+ */
+size_t lora_linear_group_bwd_workspace_size(int64_t group, const int64_t* n, int64_t m, int64_t k, int64_t r);
+
+/*
+ * Backward of lora_linear_group_fwd.  X feeds every projection, so its
+ * gradient is the sum of their contributions:
+ *
+ *     dX = sum_g (dY_g W_g + dU_g A_g),   dU_g = s dY_g B_g,
+ *     dB_g = s dY_g^T U_g,   dA_g = dU_g^T X
+ *
+ *   dY      HOST array [group] of device pointers dY_g [m, n_g] (bf16), read only
+ *   X, group, n, W, A, B, r, alpha   as in lora_linear_group_fwd
+ *   U       HOST array [group] of device pointers: the forward's U_g [m, r] (fp32)
+ *   dX      [m, k] device (bf16), written: the summed input gradient
+ *   dA, dB  HOST arrays [group] of device pointers dA_g [r, k], dB_g [n_g, r]
+ *           (fp32), written
+ *   workspace  at least lora_linear_group_bwd_workspace_size(...) bytes, 16-byte
+ *              aligned, not used concurrently by another call
+ * dX is one matrix-core GEMM over the concatenated contraction of all
+ * projections (one bf16 rounding of the whole sum); dA_g and dB_g equal what
+ * lora_linear_bwd computes for projection g.
+ */
+lora_status lora_linear_group_bwd(const lora_bf16* const* dY, const lora_bf16* X, int64_t group, const int64_t* n,
+                                  const lora_bf16* const* W, const lora_bf16* const* A,
+                                  const lora_bf16* const* B, const float* const* U, lora_bf16* dX,
+                                  float* const* dA, float* const* dB, void* workspace, size_t workspace_bytes,
+                                  int64_t m, int64_t k, int64_t r, float alpha, void* stream);
+
 /* Static, human-readable name of a status code. */
 const char* lora_status_string(lora_status s);
 

@@ -17,6 +17,7 @@ from typing import Optional
 __all__ = [
     "LoraError", "lib_path", "load_library", "lora_linear_fwd", "lora_linear_bwd",
     "lora_linear_bwd_workspace_size", "lora_linear_merge", "lora_linear_fwd_dropout", "lora_linear_bwd_dropout",
+    "lora_linear_group_fwd", "lora_linear_group_bwd", "lora_linear_group_bwd_workspace_size",
     "lora_status_string", "STATUS",
 ]
 
@@ -60,6 +61,14 @@ def load_library() -> ctypes.CDLL:
     lib.lora_linear_bwd_dropout.restype = ctypes.c_int
     lib.lora_linear_merge.argtypes = [p, p, p, p, i64, i64, i64, f32, ctypes.c_int, p]
     lib.lora_linear_merge.restype = ctypes.c_int
+    pa = ctypes.POINTER(ctypes.c_void_p)
+    pn = ctypes.POINTER(ctypes.c_int64)
+    lib.lora_linear_group_fwd.argtypes = [p, i64, pn, pa, pa, pa, pa, pa, i64, i64, i64, f32, p]
+    lib.lora_linear_group_fwd.restype = ctypes.c_int
+    lib.lora_linear_group_bwd_workspace_size.argtypes = [i64, pn, i64, i64, i64]
+    lib.lora_linear_group_bwd_workspace_size.restype = sz
+    lib.lora_linear_group_bwd.argtypes = [pa, p, i64, pn, pa, pa, pa, pa, p, pa, pa, p, sz, i64, i64, i64, f32, p]
+    lib.lora_linear_group_bwd.restype = ctypes.c_int
     lib.lora_status_string.argtypes = [ctypes.c_int]
     lib.lora_status_string.restype = ctypes.c_char_p
     _lib = lib
@@ -204,3 +213,67 @@ def lora_linear_bwd_dropout(dY, X, W, A, B, U, keep, p: float, dX, dA, dB, works
                                                 m, n, k, r, float(alpha), _stream_handle(stream))
     if st != 0:
         raise LoraError(st, "lora_linear_bwd_dropout")
+
+
+def _ptr_array(ts):
+    return (ctypes.c_void_p * len(ts))(*[_ptr(t) for t in ts])
+
+
+def _n_array(ns):
+    return (ctypes.c_int64 * len(ns))(*[int(n) for n in ns])
+
+
+def lora_linear_group_bwd_workspace_size(ns, m: int, k: int, r: int) -> int:
+    return int(load_library().lora_linear_group_bwd_workspace_size(len(ns), _n_array(ns), m, k, r))
+
+
+def lora_linear_group_fwd(X, Ws, As, Bs, Ys, Us, alpha: float, stream=None) -> None:
+    """Projections g that read one X: U_g = X A_g^T, Y_g = X W_g^T + (alpha/r) U_g B_g^T,
+    in one launch.  X [m,k], W_g [n_g,k], A_g [r,k], B_g [n_g,r], Y_g [m,n_g]:
+    torch.bfloat16; U_g [m,r]: torch.float32."""
+    import torch
+    m, k = X.shape
+    r = As[0].shape[0]
+    ns = [W.shape[0] for W in Ws]
+    if not (len(Ws) == len(As) == len(Bs) == len(Ys) == len(Us)):
+        raise ValueError("group: W, A, B, Y, U lists must have the same length")
+    _check(X, "X", torch.bfloat16, (m, k))
+    for g, n in enumerate(ns):
+        for t, name, dt, shp in ((Ws[g], "W", torch.bfloat16, (n, k)), (As[g], "A", torch.bfloat16, (r, k)),
+                                 (Bs[g], "B", torch.bfloat16, (n, r)), (Ys[g], "Y", torch.bfloat16, (m, n)),
+                                 (Us[g], "U", torch.float32, (m, r))):
+            _check(t, f"{name}[{g}]", dt, shp)
+    st = load_library().lora_linear_group_fwd(_ptr(X), len(ns), _n_array(ns), _ptr_array(Ws), _ptr_array(As),
+                                              _ptr_array(Bs), _ptr_array(Ys), _ptr_array(Us), m, k, r,
+                                              float(alpha), _stream_handle(stream))
+    if st != 0:
+        raise LoraError(st, "lora_linear_group_fwd")
+
+
+def lora_linear_group_bwd(dYs, X, Ws, As, Bs, Us, dX, dAs, dBs, workspace, alpha: float, stream=None) -> None:
+    """Backward of lora_linear_group_fwd: dX = sum_g (dY_g W_g + dU_g A_g),
+    dA_g = dU_g^T X, dB_g = s dY_g^T U_g with dU_g = s dY_g B_g.  workspace: a
+    device tensor of at least lora_linear_group_bwd_workspace_size(n, m, k, r) bytes."""
+    import torch
+    m, k = X.shape
+    r = As[0].shape[0]
+    ns = [W.shape[0] for W in Ws]
+    if not (len(dYs) == len(Ws) == len(As) == len(Bs) == len(Us) == len(dAs) == len(dBs)):
+        raise ValueError("group: dY, W, A, B, U, dA, dB lists must have the same length")
+    _check(X, "X", torch.bfloat16, (m, k))
+    _check(dX, "dX", torch.bfloat16, (m, k))
+    for g, n in enumerate(ns):
+        for t, name, dt, shp in ((dYs[g], "dY", torch.bfloat16, (m, n)), (Ws[g], "W", torch.bfloat16, (n, k)),
+                                 (As[g], "A", torch.bfloat16, (r, k)), (Bs[g], "B", torch.bfloat16, (n, r)),
+                                 (Us[g], "U", torch.float32, (m, r)), (dAs[g], "dA", torch.float32, (r, k)),
+                                 (dBs[g], "dB", torch.float32, (n, r))):
+            _check(t, f"{name}[{g}]", dt, shp)
+    if workspace.device.type != "cuda" or not workspace.is_contiguous():
+        raise ValueError("workspace: must be a contiguous device tensor")
+    ws_bytes = workspace.numel() * workspace.element_size()
+    st = load_library().lora_linear_group_bwd(_ptr_array(dYs), _ptr(X), len(ns), _n_array(ns), _ptr_array(Ws),
+                                              _ptr_array(As), _ptr_array(Bs), _ptr_array(Us), _ptr(dX),
+                                              _ptr_array(dAs), _ptr_array(dBs), _ptr(workspace), ws_bytes,
+                                              m, k, r, float(alpha), _stream_handle(stream))
+    if st != 0:
+        raise LoraError(st, "lora_linear_group_bwd")

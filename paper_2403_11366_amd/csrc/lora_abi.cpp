@@ -35,6 +35,48 @@ lora_status check_shape(int64_t m, int64_t n, int64_t k, int64_t r) {
   return LORA_OK;
 }
 
+// True if any output range overlaps an input range or another output range.
+bool any_alias(const Range* out, int n_out, const Range* in, int n_in) {
+  for (int i = 0; i < n_out; ++i) {
+    for (int j = 0; j < n_in; ++j)
+      if (overlap(out[i], in[j])) return true;
+    for (int j = i + 1; j < n_out; ++j)
+      if (overlap(out[i], out[j])) return true;
+  }
+  return false;
+}
+
+// Shape checks of a group of projections sharing X: the count, the host
+// array of output widths and each projection's shape.
+lora_status check_group(int64_t group, const int64_t* n, int64_t m, int64_t k, int64_t r) {
+  if (!n) return LORA_ERR_NULL;
+  if (group < 1) return LORA_ERR_SHAPE;
+  if (group > lora::kMaxGroup) return LORA_ERR_UNSUPPORTED;
+  int64_t total = 0;
+  for (int64_t g = 0; g < group; ++g) {
+    const lora_status st = check_shape(m, n[g], k, r);
+    if (st != LORA_OK) return st;
+    total += n[g];
+  }
+  if (total > kMaxDim) return LORA_ERR_UNSUPPORTED;
+  return LORA_OK;
+}
+
+template <typename T>
+bool all_set(const T* const* p, int64_t group) {
+  if (!p) return false;
+  for (int64_t g = 0; g < group; ++g)
+    if (!p[g]) return false;
+  return true;
+}
+
+template <typename T>
+bool all_aligned(const T* const* p, int64_t group) {
+  for (int64_t g = 0; g < group; ++g)
+    if (!aligned16(p[g])) return false;
+  return true;
+}
+
 }  // namespace
 
 extern "C" {
@@ -181,6 +223,95 @@ lora_status lora_linear_merge(const lora_bf16* W, const lora_bf16* A, const lora
 
   lora::MergeArgs a{W, A, B, W_out, n, k, r, (float)sign * ((float)alpha / (float)r)};
   hipError_t e = lora::launch_merge(a, reinterpret_cast<hipStream_t>(stream));
+  return e == hipSuccess ? LORA_OK : LORA_ERR_HIP;
+}
+
+lora_status lora_linear_group_fwd(const lora_bf16* X, int64_t group, const int64_t* n,
+                                  const lora_bf16* const* W, const lora_bf16* const* A,
+                                  const lora_bf16* const* B, lora_bf16* const* Y, float* const* U,
+                                  int64_t m, int64_t k, int64_t r, float alpha, void* stream) {
+  if (!X || !n) return LORA_ERR_NULL;
+  lora_status st = check_group(group, n, m, k, r);
+  if (st != LORA_OK) return st;
+  if (!all_set(W, group) || !all_set(A, group) || !all_set(B, group) || !all_set(Y, group) || !all_set(U, group))
+    return LORA_ERR_NULL;
+  if (!aligned16(X) || !all_aligned(W, group) || !all_aligned(A, group) || !all_aligned(B, group) ||
+      !all_aligned(Y, group) || !all_aligned(U, group))
+    return LORA_ERR_ALIGN;
+  Range in[1 + 3 * lora::kMaxGroup], out[2 * lora::kMaxGroup];
+  int ni = 0, no = 0;
+  in[ni++] = span(X, m, k, 2);
+  for (int64_t g = 0; g < group; ++g) {
+    in[ni++] = span(W[g], n[g], k, 2);
+    in[ni++] = span(A[g], r, k, 2);
+    in[ni++] = span(B[g], n[g], r, 2);
+    out[no++] = span(Y[g], m, n[g], 2);
+    out[no++] = span(U[g], m, r, 4);
+  }
+  if (any_alias(out, no, in, ni)) return LORA_ERR_ALIAS;
+
+  lora::GroupFwdArgs a{};
+  a.X = X;
+  a.count = (int)group;
+  for (int64_t g = 0; g < group; ++g) {
+    a.n[g] = n[g]; a.W[g] = W[g]; a.A[g] = A[g]; a.B[g] = B[g]; a.Y[g] = Y[g]; a.U[g] = U[g];
+  }
+  a.m = m; a.k = k; a.r = r; a.s = (float)alpha / (float)r;
+  hipError_t e = lora::launch_fwd_group(a, reinterpret_cast<hipStream_t>(stream));
+  return e == hipSuccess ? LORA_OK : LORA_ERR_HIP;
+}
+
+size_t lora_linear_group_bwd_workspace_size(int64_t group, const int64_t* n, int64_t m, int64_t k, int64_t r) {
+  if (check_group(group, n, m, k, r) != LORA_OK) return 0;
+  return lora::group_bwd_layout((int)group, n, m, k, r).total;
+}
+
+lora_status lora_linear_group_bwd(const lora_bf16* const* dY, const lora_bf16* X, int64_t group, const int64_t* n,
+                                  const lora_bf16* const* W, const lora_bf16* const* A,
+                                  const lora_bf16* const* B, const float* const* U, lora_bf16* dX,
+                                  float* const* dA, float* const* dB, void* workspace, size_t workspace_bytes,
+                                  int64_t m, int64_t k, int64_t r, float alpha, void* stream) {
+  if (!X || !n || !dX) return LORA_ERR_NULL;
+  lora_status st = check_group(group, n, m, k, r);
+  if (st != LORA_OK) return st;
+  if (!all_set(dY, group) || !all_set(W, group) || !all_set(A, group) || !all_set(B, group) ||
+      !all_set(U, group) || !all_set(dA, group) || !all_set(dB, group))
+    return LORA_ERR_NULL;
+  if (!aligned16(X) || !aligned16(dX) || !all_aligned(dY, group) || !all_aligned(W, group) ||
+      !all_aligned(A, group) || !all_aligned(B, group) || !all_aligned(U, group) || !all_aligned(dA, group) ||
+      !all_aligned(dB, group))
+    return LORA_ERR_ALIGN;
+  const size_t need = lora::group_bwd_layout((int)group, n, m, k, r).total;
+  if (!workspace || workspace_bytes < need) return LORA_ERR_WORKSPACE;
+  if (!aligned16(workspace)) return LORA_ERR_ALIGN;
+
+  Range in[1 + 5 * lora::kMaxGroup], out[2 + 2 * lora::kMaxGroup];
+  int ni = 0, no = 0;
+  in[ni++] = span(X, m, k, 2);
+  out[no++] = span(dX, m, k, 2);
+  out[no++] = Range{reinterpret_cast<uintptr_t>(workspace), reinterpret_cast<uintptr_t>(workspace) + need};
+  for (int64_t g = 0; g < group; ++g) {
+    in[ni++] = span(dY[g], m, n[g], 2);
+    in[ni++] = span(W[g], n[g], k, 2);
+    in[ni++] = span(A[g], r, k, 2);
+    in[ni++] = span(B[g], n[g], r, 2);
+    in[ni++] = span(U[g], m, r, 4);
+    out[no++] = span(dA[g], r, k, 4);
+    out[no++] = span(dB[g], n[g], r, 4);
+  }
+  if (any_alias(out, no, in, ni)) return LORA_ERR_ALIAS;
+
+  lora::GroupBwdArgs a{};
+  a.X = X;
+  a.count = (int)group;
+  for (int64_t g = 0; g < group; ++g) {
+    a.n[g] = n[g]; a.dY[g] = dY[g]; a.W[g] = W[g]; a.A[g] = A[g]; a.B[g] = B[g]; a.U[g] = U[g];
+    a.dA[g] = dA[g]; a.dB[g] = dB[g];
+  }
+  a.dX = dX;
+  a.ws = static_cast<char*>(workspace);
+  a.m = m; a.k = k; a.r = r; a.s = (float)alpha / (float)r;
+  hipError_t e = lora::launch_bwd_group(a, reinterpret_cast<hipStream_t>(stream));
   return e == hipSuccess ? LORA_OK : LORA_ERR_HIP;
 }
 

@@ -362,6 +362,32 @@ __device__ __forceinline__ void finalize_partials(const FinalizeArgs& f, int fir
   }
 }
 
+// Element q of a per-projection argument array (q uniform); compile-time
+// indices only, so the kernel argument is never indexed dynamically.
+template <typename T>
+__device__ __forceinline__ T pick(const T (&v)[kMaxGroup], int q) {
+  T x = v[0];
+#pragma unroll
+  for (int i = 1; i < kMaxGroup; ++i)
+    if (q == i) x = v[i];
+  return x;
+}
+
+// Kernel argument (by value) of the grouped dX GEMM of projections that read
+// one X: dX = sum_g (dY_g W_g + dU_g A_g).  The n stages of every projection
+// run back to back in one k loop (ceil(n_g / 64) stages each, nkb in all);
+// the rank-r terms dU_g A_g are added after the loop,
+// and the workgroup tails finalize every projection's dA_g and dB_g.
+struct DxGroup {
+  const u16* dY[kMaxGroup];
+  const u16* W[kMaxGroup];
+  const u16* dU2[kMaxGroup];
+  const u16* A[kMaxGroup];
+  int n[kMaxGroup];
+  int count, nkb;
+  FinalizeArgs fin[kMaxGroup];
+};
+
 // ---------------------------------------------------------------------------
 // dX tile of BM tokens x BN input features, formed as dX^T = W^T dY^T with
 // v_mfma_f32_32x32x16_bf16 (W as the A operand, dY as the B operand).  Stages
@@ -377,11 +403,15 @@ __device__ __forceinline__ void finalize_partials(const FinalizeArgs& f, int fir
 // are skipped; after the n stages the tile's dU2 rows, A columns and keep bits
 // are staged in LDS, dU A is formed per fragment into a temporary
 // accumulator, and added under the mask with the 1 / (1 - p) scale.
-template <int BM, int BN, int WM, int WN, int RP, bool DROP>
+//
+// With GRP (DxGroup) the n stages of all projections of a group form the k
+// loop, each stage loading from its own projection's dY_g and W_g; the slab
+// stages are skipped and each dU_g A_g is added after the loop from LDS.
+template <int BM, int BN, int WM, int WN, int RP, bool DROP, bool GRP>
 __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
     const u16* __restrict__ dY, const u16* __restrict__ W, const u16* __restrict__ dU2,
     const u16* __restrict__ A, const uint8_t* __restrict__ keep, u16* __restrict__ dX, int m, int n, int k,
-    int r, int mp, float inv_keep, int tiles_m, int tiles_n, FinalizeArgs fin) {
+    int r, int mp, float inv_keep, int tiles_m, int tiles_n, FinalizeArgs fin, DxGroup grp) {
   constexpr int NW = WM * WN;
   constexpr int NT = 64 * NW;
   constexpr int WTI = BM / WM, WTJ = BN / WN;
@@ -410,7 +440,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
   const __amdgpu_buffer_rsrc_t rsY = make_rsrc(dY + (size_t)m0 * n, (uint64_t)min(BM, m - m0) * yrow);
   const __amdgpu_buffer_rsrc_t rsU = make_rsrc(dU2 + (size_t)m0 * KS2, (uint64_t)min(BM, mp - m0) * urow);
   const __amdgpu_buffer_rsrc_t rsA = make_rsrc(A, (uint64_t)r * wrow);
-  const int nkb = (n + 63) / 64;
+  const int nkb = GRP ? grp.nkb : (n + 63) / 64;
 
   // Staging registers move in pieces, one per 16-wide substep of the stage
   // that stores them: 0 = the dY (or dU2) rows, 1 and 2 = the two halves of
@@ -419,18 +449,46 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
   int4v gy[LY], gw[LW];
   // Loads of W stage st (dY columns and W rows st*64 ..) and of slab stage sl
   // (dU2 columns and the matching A rows, high part then low part).
+  // With GRP the stages are loaded in order (piece 0 of a stage first), so a
+  // load cursor -- projection, its stage, its dY rows -- advances by one stage
+  // at each piece 0 and switches projection only at a boundary.
+  int cur_g = 0, cur_sl = -1, cur_n = GRP ? grp.n[0] : n;
+  const u16* cur_W = GRP ? grp.W[0] : W;
+  uint32_t cur_yr = GRP ? (uint32_t)grp.n[0] * 2 : yrow;
+  __amdgpu_buffer_rsrc_t cur_rsY =
+      GRP ? make_rsrc(grp.dY[0] + (size_t)m0 * grp.n[0], (uint64_t)min(BM, m - m0) * cur_yr) : rsY;
   auto gload_w = [&](int st, int piece) {
-    const int n0 = st * 64;
+    const u16* Wp = W;
+    int ns = n, sl = st;
+    if (GRP) {
+      if (piece == 0) {
+        ++cur_sl;
+        if (cur_sl * 64 >= cur_n) {   // next projection (uniform, taken count - 1 times)
+          ++cur_g;
+          cur_sl = 0;
+          cur_n = pick(grp.n, cur_g);
+          cur_W = pick(grp.W, cur_g);
+          cur_yr = (uint32_t)cur_n * 2;
+          cur_rsY = make_rsrc(pick(grp.dY, cur_g) + (size_t)m0 * cur_n, (uint64_t)min(BM, m - m0) * cur_yr);
+        }
+      }
+      Wp = cur_W;
+      ns = cur_n;
+      sl = cur_sl;
+    }
+    const int n0 = sl * 64;
     if (piece == 0) {
+      const uint32_t yr = GRP ? cur_yr : yrow;
+      const __amdgpu_buffer_rsrc_t rsYs = GRP ? cur_rsY : rsY;
 #pragma unroll
       for (int i = 0; i < LY; ++i) {
         const int q = tid + i * NT;
         if (CY % NT != 0 && wave * 64 + i * NT >= CY) break;   // wave-uniform
         const int nn = n0 + 8 * (q & 7);
-        gy[i] = buf_load16(rsY, nn < n ? (uint32_t)(q >> 3) * yrow + (uint32_t)nn * 2 : kOOB);
+        gy[i] = buf_load16(rsYs, nn < ns ? (uint32_t)(q >> 3) * yr + (uint32_t)nn * 2 : kOOB);
       }
     } else if (piece <= 2) {
-      const __amdgpu_buffer_rsrc_t rsW = make_rsrc(W + (size_t)n0 * k, (uint64_t)min(64, n - n0) * wrow);
+      const __amdgpu_buffer_rsrc_t rsW = make_rsrc(Wp + (size_t)n0 * k, (uint64_t)min(64, ns - n0) * wrow);
 #pragma unroll
       for (int i = piece == 1 ? 0 : LW1; i < (piece == 1 ? LW1 : LW); ++i) {
         const int q = tid + i * NT;
@@ -540,7 +598,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
 #pragma unroll
   for (int pc = 0; pc < 3; ++pc) swrite(0, pc);
   __syncthreads();
-  constexpr int NSL = DROP ? 0 : NSLAB;   // slab stages in the k loop
+  constexpr int NSL = (DROP || GRP) ? 0 : NSLAB;   // slab stages in the k loop
   int st = 0;
   if (nkb >= 2) {
 #pragma unroll
@@ -555,6 +613,48 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
   if (NSL > 1) stage(st++, true, LD_NONE);                     // writes slab 1
   stage(st, false, LD_NONE);
   if (ROT) multiply(1);
+
+  if (GRP) {
+    // LDS after the k loop, per projection: Us2 [BM][UP] bf16 (dU_g high |
+    // low of the tile's tokens), As2 [RP][BN] bf16 mn-contiguous (A_g rows,
+    // zero beyond r and k).  acc += [dU_hi | dU_lo] [A_g; A_g].
+    constexpr int UP = 2 * RP + 8;
+    constexpr int US_BYTES = BM * UP * 2, AS_BYTES = RP * BN * 2;
+    static_assert(US_BYTES + AS_BYTES <= 2 * STAGE, "group epilogue fits the stage LDS");
+    u16* Us2 = reinterpret_cast<u16*>(smem);
+    char* As2 = smem + US_BYTES;
+    for (int pq = 0; pq < grp.count; ++pq) {
+      if (pq > 0) __syncthreads();                  // the previous projection's reads are done
+      const __amdgpu_buffer_rsrc_t rsU2 =
+          make_rsrc(pick(grp.dU2, pq) + (size_t)m0 * KS2, (uint64_t)min(BM, mp - m0) * urow);
+      const __amdgpu_buffer_rsrc_t rsAq = make_rsrc(pick(grp.A, pq), (uint64_t)r * wrow);
+      constexpr int UCH = BM * (RP / 4);            // 16-byte chunks of the dU2 rows
+      for (int q = tid; q < UCH; q += NT) {
+        const int i = q / (RP / 4), c = q % (RP / 4);
+        *reinterpret_cast<int4v*>(Us2 + i * UP + 8 * c) = buf_load16(rsU2, (uint32_t)i * urow + (uint32_t)c * 16);
+      }
+      constexpr int ACH = RP * (BN / 8);
+      for (int q = tid; q < ACH; q += NT) {
+        const int t = q / (BN / 8), c = q % (BN / 8);
+        const int ll = l0 + 8 * c;
+        *reinterpret_cast<int4v*>(As2 + mc32_offset<BN>(t, c)) =
+            buf_load16(rsAq, (t < r && ll < k) ? (uint32_t)t * wrow + (uint32_t)ll * 2 : kOOB);
+      }
+      __syncthreads();
+#pragma unroll
+      for (int fj = 0; fj < FJ; ++fj)
+#pragma unroll
+        for (int kk = 0; kk < KS2 / 16; ++kk) {
+          const short8 af = mc32_read_tr<BN>(As2, (16 * kk) % RP, wn * WTJ + 32 * fj, lane);
+#pragma unroll
+          for (int fi = 0; fi < FI; ++fi) {
+            const short8 bf =
+                *reinterpret_cast<const short8*>(Us2 + (wm * WTI + 32 * fi + c32) * UP + 16 * kk + 8 * g);
+            acc[fj][fi] = mfma32x32x16(af, bf, acc[fj][fi]);
+          }
+        }
+    }
+  }
 
   if (DROP) {
     // LDS after the k loop: Us2 [BM][UP] bf16 (dU high | low of the tile's
@@ -639,23 +739,31 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
   }
   // After its tile, every workgroup sums a slice of the dA, dB partials
   // (complete: the token reductions ran before this launch in stream order).
-  finalize_partials(fin, (int)blockIdx.x * NT + (int)threadIdx.x, (int)gridDim.x * NT);
+  const int first = (int)blockIdx.x * NT + (int)threadIdx.x, stride = (int)gridDim.x * NT;
+  if (GRP) {
+    for (int pq = 0; pq < grp.count; ++pq) finalize_partials(pick(grp.fin, pq), first, stride);
+  } else {
+    finalize_partials(fin, first, stride);
+  }
 }
 
 // ---------------------------------------------------------------------------
-template <int BM, int BN, int WM, int WN, int RP, bool DROP>
-static hipError_t launch_dx_cfg(const BwdArgs& a, const BwdLayout& L, const FinalizeArgs& fin, hipStream_t st) {
+template <int BM, int BN, int WM, int WN, int RP, bool DROP, bool GRP>
+static hipError_t launch_dx_cfg(const BwdArgs& a, const BwdLayout& L, const FinalizeArgs& fin, const DxGroup& grp,
+                                hipStream_t st) {
   const int tiles_m = (int)((a.m + BM - 1) / BM), tiles_n = (int)((a.k + BN - 1) / BN);
   const int nt = 64 * WM * WN;
-  hipLaunchKernelGGL((lora_bwd_dx_kernel<BM, BN, WM, WN, RP, DROP>), dim3(tiles_m * tiles_n), dim3(nt), 0, st,
-                     a.dY, a.W, reinterpret_cast<const u16*>(a.ws + L.du2), a.A, a.keep, a.dX, (int)a.m, (int)a.n,
-                     (int)a.k, (int)a.r, (int)L.mp, a.inv_keep, tiles_m, tiles_n, fin);
+  const u16* dU2 = GRP ? nullptr : reinterpret_cast<const u16*>(a.ws + L.du2);
+  hipLaunchKernelGGL((lora_bwd_dx_kernel<BM, BN, WM, WN, RP, DROP, GRP>), dim3(tiles_m * tiles_n), dim3(nt), 0, st,
+                     a.dY, a.W, dU2, a.A, a.keep, a.dX, (int)a.m, (int)a.n, (int)a.k, (int)a.r, (int)L.mp,
+                     a.inv_keep, tiles_m, tiles_n, fin, grp);
   return hipGetLastError();
 }
 
+// dU (and the U^T, dU^T splits), then the dB and dA partials of one projection.
 template <int RP>
-static hipError_t launch_bwd_rp(const BwdArgs& a, const BwdLayout& L, hipStream_t st) {
-  const int m = (int)a.m, n = (int)a.n, k = (int)a.k, r = (int)a.r, mp = (int)L.mp;
+static hipError_t launch_du_tokred(const BwdArgs& a, const BwdLayout& L, hipStream_t st) {
+  const int m = (int)a.m, n = (int)a.n, r = (int)a.r, mp = (int)L.mp;
   u16* Ut2 = reinterpret_cast<u16*>(a.ws + L.ut2);
   u16* dU2 = reinterpret_cast<u16*>(a.ws + L.du2);
   u16* dUt2 = reinterpret_cast<u16*>(a.ws + L.dut2);
@@ -667,30 +775,37 @@ static hipError_t launch_bwd_rp(const BwdArgs& a, const BwdLayout& L, hipStream_
                      mp, a.s);
   if ((e = hipGetLastError()) != hipSuccess) return e;
 
-  {
-    const RedProblem pbp{Ut2, a.dY, pb, n, (int)L.plan_b.span, L.plan_b.col_tiles, nullptr};
-    const RedProblem pap{dUt2, a.X, pa, k, (int)L.plan_a.span, L.plan_a.col_tiles, a.keep};
-    const int nb0 = L.plan_b.col_tiles * L.plan_b.splits;
-    const int nb1 = L.plan_a.col_tiles * L.plan_a.splits;
-    hipLaunchKernelGGL((lora_tokred_kernel<RP>), dim3(nb0 + nb1), dim3(256), 0, st, pbp, pap, nb0, m, mp);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-  }
+  const RedProblem pbp{Ut2, a.dY, pb, n, (int)L.plan_b.span, L.plan_b.col_tiles, nullptr};
+  const RedProblem pap{dUt2, a.X, pa, (int)a.k, (int)L.plan_a.span, L.plan_a.col_tiles, a.keep};
+  const int nb0 = L.plan_b.col_tiles * L.plan_b.splits;
+  const int nb1 = L.plan_a.col_tiles * L.plan_a.splits;
+  hipLaunchKernelGGL((lora_tokred_kernel<RP>), dim3(nb0 + nb1), dim3(256), 0, st, pbp, pap, nb0, m, mp);
+  return hipGetLastError();
+}
 
-  const FinalizeArgs fin{pb, pa, a.dB, a.dA, n, k, r, RP, L.plan_b.splits, L.plan_a.splits, a.s,
-                         a.keep ? a.inv_keep : 1.0f};
+template <int RP>
+static FinalizeArgs finalize_args(const BwdArgs& a, const BwdLayout& L) {
+  return FinalizeArgs{reinterpret_cast<const float*>(a.ws + L.pb), reinterpret_cast<const float*>(a.ws + L.pa),
+                      a.dB, a.dA, (int)a.n, (int)a.k, (int)a.r, RP, L.plan_b.splits, L.plan_a.splits, a.s,
+                      a.keep ? a.inv_keep : 1.0f};
+}
+
+template <int RP>
+static hipError_t launch_bwd_rp(const BwdArgs& a, const BwdLayout& L, hipStream_t st) {
+  hipError_t e = launch_du_tokred<RP>(a, L, st);
+  if (e != hipSuccess) return e;
+  const FinalizeArgs fin = finalize_args<RP>(a, L);
+  const DxGroup none{};
   const GemmTile t = choose_gemm_tile(a.m, a.k);
   if (a.keep) {   // the 256 x 256 tile has no registers left for the dropout epilogue
-    if (t == TILE_128x128) e = launch_dx_cfg<128, 128, 2, 2, RP, true>(a, L, fin, st);
-    else e = launch_dx_cfg<128, 256, 2, 4, RP, true>(a, L, fin, st);
-  } else {
-    switch (t) {
-      case TILE_256x256: e = launch_dx_cfg<256, 256, 2, 4, RP, false>(a, L, fin, st); break;
-      case TILE_128x256: e = launch_dx_cfg<128, 256, 2, 4, RP, false>(a, L, fin, st); break;
-      default: e = launch_dx_cfg<128, 128, 2, 2, RP, false>(a, L, fin, st); break;
-    }
+    if (t == TILE_128x128) return launch_dx_cfg<128, 128, 2, 2, RP, true, false>(a, L, fin, none, st);
+    return launch_dx_cfg<128, 256, 2, 4, RP, true, false>(a, L, fin, none, st);
   }
-  if (e != hipSuccess) return e;
-  return hipSuccess;
+  switch (t) {
+    case TILE_256x256: return launch_dx_cfg<256, 256, 2, 4, RP, false, false>(a, L, fin, none, st);
+    case TILE_128x256: return launch_dx_cfg<128, 256, 2, 4, RP, false, false>(a, L, fin, none, st);
+    default: return launch_dx_cfg<128, 128, 2, 2, RP, false, false>(a, L, fin, none, st);
+  }
 }
 
 hipError_t launch_bwd(const BwdArgs& a, hipStream_t st) {
@@ -700,6 +815,58 @@ hipError_t launch_bwd(const BwdArgs& a, hipStream_t st) {
     case 32: return launch_bwd_rp<32>(a, L, st);
     case 48: return launch_bwd_rp<48>(a, L, st);
     default: return launch_bwd_rp<64>(a, L, st);
+  }
+}
+
+// Grouped backward: per projection the dU and token-reduction launches (each
+// in its own workspace region), then one dX launch over the whole group whose
+// tails finalize every projection's dA and dB.
+template <int RP>
+static hipError_t launch_bwd_group_rp(const GroupBwdArgs& a, const GroupBwdLayout& GL, hipStream_t st) {
+  DxGroup grp{};
+  int nkb = 0;
+  for (int g = 0; g < a.count; ++g) {
+    BwdArgs b{};
+    b.dY = a.dY[g]; b.X = a.X; b.W = a.W[g]; b.A = a.A[g]; b.B = a.B[g]; b.U = a.U[g];
+    b.dX = a.dX; b.dA = a.dA[g]; b.dB = a.dB[g]; b.ws = a.ws + GL.off[g];
+    b.m = a.m; b.n = a.n[g]; b.k = a.k; b.r = a.r; b.s = a.s;
+    const hipError_t e = launch_du_tokred<RP>(b, GL.L[g], st);
+    if (e != hipSuccess) return e;
+    grp.dY[g] = a.dY[g];
+    grp.W[g] = a.W[g];
+    grp.dU2[g] = reinterpret_cast<const u16*>(b.ws + GL.L[g].du2);
+    grp.A[g] = a.A[g];
+    grp.n[g] = (int)a.n[g];
+    nkb += (int)((a.n[g] + 63) / 64);
+    grp.fin[g] = finalize_args<RP>(b, GL.L[g]);
+  }
+  grp.count = a.count;
+  grp.nkb = nkb;
+  BwdArgs d{};
+  d.X = a.X; d.dX = a.dX; d.ws = a.ws;
+  d.m = a.m; d.n = 0; d.k = a.k; d.r = a.r; d.s = a.s;
+  // The 256 x 256 tile has no registers left for the per-stage projection
+  // lookup; the group runs 128 x 256 in its place.
+  const FinalizeArgs none{};
+  if (choose_gemm_tile(a.m, a.k) == TILE_128x128)
+    return launch_dx_cfg<128, 128, 2, 2, RP, false, true>(d, GL.L[0], none, grp, st);
+  return launch_dx_cfg<128, 256, 2, 4, RP, false, true>(d, GL.L[0], none, grp, st);
+}
+
+hipError_t launch_bwd_group(const GroupBwdArgs& a, hipStream_t st) {
+  if (a.count == 1) {   // a group of one is the single projection (workspace sizes agree)
+    BwdArgs b{};
+    b.dY = a.dY[0]; b.X = a.X; b.W = a.W[0]; b.A = a.A[0]; b.B = a.B[0]; b.U = a.U[0];
+    b.dX = a.dX; b.dA = a.dA[0]; b.dB = a.dB[0]; b.ws = a.ws;
+    b.m = a.m; b.n = a.n[0]; b.k = a.k; b.r = a.r; b.s = a.s;
+    return launch_bwd(b, st);
+  }
+  const GroupBwdLayout GL = group_bwd_layout(a.count, a.n, a.m, a.k, a.r);
+  switch (GL.L[0].rp) {
+    case 16: return launch_bwd_group_rp<16>(a, GL, st);
+    case 32: return launch_bwd_group_rp<32>(a, GL, st);
+    case 48: return launch_bwd_group_rp<48>(a, GL, st);
+    default: return launch_bwd_group_rp<64>(a, GL, st);
   }
 }
 

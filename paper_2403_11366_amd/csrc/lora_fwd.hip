@@ -24,11 +24,15 @@
 
 namespace lora {
 
-template <int BM, int BN, int WM, int WN, int RP, bool DROP>
+// With GRP the grid covers the output tiles of a group of projections that
+// read the same X (FwdGroup): each workgroup first selects its projection's
+// W, A, B, Y, U and n, then runs exactly the single-projection tile.
+template <int BM, int BN, int WM, int WN, int RP, bool DROP, bool GRP>
 __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
     const u16* __restrict__ X, const u16* __restrict__ W, const u16* __restrict__ A,
     const u16* __restrict__ B, const uint8_t* __restrict__ keep, u16* __restrict__ Y,
-    float* __restrict__ U, int m, int n, int k, int r, float s, float inv_keep, int tiles_m, int tiles_n) {
+    float* __restrict__ U, int m, int n, int k, int r, float s, float inv_keep, int tiles_m, int tiles_n,
+    FwdGroup grp) {
   constexpr int NW = WM * WN;
   constexpr int NT = 64 * NW;
   constexpr int WTI = BM / WM, WTJ = BN / WN;   // tokens, features per wave
@@ -65,6 +69,19 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
 
   int tm, tn;
   tile_coords(tiles_m, tiles_n, 8, (int)blockIdx.x, tm, tn);
+  if (GRP) {   // projection of this column tile (uniform; compile-time indices only)
+    int sel = 0;
+#pragma unroll
+    for (int q = 1; q < kMaxGroup; ++q)
+      if (q < grp.count && tn >= grp.tile0[q]) sel = q;
+#pragma unroll
+    for (int q = 0; q < kMaxGroup; ++q)
+      if (q == sel) {
+        W = grp.W[q]; A = grp.A[q]; B = grp.B[q]; Y = grp.Y[q]; U = grp.U[q];
+        n = grp.n[q];
+        tn -= grp.tile0[q];
+      }
+  }
   const int m0 = tm * BM, n0 = tn * BN;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = uniform(tid >> 6);
@@ -398,33 +415,71 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
   }
 }
 
-template <int BM, int BN, int WM, int WN, int RP, bool DROP>
-static hipError_t launch_fwd_cfg(const FwdArgs& a, hipStream_t st) {
-  const int tiles_m = (int)((a.m + BM - 1) / BM), tiles_n = (int)((a.n + BN - 1) / BN);
-  hipLaunchKernelGGL((lora_fwd_kernel<BM, BN, WM, WN, RP, DROP>), dim3(tiles_m * tiles_n), dim3(64 * WM * WN), 0,
-                     st, a.X, a.W, a.A, a.B, a.keep, a.Y, a.U, (int)a.m, (int)a.n, (int)a.k, (int)a.r, a.s,
-                     a.inv_keep, tiles_m, tiles_n);
+template <int BM, int BN, int WM, int WN, int RP, bool DROP, bool GRP>
+static hipError_t launch_fwd_cfg(const FwdArgs& a, const FwdGroup& grp, int tiles_n, hipStream_t st) {
+  const int tiles_m = (int)((a.m + BM - 1) / BM);
+  hipLaunchKernelGGL((lora_fwd_kernel<BM, BN, WM, WN, RP, DROP, GRP>), dim3(tiles_m * tiles_n), dim3(64 * WM * WN),
+                     0, st, a.X, a.W, a.A, a.B, a.keep, a.Y, a.U, (int)a.m, (int)a.n, (int)a.k, (int)a.r, a.s,
+                     a.inv_keep, tiles_m, tiles_n, grp);
   return hipGetLastError();
 }
 
-template <int BM, int BN, int WM, int WN, bool DROP>
-static hipError_t launch_fwd_rp(const FwdArgs& a, hipStream_t st) {
-  if (a.r <= 16) return launch_fwd_cfg<BM, BN, WM, WN, 16, DROP>(a, st);
-  if (a.r <= 32) return launch_fwd_cfg<BM, BN, WM, WN, 32, DROP>(a, st);
-  return launch_fwd_cfg<BM, BN, WM, WN, 64, DROP>(a, st);
+// Single projection: tiles_n from n.  Group: the column tiles of each
+// projection, back to back (tile0 filled here).
+template <int BM, int BN, int WM, int WN, bool DROP, bool GRP>
+static hipError_t launch_fwd_rp(const FwdArgs& a, FwdGroup grp, hipStream_t st) {
+  int tiles_n = (int)((a.n + BN - 1) / BN);
+  if (GRP) {
+    tiles_n = 0;
+    for (int g = 0; g < grp.count; ++g) {
+      grp.tile0[g] = tiles_n;
+      tiles_n += (grp.n[g] + BN - 1) / BN;
+    }
+  }
+  if (a.r <= 16) return launch_fwd_cfg<BM, BN, WM, WN, 16, DROP, GRP>(a, grp, tiles_n, st);
+  if (a.r <= 32) return launch_fwd_cfg<BM, BN, WM, WN, 32, DROP, GRP>(a, grp, tiles_n, st);
+  return launch_fwd_cfg<BM, BN, WM, WN, 64, DROP, GRP>(a, grp, tiles_n, st);
 }
 
 // With dropout the 256 x 256 tile is not used: its registers are already full.
 hipError_t launch_fwd(const FwdArgs& a, hipStream_t st) {
   const GemmTile t = choose_gemm_tile(a.m, a.n);
+  const FwdGroup none{};
   if (a.keep) {
-    if (t == TILE_128x128) return launch_fwd_rp<128, 128, 2, 2, true>(a, st);
-    return launch_fwd_rp<128, 256, 2, 4, true>(a, st);
+    if (t == TILE_128x128) return launch_fwd_rp<128, 128, 2, 2, true, false>(a, none, st);
+    return launch_fwd_rp<128, 256, 2, 4, true, false>(a, none, st);
   }
   switch (t) {
-    case TILE_256x256: return launch_fwd_rp<256, 256, 2, 4, false>(a, st);
-    case TILE_128x256: return launch_fwd_rp<128, 256, 2, 4, false>(a, st);
-    default: return launch_fwd_rp<128, 128, 2, 2, false>(a, st);
+    case TILE_256x256: return launch_fwd_rp<256, 256, 2, 4, false, false>(a, none, st);
+    case TILE_128x256: return launch_fwd_rp<128, 256, 2, 4, false, false>(a, none, st);
+    default: return launch_fwd_rp<128, 128, 2, 2, false, false>(a, none, st);
+  }
+}
+
+// One launch for the whole group; the tile is chosen for the combined output
+// of m x (sum of n) features.
+hipError_t launch_fwd_group(const GroupFwdArgs& a, hipStream_t st) {
+  if (a.count == 1) {   // a group of one is the single projection
+    FwdArgs f{};
+    f.X = a.X; f.W = a.W[0]; f.A = a.A[0]; f.B = a.B[0]; f.Y = a.Y[0]; f.U = a.U[0];
+    f.m = a.m; f.n = a.n[0]; f.k = a.k; f.r = a.r; f.s = a.s;
+    return launch_fwd(f, st);
+  }
+  FwdGroup grp{};
+  int64_t ntot = 0;
+  for (int g = 0; g < a.count; ++g) {
+    grp.W[g] = a.W[g]; grp.A[g] = a.A[g]; grp.B[g] = a.B[g]; grp.Y[g] = a.Y[g]; grp.U[g] = a.U[g];
+    grp.n[g] = (int)a.n[g];
+    ntot += a.n[g];
+  }
+  grp.count = a.count;
+  FwdArgs f{};
+  f.X = a.X;
+  f.m = a.m; f.n = 0; f.k = a.k; f.r = a.r; f.s = a.s;
+  switch (choose_gemm_tile(a.m, ntot)) {
+    case TILE_256x256: return launch_fwd_rp<256, 256, 2, 4, false, true>(f, grp, st);
+    case TILE_128x256: return launch_fwd_rp<128, 256, 2, 4, false, true>(f, grp, st);
+    default: return launch_fwd_rp<128, 128, 2, 2, false, true>(f, grp, st);
   }
 }
 

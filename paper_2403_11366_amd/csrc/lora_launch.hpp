@@ -114,6 +114,67 @@ struct BwdArgs {
   float inv_keep = 1.0f;           // 1 / (1 - p)
 };
 
+// Projections that share one input X (q, k, v of an attention block; gate and
+// up of an MLP): at most kMaxGroup, one rank and alpha for the group.
+constexpr int kMaxGroup = 8;
+
+// Kernel argument (by value) of the grouped forward: per-projection pointers;
+// the output tiles of all projections form one grid, projection g owning
+// column tiles tile0[g] .. tile0[g+1]-1.
+struct FwdGroup {
+  const uint16_t* W[kMaxGroup];
+  const uint16_t* A[kMaxGroup];
+  const uint16_t* B[kMaxGroup];
+  uint16_t* Y[kMaxGroup];
+  float* U[kMaxGroup];
+  int n[kMaxGroup];
+  int tile0[kMaxGroup];
+  int count;
+};
+
+struct GroupFwdArgs {
+  const uint16_t* X;
+  int count;
+  int64_t n[kMaxGroup];
+  const uint16_t *W[kMaxGroup], *A[kMaxGroup], *B[kMaxGroup];
+  uint16_t* Y[kMaxGroup];
+  float* U[kMaxGroup];
+  int64_t m, k, r;
+  float s;
+};
+
+struct GroupBwdArgs {
+  const uint16_t* X;
+  int count;
+  int64_t n[kMaxGroup];
+  const uint16_t *dY[kMaxGroup], *W[kMaxGroup], *A[kMaxGroup], *B[kMaxGroup];
+  const float* U[kMaxGroup];
+  uint16_t* dX;
+  float *dA[kMaxGroup], *dB[kMaxGroup];
+  char* ws;
+  int64_t m, k, r;
+  float s;
+};
+
+// Grouped backward workspace: one backward layout per projection, back to back.
+struct GroupBwdLayout {
+  BwdLayout L[kMaxGroup];
+  size_t off[kMaxGroup];
+  size_t total;
+};
+
+inline GroupBwdLayout group_bwd_layout(int count, const int64_t* n, int64_t m, int64_t k, int64_t r) {
+  GroupBwdLayout G{};
+  size_t off = 0;
+  for (int g = 0; g < count; ++g) {
+    G.L[g] = bwd_layout(m, n[g], k, r);
+    G.off[g] = off;
+    off = align256(off + G.L[g].total);
+  }
+  G.total = off;
+  return G;
+}
+
 struct MergeArgs {
   const uint16_t* W;       // [n, k]
   const uint16_t *A, *B;   // [r, k], [n, r]
@@ -125,5 +186,7 @@ struct MergeArgs {
 hipError_t launch_fwd(const FwdArgs& a, hipStream_t st);
 hipError_t launch_merge(const MergeArgs& a, hipStream_t st);
 hipError_t launch_bwd(const BwdArgs& a, hipStream_t st);
+hipError_t launch_fwd_group(const GroupFwdArgs& a, hipStream_t st);
+hipError_t launch_bwd_group(const GroupBwdArgs& a, hipStream_t st);
 
 }  // namespace lora

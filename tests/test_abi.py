@@ -201,3 +201,66 @@ def test_dropout_validation(lib):
     q = [addr(j) for j in range(11)]
     q[7] = q[6]                               # dX on top of the keep mask
     assert bwd_drop(lib, q) == 6
+
+
+def _parr(vals):
+    return (ctypes.c_void_p * len(vals))(*vals)
+
+
+def _narr(vals):
+    return (ctypes.c_int64 * len(vals))(*vals)
+
+
+def group_fwd(lib, G=3, ns=None, m=64, k=64, r=8, X=None, arrays=None):
+    ns = ns or [64] * G
+    base = 1 << 44
+    arr = arrays or {key: [base + (j * 16 + g) * (1 << 30) for g in range(G)] for j, key in enumerate("WABYU")}
+    X = addr(40) if X is None else X
+    return lib.lora_linear_group_fwd(X, G, _narr(ns), _parr(arr["W"]), _parr(arr["A"]), _parr(arr["B"]),
+                                     _parr(arr["Y"]), _parr(arr["U"]), m, k, r, 16.0, None)
+
+
+def group_bwd(lib, G=2, ns=None, m=64, k=64, r=8, ws_bytes=1 << 30, arrays=None, dX=None, ws=None):
+    ns = ns or [64] * G
+    base = 1 << 44
+    arr = arrays or {key: [base + (j * 16 + g) * (1 << 30) for g in range(G)]
+                     for j, key in enumerate(["dY", "W", "A", "B", "U", "dA", "dB"])}
+    dX = addr(41) if dX is None else dX
+    ws = addr(42) if ws is None else ws
+    return lib.lora_linear_group_bwd(_parr(arr["dY"]), addr(40), G, _narr(ns), _parr(arr["W"]), _parr(arr["A"]),
+                                     _parr(arr["B"]), _parr(arr["U"]), dX, _parr(arr["dA"]), _parr(arr["dB"]),
+                                     ws, ws_bytes, m, k, r, 16.0, None)
+
+
+def test_group_validation(lib):
+    assert group_fwd(lib, G=0) == 2
+    assert group_fwd(lib, G=9, ns=[64] * 9) == 4
+    assert group_fwd(lib, ns=[64, 72 + 4, 64]) == 2          # n not a multiple of 8
+    assert group_fwd(lib, r=65) == 4
+    assert lib.lora_linear_group_fwd(addr(40), 3, None, None, None, None, None, None, 64, 64, 8, 16.0, None) == 1
+    base = 1 << 44
+    arr = {key: [base + (j * 16 + g) * (1 << 30) for g in range(3)] for j, key in enumerate("WABYU")}
+    arr["B"][1] = 0
+    assert group_fwd(lib, arrays=arr) == 1
+    arr["B"][1] = base + 8                                   # misaligned
+    assert group_fwd(lib, arrays=arr) == 3
+    arr["B"][1] = base + (2 * 16 + 1) * (1 << 30)
+    arr["Y"][2] = arr["W"][0]                                # output on an input
+    assert group_fwd(lib, arrays=arr) == 6
+    arr["Y"][2] = arr["U"][0]                                # two outputs overlap
+    assert group_fwd(lib, arrays=arr) == 6
+    assert group_fwd(lib, X=base + (3 * 16 + 0) * (1 << 30) + 64) == 6   # X inside Y[0]
+    ns = [64, 128]
+    need = lora.lora_linear_group_bwd_workspace_size(ns, 64, 64, 8)
+    assert need >= lora.lora_linear_bwd_workspace_size(64, 64, 64, 8) + lora.lora_linear_bwd_workspace_size(64, 128, 64, 8)
+    assert lora.lora_linear_group_bwd_workspace_size([64, 60], 64, 64, 8) == 0
+    assert group_bwd(lib, ns=ns, ws_bytes=need - 1) == 5
+    assert group_bwd(lib, ns=ns, ws=addr(42, 8)) == 3
+    assert group_bwd(lib, ns=ns, dX=addr(40)) == 6           # dX on X
+    arr = {key: [base + (j * 16 + g) * (1 << 30) for g in range(2)]
+           for j, key in enumerate(["dY", "W", "A", "B", "U", "dA", "dB"])}
+    arr["dA"][1] = arr["dB"][0]
+    assert group_bwd(lib, ns=ns, arrays=arr) == 6
+    arr["dA"][1] = base + (5 * 16 + 1) * (1 << 30)
+    arr["dY"][0] = 0
+    assert group_bwd(lib, ns=ns, arrays=arr) == 1
