@@ -33,6 +33,24 @@ KERNEL_SOURCES = ["paper_2403_11366_amd/csrc/lora_fwd.hip", "paper_2403_11366_am
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "lora_fwd_kernel_llama2_7b_q_proj_traffic.json")
 
 
+def forward_kernel_name(m: int, n: int, r: int, dropout: bool) -> str:
+    """Name of the forward kernel the library launches for this shape (its tile
+    choice: rounds of 256 workgroups times tile area over a per-tile
+    efficiency; the 128 x 256 tile with rank <= 16 and no dropout runs the
+    k-split kernel)."""
+    best, cost = None, None
+    for name, bm, bn, eff in (("256x256", 256, 256, 1.0), ("128x256", 128, 256, 0.9), ("128x128", 128, 128, 0.75)):
+        tiles = -(-m // bm) * -(-n // bn)
+        c = -(-tiles // 256) * bm * bn / eff
+        if cost is None or c < cost:
+            best, cost = name, c
+    if dropout and best == "256x256":
+        best = "128x256"
+    if best == "128x256" and r <= 16 and not dropout:
+        return "lora_fwd_ks_kernel"
+    return "lora_fwd_kernel"
+
+
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
@@ -79,15 +97,18 @@ def summarize_traffic(root: str, workload: str, copy_mib: int):
         v = sorted(vals.values())
         return v[len(v) // 2], len(v)
 
-    f_fwd, nf = per_dispatch("fwd_fetch", "FETCH_SIZE", "lora_fwd_kernel")
-    w_fwd, nw = per_dispatch("fwd_write", "WRITE_SIZE", "lora_fwd_kernel")
+    from lora_synth import CONFIGS
+    s0 = CONFIGS[workload][0]
+    kname = forward_kernel_name(s0.m, s0.n, s0.r, False)
+    f_fwd, nf = per_dispatch("fwd_fetch", "FETCH_SIZE", kname + "<")
+    w_fwd, nw = per_dispatch("fwd_write", "WRITE_SIZE", kname + "<")
     f_cpy, _ = per_dispatch("copy_fetch", "FETCH_SIZE", "")
     w_cpy, _ = per_dispatch("copy_write", "WRITE_SIZE", "")
     known_kib = copy_mib * 1024.0
     sf, sw = known_kib / f_cpy, known_kib / w_cpy
     fetch_b = f_fwd * sf * 1024.0
     write_b = w_fwd * sw * 1024.0
-    rec = {"workload": workload, "kernel": "lora_fwd_kernel", "kernel_source_sha": kernel_source_hash(),
+    rec = {"workload": workload, "kernel": kname, "kernel_source_sha": kernel_source_hash(),
            "fetch_kib_raw": f_fwd, "write_kib_raw": w_fwd, "copy_mib": copy_mib,
            "copy_fetch_kib_raw": f_cpy, "copy_write_kib_raw": w_cpy,
            "fetch_scale": sf, "write_scale": sw,
@@ -488,7 +509,8 @@ def main():
                                     "alpha": s.alpha} for s in shapes],
                    "input_sets": nsets, "flops_per_step": flops, "lora_dropout": drop,
                    "operands": "bf16 in, fp32 accumulate; Y, dX bf16; U, dA, dB fp32"},
-        "roofline": {"bound": "mfma", "kernel": "lora_fwd_kernel", "achieved": round(achieved, 2),
+        "roofline": {"bound": "mfma", "kernel": forward_kernel_name(m, n, r, drop is not None),
+                     "achieved": round(achieved, 2),
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                      "traffic": traffic, "flops_per_launch": k1_flops, "avg_launch_us": round(fwd_us, 2)},
         "bwd_call_us": round(bwd_us, 2),

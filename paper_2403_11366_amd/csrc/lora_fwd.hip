@@ -415,6 +415,321 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
   }
 }
 
+// ---------------------------------------------------------------------------
+// The 128 x 256 tile for rank <= 16 with the k substeps split between wave
+// pairs.  Eight waves: wave (wk, wm, wn) multiplies the 64 tokens wm and the
+// 128 features wn of the tile over substeps 2 wk and 2 wk + 1 of every 64-wide
+// stage (the 32-wide k half wk).  Per stage a wave issues as many products as
+// in the 2 x 4 layout of 64 x 64 wave tiles but reads 12 operand fragments
+// instead of 16, and two waves still share each SIMD.  The U columns run on
+// v_mfma_f32_16x16x32_bf16: wave (wk, wm, wn) owns the 16-token groups
+// 2 wn, 2 wn + 1 of its token half, over its k half.
+//
+// After the k loop the two k-half partial sums of each output are added in
+// fixed order through LDS: wave wk keeps feature fragments 2 wk, 2 wk + 1 and
+// sends the other two to its partner, so each wave then holds a complete
+// 64 x 64 block (features wn 128 + 64 wk ..) for the epilogue, which is the one
+// of the 2 x 4 layout.  GRP selects the projection of a grouped launch as in
+// lora_fwd_kernel.
+template <bool GRP>
+__global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
+    const u16* __restrict__ X, const u16* __restrict__ W, const u16* __restrict__ A,
+    const u16* __restrict__ B, u16* __restrict__ Y, float* __restrict__ U, int m, int n, int k, int r, float s,
+    int tiles_m, int tiles_n, FwdGroup grp) {
+  constexpr int BM = 128, BN = 256, NT = 512, RP = 16;
+  constexpr int WTI = 64, WTJ = 128, FI = 2, FJ = 4;
+  constexpr int GPW = 2;                          // 16-token U groups per wave
+  constexpr int ROWS = BM + BN + RP;
+  constexpr int STAGE = ROWS * 128;
+  constexpr int CX = BM * 8, CW = BN * 8, CA = RP * 8;
+  constexpr int LX = CX / NT, LW = CW / NT, LA = (CA + NT - 1) / NT;
+  constexpr int XCH = 8 * 16 * 1024;              // exchange: 8 waves x 32 fragments x 64 lanes x 4 B
+  constexpr int SMEM = XCH > 2 * STAGE ? XCH : 2 * STAGE;
+  __shared__ __attribute__((aligned(1024))) char smem[SMEM];
+
+  int tm, tn;
+  tile_coords(tiles_m, tiles_n, 8, (int)blockIdx.x, tm, tn);
+  if (GRP) {
+    int sel = 0;
+#pragma unroll
+    for (int q = 1; q < kMaxGroup; ++q)
+      if (q < grp.count && tn >= grp.tile0[q]) sel = q;
+#pragma unroll
+    for (int q = 0; q < kMaxGroup; ++q)
+      if (q == sel) {
+        W = grp.W[q]; A = grp.A[q]; B = grp.B[q]; Y = grp.Y[q]; U = grp.U[q];
+        n = grp.n[q];
+        tn -= grp.tile0[q];
+      }
+  }
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = uniform(tid >> 6);
+  const int wk = wave >> 2, wm = (wave >> 1) & 1, wn = wave & 1;
+  const int g = lane >> 5, c32 = lane & 31;
+  const int g16 = lane >> 4, c16 = lane & 15;
+
+  const uint32_t rowbytes = (uint32_t)k * 2;
+  const __amdgpu_buffer_rsrc_t rsX = make_rsrc(X + (size_t)m0 * k, (uint64_t)min(BM, m - m0) * rowbytes);
+  const __amdgpu_buffer_rsrc_t rsW = make_rsrc(W + (size_t)n0 * k, (uint64_t)min(BN, n - n0) * rowbytes);
+  const __amdgpu_buffer_rsrc_t rsA = make_rsrc(A, (uint64_t)r * rowbytes);
+
+  // Register staging of one k-block as in lora_fwd_kernel, stored in two
+  // pieces (0 = X and A rows, 1 = W rows), one per substep of the stage.
+  int4v gx[LX], gw[LW], ga[LA];
+  auto gload = [&](int kb, int piece) {
+    const int k0 = kb * 64;
+    if (piece == 0) {
+#pragma unroll
+      for (int i = 0; i < LX; ++i) {
+        const int q = tid + i * NT;
+        const int kk = k0 + 8 * (q & 7);
+        gx[i] = buf_load16(rsX, kk < k ? (uint32_t)(q >> 3) * rowbytes + (uint32_t)kk * 2 : kOOB);
+      }
+#pragma unroll
+      for (int i = 0; i < LA; ++i) {
+        const int q = tid + i * NT;
+        if (CA % NT != 0 && wave * 64 + i * NT >= CA) break;
+        const int kk = k0 + 8 * (q & 7);
+        ga[i] = buf_load16(rsA, kk < k ? (uint32_t)(q >> 3) * rowbytes + (uint32_t)kk * 2 : kOOB);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < LW; ++i) {
+        const int q = tid + i * NT;
+        const int kk = k0 + 8 * (q & 7);
+        gw[i] = buf_load16(rsW, kk < k ? (uint32_t)(q >> 3) * rowbytes + (uint32_t)kk * 2 : kOOB);
+      }
+    }
+  };
+  auto swrite = [&](int buf, int piece) {
+    char* sb = smem + buf * STAGE;
+    if (piece == 0) {
+#pragma unroll
+      for (int i = 0; i < LX; ++i) {
+        const int q = tid + i * NT;
+        *reinterpret_cast<int4v*>(sb + kc_offset(q >> 3, q & 7)) = gx[i];
+      }
+#pragma unroll
+      for (int i = 0; i < LA; ++i) {
+        const int q = tid + i * NT;
+        if (CA % NT != 0 && wave * 64 + i * NT >= CA) break;
+        *reinterpret_cast<int4v*>(sb + (BM + BN) * 128 + kc_offset(q >> 3, q & 7)) = ga[i];
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < LW; ++i) {
+        const int q = tid + i * NT;
+        *reinterpret_cast<int4v*>(sb + BM * 128 + kc_offset(q >> 3, q & 7)) = gw[i];
+      }
+    }
+  };
+
+  floatx16 acc[FJ][FI];
+#pragma unroll
+  for (int a = 0; a < FJ; ++a)
+#pragma unroll
+    for (int b = 0; b < FI; ++b) acc[a][b] = floatx16{};
+  floatx4 uacc16[GPW];
+#pragma unroll
+  for (int a = 0; a < GPW; ++a) uacc16[a] = floatx4{0.f, 0.f, 0.f, 0.f};
+  int urow16[GPW];
+#pragma unroll
+  for (int gg = 0; gg < GPW; ++gg) urow16[gg] = wm * WTI + 16 * (wn * GPW + gg) + c16;
+
+  short8 fw[2][FJ], fx[2][FI], fa16, fxu16[GPW];
+  // Fragments of the wave's substep j (0, 1), global substep 2 wk + j; the
+  // U operands of the wave's 32-wide k half are read with substep 0.
+  auto read_frags = [&](const char* sb, int j, int p) {
+    const char* Xs = sb;
+    const char* Ws = sb + BM * 128;
+    const char* As = sb + (BM + BN) * 128;
+    const int ch = 2 * (2 * wk + j) + g;
+#pragma unroll
+    for (int fj = 0; fj < FJ; ++fj) fw[p][fj] = kc_read(Ws, wn * WTJ + 32 * fj + c32, ch);
+#pragma unroll
+    for (int fi = 0; fi < FI; ++fi) fx[p][fi] = kc_read(Xs, wm * WTI + 32 * fi + c32, ch);
+    if (j == 0) {   // the wave's 32-wide half: chunks 4 wk + g16
+      fa16 = kc_read(As, c16, 4 * wk + g16);
+#pragma unroll
+      for (int gg = 0; gg < GPW; ++gg) fxu16[gg] = kc_read(Xs, urow16[gg], 4 * wk + g16);
+    }
+  };
+  auto multiply = [&](int p, int j) {
+#pragma unroll
+    for (int fi = 0; fi < FI; ++fi)
+#pragma unroll
+      for (int fj = 0; fj < FJ; ++fj) acc[fj][fi] = mfma32x32x16(fw[p][fj], fx[p][fi], acc[fj][fi]);
+    if (j == 0) {
+#pragma unroll
+      for (int gg = 0; gg < GPW; ++gg) uacc16[gg] = mfma16x16x32(fa16, fxu16[gg], uacc16[gg]);
+    }
+  };
+  // Pipeline of lora_fwd_kernel with two substeps per wave and stage: at the
+  // top of stage kb the registers hold block kb+1; each piece is stored to the
+  // free buffer and reloaded with block kb+2; fragments of substep 1 are read
+  // while substep 0 multiplies.
+  auto stage = [&](int kb, bool write_next, bool load_next) {
+    const char* sb = smem + (kb & 1) * STAGE;
+    read_frags(sb, 0, 0);
+    if (write_next) swrite((kb + 1) & 1, 0);
+    if (load_next) gload(kb + 2, 0);
+    read_frags(sb, 1, 1);
+    multiply(0, 0);
+    if (write_next) swrite((kb + 1) & 1, 1);
+    if (load_next) gload(kb + 2, 1);
+    multiply(1, 1);
+    __syncthreads();
+  };
+  const int nkb = (k + 63) / 64;
+  gload(0, 0);
+  gload(0, 1);
+  swrite(0, 0);
+  swrite(0, 1);
+  __syncthreads();
+  if (nkb > 1) {
+    gload(1, 0);
+    gload(1, 1);
+  }
+  int kb = 0;
+  for (; kb + 2 < nkb; ++kb) stage(kb, true, true);
+  if (kb + 1 < nkb) stage(kb++, true, false);
+  stage(kb, false, false);
+
+  // ---- exchange of the k-half partial sums (LDS is free after the loop's
+  // last barrier): region (pair, h) holds, for the wave of the pair that keeps
+  // half h, the partner's fragments [fjl][fi][q4] as float4 x 64 lanes.
+  {
+    float4* xb = reinterpret_cast<float4*>(smem);
+    const int pair = wm * 2 + wn;
+    // region of (pair, destination half h): [fjl][fi][q4] float4 x 64 lanes
+    auto region = [&](int h) { return xb + (size_t)((pair * 2 + h) * 16) * 64; };
+    float4* dst = region(1 - wk);
+#pragma unroll
+    for (int fjl = 0; fjl < 2; ++fjl)
+#pragma unroll
+      for (int fi = 0; fi < FI; ++fi) {
+        const floatx16 v = wk == 0 ? acc[2 + fjl][fi] : acc[fjl][fi];
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4)
+          dst[((fjl * FI + fi) * 4 + q4) * 64 + lane] = float4{v[4 * q4], v[4 * q4 + 1], v[4 * q4 + 2], v[4 * q4 + 3]};
+      }
+    __syncthreads();
+    const float4* src = region(wk);
+#pragma unroll
+    for (int fjl = 0; fjl < 2; ++fjl)
+#pragma unroll
+      for (int fi = 0; fi < FI; ++fi)
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+          const float4 o = src[((fjl * FI + fi) * 4 + q4) * 64 + lane];
+          if (wk == 0) {
+            acc[fjl][fi][4 * q4] += o.x; acc[fjl][fi][4 * q4 + 1] += o.y;
+            acc[fjl][fi][4 * q4 + 2] += o.z; acc[fjl][fi][4 * q4 + 3] += o.w;
+          } else {
+            acc[2 + fjl][fi][4 * q4] += o.x; acc[2 + fjl][fi][4 * q4 + 1] += o.y;
+            acc[2 + fjl][fi][4 * q4 + 2] += o.z; acc[2 + fjl][fi][4 * q4 + 3] += o.w;
+          }
+        }
+    __syncthreads();
+  }
+
+  // ---- epilogue as in lora_fwd_kernel on the wave's 64 x 64 block:
+  // Us [2][BM][RP] fp32 (the two k-half partials of U, summed in fixed order),
+  // Bs [BN][RP] bf16 (B rows of the tile, zero beyond r and n).
+  float* Us = reinterpret_cast<float*>(smem);
+  u16* Bs = reinterpret_cast<u16*>(smem + 2 * BM * RP * 4);
+  constexpr int BCH = (BN * RP / 8 + NT - 1) / NT;
+  const int jn = min(BN, n - n0);
+  const int nch = jn * r / 8;
+  const __amdgpu_buffer_rsrc_t rsB = make_rsrc(B + (size_t)n0 * r, (uint64_t)nch * 16);
+  int4v bv[BCH];
+#pragma unroll
+  for (int i = 0; i < BCH; ++i) {
+    const int q = tid + i * NT;
+    bv[i] = buf_load16(rsB, q < nch ? (uint32_t)q * 16 : kOOB);
+  }
+#pragma unroll
+  for (int gg = 0; gg < GPW; ++gg)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) Us[(wk * BM + urow16[gg]) * RP + 4 * g16 + q] = uacc16[gg][q];
+  for (int e = tid; e < BN * RP / 8; e += NT) reinterpret_cast<int4v*>(Bs)[e] = int4v{0, 0, 0, 0};
+  __syncthreads();
+  {
+    const float rinv = 1.0f / (float)r;
+#pragma unroll
+    for (int i = 0; i < BCH; ++i) {
+      const int q = tid + i * NT;
+      if (q < nch) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int idx = 8 * q + e;
+          const int j = (int)(((float)idx + 0.5f) * rinv);
+          const int t = idx - j * r;
+          Bs[j * RP + t] = (u16)((uint32_t)bv[i][e >> 1] >> (16 * (e & 1)));
+        }
+      }
+    }
+  }
+  for (int e = tid; e < BM * RP; e += NT) Us[e] = Us[e] + Us[BM * RP + e];
+  __syncthreads();
+  if (tn == 0) {
+    for (int e = tid; e < BM * RP; e += NT) {
+      const int il = e / RP, t = e - il * RP;
+      if (m0 + il < m && t < r) U[(size_t)(m0 + il) * r + t] = Us[e];
+    }
+  }
+  // acc += s U B^T (high and low bf16 parts of s U), then Y rounded to bf16;
+  // the block: features wn WTJ + 64 wk + 32 fjl, tokens wm WTI + 32 fi.
+  auto finish = [&](floatx16 (&a2)[FI], floatx16 (&b2)[FI]) {
+    floatx16* own[2] = {a2, b2};
+    const int t0 = 8 * g;
+    short8 bfr[2];
+#pragma unroll
+    for (int fjl = 0; fjl < 2; ++fjl) {
+      const int jl = wn * WTJ + 64 * wk + 32 * fjl + c32;
+      bfr[fjl] = *reinterpret_cast<const short8*>(Bs + jl * RP + t0);
+    }
+#pragma unroll
+    for (int fi = 0; fi < FI; ++fi) {
+      const int il = wm * WTI + 32 * fi + c32;
+      const float* up = Us + il * RP + t0;
+      short8 uh, ul;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float v = s * up[e];
+        const u16 hi = f32_to_bf16(v);
+        uh[e] = (short)hi;
+        ul[e] = (short)f32_to_bf16(v - bf16_to_f32(hi));
+      }
+#pragma unroll
+      for (int fjl = 0; fjl < 2; ++fjl) {
+        own[fjl][fi] = mfma32x32x16(bfr[fjl], uh, own[fjl][fi]);
+        own[fjl][fi] = mfma32x32x16(bfr[fjl], ul, own[fjl][fi]);
+      }
+    }
+#pragma unroll
+    for (int fi = 0; fi < FI; ++fi) {
+      const int i = m0 + wm * WTI + 32 * fi + c32;
+      if (i >= m) continue;
+      u16* yrow = Y + (size_t)i * n;
+#pragma unroll
+      for (int fjl = 0; fjl < 2; ++fjl)
+#pragma unroll
+        for (int qq = 0; qq < 4; ++qq) {
+          const int j = n0 + wn * WTJ + 64 * wk + 32 * fjl + 8 * qq + 4 * g;
+          if (j >= n) continue;
+          const floatx16& a = own[fjl][fi];
+          const uint32_t lo = (uint32_t)f32_to_bf16(a[4 * qq]) | ((uint32_t)f32_to_bf16(a[4 * qq + 1]) << 16);
+          const uint32_t hi = (uint32_t)f32_to_bf16(a[4 * qq + 2]) | ((uint32_t)f32_to_bf16(a[4 * qq + 3]) << 16);
+          *reinterpret_cast<uint2*>(yrow + j) = uint2{lo, hi};
+        }
+    }
+  };
+  if (wk == 0) finish(acc[0], acc[1]);
+  else finish(acc[2], acc[3]);
+}
+
 template <int BM, int BN, int WM, int WN, int RP, bool DROP, bool GRP>
 static hipError_t launch_fwd_cfg(const FwdArgs& a, const FwdGroup& grp, int tiles_n, hipStream_t st) {
   const int tiles_m = (int)((a.m + BM - 1) / BM);
@@ -425,7 +740,8 @@ static hipError_t launch_fwd_cfg(const FwdArgs& a, const FwdGroup& grp, int tile
 }
 
 // Single projection: tiles_n from n.  Group: the column tiles of each
-// projection, back to back (tile0 filled here).
+// projection, back to back (tile0 filled here).  The 128 x 256 tile with
+// rank <= 16 and no dropout runs the k-split kernel.
 template <int BM, int BN, int WM, int WN, bool DROP, bool GRP>
 static hipError_t launch_fwd_rp(const FwdArgs& a, FwdGroup grp, hipStream_t st) {
   int tiles_n = (int)((a.n + BN - 1) / BN);
@@ -435,6 +751,12 @@ static hipError_t launch_fwd_rp(const FwdArgs& a, FwdGroup grp, hipStream_t st) 
       grp.tile0[g] = tiles_n;
       tiles_n += (grp.n[g] + BN - 1) / BN;
     }
+  }
+  if (BM == 128 && BN == 256 && !DROP && a.r <= 16) {
+    const int tiles_m = (int)((a.m + BM - 1) / BM);
+    hipLaunchKernelGGL((lora_fwd_ks_kernel<GRP>), dim3(tiles_m * tiles_n), dim3(512), 0, st, a.X, a.W, a.A, a.B,
+                       a.Y, a.U, (int)a.m, (int)a.n, (int)a.k, (int)a.r, a.s, tiles_m, tiles_n, grp);
+    return hipGetLastError();
   }
   if (a.r <= 16) return launch_fwd_cfg<BM, BN, WM, WN, 16, DROP, GRP>(a, grp, tiles_n, st);
   if (a.r <= 32) return launch_fwd_cfg<BM, BN, WM, WN, 32, DROP, GRP>(a, grp, tiles_n, st);
