@@ -30,7 +30,11 @@ PEAK_BF16_TFLOPS = 2500.0    # MI355X dense bf16 matrix-core peak
 PEAK_HBM_GBS = 8000.0        # MI355X HBM3E
 MALL_BYTES = 256 << 20       # Infinity Cache
 KERNEL_SOURCES = ["paper_2403_11366_amd/csrc/lora_fwd.hip", "paper_2403_11366_amd/csrc/lora_device.hpp"]
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "lora_fwd_kernel_llama2_7b_q_proj_traffic.json")
+def traffic_file(workload: str) -> str:
+    """Committed HBM-traffic record of the forward kernel of `workload`."""
+    from lora_synth import CONFIGS
+    s0 = CONFIGS[workload][0]
+    return os.path.join(ROOT, "profiles", f"{forward_kernel_name(s0.m, s0.n, s0.r, False)}_{workload}_traffic.json")
 
 
 def forward_kernel_name(m: int, n: int, r: int, dropout: bool) -> str:
@@ -67,7 +71,7 @@ def measured_traffic(workload: str):
     """HBM bytes per forward-kernel launch from the committed rocprofv3 counter
     runs, if they were taken on the current kernel source; else None."""
     try:
-        with open(TRAFFIC_FILE) as f:
+        with open(traffic_file(workload)) as f:
             rec = json.load(f)
     except (OSError, ValueError):
         return None
@@ -114,8 +118,9 @@ def summarize_traffic(root: str, workload: str, copy_mib: int):
            "fetch_scale": sf, "write_scale": sw,
            "hbm_fetch_bytes_per_launch": fetch_b, "hbm_write_bytes_per_launch": write_b,
            "hbm_bytes_per_launch": fetch_b + write_b, "dispatches": [nf, nw]}
-    os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)
-    with open(TRAFFIC_FILE, "w") as f:
+    out = traffic_file(workload)
+    os.makedirs(os.path.dirname(out), exist_ok=True)
+    with open(out, "w") as f:
         json.dump(rec, f, indent=1)
     print(json.dumps(rec))
 

@@ -194,7 +194,9 @@ struct RedProblem {
   const uint8_t* keep;   // dropout keep bits of Q ([m][ncols/8]) or null: masked Q elements count as 0
 };
 
-template <int RP>
+// KEEP instantiates the masked-Q path (LoRA dropout); without it the keep
+// pointers are ignored and the kernel carries none of the mask registers.
+template <int RP, bool KEEP>
 __global__ __launch_bounds__(256) void lora_tokred_kernel(RedProblem p0, RedProblem p1, int nb0, int m, int mp) {
   constexpr int CB = kRedCols;                // columns per workgroup
   constexpr int FC = CB / 16;                 // column fragments
@@ -232,9 +234,9 @@ __global__ __launch_bounds__(256) void lora_tokred_kernel(RedProblem p0, RedProb
   // Slice loads: Q chunk u of this lane is row (lane + 64u) / CPR, chunk
   // (lane + 64u) % CPR; P fragment f is row 16f + c16, tokens ts + 8g .. +7.
   int4v qv[2][QL];
-  uint32_t kq[2][QL];          // keep byte of each Q chunk (dropout)
+  uint32_t kq[KEEP ? 2 : 1][KEEP ? QL : 1];   // keep byte of each Q chunk (dropout)
   short8 pv[2][FP];
-  const uint8_t* keep = pr.keep;
+  const uint8_t* keep = KEEP ? pr.keep : nullptr;
   const uint32_t kb8 = (uint32_t)ncols / 8;
   auto load = [&](int ts, int b) {
     const int rows = uniform(max(0, min(32, m - ts)));   // keeps the resource in scalar registers
@@ -245,13 +247,13 @@ __global__ __launch_bounds__(256) void lora_tokred_kernel(RedProblem p0, RedProb
       const int cc = c0 + 8 * (q % CPR);
       qv[b][u] = buf_load16(rsQ, cc < ncols ? (uint32_t)(q / CPR) * qrow + (uint32_t)cc * 2 : kOOB);
     }
-    if (keep) {   // workgroup-uniform
+    if (KEEP && keep) {   // workgroup-uniform
       const __amdgpu_buffer_rsrc_t rsK = make_rsrc(keep + (size_t)ts * kb8, (uint64_t)rows * kb8);
 #pragma unroll
       for (int u = 0; u < QL; ++u) {
         const int q = lane + 64 * u;
         const int cc = c0 + 8 * (q % CPR);
-        kq[b][u] = buf_load_u8(rsK, cc < ncols ? (uint32_t)(q / CPR) * kb8 + (uint32_t)cc / 8 : kOOB);
+        kq[KEEP ? b : 0][KEEP ? u : 0] = buf_load_u8(rsK, cc < ncols ? (uint32_t)(q / CPR) * kb8 + (uint32_t)cc / 8 : kOOB);
       }
     }
 #pragma unroll
@@ -265,7 +267,8 @@ __global__ __launch_bounds__(256) void lora_tokred_kernel(RedProblem p0, RedProb
     for (int u = 0; u < QL; ++u) {
       const int q = lane + 64 * u;
       int4v v = qv[b][u];
-      if (keep) v = __builtin_bit_cast(int4v, keep_mask8(__builtin_bit_cast(short8, v), kq[b][u]));
+      if (KEEP && keep)
+        v = __builtin_bit_cast(int4v, keep_mask8(__builtin_bit_cast(short8, v), kq[KEEP ? b : 0][KEEP ? u : 0]));
       *reinterpret_cast<int4v*>(qs + mc16_offset<CB>(q / CPR, q % CPR)) = v;
     }
 #pragma unroll
@@ -779,7 +782,10 @@ static hipError_t launch_du_tokred(const BwdArgs& a, const BwdLayout& L, hipStre
   const RedProblem pap{dUt2, a.X, pa, (int)a.k, (int)L.plan_a.span, L.plan_a.col_tiles, a.keep};
   const int nb0 = L.plan_b.col_tiles * L.plan_b.splits;
   const int nb1 = L.plan_a.col_tiles * L.plan_a.splits;
-  hipLaunchKernelGGL((lora_tokred_kernel<RP>), dim3(nb0 + nb1), dim3(256), 0, st, pbp, pap, nb0, m, mp);
+  if (a.keep)
+    hipLaunchKernelGGL((lora_tokred_kernel<RP, true>), dim3(nb0 + nb1), dim3(256), 0, st, pbp, pap, nb0, m, mp);
+  else
+    hipLaunchKernelGGL((lora_tokred_kernel<RP, false>), dim3(nb0 + nb1), dim3(256), 0, st, pbp, pap, nb0, m, mp);
   return hipGetLastError();
 }
 
