@@ -69,6 +69,7 @@ CASES = [  # (ns, m, k, r, alpha)
     ([392, 128, 520], 264, 448, 64, 128.0),        # rank 64
     ([1032, 1032], 520, 640, 16, 32.0),            # gate, up
     ([64, 72, 80, 88, 96, 104, 112, 120], 96, 136, 3, 6.0),   # the largest group
+    ([1368, 1368, 1360], 2000, 1024, 8, 16.0),    # the k-split forward tile, ragged members
 ]
 
 

@@ -48,6 +48,8 @@ RAGGED = [
     Shape("ragged", 1000, 128, 8, 8, 16.0, 107),
     Shape("ragged", 2051, 4096, 4096, 8, 16.0, 108),
     Shape("ragged", 4100, 2048, 1024, 24, 48.0, 109),
+    Shape("ragged", 2000, 4000, 4104, 5, 10.0, 110),     # k-split forward tile, every edge ragged
+    Shape("ragged", 1500, 3000, 2056, 13, 26.0, 111),
 ]
 
 
