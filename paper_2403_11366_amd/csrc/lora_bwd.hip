@@ -37,8 +37,10 @@ __device__ __forceinline__ short8 tr16_read(const char* tile, int pitch, int col
 }
 
 // ---------------------------------------------------------------------------
-// dU = s dY B for 16 tokens per workgroup, reducing over all of n, plus the
-// U^T high/low split of the same tokens.  The 8 waves take interleaved
+// dU = s dY B for TPW (16 or 8) tokens per workgroup, reducing over all of
+// n, plus the U^T high/low split of the same tokens.  TPW = 8 doubles the
+// workgroups for token counts that would leave compute units idle (the
+// matrix-core B operand then carries 8 zero token columns).  The 8 waves take interleaved
 // 32-wide chunks of n, UNR chunks per batch with all of a batch's loads
 // issued together.  A chunk's B rows (32 x r, contiguous in B) are staged in a
 // wave-private LDS slot as [32][RP] (columns t >= r stay zero) and read back
@@ -49,7 +51,7 @@ __device__ __forceinline__ short8 tr16_read(const char* tile, int pitch, int col
 // back the per-XCD L2s -- far dearer than the work.)  Writes dU2 (token-major,
 // high | low parts), dUt2 (its transpose) and Ut2 (U^T, high rows then low
 // rows).  Index math is 32-bit: validation bounds every index below 2^30.
-template <int RP>
+template <int RP, int TPW>
 __global__ __launch_bounds__(512) void lora_bwd_du_kernel(
     const u16* __restrict__ dY, const u16* __restrict__ B, const float* __restrict__ U,
     u16* __restrict__ dU2, u16* __restrict__ dUt2, u16* __restrict__ Ut2,
@@ -61,11 +63,12 @@ __global__ __launch_bounds__(512) void lora_bwd_du_kernel(
   constexpr int BL = RP / 16;                       // 16-byte B loads per lane per chunk (4r <= 4 RP)
   static_assert(NWV * FT * 64 * 16 <= NWV * UNR * SLOT, "reduction fits the staging LDS");
   __shared__ __attribute__((aligned(1024))) char sm[NWV * UNR * SLOT];
-  const int i0 = blockIdx.x * 16;
+  static_assert(TPW == 16 || TPW == 8, "tokens per workgroup");
+  const int i0 = blockIdx.x * TPW;
   const int tid = threadIdx.x, lane = tid & 63, wave = uniform(tid >> 6);
   const int g = lane >> 4, c16 = lane & 15;
   const uint32_t rowbytes = (uint32_t)n * 2;
-  const int rows = uniform(max(0, min(16, m - i0)));
+  const int rows = uniform(max(0, min(TPW, m - i0)));
   const __amdgpu_buffer_rsrc_t rsY = make_rsrc(dY + (size_t)i0 * n, (uint64_t)rows * rowbytes);
   const __amdgpu_buffer_rsrc_t rsB = make_rsrc(B, (uint64_t)n * r * 2);
   char* slots = sm + wave * UNR * SLOT;
@@ -133,8 +136,8 @@ __global__ __launch_bounds__(512) void lora_bwd_du_kernel(
   }
 
   // U^T high/low split of this workgroup's tokens (tokens >= m are zero).
-  for (int e = tid; e < 2 * RP * 16; e += 64 * NWV) {
-    const int tt = e >> 4, i = i0 + (e & 15);
+  for (int e = tid; e < 2 * RP * TPW; e += 64 * NWV) {
+    const int tt = e / TPW, i = i0 + e % TPW;
     const int t = tt < RP ? tt : tt - RP;
     const float v = (i < m && t < r) ? U[(size_t)i * r + t] : 0.f;
     const u16 h = f32_to_bf16(v);
@@ -151,6 +154,7 @@ __global__ __launch_bounds__(512) void lora_bwd_du_kernel(
   floatx4 v = red[ft * 64 + lane];
 #pragma unroll
   for (int w = 1; w < NWV; ++w) v += red[(w * FT + ft) * 64 + lane];
+  if (c16 >= TPW) return;   // the zero token columns of TPW = 8
   const int i = i0 + c16;  // < mp: the grid covers exactly mp tokens
   u16 hi[4], lo[4];
 #pragma unroll
@@ -774,8 +778,12 @@ static hipError_t launch_du_tokred(const BwdArgs& a, const BwdLayout& L, hipStre
   float* pa = reinterpret_cast<float*>(a.ws + L.pa);
   hipError_t e;
 
-  hipLaunchKernelGGL((lora_bwd_du_kernel<RP>), dim3(mp / 16), dim3(512), 0, st, a.dY, a.B, a.U, dU2, dUt2, Ut2, m, n, r,
-                     mp, a.s);
+  if (mp / 16 < 512)   // fewer than two workgroups of 16 tokens per compute unit: 8 tokens each
+    hipLaunchKernelGGL((lora_bwd_du_kernel<RP, 8>), dim3(mp / 8), dim3(512), 0, st, a.dY, a.B, a.U, dU2, dUt2, Ut2, m,
+                       n, r, mp, a.s);
+  else
+    hipLaunchKernelGGL((lora_bwd_du_kernel<RP, 16>), dim3(mp / 16), dim3(512), 0, st, a.dY, a.B, a.U, dU2, dUt2, Ut2, m,
+                       n, r, mp, a.s);
   if ((e = hipGetLastError()) != hipSuccess) return e;
 
   const RedProblem pbp{Ut2, a.dY, pb, n, (int)L.plan_b.span, L.plan_b.col_tiles, nullptr};
