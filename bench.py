@@ -40,8 +40,8 @@ def traffic_file(workload: str) -> str:
 def forward_kernel_name(m: int, n: int, r: int, dropout: bool) -> str:
     """Name of the forward kernel the library launches for this shape (its tile
     choice: rounds of 256 workgroups times tile area over a per-tile
-    efficiency; the 128 x 256 tile with rank <= 16 and no dropout runs the
-    k-split kernel)."""
+    efficiency, with 128 x 256 in place of 256 x 256 under dropout; the
+    128 x 256 tile with rank <= 16 and no dropout runs the k-split kernel)."""
     best, cost = None, None
     for name, bm, bn, eff in (("256x256", 256, 256, 1.0), ("128x256", 128, 256, 0.9), ("128x128", 128, 128, 0.75)):
         tiles = -(-m // bm) * -(-n // bn)

@@ -47,6 +47,7 @@ def check(t, shape, keep, p, out):
 
 
 SHAPES = [Shape("drop_tiny", 256, 512, 512, 8, 16.0, 21), Shape("drop_ragged", 200, 264, 320, 5, 10.0, 22),
+          Shape("drop_128x256", 2000, 4000, 1024, 5, 10.0, 28),  # the 128 x 256 tile, ragged m and n
           Shape("drop_r33", 130, 136, 192, 33, 66.0, 23), Shape("drop_r64", 264, 392, 448, 64, 128.0, 24),
           Shape("drop_r16", 520, 1032, 640, 16, 32.0, 25)]
 
