@@ -778,7 +778,7 @@ static hipError_t launch_du_tokred(const BwdArgs& a, const BwdLayout& L, hipStre
   float* pa = reinterpret_cast<float*>(a.ws + L.pa);
   hipError_t e;
 
-  if (mp / 16 < 512)   // fewer than two workgroups of 16 tokens per compute unit: 8 tokens each
+  if (mp / 16 < 256)   // fewer workgroups of 16 tokens than compute units: 8 tokens each
     hipLaunchKernelGGL((lora_bwd_du_kernel<RP, 8>), dim3(mp / 8), dim3(512), 0, st, a.dY, a.B, a.U, dU2, dUt2, Ut2, m,
                        n, r, mp, a.s);
   else

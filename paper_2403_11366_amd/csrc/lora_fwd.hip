@@ -27,7 +27,10 @@ namespace lora {
 // With GRP the grid covers the output tiles of a group of projections that
 // read the same X (FwdGroup): each workgroup first selects its projection's
 // W, A, B, Y, U and n, then runs exactly the single-projection tile.
-template <int BM, int BN, int WM, int WN, int RP, bool DROP, bool GRP>
+//
+// With UPRE, U = X A^T has been computed by lora_u_kernel: the k loop stages
+// no A rows and runs no U products, and the epilogue reads U back.
+template <int BM, int BN, int WM, int WN, int RP, bool DROP, bool GRP, bool UPRE>
 __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
     const u16* __restrict__ X, const u16* __restrict__ W, const u16* __restrict__ A,
     const u16* __restrict__ B, const uint8_t* __restrict__ keep, u16* __restrict__ Y,
@@ -50,13 +53,14 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
   constexpr int FUW = U16 ? 1 : (FI >= WN ? FI / WN : 1);
   constexpr int NDUP = U16 ? 1 : (FI >= WN ? 1 : WN / FI);
   constexpr int GPW = U16 ? (WTI / 16) / WN : 1;
-  constexpr int ROWS = BM + BN + RP;             // 128-byte rows per 64-wide stage
+  constexpr int RPS = UPRE ? 0 : RP;             // A rows staged per stage
+  constexpr int ROWS = BM + BN + RPS;            // 128-byte rows per 64-wide stage
   // With dropout the stage also holds the keep bits of its X rows: 8 bytes
   // (64 k) per row.
   constexpr int KS_OFF = ROWS * 128;
   constexpr int STAGE = KS_OFF + (DROP ? BM * 8 : 0);
-  constexpr int CX = BM * 8, CW = BN * 8, CA = RP * 8;   // 16-byte chunks per region
-  constexpr int LX = (CX + NT - 1) / NT, LW = (CW + NT - 1) / NT, LA = (CA + NT - 1) / NT;
+  constexpr int CX = BM * 8, CW = BN * 8, CA = RPS * 8;  // 16-byte chunks per region
+  constexpr int LX = (CX + NT - 1) / NT, LW = (CW + NT - 1) / NT, LA = UPRE ? 1 : (CA + NT - 1) / NT;
   static_assert(WTI % 32 == 0 && WTJ % 32 == 0 && (U16 || RP % 32 == 0), "32x32 fragments");
   static_assert(!U16 || ((WTI / 16) % WN == 0 && GPW >= 1), "U groups split evenly");
   static_assert(CX % 64 == 0 && CW % 64 == 0 && CA % 64 == 0, "regions end on wave boundaries");
@@ -125,7 +129,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
         const int kk = k0 + 8 * (q & 7);
         gw[i] = buf_load16(rsW, kk < k ? (uint32_t)(q >> 3) * rowbytes + (uint32_t)kk * 2 : kOOB);
       }
-    } else {
+    } else if (!UPRE) {
 #pragma unroll
       for (int i = 0; i < LA; ++i) {
         const int q = tid + i * NT;
@@ -152,7 +156,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
         if (CW % NT != 0 && wave * 64 + i * NT >= CW) break;   // wave-uniform
         *reinterpret_cast<int4v*>(sb + BM * 128 + kc_offset(q >> 3, q & 7)) = gw[i];
       }
-    } else {
+    } else if (!UPRE) {
 #pragma unroll
       for (int i = 0; i < LA; ++i) {
         const int q = tid + i * NT;
@@ -201,7 +205,8 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
     // Dropout acts on the U operand only (the W path reads X unmasked): each
     // 8-k chunk of a row has one keep byte in the stage.
     const uint8_t* Ks = reinterpret_cast<const uint8_t*>(sb + KS_OFF);
-    if (U16) {
+    if (UPRE) {
+    } else if (U16) {
       if (ks % 2 == 0) {   // the 32-wide half starting at substep ks: chunks 2 ks + g16
         fa16[p] = kc_read(As, c16, 2 * ks + g16);
 #pragma unroll
@@ -226,7 +231,8 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
     for (int fi = 0; fi < FI; ++fi)
 #pragma unroll
       for (int fj = 0; fj < FJ; ++fj) acc[fj][fi] = mfma32x32x16(fw[p][fj], fx[p][fi], acc[fj][fi]);
-    if (U16) {
+    if (UPRE) {
+    } else if (U16) {
       if (ks % 2 == 0) {
 #pragma unroll
         for (int gg = 0; gg < GPW; ++gg) uacc16[gg] = mfma16x16x32(fa16[p], fxu16[p][gg], uacc16[gg]);
@@ -309,7 +315,12 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
   }
   // (with dropout the accumulated products are scaled by 1 / (1 - p) here)
   const float uscale = DROP ? inv_keep : 1.0f;
-  if (U16) {   // lane holds token column c16 of its group, U rows t = 4 g16 .. +3
+  if (UPRE) {   // U of the tile's tokens from the U pass (zero beyond r and m)
+    for (int e = tid; e < BM * RP; e += NT) {
+      const int il = e / RP, t = e - il * RP;
+      Us[e] = (m0 + il < m && t < r) ? U[(size_t)(m0 + il) * r + t] : 0.f;
+    }
+  } else if (U16) {   // lane holds token column c16 of its group, U rows t = 4 g16 .. +3
 #pragma unroll
     for (int gg = 0; gg < GPW; ++gg)
 #pragma unroll
@@ -347,7 +358,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
       }
     }
   }
-  if (NDUP > 1) {  // fold the partial U sums into copy 0 (fixed order)
+  if (NDUP > 1 && !UPRE) {  // fold the partial U sums into copy 0 (fixed order)
     for (int e = tid; e < BM * RP; e += NT) {
       float v = Us[e];
 #pragma unroll
@@ -356,7 +367,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
     }
   }
   __syncthreads();
-  if (tn == 0) {   // U output: one tile column writes it
+  if (tn == 0 && !UPRE) {   // U output: one tile column writes it
     for (int e = tid; e < BM * RP; e += NT) {
       const int il = e / RP, t = e - il * RP;
       if (m0 + il < m && t < r) U[(size_t)(m0 + il) * r + t] = Us[e];
@@ -412,6 +423,89 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
         const uint32_t hi = (uint32_t)f32_to_bf16(a[4 * qq + 2]) | ((uint32_t)f32_to_bf16(a[4 * qq + 3]) << 16);
         *reinterpret_cast<uint2*>(yrow + j) = uint2{lo, hi};
       }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// U = X A^T on its own, for ranks above 16.  In the fused tile every output
+// tile recomputes all RP U columns of its tokens, RP / BN more matrix-core
+// work (a quarter at RP = 64 on the 256-wide tile); this pass computes them
+// once.  TPW tokens per workgroup; the 8 waves take interleaved 32-wide chunks
+// of k, UNR per batch with the next batch's loads in flight, loading X and A
+// straight into v_mfma_f32_16x16x32_bf16 operands (A rows as the A operand,
+// 16 tokens as the B operand).  The waves' sums are added in wave order
+// through LDS (bit-identical from run to run) and written as fp32 U [m][r].
+template <int RP, int TPW>
+__global__ __launch_bounds__(512) void lora_u_kernel(const u16* __restrict__ X, const u16* __restrict__ A,
+                                                     float* __restrict__ U, int m, int k, int r) {
+  constexpr int FT = RP / 16, TG = TPW / 16, NWV = 8, UNR = 2;
+  __shared__ __attribute__((aligned(16))) floatx4 red[NWV][FT][TG][64];
+  const int i0 = blockIdx.x * TPW;
+  const int tid = threadIdx.x, lane = tid & 63, wave = uniform(tid >> 6);
+  const int g = lane >> 4, c16 = lane & 15;
+  const uint32_t rowbytes = (uint32_t)k * 2;
+  const int rows = uniform(max(0, min(TPW, m - i0)));
+  const __amdgpu_buffer_rsrc_t rsX = make_rsrc(X + (size_t)i0 * k, (uint64_t)rows * rowbytes);
+  const __amdgpu_buffer_rsrc_t rsA = make_rsrc(A, (uint64_t)r * rowbytes);
+
+  floatx4 acc[FT][TG];
+#pragma unroll
+  for (int ft = 0; ft < FT; ++ft)
+#pragma unroll
+    for (int tg = 0; tg < TG; ++tg) acc[ft][tg] = floatx4{0.f, 0.f, 0.f, 0.f};
+  // chunk j of this wave: k columns 32 (wave + NWV j) .. +31; lane (g, c16)
+  // loads k 8g .. 8g+7 of token row 16 tg + c16 and of A row 16 ft + c16
+  short8 xf[2][UNR][TG], af[2][UNR][FT];
+  auto load = [&](int bt, int p) {
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) {
+      const int kk = 32 * (wave + NWV * (UNR * bt + u)) + 8 * g;
+#pragma unroll
+      for (int tg = 0; tg < TG; ++tg)
+        xf[p][u][tg] = __builtin_bit_cast(
+            short8, buf_load16(rsX, kk < k ? (uint32_t)(16 * tg + c16) * rowbytes + (uint32_t)kk * 2 : kOOB));
+#pragma unroll
+      for (int ft = 0; ft < FT; ++ft)
+        af[p][u][ft] = __builtin_bit_cast(
+            short8, buf_load16(rsA, kk < k ? (uint32_t)(16 * ft + c16) * rowbytes + (uint32_t)kk * 2 : kOOB));
+    }
+  };
+  auto process = [&](int p) {
+#pragma unroll
+    for (int u = 0; u < UNR; ++u)
+#pragma unroll
+      for (int ft = 0; ft < FT; ++ft)
+#pragma unroll
+        for (int tg = 0; tg < TG; ++tg) acc[ft][tg] = mfma16x16x32(af[p][u][ft], xf[p][u][tg], acc[ft][tg]);
+  };
+  const int nbt = uniform(32 * wave < k ? (k - 32 * wave + 32 * NWV * UNR - 1) / (32 * NWV * UNR) : 0);
+  if (nbt > 0) load(0, 0);
+  for (int bt = 0; bt < nbt; bt += 2) {
+    if (bt + 1 < nbt) load(bt + 1, 1);
+    process(0);
+    if (bt + 1 >= nbt) break;
+    if (bt + 2 < nbt) load(bt + 2, 0);
+    process(1);
+  }
+#pragma unroll
+  for (int ft = 0; ft < FT; ++ft)
+#pragma unroll
+    for (int tg = 0; tg < TG; ++tg) red[wave][ft][tg][lane] = acc[ft][tg];
+  __syncthreads();
+  // lane of (ft, tg): token 16 tg + c16, rank rows 16 ft + 4 g .. +3
+  for (int e = wave; e < FT * TG; e += NWV) {
+    const int ft = e / TG, tg = e - ft * TG;
+    floatx4 v = red[0][ft][tg][lane];
+#pragma unroll
+    for (int w = 1; w < NWV; ++w) v += red[w][ft][tg][lane];
+    const int i = i0 + 16 * tg + c16;
+    if (i < m) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int t = 16 * ft + 4 * g + q;
+        if (t < r) U[(size_t)i * r + t] = v[q];
+      }
+    }
   }
 }
 
@@ -733,10 +827,21 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
 template <int BM, int BN, int WM, int WN, int RP, bool DROP, bool GRP>
 static hipError_t launch_fwd_cfg(const FwdArgs& a, const FwdGroup& grp, int tiles_n, hipStream_t st) {
   const int tiles_m = (int)((a.m + BM - 1) / BM);
-  hipLaunchKernelGGL((lora_fwd_kernel<BM, BN, WM, WN, RP, DROP, GRP>), dim3(tiles_m * tiles_n), dim3(64 * WM * WN),
-                     0, st, a.X, a.W, a.A, a.B, a.keep, a.Y, a.U, (int)a.m, (int)a.n, (int)a.k, (int)a.r, a.s,
-                     a.inv_keep, tiles_m, tiles_n, grp);
-  return hipGetLastError();
+  if constexpr (RP >= 32 && !DROP && !GRP) {   // U in a pass of its own, then the tile without U columns
+    hipLaunchKernelGGL((lora_u_kernel<RP, 32>), dim3((a.m + 31) / 32), dim3(512), 0, st, a.X, a.A, a.U, (int)a.m,
+                       (int)a.k, (int)a.r);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((lora_fwd_kernel<BM, BN, WM, WN, RP, false, false, true>), dim3(tiles_m * tiles_n),
+                       dim3(64 * WM * WN), 0, st, a.X, a.W, a.A, a.B, a.keep, a.Y, a.U, (int)a.m, (int)a.n, (int)a.k,
+                       (int)a.r, a.s, a.inv_keep, tiles_m, tiles_n, grp);
+    return hipGetLastError();
+  } else {
+    hipLaunchKernelGGL((lora_fwd_kernel<BM, BN, WM, WN, RP, DROP, GRP, false>), dim3(tiles_m * tiles_n),
+                       dim3(64 * WM * WN), 0, st, a.X, a.W, a.A, a.B, a.keep, a.Y, a.U, (int)a.m, (int)a.n, (int)a.k,
+                       (int)a.r, a.s, a.inv_keep, tiles_m, tiles_n, grp);
+    return hipGetLastError();
+  }
 }
 
 // Single projection: tiles_n from n.  Group: the column tiles of each
