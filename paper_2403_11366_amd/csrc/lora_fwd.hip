@@ -1,7 +1,16 @@
 // Forward of the LoRA-adapted linear layer (Eq. 1 of JORA, Section 3):
 //   U = X A^T,   Y = X W^T + s U B^T,   s = alpha / r.
 //
-// One kernel.  Each workgroup owns a BM x BN tile of Y (BM tokens x BN output
+// Kernels (one launch, or two for rank > 16):
+//   lora_fwd_ks_kernel  the 128 x 256 tile for rank <= 16 without dropout
+//                       (the 7B q_proj shape): wave pairs split the k
+//                       substeps of each stage, see its own comment.
+//   lora_fwd_kernel     the other tiles (256 x 256, 128 x 256, 128 x 128),
+//                       dropout and grouped launches; described below.
+//   lora_u_kernel       U = X A^T on its own for rank > 16, followed by
+//                       lora_fwd_kernel without U columns.
+//
+// lora_fwd_kernel: each workgroup owns a BM x BN tile of Y (BM tokens x BN output
 // features) and walks k in stages of 64.  Per stage it stages three
 // k-contiguous tiles in LDS -- X[BM rows], W[BN rows] and the LoRA
 // down-projection A padded to RP rows -- so each X tile is read once and
