@@ -63,17 +63,6 @@ __device__ __forceinline__ floatx16 mfma32x32x16(short8 a, short8 b, floatx16 c)
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16((bf16x8)a, (bf16x8)b, c, 0, 0, 0);
 }
 
-// Global -> LDS copy of 16 bytes per lane through a buffer resource: lane L's
-// bytes land at lds_base + 16 L (lds_base must be wave-uniform).  Out-of-range
-// offsets write zeros.  Completion is tracked by vmcnt.
-__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t rs, uint32_t byte_off, void* lds_base) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void*)lds_base, 16, byte_off, 0, 0, 0);
-}
-
-// Wait until this wave's outstanding vector-memory operations (including the
-// global -> LDS copies) have completed; other counters are not waited on.
-__device__ __forceinline__ void wait_vmcnt0() { __builtin_amdgcn_s_waitcnt(0x0F70); }
-
 __device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
 
 // 8-byte load through a buffer resource (byte_off a multiple of 8).
@@ -115,29 +104,6 @@ __device__ __forceinline__ uint32_t kc_offset(int row, int chunk) {
 
 __device__ __forceinline__ short8 kc_read(const char* tile, int row, int chunk) {
   return *reinterpret_cast<const short8*>(tile + kc_offset(row, chunk));
-}
-
-// ---- k-contiguous LDS tiles of 32 k (rows of 64 bytes = 4 chunks) ----------
-// Chunk q of row p sits at position q ^ ((p >> 2) & 3): the 16 rows read by 16
-// lanes in one cycle then cover all 64 banks.
-__device__ __forceinline__ int kc32_swz(int row) { return (row >> 2) & 3; }
-
-__device__ __forceinline__ uint32_t kc32_offset(int row, int chunk) {
-  return (uint32_t)(row * 64 + ((chunk ^ kc32_swz(row)) << 4));
-}
-
-__device__ __forceinline__ short8 kc32_read(const char* tile, int row, int chunk) {
-  return *reinterpret_cast<const short8*>(tile + kc32_offset(row, chunk));
-}
-
-// s_waitcnt with only the vector-memory count: wait until at most N of this
-// wave's vector-memory operations (global -> LDS copies included) are
-// outstanding.  gfx9 encoding: vmcnt[3:0] in bits 3:0, vmcnt[5:4] in bits 15:14,
-// expcnt (bits 6:4) and lgkmcnt (bits 11:8) left at their maxima.
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
 // ---- mn-contiguous LDS tiles (rows of COLS bf16, COLS >= 128) --------------
