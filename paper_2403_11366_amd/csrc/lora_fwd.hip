@@ -28,6 +28,8 @@
 // epilogue parks U in LDS, writes it out (tile column 0 only), and adds
 // s U B^T to the accumulators with a short matrix-core pass over t in which
 // s U enters as a bf16 high part and a bf16 low part, then rounds Y to bf16.
+#include <type_traits>
+
 #include "lora_device.hpp"
 #include "lora_launch.hpp"
 
@@ -534,7 +536,7 @@ __global__ __launch_bounds__(512) void lora_u_kernel(const u16* __restrict__ X, 
 // 64 x 64 block (features wn 128 + 64 wk ..) for the epilogue, which is the one
 // of the 2 x 4 layout.  GRP selects the projection of a grouped launch as in
 // lora_fwd_kernel.
-template <bool GRP>
+template <bool GRP, bool KFULL>
 __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
     const u16* __restrict__ X, const u16* __restrict__ W, const u16* __restrict__ A,
     const u16* __restrict__ B, u16* __restrict__ Y, float* __restrict__ U, int m, int n, int k, int r, float s,
@@ -587,21 +589,21 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
       for (int i = 0; i < LX; ++i) {
         const int q = tid + i * NT;
         const int kk = k0 + 8 * (q & 7);
-        gx[i] = buf_load16(rsX, kk < k ? (uint32_t)(q >> 3) * rowbytes + (uint32_t)kk * 2 : kOOB);
+        gx[i] = buf_load16(rsX, (KFULL || kk < k) ? (uint32_t)(q >> 3) * rowbytes + (uint32_t)kk * 2 : kOOB);
       }
 #pragma unroll
       for (int i = 0; i < LA; ++i) {
         const int q = tid + i * NT;
         if (CA % NT != 0 && wave * 64 + i * NT >= CA) break;
         const int kk = k0 + 8 * (q & 7);
-        ga[i] = buf_load16(rsA, kk < k ? (uint32_t)(q >> 3) * rowbytes + (uint32_t)kk * 2 : kOOB);
+        ga[i] = buf_load16(rsA, (KFULL || kk < k) ? (uint32_t)(q >> 3) * rowbytes + (uint32_t)kk * 2 : kOOB);
       }
     } else {
 #pragma unroll
       for (int i = 0; i < LW; ++i) {
         const int q = tid + i * NT;
         const int kk = k0 + 8 * (q & 7);
-        gw[i] = buf_load16(rsW, kk < k ? (uint32_t)(q >> 3) * rowbytes + (uint32_t)kk * 2 : kOOB);
+        gw[i] = buf_load16(rsW, (KFULL || kk < k) ? (uint32_t)(q >> 3) * rowbytes + (uint32_t)kk * 2 : kOOB);
       }
     }
   };
@@ -672,18 +674,23 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
   // top of stage kb the registers hold block kb+1; each piece is stored to the
   // free buffer and reloaded with block kb+2; fragments of substep 1 are read
   // while substep 0 multiplies.
-  auto stage = [&](int kb, bool write_next, bool load_next) {
-    const char* sb = smem + (kb & 1) * STAGE;
+  auto stage = [&](int kb, auto bufc, bool write_next, bool load_next) {
+    constexpr int BUF = decltype(bufc)::value;    // -1: the buffer of kb's parity at run time
+    const int cur = BUF >= 0 ? BUF : (kb & 1);
+    const char* sb = smem + cur * STAGE;
     read_frags(sb, 0, 0);
-    if (write_next) swrite((kb + 1) & 1, 0);
+    if (write_next) swrite(cur ^ 1, 0);
     if (load_next) gload(kb + 2, 0);
     read_frags(sb, 1, 1);
     multiply(0, 0);
-    if (write_next) swrite((kb + 1) & 1, 1);
+    if (write_next) swrite(cur ^ 1, 1);
     if (load_next) gload(kb + 2, 1);
     multiply(1, 1);
     __syncthreads();
   };
+  using B0 = std::integral_constant<int, 0>;
+  using B1 = std::integral_constant<int, 1>;
+  using BR = std::integral_constant<int, -1>;
   const int nkb = (k + 63) / 64;
   gload(0, 0);
   gload(0, 1);
@@ -695,9 +702,23 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
     gload(1, 1);
   }
   int kb = 0;
-  for (; kb + 2 < nkb; ++kb) stage(kb, true, true);
-  if (kb + 1 < nkb) stage(kb++, true, false);
-  stage(kb, false, false);
+  if constexpr (KFULL) {
+    // k a multiple of 64: no bound checks on the loads, and stages in pairs
+    // so that the LDS buffer of every stage is a compile-time constant (its
+    // offset rides in the instructions' immediates).  kb is even after the
+    // loop and at most three stages remain.
+    for (; kb + 3 < nkb; kb += 2) {
+      stage(kb, B0{}, true, true);
+      stage(kb + 1, B1{}, true, true);
+    }
+    if (kb < nkb) stage(kb, B0{}, kb + 1 < nkb, kb + 2 < nkb);
+    if (kb + 1 < nkb) stage(kb + 1, B1{}, kb + 2 < nkb, kb + 3 < nkb);
+    if (kb + 2 < nkb) stage(kb + 2, B0{}, false, false);
+  } else {
+    for (; kb + 2 < nkb; ++kb) stage(kb, BR{}, true, true);
+    if (kb + 1 < nkb) stage(kb++, BR{}, true, false);
+    stage(kb, BR{}, false, false);
+  }
 
   // ---- exchange of the k-half partial sums (LDS is free after the loop's
   // last barrier): region (pair, h) holds, for the wave of the pair that keeps
@@ -868,8 +889,12 @@ static hipError_t launch_fwd_rp(const FwdArgs& a, FwdGroup grp, hipStream_t st) 
   }
   if (BM == 128 && BN == 256 && !DROP && a.r <= 16) {
     const int tiles_m = (int)((a.m + BM - 1) / BM);
-    hipLaunchKernelGGL((lora_fwd_ks_kernel<GRP>), dim3(tiles_m * tiles_n), dim3(512), 0, st, a.X, a.W, a.A, a.B,
-                       a.Y, a.U, (int)a.m, (int)a.n, (int)a.k, (int)a.r, a.s, tiles_m, tiles_n, grp);
+    if (a.k % 64 == 0)
+      hipLaunchKernelGGL((lora_fwd_ks_kernel<GRP, true>), dim3(tiles_m * tiles_n), dim3(512), 0, st, a.X, a.W, a.A,
+                         a.B, a.Y, a.U, (int)a.m, (int)a.n, (int)a.k, (int)a.r, a.s, tiles_m, tiles_n, grp);
+    else
+      hipLaunchKernelGGL((lora_fwd_ks_kernel<GRP, false>), dim3(tiles_m * tiles_n), dim3(512), 0, st, a.X, a.W, a.A,
+                         a.B, a.Y, a.U, (int)a.m, (int)a.n, (int)a.k, (int)a.r, a.s, tiles_m, tiles_n, grp);
     return hipGetLastError();
   }
   if (a.r <= 16) return launch_fwd_cfg<BM, BN, WM, WN, 16, DROP, GRP>(a, grp, tiles_n, st);
