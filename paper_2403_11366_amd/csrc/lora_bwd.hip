@@ -19,6 +19,8 @@
 //             sums a slice of the dB and dA partials in a fixed order (no
 //             atomics, so results are bit-identical from run to run) and
 //             applies s to dB.
+#include <type_traits>
+
 #include "lora_device.hpp"
 #include "lora_launch.hpp"
 
@@ -414,7 +416,11 @@ struct DxGroup {
 // With GRP (DxGroup) the n stages of all projections of a group form the k
 // loop, each stage loading from its own projection's dY_g and W_g; the slab
 // stages are skipped and each dU_g A_g is added after the loop from LDS.
-template <int BM, int BN, int WM, int WN, int RP, bool DROP, bool GRP>
+//
+// FULL (every n a multiple of 64 and k of BN): the n-stage loads carry no
+// bound checks, and below the 256 x 256 tile the n stages run in pairs with
+// compile-time LDS buffers.
+template <int BM, int BN, int WM, int WN, int RP, bool DROP, bool GRP, bool FULL>
 __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
     const u16* __restrict__ dY, const u16* __restrict__ W, const u16* __restrict__ dU2,
     const u16* __restrict__ A, const uint8_t* __restrict__ keep, u16* __restrict__ dX, int m, int n, int k,
@@ -492,7 +498,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
         const int q = tid + i * NT;
         if (CY % NT != 0 && wave * 64 + i * NT >= CY) break;   // wave-uniform
         const int nn = n0 + 8 * (q & 7);
-        gy[i] = buf_load16(rsYs, nn < ns ? (uint32_t)(q >> 3) * yr + (uint32_t)nn * 2 : kOOB);
+        gy[i] = buf_load16(rsYs, (FULL || nn < ns) ? (uint32_t)(q >> 3) * yr + (uint32_t)nn * 2 : kOOB);
       }
     } else if (piece <= 2) {
       const __amdgpu_buffer_rsrc_t rsW = make_rsrc(Wp + (size_t)n0 * k, (uint64_t)min(64, ns - n0) * wrow);
@@ -501,7 +507,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
         const int q = tid + i * NT;
         if (CW % NT != 0 && wave * 64 + i * NT >= CW) break;   // wave-uniform
         const int ll = l0 + 8 * (q % CPR);
-        gw[i] = buf_load16(rsW, ll < k ? (uint32_t)(q / CPR) * wrow + (uint32_t)ll * 2 : kOOB);
+        gw[i] = buf_load16(rsW, (FULL || ll < k) ? (uint32_t)(q / CPR) * wrow + (uint32_t)ll * 2 : kOOB);
       }
     }
   };
@@ -585,13 +591,17 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
     for (int j = 0; j < FI; ++j) fy[1][j] = short8{};
   }
   enum { LD_NONE, LD_W, LD_S0, LD_S1 };
-  auto stage = [&](int st, bool write_next, int load) {
-    const char* sb = smem + (st & 1) * STAGE;
+  // bufc: the stage's LDS buffer as a compile-time constant, or -1 for the
+  // parity of st at run time
+  auto stage = [&](int st, auto bufc, bool write_next, int load) {
+    constexpr int BUF = decltype(bufc)::value;
+    const int cur = BUF >= 0 ? BUF : (st & 1);
+    const char* sb = smem + cur * STAGE;
     read_frags(sb, 0, 0);
     if (ROT) multiply(1);
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
-      if (write_next) swrite((st + 1) & 1, ks);
+      if (write_next) swrite(cur ^ 1, ks);
       if (load == LD_W) gload_w(st + 2, ks);
       if (load == LD_S0) gload_s(0, ks);
       if (load == LD_S1) gload_s(1, ks);
@@ -606,19 +616,29 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
   for (int pc = 0; pc < 3; ++pc) swrite(0, pc);
   __syncthreads();
   constexpr int NSL = (DROP || GRP) ? 0 : NSLAB;   // slab stages in the k loop
+  using B0 = std::integral_constant<int, 0>;
+  using B1 = std::integral_constant<int, 1>;
+  using BR = std::integral_constant<int, -1>;
   int st = 0;
   if (nkb >= 2) {
 #pragma unroll
     for (int pc = 0; pc < 3; ++pc) gload_w(1, pc);
-    for (; st + 2 < nkb; ++st) stage(st, true, LD_W);
-    stage(st++, true, NSL > 0 ? LD_S0 : LD_NONE);   // st = nkb - 2
+    if constexpr (FULL && BM * BN < 256 * 256) {   // the 256 x 256 tile has no registers for the pairs
+      for (; st + 3 < nkb; st += 2) {
+        stage(st, B0{}, true, LD_W);
+        stage(st + 1, B1{}, true, LD_W);
+      }
+    }
+    for (; st + 2 < nkb; ++st) stage(st, BR{}, true, LD_W);
+    stage(st, BR{}, true, NSL > 0 ? LD_S0 : LD_NONE);   // st = nkb - 2
+    ++st;
   } else if (NSL > 0) {
 #pragma unroll
     for (int pc = 0; pc < 3; ++pc) gload_s(0, pc);
   }
-  if (NSL > 0) stage(st++, true, NSL > 1 ? LD_S1 : LD_NONE);   // writes slab 0
-  if (NSL > 1) stage(st++, true, LD_NONE);                     // writes slab 1
-  stage(st, false, LD_NONE);
+  if (NSL > 0) stage(st++, BR{}, true, NSL > 1 ? LD_S1 : LD_NONE);   // writes slab 0
+  if (NSL > 1) stage(st++, BR{}, true, LD_NONE);                     // writes slab 1
+  stage(st, BR{}, false, LD_NONE);
   if (ROT) multiply(1);
 
   if (GRP) {
@@ -761,9 +781,20 @@ static hipError_t launch_dx_cfg(const BwdArgs& a, const BwdLayout& L, const Fina
   const int tiles_m = (int)((a.m + BM - 1) / BM), tiles_n = (int)((a.k + BN - 1) / BN);
   const int nt = 64 * WM * WN;
   const u16* dU2 = GRP ? nullptr : reinterpret_cast<const u16*>(a.ws + L.du2);
-  hipLaunchKernelGGL((lora_bwd_dx_kernel<BM, BN, WM, WN, RP, DROP, GRP>), dim3(tiles_m * tiles_n), dim3(nt), 0, st,
-                     a.dY, a.W, dU2, a.A, a.keep, a.dX, (int)a.m, (int)a.n, (int)a.k, (int)a.r, (int)L.mp,
-                     a.inv_keep, tiles_m, tiles_n, fin, grp);
+  bool full = a.k % BN == 0;
+  if (GRP) {
+    for (int g = 0; g < grp.count; ++g) full = full && grp.n[g] % 64 == 0;
+  } else {
+    full = full && a.n % 64 == 0;
+  }
+  if (full)
+    hipLaunchKernelGGL((lora_bwd_dx_kernel<BM, BN, WM, WN, RP, DROP, GRP, true>), dim3(tiles_m * tiles_n), dim3(nt),
+                       0, st, a.dY, a.W, dU2, a.A, a.keep, a.dX, (int)a.m, (int)a.n, (int)a.k, (int)a.r, (int)L.mp,
+                       a.inv_keep, tiles_m, tiles_n, fin, grp);
+  else
+    hipLaunchKernelGGL((lora_bwd_dx_kernel<BM, BN, WM, WN, RP, DROP, GRP, false>), dim3(tiles_m * tiles_n),
+                       dim3(nt), 0, st, a.dY, a.W, dU2, a.A, a.keep, a.dX, (int)a.m, (int)a.n, (int)a.k, (int)a.r,
+                       (int)L.mp, a.inv_keep, tiles_m, tiles_n, fin, grp);
   return hipGetLastError();
 }
 
