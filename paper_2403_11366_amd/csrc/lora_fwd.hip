@@ -41,7 +41,10 @@ namespace lora {
 //
 // With UPRE, U = X A^T has been computed by lora_u_kernel: the k loop stages
 // no A rows and runs no U products, and the epilogue reads U back.
-template <int BM, int BN, int WM, int WN, int RP, bool DROP, bool GRP, bool UPRE>
+//
+// KFULL (k a multiple of 64): the loads carry no k-bound checks, and below the
+// 256 x 256 tile the stages run in pairs with compile-time LDS buffers.
+template <int BM, int BN, int WM, int WN, int RP, bool DROP, bool GRP, bool UPRE, bool KFULL>
 __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
     const u16* __restrict__ X, const u16* __restrict__ W, const u16* __restrict__ A,
     const u16* __restrict__ B, const uint8_t* __restrict__ keep, u16* __restrict__ Y,
@@ -130,7 +133,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
         const int q = tid + i * NT;
         if (CX % NT != 0 && wave * 64 + i * NT >= CX) break;   // wave-uniform
         const int kk = k0 + 8 * (q & 7);
-        gx[i] = buf_load16(rsX, kk < k ? (uint32_t)(q >> 3) * rowbytes + (uint32_t)kk * 2 : kOOB);
+        gx[i] = buf_load16(rsX, (KFULL || kk < k) ? (uint32_t)(q >> 3) * rowbytes + (uint32_t)kk * 2 : kOOB);
       }
     } else if (piece <= 2) {
 #pragma unroll
@@ -138,7 +141,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
         const int q = tid + i * NT;
         if (CW % NT != 0 && wave * 64 + i * NT >= CW) break;   // wave-uniform
         const int kk = k0 + 8 * (q & 7);
-        gw[i] = buf_load16(rsW, kk < k ? (uint32_t)(q >> 3) * rowbytes + (uint32_t)kk * 2 : kOOB);
+        gw[i] = buf_load16(rsW, (KFULL || kk < k) ? (uint32_t)(q >> 3) * rowbytes + (uint32_t)kk * 2 : kOOB);
       }
     } else if (!UPRE) {
 #pragma unroll
@@ -146,7 +149,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
         const int q = tid + i * NT;
         if (CA % NT != 0 && wave * 64 + i * NT >= CA) break;   // wave-uniform
         const int kk = k0 + 8 * (q & 7);
-        ga[i] = buf_load16(rsA, kk < k ? (uint32_t)(q >> 3) * rowbytes + (uint32_t)kk * 2 : kOOB);
+        ga[i] = buf_load16(rsA, (KFULL || kk < k) ? (uint32_t)(q >> 3) * rowbytes + (uint32_t)kk * 2 : kOOB);
       }
     }
   };
@@ -278,13 +281,17 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
 #pragma unroll
     for (int j = 0; j < GPW; ++j) fxu16[1][j] = short8{};
   }
-  auto stage = [&](int kb, bool write_next, bool load_next) {
-    const char* sb = smem + (kb & 1) * STAGE;
+  // bufc: the stage's LDS buffer as a compile-time constant, or -1 for the
+  // parity of kb at run time
+  auto stage = [&](int kb, auto bufc, bool write_next, bool load_next) {
+    constexpr int BUF = decltype(bufc)::value;
+    const int cur = BUF >= 0 ? BUF : (kb & 1);
+    const char* sb = smem + cur * STAGE;
     read_frags(sb, 0, 0);
     if (ROT) multiply(1, 3);
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
-      if (write_next) swrite((kb + 1) & 1, ks);
+      if (write_next) swrite(cur ^ 1, ks);
       if (load_next) gload(kb + 2, ks);
       if (ks < 3) read_frags(sb, ks + 1, (ks + 1) & 1);
       if (ks < 3 || !ROT) multiply(ks & 1, ks);
@@ -301,10 +308,19 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
 #pragma unroll
     for (int pc = 0; pc < 4; ++pc) gload(1, pc);
   }
+  using B0 = std::integral_constant<int, 0>;
+  using B1 = std::integral_constant<int, 1>;
+  using BR = std::integral_constant<int, -1>;
   int kb = 0;
-  for (; kb + 2 < nkb; ++kb) stage(kb, true, true);
-  if (kb + 1 < nkb) stage(kb++, true, false);
-  stage(kb, false, false);
+  if constexpr (KFULL && BM * BN < 256 * 256) {
+    for (; kb + 3 < nkb; kb += 2) {
+      stage(kb, B0{}, true, true);
+      stage(kb + 1, B1{}, true, true);
+    }
+  }
+  for (; kb + 2 < nkb; ++kb) stage(kb, BR{}, true, true);
+  if (kb + 1 < nkb) stage(kb++, BR{}, true, false);
+  stage(kb, BR{}, false, false);
   if (ROT) multiply(1, 3);
 
   // ---- epilogue ------------------------------------------------------------
@@ -862,14 +878,24 @@ static hipError_t launch_fwd_cfg(const FwdArgs& a, const FwdGroup& grp, int tile
                        (int)a.k, (int)a.r);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((lora_fwd_kernel<BM, BN, WM, WN, RP, false, false, true>), dim3(tiles_m * tiles_n),
-                       dim3(64 * WM * WN), 0, st, a.X, a.W, a.A, a.B, a.keep, a.Y, a.U, (int)a.m, (int)a.n, (int)a.k,
-                       (int)a.r, a.s, a.inv_keep, tiles_m, tiles_n, grp);
+    if (a.k % 64 == 0)
+      hipLaunchKernelGGL((lora_fwd_kernel<BM, BN, WM, WN, RP, false, false, true, true>), dim3(tiles_m * tiles_n),
+                         dim3(64 * WM * WN), 0, st, a.X, a.W, a.A, a.B, a.keep, a.Y, a.U, (int)a.m, (int)a.n, (int)a.k,
+                         (int)a.r, a.s, a.inv_keep, tiles_m, tiles_n, grp);
+    else
+      hipLaunchKernelGGL((lora_fwd_kernel<BM, BN, WM, WN, RP, false, false, true, false>), dim3(tiles_m * tiles_n),
+                         dim3(64 * WM * WN), 0, st, a.X, a.W, a.A, a.B, a.keep, a.Y, a.U, (int)a.m, (int)a.n, (int)a.k,
+                         (int)a.r, a.s, a.inv_keep, tiles_m, tiles_n, grp);
     return hipGetLastError();
   } else {
-    hipLaunchKernelGGL((lora_fwd_kernel<BM, BN, WM, WN, RP, DROP, GRP, false>), dim3(tiles_m * tiles_n),
-                       dim3(64 * WM * WN), 0, st, a.X, a.W, a.A, a.B, a.keep, a.Y, a.U, (int)a.m, (int)a.n, (int)a.k,
-                       (int)a.r, a.s, a.inv_keep, tiles_m, tiles_n, grp);
+    if (a.k % 64 == 0)
+      hipLaunchKernelGGL((lora_fwd_kernel<BM, BN, WM, WN, RP, DROP, GRP, false, true>), dim3(tiles_m * tiles_n),
+                         dim3(64 * WM * WN), 0, st, a.X, a.W, a.A, a.B, a.keep, a.Y, a.U, (int)a.m, (int)a.n, (int)a.k,
+                         (int)a.r, a.s, a.inv_keep, tiles_m, tiles_n, grp);
+    else
+      hipLaunchKernelGGL((lora_fwd_kernel<BM, BN, WM, WN, RP, DROP, GRP, false, false>), dim3(tiles_m * tiles_n),
+                         dim3(64 * WM * WN), 0, st, a.X, a.W, a.A, a.B, a.keep, a.Y, a.U, (int)a.m, (int)a.n, (int)a.k,
+                         (int)a.r, a.s, a.inv_keep, tiles_m, tiles_n, grp);
     return hipGetLastError();
   }
 }
