@@ -417,8 +417,8 @@ struct DxGroup {
 // loop, each stage loading from its own projection's dY_g and W_g; the slab
 // stages are skipped and each dU_g A_g is added after the loop from LDS.
 //
-// FULL (every n a multiple of 64 and k of BN): the n-stage loads carry no
-// bound checks, and below the 256 x 256 tile the n stages run in pairs with
+// FULL (every n a multiple of 64 and k of BN; tiles below 256 x 256): the
+// n-stage loads carry no bound checks and the n stages run in pairs with
 // compile-time LDS buffers.
 template <int BM, int BN, int WM, int WN, int RP, bool DROP, bool GRP, bool FULL>
 __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
@@ -623,7 +623,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
   if (nkb >= 2) {
 #pragma unroll
     for (int pc = 0; pc < 3; ++pc) gload_w(1, pc);
-    if constexpr (FULL && BM * BN < 256 * 256) {   // the 256 x 256 tile has no registers for the pairs
+    if constexpr (FULL) {
       for (; st + 3 < nkb; st += 2) {
         stage(st, B0{}, true, LD_W);
         stage(st + 1, B1{}, true, LD_W);
@@ -781,7 +781,8 @@ static hipError_t launch_dx_cfg(const BwdArgs& a, const BwdLayout& L, const Fina
   const int tiles_m = (int)((a.m + BM - 1) / BM), tiles_n = (int)((a.k + BN - 1) / BN);
   const int nt = 64 * WM * WN;
   const u16* dU2 = GRP ? nullptr : reinterpret_cast<const u16*>(a.ws + L.du2);
-  bool full = a.k % BN == 0;
+  // (the 256 x 256 tile measured no faster without the checks, and spilled more)
+  bool full = a.k % BN == 0 && BM * BN < 256 * 256;
   if (GRP) {
     for (int g = 0; g < grp.count; ++g) full = full && grp.n[g] % 64 == 0;
   } else {
