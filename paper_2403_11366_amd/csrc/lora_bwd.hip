@@ -782,17 +782,20 @@ static hipError_t launch_dx_cfg(const BwdArgs& a, const BwdLayout& L, const Fina
   const int nt = 64 * WM * WN;
   const u16* dU2 = GRP ? nullptr : reinterpret_cast<const u16*>(a.ws + L.du2);
   // (the 256 x 256 tile measured no faster without the checks, and spilled more)
-  bool full = a.k % BN == 0 && BM * BN < 256 * 256;
-  if (GRP) {
-    for (int g = 0; g < grp.count; ++g) full = full && grp.n[g] % 64 == 0;
-  } else {
-    full = full && a.n % 64 == 0;
+  bool full = false;
+  if constexpr (BM * BN < 256 * 256) {
+    full = a.k % BN == 0;
+    if (GRP) {
+      for (int g = 0; g < grp.count; ++g) full = full && grp.n[g] % 64 == 0;
+    } else {
+      full = full && a.n % 64 == 0;
+    }
+    if (full)
+      hipLaunchKernelGGL((lora_bwd_dx_kernel<BM, BN, WM, WN, RP, DROP, GRP, true>), dim3(tiles_m * tiles_n),
+                         dim3(nt), 0, st, a.dY, a.W, dU2, a.A, a.keep, a.dX, (int)a.m, (int)a.n, (int)a.k, (int)a.r,
+                         (int)L.mp, a.inv_keep, tiles_m, tiles_n, fin, grp);
   }
-  if (full)
-    hipLaunchKernelGGL((lora_bwd_dx_kernel<BM, BN, WM, WN, RP, DROP, GRP, true>), dim3(tiles_m * tiles_n), dim3(nt),
-                       0, st, a.dY, a.W, dU2, a.A, a.keep, a.dX, (int)a.m, (int)a.n, (int)a.k, (int)a.r, (int)L.mp,
-                       a.inv_keep, tiles_m, tiles_n, fin, grp);
-  else
+  if (!full)
     hipLaunchKernelGGL((lora_bwd_dx_kernel<BM, BN, WM, WN, RP, DROP, GRP, false>), dim3(tiles_m * tiles_n),
                        dim3(nt), 0, st, a.dY, a.W, dU2, a.A, a.keep, a.dX, (int)a.m, (int)a.n, (int)a.k, (int)a.r,
                        (int)L.mp, a.inv_keep, tiles_m, tiles_n, fin, grp);
