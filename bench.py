@@ -337,7 +337,7 @@ def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=100)
     ap.add_argument("--config", default="llama2_7b_q_proj")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -460,12 +460,21 @@ def main():
         step(i)
     torch.cuda.synchronize()
     log(f"[bench] warmup {args.warmup} steps done; timing {args.steps} steps")
+    # HIP events split the timed steps into 5 repetitions (recorded on the
+    # stream, no synchronisation inside the timed region)
+    nrep = 5 if args.steps >= 5 else 1
+    marks = [round(j * args.steps / nrep) for j in range(nrep + 1)]
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(nrep + 1)]
     t0 = time.perf_counter()
+    evs[0].record(stream)
     for i in range(args.steps):
         step(i)
+        if i + 1 in marks:
+            evs[marks.index(i + 1)].record(stream)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     ms_per_step = elapsed / args.steps * 1e3
+    rep_ms = [evs[j].elapsed_time(evs[j + 1]) / (marks[j + 1] - marks[j]) for j in range(nrep)]
     flops = sum(s.flops_fwd_bwd for s, _, _ in proj)
     tflops = flops / (ms_per_step / 1e3) / 1e12
     log(f"[bench] {ms_per_step * 1e3:.1f} us/step, {tflops:.1f} TFLOP/s")
@@ -526,6 +535,9 @@ def main():
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                      "traffic": traffic, "flops_per_launch": k1_flops, "avg_launch_us": round(fwd_us, 2)},
         "bwd_call_us": round(bwd_us, 2),
+        "repetitions": {"count": nrep, "ms_per_step": [round(x, 4) for x in rep_ms],
+                        "median": round(sorted(rep_ms)[nrep // 2], 4),
+                        "std": round((sum((x - sum(rep_ms) / nrep) ** 2 for x in rep_ms) / nrep) ** 0.5, 4)},
         "cpu_baseline": cpu,
     }
     print(json.dumps(rec), flush=True)
