@@ -117,6 +117,31 @@ def test_integer_inputs_bit_exact(shape):
     assert np.array_equal(out["dB"].astype(np.float64), dB)
 
 
+# Pipeline depth of the large GEMMs: the tiles of the k-split forward (m=2000,
+# n=2304) and of the dX kernel (m=2000, k=2304) with 1 to 7 stages of 64 along
+# their reduction (k for the forward, n for dX), whole and ragged, so that
+# every prologue and tail of the LDS pipeline is exercised.
+DEPTH = ([Shape("fdepth", 2000, 2304, k, 8, 8.0, 600 + k) for k in (64, 128, 192, 256, 320, 384, 448)]
+         + [Shape("fdepth", 2000, 2304, k, r, float(r), 700 + k) for k, r in ((8, 5), (72, 16), (200, 13), (328, 8))]
+         + [Shape("xdepth", 2000, n, 2304, 8, 8.0, 800 + n) for n in (64, 128, 192, 256, 320, 384, 448)]
+         + [Shape("xdepth", 2000, n, 2304, r, float(r), 900 + n) for n, r in ((8, 3), (136, 16), (264, 8))])
+
+
+@pytest.mark.parametrize("shape", DEPTH, ids=_shape_id)
+def test_pipeline_depths_bit_exact(shape):
+    """Integer inputs as above (s = 1), bit for bit, at every pipeline depth."""
+    t = gen_ternary_inputs(shape.m, shape.n, shape.k, shape.r, shape.seed, density=0.1)
+    U, Y = oracle.lora_forward(t["X"], t["W"], t["A"], t["B"], shape.alpha)
+    dU, dX, dA, dB = oracle.lora_backward(t["dY"], t["X"], t["W"], t["A"], t["B"], shape.alpha)
+    assert np.abs(Y).max() <= 256 and np.abs(dX).max() <= 256 and np.abs(dU).max() <= 256
+    out = run_gpu(t, shape)
+    assert np.array_equal(out["Y"], oracle.f64_to_bf16_bits(Y))
+    assert np.array_equal(out["dX"], oracle.f64_to_bf16_bits(dX))
+    assert np.array_equal(out["U"].astype(np.float64), U)
+    assert np.array_equal(out["dA"].astype(np.float64), dA)
+    assert np.array_equal(out["dB"].astype(np.float64), dB)
+
+
 def test_hand_example_embedded():
     """The first hand-worked example of tests/golden, zero-padded to 64 x 64 x 64."""
     shape = Shape("hand", 64, 64, 64, 1, 2.0, 0)
