@@ -424,7 +424,7 @@ template <int BM, int BN, int WM, int WN, int RP, bool DROP, bool GRP, bool FULL
 __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
     const u16* __restrict__ dY, const u16* __restrict__ W, const u16* __restrict__ dU2,
     const u16* __restrict__ A, const uint8_t* __restrict__ keep, u16* __restrict__ dX, int m, int n, int k,
-    int r, int mp, float inv_keep, int tiles_m, int tiles_n, FinalizeArgs fin, DxGroup grp) {
+    int r, int mp, float inv_keep, int tiles_m, int tiles_n, int l_begin, FinalizeArgs fin, DxGroup grp) {
   constexpr int NW = WM * WN;
   constexpr int NT = 64 * NW;
   constexpr int WTI = BM / WM, WTJ = BN / WN;
@@ -444,7 +444,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
 
   int tm, tn;
   tile_coords(tiles_m, tiles_n, 8, (int)blockIdx.x, tm, tn);
-  const int m0 = tm * BM, l0 = tn * BN;
+  const int m0 = tm * BM, l0 = l_begin + tn * BN;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = uniform(tid >> 6);
   const int wm = wave / WN, wn = wave % WN;
@@ -775,16 +775,19 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
 }
 
 // ---------------------------------------------------------------------------
+// dX columns [l_begin, l_end) with one tile; the workgroups' tails also
+// finalize the dA and dB partials described by fin (none when fin is empty).
 template <int BM, int BN, int WM, int WN, int RP, bool DROP, bool GRP>
 static hipError_t launch_dx_cfg(const BwdArgs& a, const BwdLayout& L, const FinalizeArgs& fin, const DxGroup& grp,
-                                hipStream_t st) {
-  const int tiles_m = (int)((a.m + BM - 1) / BM), tiles_n = (int)((a.k + BN - 1) / BN);
+                                int64_t l_begin, int64_t l_end, hipStream_t st) {
+  const int tiles_m = (int)((a.m + BM - 1) / BM), tiles_n = (int)((l_end - l_begin + BN - 1) / BN);
   const int nt = 64 * WM * WN;
+  const int lb = (int)l_begin;
   const u16* dU2 = GRP ? nullptr : reinterpret_cast<const u16*>(a.ws + L.du2);
   // (the 256 x 256 tile measured no faster without the checks, and spilled more)
   bool full = false;
   if constexpr (BM * BN < 256 * 256) {
-    full = a.k % BN == 0;
+    full = (l_end - l_begin) % BN == 0 && l_end <= a.k;
     if (GRP) {
       for (int g = 0; g < grp.count; ++g) full = full && grp.n[g] % 64 == 0;
     } else {
@@ -793,12 +796,12 @@ static hipError_t launch_dx_cfg(const BwdArgs& a, const BwdLayout& L, const Fina
     if (full)
       hipLaunchKernelGGL((lora_bwd_dx_kernel<BM, BN, WM, WN, RP, DROP, GRP, true>), dim3(tiles_m * tiles_n),
                          dim3(nt), 0, st, a.dY, a.W, dU2, a.A, a.keep, a.dX, (int)a.m, (int)a.n, (int)a.k, (int)a.r,
-                         (int)L.mp, a.inv_keep, tiles_m, tiles_n, fin, grp);
+                         (int)L.mp, a.inv_keep, tiles_m, tiles_n, lb, fin, grp);
   }
   if (!full)
     hipLaunchKernelGGL((lora_bwd_dx_kernel<BM, BN, WM, WN, RP, DROP, GRP, false>), dim3(tiles_m * tiles_n),
                        dim3(nt), 0, st, a.dY, a.W, dU2, a.A, a.keep, a.dX, (int)a.m, (int)a.n, (int)a.k, (int)a.r,
-                       (int)L.mp, a.inv_keep, tiles_m, tiles_n, fin, grp);
+                       (int)L.mp, a.inv_keep, tiles_m, tiles_n, lb, fin, grp);
   return hipGetLastError();
 }
 
@@ -845,16 +848,24 @@ static hipError_t launch_bwd_rp(const BwdArgs& a, const BwdLayout& L, hipStream_
   if (e != hipSuccess) return e;
   const FinalizeArgs fin = finalize_args<RP>(a, L);
   const DxGroup none{};
-  const GemmTile t = choose_gemm_tile(a.m, a.k);
   if (a.keep) {   // the 256 x 256 tile has no registers left for the dropout epilogue
-    if (t == TILE_128x128) return launch_dx_cfg<128, 128, 2, 2, RP, true, false>(a, L, fin, none, st);
-    return launch_dx_cfg<128, 256, 2, 4, RP, true, false>(a, L, fin, none, st);
+    if (choose_gemm_tile(a.m, a.k) == TILE_128x128)
+      return launch_dx_cfg<128, 128, 2, 2, RP, true, false>(a, L, fin, none, 0, a.k, st);
+    return launch_dx_cfg<128, 256, 2, 4, RP, true, false>(a, L, fin, none, 0, a.k, st);
   }
-  switch (t) {
-    case TILE_256x256: return launch_dx_cfg<256, 256, 2, 4, RP, false, false>(a, L, fin, none, st);
-    case TILE_128x256: return launch_dx_cfg<128, 256, 2, 4, RP, false, false>(a, L, fin, none, st);
-    default: return launch_dx_cfg<128, 128, 2, 2, RP, false, false>(a, L, fin, none, st);
-  }
+  // Columns of dX split between two launches as for the forward; the first
+  // launch's tails finalize dA and dB.
+  auto tile = [&](GemmTile t, const FinalizeArgs& f, int64_t lb, int64_t le) {
+    switch (t) {
+      case TILE_256x256: return launch_dx_cfg<256, 256, 2, 4, RP, false, false>(a, L, f, none, lb, le, st);
+      case TILE_128x256: return launch_dx_cfg<128, 256, 2, 4, RP, false, false>(a, L, f, none, lb, le, st);
+      default: return launch_dx_cfg<128, 128, 2, 2, RP, false, false>(a, L, f, none, lb, le, st);
+    }
+  };
+  const GemmSplit p = plan_gemm_split(a.m, a.k);
+  e = tile(p.t1, fin, 0, p.n1);
+  if (e != hipSuccess || p.n1 >= a.k) return e;
+  return tile(p.t2, FinalizeArgs{}, p.n1, a.k);
 }
 
 hipError_t launch_bwd(const BwdArgs& a, hipStream_t st) {
@@ -898,8 +909,8 @@ static hipError_t launch_bwd_group_rp(const GroupBwdArgs& a, const GroupBwdLayou
   // lookup; the group runs 128 x 256 in its place.
   const FinalizeArgs none{};
   if (choose_gemm_tile(a.m, a.k) == TILE_128x128)
-    return launch_dx_cfg<128, 128, 2, 2, RP, false, true>(d, GL.L[0], none, grp, st);
-  return launch_dx_cfg<128, 256, 2, 4, RP, false, true>(d, GL.L[0], none, grp, st);
+    return launch_dx_cfg<128, 128, 2, 2, RP, false, true>(d, GL.L[0], none, grp, 0, a.k, st);
+  return launch_dx_cfg<128, 256, 2, 4, RP, false, true>(d, GL.L[0], none, grp, 0, a.k, st);
 }
 
 hipError_t launch_bwd_group(const GroupBwdArgs& a, hipStream_t st) {

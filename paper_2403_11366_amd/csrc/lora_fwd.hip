@@ -49,7 +49,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
     const u16* __restrict__ X, const u16* __restrict__ W, const u16* __restrict__ A,
     const u16* __restrict__ B, const uint8_t* __restrict__ keep, u16* __restrict__ Y,
     float* __restrict__ U, int m, int n, int k, int r, float s, float inv_keep, int tiles_m, int tiles_n,
-    FwdGroup grp) {
+    int n_begin, FwdGroup grp) {
   constexpr int NW = WM * WN;
   constexpr int NT = 64 * NW;
   constexpr int WTI = BM / WM, WTJ = BN / WN;   // tokens, features per wave
@@ -100,7 +100,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
         tn -= grp.tile0[q];
       }
   }
-  const int m0 = tm * BM, n0 = tn * BN;
+  const int m0 = tm * BM, n0 = n_begin + tn * BN;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = uniform(tid >> 6);
   const int wm = wave / WN, wn = wave % WN;
@@ -394,7 +394,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
     }
   }
   __syncthreads();
-  if (tn == 0 && !UPRE) {   // U output: one tile column writes it
+  if (n0 == 0 && !UPRE) {   // U output: the first tile column writes it
     for (int e = tid; e < BM * RP; e += NT) {
       const int il = e / RP, t = e - il * RP;
       if (m0 + il < m && t < r) U[(size_t)(m0 + il) * r + t] = Us[e];
@@ -556,7 +556,7 @@ template <bool GRP, bool KFULL>
 __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
     const u16* __restrict__ X, const u16* __restrict__ W, const u16* __restrict__ A,
     const u16* __restrict__ B, u16* __restrict__ Y, float* __restrict__ U, int m, int n, int k, int r, float s,
-    int tiles_m, int tiles_n, FwdGroup grp) {
+    int tiles_m, int tiles_n, int n_begin, FwdGroup grp) {
   constexpr int BM = 128, BN = 256, NT = 512, RP = 16;
   constexpr int WTI = 64, WTJ = 128, FI = 2, FJ = 4;
   constexpr int GPW = 2;                          // 16-token U groups per wave
@@ -583,7 +583,7 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
         tn -= grp.tile0[q];
       }
   }
-  const int m0 = tm * BM, n0 = tn * BN;
+  const int m0 = tm * BM, n0 = n_begin + tn * BN;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = uniform(tid >> 6);
   const int wk = wave >> 2, wm = (wave >> 1) & 1, wn = wave & 1;
@@ -813,7 +813,7 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
   }
   for (int e = tid; e < BM * RP; e += NT) Us[e] = Us[e] + Us[BM * RP + e];
   __syncthreads();
-  if (tn == 0) {
+  if (n0 == 0) {
     for (int e = tid; e < BM * RP; e += NT) {
       const int il = e / RP, t = e - il * RP;
       if (m0 + il < m && t < r) U[(size_t)(m0 + il) * r + t] = Us[e];
@@ -871,41 +871,44 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
 }
 
 template <int BM, int BN, int WM, int WN, int RP, bool DROP, bool GRP>
-static hipError_t launch_fwd_cfg(const FwdArgs& a, const FwdGroup& grp, int tiles_n, hipStream_t st) {
+static hipError_t launch_fwd_cfg(const FwdArgs& a, const FwdGroup& grp, int tiles_n, int n_begin, hipStream_t st) {
   const int tiles_m = (int)((a.m + BM - 1) / BM);
   if constexpr (RP >= 32 && !DROP && !GRP) {   // U in a pass of its own, then the tile without U columns
-    hipLaunchKernelGGL((lora_u_kernel<RP, 32>), dim3((a.m + 31) / 32), dim3(512), 0, st, a.X, a.A, a.U, (int)a.m,
-                       (int)a.k, (int)a.r);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
+    if (!a.u_ready) {
+      hipLaunchKernelGGL((lora_u_kernel<RP, 32>), dim3((a.m + 31) / 32), dim3(512), 0, st, a.X, a.A, a.U,
+                         (int)a.m, (int)a.k, (int)a.r);
+      const hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
+    }
     if (a.k % 64 == 0)
       hipLaunchKernelGGL((lora_fwd_kernel<BM, BN, WM, WN, RP, false, false, true, true>), dim3(tiles_m * tiles_n),
                          dim3(64 * WM * WN), 0, st, a.X, a.W, a.A, a.B, a.keep, a.Y, a.U, (int)a.m, (int)a.n, (int)a.k,
-                         (int)a.r, a.s, a.inv_keep, tiles_m, tiles_n, grp);
+                         (int)a.r, a.s, a.inv_keep, tiles_m, tiles_n, n_begin, grp);
     else
       hipLaunchKernelGGL((lora_fwd_kernel<BM, BN, WM, WN, RP, false, false, true, false>), dim3(tiles_m * tiles_n),
                          dim3(64 * WM * WN), 0, st, a.X, a.W, a.A, a.B, a.keep, a.Y, a.U, (int)a.m, (int)a.n, (int)a.k,
-                         (int)a.r, a.s, a.inv_keep, tiles_m, tiles_n, grp);
+                         (int)a.r, a.s, a.inv_keep, tiles_m, tiles_n, n_begin, grp);
     return hipGetLastError();
   } else {
     if (a.k % 64 == 0)
       hipLaunchKernelGGL((lora_fwd_kernel<BM, BN, WM, WN, RP, DROP, GRP, false, true>), dim3(tiles_m * tiles_n),
                          dim3(64 * WM * WN), 0, st, a.X, a.W, a.A, a.B, a.keep, a.Y, a.U, (int)a.m, (int)a.n, (int)a.k,
-                         (int)a.r, a.s, a.inv_keep, tiles_m, tiles_n, grp);
+                         (int)a.r, a.s, a.inv_keep, tiles_m, tiles_n, n_begin, grp);
     else
       hipLaunchKernelGGL((lora_fwd_kernel<BM, BN, WM, WN, RP, DROP, GRP, false, false>), dim3(tiles_m * tiles_n),
                          dim3(64 * WM * WN), 0, st, a.X, a.W, a.A, a.B, a.keep, a.Y, a.U, (int)a.m, (int)a.n, (int)a.k,
-                         (int)a.r, a.s, a.inv_keep, tiles_m, tiles_n, grp);
+                         (int)a.r, a.s, a.inv_keep, tiles_m, tiles_n, n_begin, grp);
     return hipGetLastError();
   }
 }
 
-// Single projection: tiles_n from n.  Group: the column tiles of each
-// projection, back to back (tile0 filled here).  The 128 x 256 tile with
-// rank <= 16 and no dropout runs the k-split kernel.
+// Single projection: the column tiles of output columns [n_begin, n_end).
+// Group: the column tiles of each projection, back to back (tile0 filled
+// here).  The 128 x 256 tile with rank <= 16 and no dropout runs the k-split
+// kernel.
 template <int BM, int BN, int WM, int WN, bool DROP, bool GRP>
-static hipError_t launch_fwd_rp(const FwdArgs& a, FwdGroup grp, hipStream_t st) {
-  int tiles_n = (int)((a.n + BN - 1) / BN);
+static hipError_t launch_fwd_rp(const FwdArgs& a, FwdGroup grp, int64_t n_begin, int64_t n_end, hipStream_t st) {
+  int tiles_n = (int)((n_end - n_begin + BN - 1) / BN);
   if (GRP) {
     tiles_n = 0;
     for (int g = 0; g < grp.count; ++g) {
@@ -917,30 +920,47 @@ static hipError_t launch_fwd_rp(const FwdArgs& a, FwdGroup grp, hipStream_t st) 
     const int tiles_m = (int)((a.m + BM - 1) / BM);
     if (a.k % 64 == 0)
       hipLaunchKernelGGL((lora_fwd_ks_kernel<GRP, true>), dim3(tiles_m * tiles_n), dim3(512), 0, st, a.X, a.W, a.A,
-                         a.B, a.Y, a.U, (int)a.m, (int)a.n, (int)a.k, (int)a.r, a.s, tiles_m, tiles_n, grp);
+                         a.B, a.Y, a.U, (int)a.m, (int)a.n, (int)a.k, (int)a.r, a.s, tiles_m, tiles_n, (int)n_begin,
+                         grp);
     else
       hipLaunchKernelGGL((lora_fwd_ks_kernel<GRP, false>), dim3(tiles_m * tiles_n), dim3(512), 0, st, a.X, a.W, a.A,
-                         a.B, a.Y, a.U, (int)a.m, (int)a.n, (int)a.k, (int)a.r, a.s, tiles_m, tiles_n, grp);
+                         a.B, a.Y, a.U, (int)a.m, (int)a.n, (int)a.k, (int)a.r, a.s, tiles_m, tiles_n, (int)n_begin,
+                         grp);
     return hipGetLastError();
   }
-  if (a.r <= 16) return launch_fwd_cfg<BM, BN, WM, WN, 16, DROP, GRP>(a, grp, tiles_n, st);
-  if (a.r <= 32) return launch_fwd_cfg<BM, BN, WM, WN, 32, DROP, GRP>(a, grp, tiles_n, st);
-  return launch_fwd_cfg<BM, BN, WM, WN, 64, DROP, GRP>(a, grp, tiles_n, st);
+  const int nb = (int)n_begin;
+  if (a.r <= 16) return launch_fwd_cfg<BM, BN, WM, WN, 16, DROP, GRP>(a, grp, tiles_n, nb, st);
+  if (a.r <= 32) return launch_fwd_cfg<BM, BN, WM, WN, 32, DROP, GRP>(a, grp, tiles_n, nb, st);
+  return launch_fwd_cfg<BM, BN, WM, WN, 64, DROP, GRP>(a, grp, tiles_n, nb, st);
+}
+
+// Output columns [n_begin, n_end) of one projection with tile t.
+static hipError_t launch_fwd_tile(const FwdArgs& a, GemmTile t, int64_t n_begin, int64_t n_end, hipStream_t st) {
+  const FwdGroup none{};
+  switch (t) {
+    case TILE_256x256: return launch_fwd_rp<256, 256, 2, 4, false, false>(a, none, n_begin, n_end, st);
+    case TILE_128x256: return launch_fwd_rp<128, 256, 2, 4, false, false>(a, none, n_begin, n_end, st);
+    default: return launch_fwd_rp<128, 128, 2, 2, false, false>(a, none, n_begin, n_end, st);
+  }
 }
 
 // With dropout the 256 x 256 tile is not used: its registers are already full.
+// Without, the columns may be split between two launches of different tiles
+// (plan_gemm_split); the first launch writes U (its first column tile), the
+// second only reads it where its tile takes U precomputed.
 hipError_t launch_fwd(const FwdArgs& a, hipStream_t st) {
-  const GemmTile t = choose_gemm_tile(a.m, a.n);
-  const FwdGroup none{};
   if (a.keep) {
-    if (t == TILE_128x128) return launch_fwd_rp<128, 128, 2, 2, true, false>(a, none, st);
-    return launch_fwd_rp<128, 256, 2, 4, true, false>(a, none, st);
+    const FwdGroup none{};
+    if (choose_gemm_tile(a.m, a.n) == TILE_128x128)
+      return launch_fwd_rp<128, 128, 2, 2, true, false>(a, none, 0, a.n, st);
+    return launch_fwd_rp<128, 256, 2, 4, true, false>(a, none, 0, a.n, st);
   }
-  switch (t) {
-    case TILE_256x256: return launch_fwd_rp<256, 256, 2, 4, false, false>(a, none, st);
-    case TILE_128x256: return launch_fwd_rp<128, 256, 2, 4, false, false>(a, none, st);
-    default: return launch_fwd_rp<128, 128, 2, 2, false, false>(a, none, st);
-  }
+  const GemmSplit p = plan_gemm_split(a.m, a.n);
+  const hipError_t e = launch_fwd_tile(a, p.t1, 0, p.n1, st);
+  if (e != hipSuccess || p.n1 >= a.n) return e;
+  FwdArgs b = a;
+  b.u_ready = true;
+  return launch_fwd_tile(b, p.t2, p.n1, a.n, st);
 }
 
 // One launch for the whole group; the tile is chosen for the combined output
@@ -964,9 +984,9 @@ hipError_t launch_fwd_group(const GroupFwdArgs& a, hipStream_t st) {
   f.X = a.X;
   f.m = a.m; f.n = 0; f.k = a.k; f.r = a.r; f.s = a.s;
   switch (choose_gemm_tile(a.m, ntot)) {
-    case TILE_256x256: return launch_fwd_rp<256, 256, 2, 4, false, true>(f, grp, st);
-    case TILE_128x256: return launch_fwd_rp<128, 256, 2, 4, false, true>(f, grp, st);
-    default: return launch_fwd_rp<128, 128, 2, 2, false, true>(f, grp, st);
+    case TILE_256x256: return launch_fwd_rp<256, 256, 2, 4, false, true>(f, grp, 0, 0, st);
+    case TILE_128x256: return launch_fwd_rp<128, 256, 2, 4, false, true>(f, grp, 0, 0, st);
+    default: return launch_fwd_rp<128, 128, 2, 2, false, true>(f, grp, 0, 0, st);
   }
 }
 

@@ -39,6 +39,35 @@ inline GemmTile choose_gemm_tile(int64_t M, int64_t N) {
   return best;
 }
 
+// Column split of one large GEMM with an M x N output: columns [0, n1) with
+// tile t1, then columns [n1, N) with tile t2 in a second launch.  Taken when
+// the split, whose second part is at most one round of 256 workgroups, is
+// estimated at least 5% faster than the single tiling (estimate: rounds x
+// tile area / relative efficiency, 1.0, 0.95 and 0.72 for 256x256, 128x256
+// and 128x128 as measured at 4096 x 5120 x 5120).  Typical case: 4096 x 5120,
+// where 640 tiles of 128x256 take three rounds and 256 tiles of 256x256 plus
+// 256 tiles of 128x128 take two.  Among equal estimates the largest n1 wins.
+// n1 == N: no split.
+struct GemmSplit { GemmTile t1, t2; int64_t n1; };
+inline GemmSplit plan_gemm_split(int64_t M, int64_t N) {
+  struct C { GemmTile t; int bm, bn; double eff; };
+  const C cands[3] = {{TILE_256x256, 256, 256, 1.0}, {TILE_128x256, 128, 256, 0.95},
+                      {TILE_128x128, 128, 128, 0.72}};
+  auto tiles = [&](const C& c, int64_t n) { return ((M + c.bm - 1) / c.bm) * ((n + c.bn - 1) / c.bn); };
+  auto cost = [&](const C& c, int64_t n) { return (double)((tiles(c, n) + 255) / 256) * c.bm * c.bn / c.eff; };
+  const GemmTile t0 = choose_gemm_tile(M, N);
+  GemmSplit best{t0, t0, N};
+  double best_cost = 0.95 * cost(cands[(int)t0], N);
+  for (const C& c1 : cands)
+    for (int64_t n1 = c1.bn; n1 < N; n1 += c1.bn)
+      for (const C& c2 : cands) {
+        if (tiles(c2, N - n1) > 256) continue;
+        const double c = cost(c1, n1) + cost(c2, N - n1);
+        if (c <= best_cost) { best_cost = c; best = GemmSplit{c1.t, c2.t, n1}; }
+      }
+  return best;
+}
+
 // Split-K plan of a token reduction out[t][c] = sum_i P[t][i] Q[i][c] over
 // `cols` columns: columns in tiles of kRedCols, tokens in `splits` ranges of
 // `span` tokens (a multiple of 64).  Splits are capped so the fp32 partial
@@ -101,6 +130,7 @@ struct FwdArgs {
   float s;
   const uint8_t* keep = nullptr;   // dropout keep bits [m][k/8], or none
   float inv_keep = 1.0f;           // 1 / (1 - p)
+  bool u_ready = false;            // U already in place (second launch of a column split)
 };
 
 struct BwdArgs {

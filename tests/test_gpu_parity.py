@@ -50,6 +50,8 @@ RAGGED = [
     Shape("ragged", 4100, 2048, 1024, 24, 48.0, 109),
     Shape("ragged", 2000, 4000, 4104, 5, 10.0, 110),     # k-split forward tile, every edge ragged
     Shape("ragged", 1500, 3000, 2056, 13, 26.0, 111),
+    Shape("ragged", 3900, 4864, 5056, 13, 26.0, 112),    # forward and dX columns split between two tiles
+    Shape("ragged", 4000, 5000, 264, 5, 10.0, 113),      # forward split, ragged second part
 ]
 
 
@@ -96,6 +98,8 @@ EXACT = [
     Shape("exact", 2048, 2048, 4104, 64, 128.0, 203),
     Shape("exact", 4100, 11008, 512, 16, 32.0, 204),
     Shape("exact", 4096, 512, 11008, 8, 16.0, 205),
+    Shape("exact", 4096, 5120, 256, 8, 16.0, 206),       # forward columns split: 256x256, then 128x128
+    Shape("exact", 4096, 5120, 256, 40, 80.0, 207),      # the same with U from its own pass
 ]
 
 
