@@ -70,6 +70,7 @@ CASES = [  # (ns, m, k, r, alpha)
     ([1032, 1032], 520, 640, 16, 32.0),            # gate, up
     ([64, 72, 80, 88, 96, 104, 112, 120], 96, 136, 3, 6.0),   # the largest group
     ([1368, 1368, 1360], 2000, 1024, 8, 16.0),    # the k-split forward tile, ragged members
+    ([264, 392], 2000, 5120, 8, 16.0),             # 2.5 rounds of 128x256 dX tiles
 ]
 
 
@@ -92,10 +93,12 @@ def test_group_of_one_matches_plain():
     check(t, alpha, got)
 
 
-def test_group_integer_exact():
+@pytest.mark.parametrize("m,k,ns", [(264, 1024, [512, 1024, 256]), (2048, 5120, [256, 512])],
+                         ids=["m264k1024", "m2048k5120"])
+def test_group_integer_exact(m, k, ns):
     """Sparse {-1, 0, 1} inputs and s = 2: every sum is a small integer, so
     the GPU matches the oracle bit for bit whatever the summation order."""
-    m, k, r, alpha, ns = 264, 1024, 8, 16.0, [512, 1024, 256]
+    r, alpha = 8, 16.0
     per = [gen_ternary_inputs(m, n, k, r, 50 + g, density=0.01) for g, n in enumerate(ns)]
     t = {"X": per[0]["X"], "W": [p["W"] for p in per], "A": [p["A"] for p in per],
          "B": [p["B"] for p in per], "dY": [p["dY"] for p in per]}
