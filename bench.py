@@ -37,22 +37,62 @@ def traffic_file(workload: str) -> str:
     return os.path.join(ROOT, "profiles", f"{forward_kernel_name(s0.m, s0.n, s0.r, False)}_{workload}_traffic.json")
 
 
-def forward_kernel_name(m: int, n: int, r: int, dropout: bool) -> str:
-    """Name of the forward kernel the library launches for this shape (its tile
-    choice: rounds of 256 workgroups times tile area over a per-tile
-    efficiency, with 128 x 256 in place of 256 x 256 under dropout; the
-    128 x 256 tile with rank <= 16 and no dropout runs the k-split kernel)."""
+_TILES = (("256x256", 256, 256), ("128x256", 128, 256), ("128x128", 128, 128))
+
+
+def _rounds(m: int, n: int, bm: int, bn: int) -> int:
+    return -(-(-(-m // bm) * -(-n // bn)) // 256)
+
+
+def _choose_tile(m: int, n: int) -> str:
+    """The library's single-tile choice: rounds of 256 workgroups times tile
+    area over a per-tile efficiency (1.0, 0.9, 0.75)."""
     best, cost = None, None
-    for name, bm, bn, eff in (("256x256", 256, 256, 1.0), ("128x256", 128, 256, 0.9), ("128x128", 128, 128, 0.75)):
-        tiles = -(-m // bm) * -(-n // bn)
-        c = -(-tiles // 256) * bm * bn / eff
+    for (name, bm, bn), eff in zip(_TILES, (1.0, 0.9, 0.75)):
+        c = _rounds(m, n, bm, bn) * bm * bn / eff
         if cost is None or c < cost:
             best, cost = name, c
-    if dropout and best == "256x256":
-        best = "128x256"
-    if best == "128x256" and r <= 16 and not dropout:
-        return "lora_fwd_ks_kernel"
-    return "lora_fwd_kernel"
+    return best
+
+
+def _column_split(m: int, n: int):
+    """The library's column split of an m x n GEMM output (same estimate as
+    its launcher: efficiencies 1.0, 0.95, 0.72, second part at most one
+    round, taken when more than 5% cheaper, ties to the larger n1): returns
+    [(tile, first column, end column), ...]."""
+    eff = {"256x256": 1.0, "128x256": 0.95, "128x128": 0.72}
+    dims = {name: (bm, bn) for name, bm, bn in _TILES}
+    cost = lambda t, cols: _rounds(m, cols, *dims[t]) * dims[t][0] * dims[t][1] / eff[t]
+    t0 = _choose_tile(m, n)
+    best, best_cost, found = [(t0, 0, n)], 0.95 * cost(t0, n), False
+    for t1, _, bn1 in _TILES:
+        for n1 in range(bn1, n, bn1):
+            for t2, bm2, bn2 in _TILES:
+                if -(-m // bm2) * -(-(n - n1) // bn2) > 256:
+                    continue
+                c = cost(t1, n1) + cost(t2, n - n1)
+                if c < best_cost or (found and c == best_cost and n1 > best[0][2]):
+                    best, best_cost, found = [(t1, 0, n1), (t2, n1, n)], c, True
+    return best
+
+
+def forward_launches(m: int, n: int, r: int, dropout: bool):
+    """Forward GEMM launches the library makes for this shape, as (kernel,
+    tile, first column, end column): 128 x 256 in place of 256 x 256 and no
+    column split under dropout; the 128 x 256 tile with rank <= 16 and no
+    dropout runs the k-split kernel."""
+    if dropout:
+        t = _choose_tile(m, n)
+        parts = [("128x256" if t == "256x256" else t, 0, n)]
+    else:
+        parts = _column_split(m, n)
+    return [("lora_fwd_ks_kernel" if t == "128x256" and r <= 16 and not dropout else "lora_fwd_kernel", t, a, b)
+            for t, a, b in parts]
+
+
+def forward_kernel_name(m: int, n: int, r: int, dropout: bool) -> str:
+    """Name of the (first) forward kernel the library launches for this shape."""
+    return forward_launches(m, n, r, dropout)[0][0]
 
 
 def log(*a):
@@ -502,6 +542,13 @@ def main():
     m, n, k, r = s0.m, s0.n, s0.k, s0.r
     k1_flops = 2 * m * n * k + 2 * m * k * r + 2 * m * n * r
     achieved = k1_flops / (fwd_us * 1e-6) / 1e12
+    # The forward call is one launch at the 7B q_proj shape; elsewhere it may
+    # be a U pass (rank > 16, no dropout) and/or a column split in two launches,
+    # all inside the timed call.
+    launches = forward_launches(m, n, r, drop is not None)
+    kernel_label = " + ".join((["lora_u_kernel"] if r > 16 and drop is None else [])
+                              + [name if len(launches) == 1 else f"{name} {t} columns [{a}, {b})"
+                                 for name, t, a, b in launches])
     traffic = measured_traffic(args.config) if drop is None else None
     log(f"[bench] forward kernel {fwd_us:.1f} us ({achieved:.1f} TFLOP/s); backward call {bwd_us:.1f} us")
 
@@ -530,7 +577,7 @@ def main():
                                     "alpha": s.alpha} for s in shapes],
                    "input_sets": nsets, "flops_per_step": flops, "lora_dropout": drop,
                    "operands": "bf16 in, fp32 accumulate; Y, dX bf16; U, dA, dB fp32"},
-        "roofline": {"bound": "mfma", "kernel": forward_kernel_name(m, n, r, drop is not None),
+        "roofline": {"bound": "mfma", "kernel": kernel_label,
                      "achieved": round(achieved, 2),
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                      "traffic": traffic, "flops_per_launch": k1_flops, "avg_launch_us": round(fwd_us, 2)},

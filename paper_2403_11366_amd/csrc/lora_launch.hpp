@@ -42,7 +42,7 @@ inline GemmTile choose_gemm_tile(int64_t M, int64_t N) {
 // Column split of one large GEMM with an M x N output: columns [0, n1) with
 // tile t1, then columns [n1, N) with tile t2 in a second launch.  Taken when
 // the split, whose second part is at most one round of 256 workgroups, is
-// estimated at least 5% faster than the single tiling (estimate: rounds x
+// estimated more than 5% faster than the single tiling (estimate: rounds x
 // tile area / relative efficiency, 1.0, 0.95 and 0.72 for 256x256, 128x256
 // and 128x128 as measured at 4096 x 5120 x 5120).  Typical case: 4096 x 5120,
 // where 640 tiles of 128x256 take three rounds and 256 tiles of 256x256 plus
@@ -58,12 +58,17 @@ inline GemmSplit plan_gemm_split(int64_t M, int64_t N) {
   const GemmTile t0 = choose_gemm_tile(M, N);
   GemmSplit best{t0, t0, N};
   double best_cost = 0.95 * cost(cands[(int)t0], N);
+  bool found = false;
   for (const C& c1 : cands)
     for (int64_t n1 = c1.bn; n1 < N; n1 += c1.bn)
       for (const C& c2 : cands) {
         if (tiles(c2, N - n1) > 256) continue;
         const double c = cost(c1, n1) + cost(c2, N - n1);
-        if (c <= best_cost) { best_cost = c; best = GemmSplit{c1.t, c2.t, n1}; }
+        if (c < best_cost || (found && c == best_cost && n1 > best.n1)) {
+          best_cost = c;
+          best = GemmSplit{c1.t, c2.t, n1};
+          found = true;
+        }
       }
   return best;
 }
