@@ -565,7 +565,8 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
   constexpr int CX = BM * 8, CW = BN * 8, CA = RP * 8;
   constexpr int LX = CX / NT, LW = CW / NT, LA = (CA + NT - 1) / NT;
   constexpr int XCH = 8 * 16 * 1024;              // exchange: 8 waves x 32 fragments x 64 lanes x 4 B
-  constexpr int SMEM = XCH > 2 * STAGE ? XCH : 2 * STAGE;
+  constexpr int EPI = XCH + 2 * BM * RP * 4 + BN * RP * 2;   // exchange, Us, Bs
+  constexpr int SMEM = EPI > 2 * STAGE ? EPI : 2 * STAGE;
   __shared__ __attribute__((aligned(1024))) char smem[SMEM];
 
   int tm, tn;
@@ -736,14 +737,30 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
     stage(kb, BR{}, false, false);
   }
 
-  // ---- exchange of the k-half partial sums (LDS is free after the loop's
-  // last barrier): region (pair, h) holds, for the wave of the pair that keeps
-  // half h, the partner's fragments [fjl][fi][q4] as float4 x 64 lanes.
+  // ---- epilogue (LDS is free after the loop's last barrier).  Regions:
+  // [0, XCH) the exchange of the k-half partial sums, later the per-wave
+  // staging of the bf16 output block; then Us [2][BM][RP] fp32 (the two
+  // k-half partials of U, summed in fixed order) and Bs [BN][RP] bf16 (B rows
+  // of the tile, zero beyond r and n).  Two barriers in all.
+  float* Us = reinterpret_cast<float*>(smem + XCH);
+  u16* Bs = reinterpret_cast<u16*>(smem + XCH + 2 * BM * RP * 4);
+  constexpr int BCH = (BN * RP / 8 + NT - 1) / NT;
+  const int jn = min(BN, n - n0);
+  const int nch = jn * r / 8;
+  const __amdgpu_buffer_rsrc_t rsB = make_rsrc(B + (size_t)n0 * r, (uint64_t)nch * 16);
+  int4v bv[BCH];
+#pragma unroll
+  for (int i = 0; i < BCH; ++i) {
+    const int q = tid + i * NT;
+    bv[i] = buf_load16(rsB, q < nch ? (uint32_t)q * 16 : kOOB);
+  }
+  // Exchange region of (pair, destination half h): the partner's fragments
+  // [fjl][fi][q4] as float4 x 64 lanes; wave wk keeps feature fragments
+  // 2 wk, 2 wk + 1 and sends the other two.
+  float4* xb = reinterpret_cast<float4*>(smem);
+  const int pair = wm * 2 + wn;
+  auto region = [&](int h) { return xb + (size_t)((pair * 2 + h) * 16) * 64; };
   {
-    float4* xb = reinterpret_cast<float4*>(smem);
-    const int pair = wm * 2 + wn;
-    // region of (pair, destination half h): [fjl][fi][q4] float4 x 64 lanes
-    auto region = [&](int h) { return xb + (size_t)((pair * 2 + h) * 16) * 64; };
     float4* dst = region(1 - wk);
 #pragma unroll
     for (int fjl = 0; fjl < 2; ++fjl)
@@ -754,7 +771,14 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
         for (int q4 = 0; q4 < 4; ++q4)
           dst[((fjl * FI + fi) * 4 + q4) * 64 + lane] = float4{v[4 * q4], v[4 * q4 + 1], v[4 * q4 + 2], v[4 * q4 + 3]};
       }
-    __syncthreads();
+  }
+#pragma unroll
+  for (int gg = 0; gg < GPW; ++gg)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) Us[(wk * BM + urow16[gg]) * RP + 4 * g16 + q] = uacc16[gg][q];
+  for (int e = tid; e < BN * RP / 8; e += NT) reinterpret_cast<int4v*>(Bs)[e] = int4v{0, 0, 0, 0};
+  __syncthreads();
+  {
     const float4* src = region(wk);
 #pragma unroll
     for (int fjl = 0; fjl < 2; ++fjl)
@@ -771,30 +795,7 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
             acc[2 + fjl][fi][4 * q4 + 2] += o.z; acc[2 + fjl][fi][4 * q4 + 3] += o.w;
           }
         }
-    __syncthreads();
   }
-
-  // ---- epilogue as in lora_fwd_kernel on the wave's 64 x 64 block:
-  // Us [2][BM][RP] fp32 (the two k-half partials of U, summed in fixed order),
-  // Bs [BN][RP] bf16 (B rows of the tile, zero beyond r and n).
-  float* Us = reinterpret_cast<float*>(smem);
-  u16* Bs = reinterpret_cast<u16*>(smem + 2 * BM * RP * 4);
-  constexpr int BCH = (BN * RP / 8 + NT - 1) / NT;
-  const int jn = min(BN, n - n0);
-  const int nch = jn * r / 8;
-  const __amdgpu_buffer_rsrc_t rsB = make_rsrc(B + (size_t)n0 * r, (uint64_t)nch * 16);
-  int4v bv[BCH];
-#pragma unroll
-  for (int i = 0; i < BCH; ++i) {
-    const int q = tid + i * NT;
-    bv[i] = buf_load16(rsB, q < nch ? (uint32_t)q * 16 : kOOB);
-  }
-#pragma unroll
-  for (int gg = 0; gg < GPW; ++gg)
-#pragma unroll
-    for (int q = 0; q < 4; ++q) Us[(wk * BM + urow16[gg]) * RP + 4 * g16 + q] = uacc16[gg][q];
-  for (int e = tid; e < BN * RP / 8; e += NT) reinterpret_cast<int4v*>(Bs)[e] = int4v{0, 0, 0, 0};
-  __syncthreads();
   {
     const float rinv = 1.0f / (float)r;
 #pragma unroll
@@ -811,6 +812,7 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
       }
     }
   }
+  // (the partial of half 1 is read here and written before the barrier above)
   for (int e = tid; e < BM * RP; e += NT) Us[e] = Us[e] + Us[BM * RP + e];
   __syncthreads();
   if (n0 == 0) {
@@ -819,8 +821,14 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
       if (m0 + il < m && t < r) U[(size_t)(m0 + il) * r + t] = Us[e];
     }
   }
-  // acc += s U B^T (high and low bf16 parts of s U), then Y rounded to bf16;
-  // the block: features wn WTJ + 64 wk + 32 fjl, tokens wm WTI + 32 fi.
+  // acc += s U B^T (high and low bf16 parts of s U), then Y rounded to bf16
+  // on the wave's 64 x 64 block: features wn WTJ + 64 wk + 32 fjl, tokens
+  // wm WTI + 32 fi.  The block goes through a wave-private LDS region (rows
+  // of 64 bf16 tokens-major, padded to 144 bytes) so that every global store
+  // writes whole 128-byte row segments.
+  constexpr int YP = 144;
+  char* ys = smem + wave * (WTI * YP);
+  static_assert(8 * WTI * YP <= XCH, "output staging fits the exchange region");
   auto finish = [&](floatx16 (&a2)[FI], floatx16 (&b2)[FI]) {
     floatx16* own[2] = {a2, b2};
     const int t0 = 8 * g;
@@ -848,26 +856,33 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
         own[fjl][fi] = mfma32x32x16(bfr[fjl], ul, own[fjl][fi]);
       }
     }
+    // lane (g, c32) holds token 32 fi + c32, features 32 fjl + 8 qq + 4 g .. + 3
 #pragma unroll
-    for (int fi = 0; fi < FI; ++fi) {
-      const int i = m0 + wm * WTI + 32 * fi + c32;
-      if (i >= m) continue;
-      u16* yrow = Y + (size_t)i * n;
+    for (int fi = 0; fi < FI; ++fi)
 #pragma unroll
       for (int fjl = 0; fjl < 2; ++fjl)
 #pragma unroll
         for (int qq = 0; qq < 4; ++qq) {
-          const int j = n0 + wn * WTJ + 64 * wk + 32 * fjl + 8 * qq + 4 * g;
-          if (j >= n) continue;
           const floatx16& a = own[fjl][fi];
           const uint32_t lo = (uint32_t)f32_to_bf16(a[4 * qq]) | ((uint32_t)f32_to_bf16(a[4 * qq + 1]) << 16);
           const uint32_t hi = (uint32_t)f32_to_bf16(a[4 * qq + 2]) | ((uint32_t)f32_to_bf16(a[4 * qq + 3]) << 16);
-          *reinterpret_cast<uint2*>(yrow + j) = uint2{lo, hi};
+          *reinterpret_cast<uint2*>(ys + (32 * fi + c32) * YP + (32 * fjl + 8 * qq + 4 * g) * 2) = uint2{lo, hi};
         }
-    }
   };
   if (wk == 0) finish(acc[0], acc[1]);
   else finish(acc[2], acc[3]);
+  __syncthreads();
+  {
+    // 8 rows of 128 bytes per store: lane l takes row 8 p + l / 8, chunk l % 8
+    const int ch = lane & 7, jcol = n0 + wn * WTJ + 64 * wk + 8 * ch;
+#pragma unroll
+    for (int p = 0; p < WTI / 8; ++p) {
+      const int row = 8 * p + (lane >> 3);
+      const int i = m0 + wm * WTI + row;
+      const int4v v = *reinterpret_cast<const int4v*>(ys + row * YP + ch * 16);
+      if (i < m && jcol < n) *reinterpret_cast<int4v*>(Y + (size_t)i * n + jcol) = v;
+    }
+  }
 }
 
 template <int BM, int BN, int WM, int WN, int RP, bool DROP, bool GRP>
