@@ -711,6 +711,31 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
   const int nkb = (k + 63) / 64;
   gload(0, 0);
   gload(0, 1);
+  // B rows of the tile for the epilogue, staged once beside the pipeline's
+  // buffers: Bs [BN][RP] bf16, zero beyond r and n; thread tid fills entries
+  // t0b .. t0b + 7 of row tid / (RP / 8).
+  u16* Bs = reinterpret_cast<u16*>(smem + XCH + 2 * BM * RP * 4);
+  {
+    static_assert(BN * RP / 8 == NT, "one chunk of Bs per thread");
+    const int j = tid / (RP / 8), t0b = 8 * (tid % (RP / 8));
+    int4v v = int4v{0, 0, 0, 0};
+    if (j < min(BN, n - n0) && t0b < r) {
+      const u16* brow = B + (size_t)(n0 + j) * r;
+      if ((r & 7) == 0) {
+        v = *reinterpret_cast<const int4v*>(brow + t0b);
+      } else {
+        uint32_t w[4];
+#pragma unroll
+        for (int x = 0; x < 4; ++x) {
+          const uint32_t lo = t0b + 2 * x < r ? brow[t0b + 2 * x] : 0u;
+          const uint32_t hi = t0b + 2 * x + 1 < r ? brow[t0b + 2 * x + 1] : 0u;
+          w[x] = lo | (hi << 16);
+        }
+        v = int4v{(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
+      }
+    }
+    *reinterpret_cast<int4v*>(Bs + j * RP + t0b) = v;
+  }
   swrite(0, 0);
   swrite(0, 1);
   __syncthreads();
@@ -741,19 +766,9 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
   // [0, XCH) the exchange of the k-half partial sums, later the per-wave
   // staging of the bf16 output block; then Us [2][BM][RP] fp32 (the two
   // k-half partials of U, summed in fixed order) and Bs [BN][RP] bf16 (B rows
-  // of the tile, zero beyond r and n).  Two barriers in all.
+  // of the tile, zero beyond r and n, staged in the prologue).  Two
+  // barriers in all.
   float* Us = reinterpret_cast<float*>(smem + XCH);
-  u16* Bs = reinterpret_cast<u16*>(smem + XCH + 2 * BM * RP * 4);
-  constexpr int BCH = (BN * RP / 8 + NT - 1) / NT;
-  const int jn = min(BN, n - n0);
-  const int nch = jn * r / 8;
-  const __amdgpu_buffer_rsrc_t rsB = make_rsrc(B + (size_t)n0 * r, (uint64_t)nch * 16);
-  int4v bv[BCH];
-#pragma unroll
-  for (int i = 0; i < BCH; ++i) {
-    const int q = tid + i * NT;
-    bv[i] = buf_load16(rsB, q < nch ? (uint32_t)q * 16 : kOOB);
-  }
   // Exchange region of (pair, destination half h): the partner's fragments
   // [fjl][fi][q4] as float4 x 64 lanes; wave wk keeps feature fragments
   // 2 wk, 2 wk + 1 and sends the other two.
@@ -776,7 +791,6 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
   for (int gg = 0; gg < GPW; ++gg)
 #pragma unroll
     for (int q = 0; q < 4; ++q) Us[(wk * BM + urow16[gg]) * RP + 4 * g16 + q] = uacc16[gg][q];
-  for (int e = tid; e < BN * RP / 8; e += NT) reinterpret_cast<int4v*>(Bs)[e] = int4v{0, 0, 0, 0};
   __syncthreads();
   {
     const float4* src = region(wk);
@@ -795,22 +809,6 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
             acc[2 + fjl][fi][4 * q4 + 2] += o.z; acc[2 + fjl][fi][4 * q4 + 3] += o.w;
           }
         }
-  }
-  {
-    const float rinv = 1.0f / (float)r;
-#pragma unroll
-    for (int i = 0; i < BCH; ++i) {
-      const int q = tid + i * NT;
-      if (q < nch) {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int idx = 8 * q + e;
-          const int j = (int)(((float)idx + 0.5f) * rinv);
-          const int t = idx - j * r;
-          Bs[j * RP + t] = (u16)((uint32_t)bv[i][e >> 1] >> (16 * (e & 1)));
-        }
-      }
-    }
   }
   // (the partial of half 1 is read here and written before the barrier above)
   for (int e = tid; e < BM * RP; e += NT) Us[e] = Us[e] + Us[BM * RP + e];
@@ -871,16 +869,19 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
   };
   if (wk == 0) finish(acc[0], acc[1]);
   else finish(acc[2], acc[3]);
-  __syncthreads();
+  // each wave reads back only its own block: its LDS writes complete first
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
   {
     // 8 rows of 128 bytes per store: lane l takes row 8 p + l / 8, chunk l % 8
     const int ch = lane & 7, jcol = n0 + wn * WTJ + 64 * wk + 8 * ch;
+    int4v v[WTI / 8];
+#pragma unroll
+    for (int p = 0; p < WTI / 8; ++p) v[p] = *reinterpret_cast<const int4v*>(ys + (8 * p + (lane >> 3)) * YP + ch * 16);
 #pragma unroll
     for (int p = 0; p < WTI / 8; ++p) {
-      const int row = 8 * p + (lane >> 3);
-      const int i = m0 + wm * WTI + row;
-      const int4v v = *reinterpret_cast<const int4v*>(ys + row * YP + ch * 16);
-      if (i < m && jcol < n) *reinterpret_cast<int4v*>(Y + (size_t)i * n + jcol) = v;
+      const int i = m0 + wm * WTI + 8 * p + (lane >> 3);
+      if (i < m && jcol < n) *reinterpret_cast<int4v*>(Y + (size_t)i * n + jcol) = v[p];
     }
   }
 }
