@@ -747,22 +747,19 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
     }
   }
 
+  // store dX: each wave's 32-token blocks of its 64 features through a
+  // wave-private LDS region (the k loop ended with a barrier; the group and
+  // dropout epilogues read LDS until here)
+  static_assert(FJ == 2 && NW * kYsBytes <= 2 * STAGE, "output staging");
+  if (GRP || DROP) __syncthreads();
+  {
+    const int j0 = l0 + wn * WTJ;
 #pragma unroll
-  for (int fi = 0; fi < FI; ++fi) {
-    const int i = m0 + wm * WTI + 32 * fi + c32;
-    if (i >= m) continue;
-    u16* xrow = dX + (size_t)i * k;
-#pragma unroll
-    for (int fj = 0; fj < FJ; ++fj)
-#pragma unroll
-      for (int qq = 0; qq < 4; ++qq) {
-        const int l = l0 + wn * WTJ + 32 * fj + 8 * qq + 4 * g;
-        if (l >= k) continue;
-        const floatx16& a = acc[fj][fi];
-        const uint32_t lo = (uint32_t)f32_to_bf16(a[4 * qq]) | ((uint32_t)f32_to_bf16(a[4 * qq + 1]) << 16);
-        const uint32_t hi = (uint32_t)f32_to_bf16(a[4 * qq + 2]) | ((uint32_t)f32_to_bf16(a[4 * qq + 3]) << 16);
-        *reinterpret_cast<uint2*>(xrow + l) = uint2{lo, hi};
-      }
+    for (int fi = 0; fi < FI; ++fi) {
+      const int i0 = m0 + wm * WTI + 32 * fi;
+      store_block_32x64(acc[0][fi], acc[1][fi], smem + wave * kYsBytes, dX + (size_t)i0 * k + j0, (size_t)k,
+                        m - i0, k - j0, lane);
+    }
   }
   // After its tile, every workgroup sums a slice of the dA, dB partials
   // (complete: the token reductions ran before this launch in stream order).

@@ -154,6 +154,47 @@ __device__ __forceinline__ short8 mc32_read_tr(const char* tile, int krow0, int 
                __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4v*)p1));
 }
 
+// Output block store.  A wave holds a 32 x 64 block of fp32 outputs in the
+// v_mfma_f32_32x32x16 result layout (v0: columns 0..31, v1: columns 32..63;
+// lane (g, c) holds row c, columns 8 (q / 4) + 4 g + q % 4).  Stored directly,
+// every store instruction would touch 32 rows with 16 bytes each.  Instead
+// the block goes through a wave-private LDS region of 32 rows of 64 bf16
+// (kYsPitch bytes per row, conflict-free for both access patterns) and is
+// written back with 16 bytes per lane, 8 whole 128-byte row segments per
+// store.  dst points at the block's (row 0, column 0), ld is the row pitch in
+// elements; rows >= nrows and columns >= ncols (a multiple of 8) are not
+// written.  The caller provides kYsBytes of LDS that no other wave touches
+// meanwhile; the fences order this wave's accesses to it.
+constexpr int kYsPitch = 144, kYsBytes = 32 * kYsPitch;
+
+__device__ __forceinline__ void store_block_32x64(const floatx16& v0, const floatx16& v1, char* ys, u16* dst,
+                                                  size_t ld, int nrows, int ncols, int lane) {
+  const int g = lane >> 5, c = lane & 31;
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");   // earlier reads of the region
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const floatx16& a = h ? v1 : v0;
+#pragma unroll
+    for (int qq = 0; qq < 4; ++qq) {
+      const uint32_t lo = (uint32_t)f32_to_bf16(a[4 * qq]) | ((uint32_t)f32_to_bf16(a[4 * qq + 1]) << 16);
+      const uint32_t hi = (uint32_t)f32_to_bf16(a[4 * qq + 2]) | ((uint32_t)f32_to_bf16(a[4 * qq + 3]) << 16);
+      *reinterpret_cast<uint2*>(ys + c * kYsPitch + (32 * h + 8 * qq + 4 * g) * 2) = uint2{lo, hi};
+    }
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+  const int ch = lane & 7, r8 = lane >> 3;
+  int4v v[4];
+#pragma unroll
+  for (int p = 0; p < 4; ++p) v[p] = *reinterpret_cast<const int4v*>(ys + (8 * p + r8) * kYsPitch + ch * 16);
+  if (8 * ch < ncols) {
+#pragma unroll
+    for (int p = 0; p < 4; ++p)
+      if (8 * p + r8 < nrows) *reinterpret_cast<int4v*>(dst + (size_t)(8 * p + r8) * ld + 8 * ch) = v[p];
+  }
+}
+
 // Tile workgroup index -> tile coordinates.  Workgroups are dealt to the 8
 // XCDs round robin (block b runs on XCD b % 8); the first step renumbers blocks so each
 // XCD receives a contiguous range of tile ids, the second walks tiles in

@@ -432,24 +432,16 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
     }
   }
 
-  // store Y: lane holds token c32 of fragment fi and features
-  // 8(q/4) + 4g + q%4 of fragment fj, i.e. 4 runs of 4 consecutive features.
+  // store Y: each wave's 32-token blocks of its 64 features through a
+  // wave-private LDS region (free once every wave is past the reads above)
+  static_assert(FJ == 2 && NW * kYsBytes <= 2 * STAGE, "output staging");
+  __syncthreads();
+  const int j0 = n0 + wn * WTJ;
 #pragma unroll
   for (int fi = 0; fi < FI; ++fi) {
-    const int i = m0 + wm * WTI + 32 * fi + c32;
-    if (i >= m) continue;
-    u16* yrow = Y + (size_t)i * n;
-#pragma unroll
-    for (int fj = 0; fj < FJ; ++fj)
-#pragma unroll
-      for (int qq = 0; qq < 4; ++qq) {
-        const int j = n0 + wn * WTJ + 32 * fj + 8 * qq + 4 * g;
-        if (j >= n) continue;
-        const floatx16& a = acc[fj][fi];
-        const uint32_t lo = (uint32_t)f32_to_bf16(a[4 * qq]) | ((uint32_t)f32_to_bf16(a[4 * qq + 1]) << 16);
-        const uint32_t hi = (uint32_t)f32_to_bf16(a[4 * qq + 2]) | ((uint32_t)f32_to_bf16(a[4 * qq + 3]) << 16);
-        *reinterpret_cast<uint2*>(yrow + j) = uint2{lo, hi};
-      }
+    const int i0 = m0 + wm * WTI + 32 * fi;
+    store_block_32x64(acc[0][fi], acc[1][fi], smem + wave * kYsBytes, Y + (size_t)i0 * n + j0, (size_t)n, m - i0,
+                      n - j0, lane);
   }
 }
 
@@ -821,12 +813,8 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
   }
   // acc += s U B^T (high and low bf16 parts of s U), then Y rounded to bf16
   // on the wave's 64 x 64 block: features wn WTJ + 64 wk + 32 fjl, tokens
-  // wm WTI + 32 fi.  The block goes through a wave-private LDS region (rows
-  // of 64 bf16 tokens-major, padded to 144 bytes) so that every global store
-  // writes whole 128-byte row segments.
-  constexpr int YP = 144;
-  char* ys = smem + wave * (WTI * YP);
-  static_assert(8 * WTI * YP <= XCH, "output staging fits the exchange region");
+  // wm WTI + 32 fi, stored through a wave-private LDS region (the exchange
+  // region is free after the barrier above).
   auto finish = [&](floatx16 (&a2)[FI], floatx16 (&b2)[FI]) {
     floatx16* own[2] = {a2, b2};
     const int t0 = 8 * g;
@@ -854,36 +842,17 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
         own[fjl][fi] = mfma32x32x16(bfr[fjl], ul, own[fjl][fi]);
       }
     }
-    // lane (g, c32) holds token 32 fi + c32, features 32 fjl + 8 qq + 4 g .. + 3
+    const int j0 = n0 + wn * WTJ + 64 * wk;
 #pragma unroll
-    for (int fi = 0; fi < FI; ++fi)
-#pragma unroll
-      for (int fjl = 0; fjl < 2; ++fjl)
-#pragma unroll
-        for (int qq = 0; qq < 4; ++qq) {
-          const floatx16& a = own[fjl][fi];
-          const uint32_t lo = (uint32_t)f32_to_bf16(a[4 * qq]) | ((uint32_t)f32_to_bf16(a[4 * qq + 1]) << 16);
-          const uint32_t hi = (uint32_t)f32_to_bf16(a[4 * qq + 2]) | ((uint32_t)f32_to_bf16(a[4 * qq + 3]) << 16);
-          *reinterpret_cast<uint2*>(ys + (32 * fi + c32) * YP + (32 * fjl + 8 * qq + 4 * g) * 2) = uint2{lo, hi};
-        }
+    for (int fi = 0; fi < FI; ++fi) {
+      const int i0 = m0 + wm * WTI + 32 * fi;
+      store_block_32x64(a2[fi], b2[fi], smem + wave * kYsBytes, Y + (size_t)i0 * n + j0, (size_t)n, m - i0, n - j0,
+                        lane);
+    }
   };
+  static_assert(8 * kYsBytes <= XCH, "output staging fits the exchange region");
   if (wk == 0) finish(acc[0], acc[1]);
   else finish(acc[2], acc[3]);
-  // each wave reads back only its own block: its LDS writes complete first
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
-  {
-    // 8 rows of 128 bytes per store: lane l takes row 8 p + l / 8, chunk l % 8
-    const int ch = lane & 7, jcol = n0 + wn * WTJ + 64 * wk + 8 * ch;
-    int4v v[WTI / 8];
-#pragma unroll
-    for (int p = 0; p < WTI / 8; ++p) v[p] = *reinterpret_cast<const int4v*>(ys + (8 * p + (lane >> 3)) * YP + ch * 16);
-#pragma unroll
-    for (int p = 0; p < WTI / 8; ++p) {
-      const int i = m0 + wm * WTI + 8 * p + (lane >> 3);
-      if (i < m && jcol < n) *reinterpret_cast<int4v*>(Y + (size_t)i * n + jcol) = v[p];
-    }
-  }
 }
 
 template <int BM, int BN, int WM, int WN, int RP, bool DROP, bool GRP>
