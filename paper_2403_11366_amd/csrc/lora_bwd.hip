@@ -902,12 +902,24 @@ static hipError_t launch_bwd_group_rp(const GroupBwdArgs& a, const GroupBwdLayou
   BwdArgs d{};
   d.X = a.X; d.dX = a.dX; d.ws = a.ws;
   d.m = a.m; d.n = 0; d.k = a.k; d.r = a.r; d.s = a.s;
-  // The 256 x 256 tile has no registers left for the per-stage projection
-  // lookup; the group runs 128 x 256 in its place.
+  // Columns of dX may be split between two launches as for one projection;
+  // the first one's tails finalize every projection's dA and dB.  (The
+  // 256 x 256 tile keeps a few values it needs only after the k loop in
+  // scratch across the loop.)
   const FinalizeArgs none{};
-  if (choose_gemm_tile(a.m, a.k) == TILE_128x128)
-    return launch_dx_cfg<128, 128, 2, 2, RP, false, true>(d, GL.L[0], none, grp, 0, a.k, st);
-  return launch_dx_cfg<128, 256, 2, 4, RP, false, true>(d, GL.L[0], none, grp, 0, a.k, st);
+  auto tile = [&](GemmTile t, const DxGroup& gg, int64_t lb, int64_t le) {
+    switch (t) {
+      case TILE_256x256: return launch_dx_cfg<256, 256, 2, 4, RP, false, true>(d, GL.L[0], none, gg, lb, le, st);
+      case TILE_128x256: return launch_dx_cfg<128, 256, 2, 4, RP, false, true>(d, GL.L[0], none, gg, lb, le, st);
+      default: return launch_dx_cfg<128, 128, 2, 2, RP, false, true>(d, GL.L[0], none, gg, lb, le, st);
+    }
+  };
+  const GemmSplit p = plan_gemm_split(a.m, a.k);
+  const hipError_t e = tile(p.t1, grp, 0, p.n1);
+  if (e != hipSuccess || p.n1 >= a.k) return e;
+  DxGroup rest = grp;
+  for (int g = 0; g < kMaxGroup; ++g) rest.fin[g] = FinalizeArgs{};
+  return tile(p.t2, rest, p.n1, a.k);
 }
 
 hipError_t launch_bwd_group(const GroupBwdArgs& a, hipStream_t st) {

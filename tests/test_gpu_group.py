@@ -71,6 +71,7 @@ CASES = [  # (ns, m, k, r, alpha)
     ([64, 72, 80, 88, 96, 104, 112, 120], 96, 136, 3, 6.0),   # the largest group
     ([1368, 1368, 1360], 2000, 1024, 8, 16.0),    # the k-split forward tile, ragged members
     ([264, 392], 2000, 5120, 8, 16.0),             # 2.5 rounds of 128x256 dX tiles
+    ([264, 392], 4096, 4096, 8, 16.0),             # the 256x256 dX tile for a group
 ]
 
 
@@ -93,8 +94,8 @@ def test_group_of_one_matches_plain():
     check(t, alpha, got)
 
 
-@pytest.mark.parametrize("m,k,ns", [(264, 1024, [512, 1024, 256]), (2048, 5120, [256, 512])],
-                         ids=["m264k1024", "m2048k5120"])
+@pytest.mark.parametrize("m,k,ns", [(264, 1024, [512, 1024, 256]), (4096, 5120, [256, 512])],
+                         ids=["m264k1024", "m4096k5120-dx-split"])
 def test_group_integer_exact(m, k, ns):
     """Sparse {-1, 0, 1} inputs and s = 2: every sum is a small integer, so
     the GPU matches the oracle bit for bit whatever the summation order."""
