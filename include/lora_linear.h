@@ -70,9 +70,11 @@ typedef enum {
  *   U  [m, r]  output (fp32), written: the unscaled X A^T, needed by the backward
  *   alpha      LoRA alpha; the scale is s = alpha / r, computed in fp32
  *
- * One kernel: a bf16 matrix-core GEMM over k that streams each X tile through
- * LDS once for both W and A, then adds s U B^T to the accumulators in its
- * epilogue before rounding Y to bf16.
+ * A bf16 matrix-core GEMM over k that streams each X tile through LDS once
+ * for both W and A, then adds s U B^T to the accumulators in its epilogue
+ * before rounding Y to bf16.  One launch for most shapes; where it fills the
+ * compute units better, the output columns are split between two launches
+ * of different tile sizes, and for r > 16 a pass computing U runs first.
  */
 lora_status lora_linear_fwd(const lora_bf16* X, const lora_bf16* W, const lora_bf16* A,
                             const lora_bf16* B, lora_bf16* Y, float* U,

@@ -2,8 +2,9 @@
 // Section 3, for the trainable A and B; W0 is frozen so no dW is formed):
 //   dU = s dY B,   dX = dY W + dU A,   dB = s dY^T U,   dA = dU^T X.
 //
-// Kernels, in stream order (three launches; each launch costs a few
-// microseconds on its own, so small steps share launches):
+// Kernels, in stream order (three launches, four when the dX columns are
+// split between two tiles; each launch costs a few microseconds on its own,
+// so small steps share launches):
 //   du        dU = s dY B, reducing over n.  Writes dU2 (token-major, high |
 //             low) for the dX GEMM and dUt2 (its transpose) for dA, and Ut2
 //             = U^T split into a bf16 high part and a bf16 low part (tokens
@@ -16,9 +17,9 @@
 //             against the same A rows).  W is read through LDS with the
 //             transposing ds_read_b64_tr_b16, since the product contracts
 //             W over its rows.  After its tile, each workgroup of this launch
-//             sums a slice of the dB and dA partials in a fixed order (no
-//             atomics, so results are bit-identical from run to run) and
-//             applies s to dB.
+//             (the first one of a split) sums a slice of the dB and dA
+//             partials in a fixed order (no atomics, so results are
+//             bit-identical from run to run) and applies s to dB.
 #include <type_traits>
 
 #include "lora_device.hpp"

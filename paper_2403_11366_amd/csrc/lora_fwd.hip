@@ -1,7 +1,8 @@
 // Forward of the LoRA-adapted linear layer (Eq. 1 of JORA, Section 3):
 //   U = X A^T,   Y = X W^T + s U B^T,   s = alpha / r.
 //
-// Kernels (one launch, or two for rank > 16):
+// Kernels (one launch per call; a U pass before it for rank > 16, and a
+// second GEMM launch when the columns are split between two tiles):
 //   lora_fwd_ks_kernel  the 128 x 256 tile for rank <= 16 without dropout
 //                       (the 7B q_proj shape): wave pairs split the k
 //                       substeps of each stage, see its own comment.
@@ -9,6 +10,8 @@
 //                       dropout and grouped launches; described below.
 //   lora_u_kernel       U = X A^T on its own for rank > 16, followed by
 //                       lora_fwd_kernel without U columns.
+// A launch covers the output columns from n_begin on (plan_gemm_split);
+// the launch whose range starts at column 0 writes U.
 //
 // lora_fwd_kernel: each workgroup owns a BM x BN tile of Y (BM tokens x BN output
 // features) and walks k in stages of 64.  Per stage it stages three
@@ -24,10 +27,11 @@
 //
 // The U columns of a token fragment are accumulated by the waves that share
 // it (each wave owns fixed fragments and k substeps, so the U products are
-// branch-free).  After the k loop the
-// epilogue parks U in LDS, writes it out (tile column 0 only), and adds
-// s U B^T to the accumulators with a short matrix-core pass over t in which
-// s U enters as a bf16 high part and a bf16 low part, then rounds Y to bf16.
+// branch-free).  After the k loop the epilogue parks U in LDS, writes it out
+// (first tile column only), and adds s U B^T to the accumulators with a
+// short matrix-core pass over t in which s U enters as a bf16 high part and
+// a bf16 low part, then rounds Y to bf16 and stores it through a per-wave
+// LDS block (store_block_32x64) so that stores write whole 128-byte rows.
 #include <type_traits>
 
 #include "lora_device.hpp"
