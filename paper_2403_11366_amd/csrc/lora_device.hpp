@@ -65,6 +65,36 @@ __device__ __forceinline__ floatx16 mfma32x32x16(short8 a, short8 b, floatx16 c)
 
 __device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
 
+// Global -> LDS copy of 16 bytes per lane through a buffer resource (offset
+// voff + soff): lane l's bytes land at lds_base + 16 l (lds_base wave-uniform).
+// Out-of-range offsets write zeros.  Completion is counted by vmcnt.
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t rs, uint32_t voff, uint32_t soff, void* lds_base) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void*)lds_base, 16, voff, soff, 0,
+                                           0);
+}
+
+// s_waitcnt on the vector-memory count only: wait until at most N of this
+// wave's vector-memory operations (global -> LDS copies included) are
+// outstanding.  gfx9 encoding: vmcnt[3:0] in bits 3:0, vmcnt[5:4] in bits
+// 15:14, expcnt (bits 6:4) and lgkmcnt (bits 11:8) left at their maxima.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// Workgroup barrier for pipelines fed by global -> LDS copies: waits until at
+// most N of this wave's copies are outstanding and all of its LDS accesses
+// are done, then s_barrier.  (__syncthreads would also wait for the copies
+// still in flight for later stages.)  The asm statement keeps the compiler
+// from moving memory accesses across the barrier.
+template <int N>
+__device__ __forceinline__ void copy_barrier() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4));
+  asm volatile("s_barrier" ::: "memory");
+}
+
 // 8-byte load through a buffer resource (byte_off a multiple of 8).
 __device__ __forceinline__ uint2 buf_load8(__amdgpu_buffer_rsrc_t rs, uint32_t byte_off) {
   const auto v = __builtin_amdgcn_raw_buffer_load_b64(rs, byte_off, 0, 0);

@@ -548,7 +548,14 @@ __global__ __launch_bounds__(512) void lora_u_kernel(const u16* __restrict__ X, 
 // 64 x 64 block (features wn 128 + 64 wk ..) for the epilogue, which is the one
 // of the 2 x 4 layout.  GRP selects the projection of a grouped launch as in
 // lora_fwd_kernel.
-template <bool GRP, bool KFULL>
+//
+// DMA (k a multiple of 64; used for launches of at most one round): the
+// stages go from global memory straight into three LDS buffers (one 16-byte
+// chunk per lane per copy instruction, the chunk swizzle applied to the
+// global addresses), two stages ahead and without staging registers; each
+// stage ends with a barrier that waits only for this wave's copies of the
+// next stage (copy_barrier).
+template <bool GRP, bool KFULL, bool DMA>
 __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
     const u16* __restrict__ X, const u16* __restrict__ W, const u16* __restrict__ A,
     const u16* __restrict__ B, u16* __restrict__ Y, float* __restrict__ U, int m, int n, int k, int r, float s,
@@ -561,8 +568,11 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
   constexpr int CX = BM * 8, CW = BN * 8, CA = RP * 8;
   constexpr int LX = CX / NT, LW = CW / NT, LA = (CA + NT - 1) / NT;
   constexpr int XCH = 8 * 16 * 1024;              // exchange: 8 waves x 32 fragments x 64 lanes x 4 B
-  constexpr int EPI = XCH + 2 * BM * RP * 4 + BN * RP * 2;   // exchange, Us, Bs
-  constexpr int SMEM = EPI > 2 * STAGE ? EPI : 2 * STAGE;
+  static_assert(!DMA || KFULL, "the copies carry no k-bound checks");
+  constexpr int NBUF = DMA ? 3 : 2;                       // LDS stage buffers
+  constexpr int BS_OFF = DMA ? NBUF * STAGE : XCH + 2 * BM * RP * 4;
+  constexpr int EPI = (BS_OFF > XCH + 2 * BM * RP * 4 ? BS_OFF : XCH + 2 * BM * RP * 4) + BN * RP * 2;
+  constexpr int SMEM = EPI > NBUF * STAGE ? EPI : NBUF * STAGE;
   __shared__ __attribute__((aligned(1024))) char smem[SMEM];
 
   int tm, tn;
@@ -704,13 +714,90 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
   using B0 = std::integral_constant<int, 0>;
   using B1 = std::integral_constant<int, 1>;
   using BR = std::integral_constant<int, -1>;
+  u16* Bs = reinterpret_cast<u16*>(smem + BS_OFF);   // B rows for the epilogue, staged in the prologue
+  if constexpr (DMA) {
+  const int nkb = (k + 63) / 64;
+  // Copies straight into LDS: instruction j of a tile covers its rows 8j ..
+  // 8j + 7, lane l position l % 8 of row 8j + l / 8, which holds the row's
+  // logical chunk (l % 8) ^ kc_swz(row) (the swizzle is applied on the global
+  // side).  Per stage a wave issues 2 X, 4 W and (waves 0, 1) 1 A copies.
+  const int dl_row = lane >> 3, dl_cp = lane & 7;
+  auto voff = [&](int j) {
+    const int row = 8 * j + dl_row;
+    return (uint32_t)row * rowbytes + (uint32_t)((dl_cp ^ kc_swz(row)) << 4);
+  };
+  auto dload = [&](int kb, int buf) {
+    const uint32_t k0b = (uint32_t)kb * 128;
+    char* sb = smem + buf * STAGE;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) dma16(rsX, voff(wave + 8 * i), k0b, sb + (wave + 8 * i) * 1024);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) dma16(rsW, voff(wave + 8 * i), k0b, sb + BM * 128 + (wave + 8 * i) * 1024);
+    if (wave < 2) dma16(rsA, voff(wave), k0b, sb + (BM + BN) * 128 + wave * 1024);
+  };
+  constexpr int NDMA_MIN = 6;   // fewest copies any wave issues per stage
+  dload(0, 0);
+  if (nkb > 1) dload(1, 1);
+  // B rows of the tile for the epilogue, staged once beside the pipeline's
+  // buffers: Bs [BN][RP] bf16, zero beyond r and n; thread tid fills entries
+  // t0b .. t0b + 7 of row tid / (RP / 8).
+  {
+    static_assert(BN * RP / 8 == NT, "one chunk of Bs per thread");
+    const int j = tid / (RP / 8), t0b = 8 * (tid % (RP / 8));
+    int4v v = int4v{0, 0, 0, 0};
+    if (j < min(BN, n - n0) && t0b < r) {
+      const u16* brow = B + (size_t)(n0 + j) * r;
+      if ((r & 7) == 0) {
+        v = *reinterpret_cast<const int4v*>(brow + t0b);
+      } else {
+        uint32_t w[4];
+#pragma unroll
+        for (int x = 0; x < 4; ++x) {
+          const uint32_t lo = t0b + 2 * x < r ? brow[t0b + 2 * x] : 0u;
+          const uint32_t hi = t0b + 2 * x + 1 < r ? brow[t0b + 2 * x + 1] : 0u;
+          w[x] = lo | (hi << 16);
+        }
+        v = int4v{(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
+      }
+    }
+    *reinterpret_cast<int4v*>(Bs + j * RP + t0b) = v;
+  }
+  copy_barrier<0>();   // every copy and load of the prologue has landed
+  // Stage kb reads buffer kb % 3; at its top the copies of stage kb+2 go to
+  // buffer (kb+2) % 3, which every wave finished reading in stage kb-1; at
+  // its end each wave waits for its copies of stage kb+1 before the barrier.
+  auto dstage = [&](int kb, auto bufc, bool load_next) {
+    constexpr int BUF = decltype(bufc)::value;
+    if (load_next) dload(kb + 2, (BUF + 2) % 3);
+    const char* sb = smem + BUF * STAGE;
+    read_frags(sb, 0, 0);
+    read_frags(sb, 1, 1);
+    multiply(0, 0);
+    multiply(1, 1);
+    if (load_next) copy_barrier<NDMA_MIN>();
+    else copy_barrier<0>();
+  };
+  using D0 = std::integral_constant<int, 0>;
+  using D1 = std::integral_constant<int, 1>;
+  using D2 = std::integral_constant<int, 2>;
+  int kb = 0;
+  for (; kb + 5 < nkb; kb += 3) {
+    dstage(kb, D0{}, true);
+    dstage(kb + 1, D1{}, true);
+    dstage(kb + 2, D2{}, true);
+  }
+  if (kb < nkb) dstage(kb, D0{}, kb + 2 < nkb);
+  if (kb + 1 < nkb) dstage(kb + 1, D1{}, kb + 3 < nkb);
+  if (kb + 2 < nkb) dstage(kb + 2, D2{}, kb + 4 < nkb);
+  if (kb + 3 < nkb) dstage(kb + 3, D0{}, false);
+  if (kb + 4 < nkb) dstage(kb + 4, D1{}, false);
+  } else {
   const int nkb = (k + 63) / 64;
   gload(0, 0);
   gload(0, 1);
   // B rows of the tile for the epilogue, staged once beside the pipeline's
   // buffers: Bs [BN][RP] bf16, zero beyond r and n; thread tid fills entries
   // t0b .. t0b + 7 of row tid / (RP / 8).
-  u16* Bs = reinterpret_cast<u16*>(smem + XCH + 2 * BM * RP * 4);
   {
     static_assert(BN * RP / 8 == NT, "one chunk of Bs per thread");
     const int j = tid / (RP / 8), t0b = 8 * (tid % (RP / 8));
@@ -758,6 +845,7 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
     stage(kb, BR{}, false, false);
   }
 
+  }
   // ---- epilogue (LDS is free after the loop's last barrier).  Regions:
   // [0, XCH) the exchange of the k-half partial sums, later the per-wave
   // staging of the bf16 output block; then Us [2][BM][RP] fp32 (the two
@@ -907,12 +995,19 @@ static hipError_t launch_fwd_rp(const FwdArgs& a, FwdGroup grp, int64_t n_begin,
   }
   if (BM == 128 && BN == 256 && !DROP && a.r <= 16) {
     const int tiles_m = (int)((a.m + BM - 1) / BM);
-    if (a.k % 64 == 0)
-      hipLaunchKernelGGL((lora_fwd_ks_kernel<GRP, true>), dim3(tiles_m * tiles_n), dim3(512), 0, st, a.X, a.W, a.A,
-                         a.B, a.Y, a.U, (int)a.m, (int)a.n, (int)a.k, (int)a.r, a.s, tiles_m, tiles_n, (int)n_begin,
-                         grp);
+    // Single-round launches (at most one tile per compute unit) copy straight
+    // into LDS: measured faster there (7B q_proj forward 83-86 -> 77-79 us),
+    // slightly slower over many rounds (13B gate_proj 630-633 -> 636-639 us).
+    if (a.k % 64 == 0 && !GRP && tiles_m * tiles_n <= 256)
+      hipLaunchKernelGGL((lora_fwd_ks_kernel<false, true, true>), dim3(tiles_m * tiles_n), dim3(512), 0, st, a.X, a.W,
+                         a.A, a.B, a.Y, a.U, (int)a.m, (int)a.n, (int)a.k, (int)a.r, a.s, tiles_m, tiles_n,
+                         (int)n_begin, grp);
+    else if (a.k % 64 == 0)
+      hipLaunchKernelGGL((lora_fwd_ks_kernel<GRP, true, false>), dim3(tiles_m * tiles_n), dim3(512), 0, st, a.X, a.W,
+                         a.A, a.B, a.Y, a.U, (int)a.m, (int)a.n, (int)a.k, (int)a.r, a.s, tiles_m, tiles_n,
+                         (int)n_begin, grp);
     else
-      hipLaunchKernelGGL((lora_fwd_ks_kernel<GRP, false>), dim3(tiles_m * tiles_n), dim3(512), 0, st, a.X, a.W, a.A,
+      hipLaunchKernelGGL((lora_fwd_ks_kernel<GRP, false, false>), dim3(tiles_m * tiles_n), dim3(512), 0, st, a.X, a.W, a.A,
                          a.B, a.Y, a.U, (int)a.m, (int)a.n, (int)a.k, (int)a.r, a.s, tiles_m, tiles_n, (int)n_begin,
                          grp);
     return hipGetLastError();
