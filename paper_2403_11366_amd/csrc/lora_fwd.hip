@@ -48,7 +48,13 @@ namespace lora {
 //
 // KFULL (k a multiple of 64): the loads carry no k-bound checks, and below the
 // 256 x 256 tile the stages run in pairs with compile-time LDS buffers.
-template <int BM, int BN, int WM, int WN, int RP, bool DROP, bool GRP, bool UPRE, bool KFULL>
+//
+// DMA (the 256 x 256 tile with KFULL, no dropout): each stage is copied from
+// global memory straight into the free LDS buffer at the top of the stage
+// before it (one 16-byte chunk per lane per copy instruction, the swizzle
+// applied to the global addresses), with no staging registers; the stage's
+// closing barrier waits for those copies (copy_barrier).
+template <int BM, int BN, int WM, int WN, int RP, bool DROP, bool GRP, bool UPRE, bool KFULL, bool DMA>
 __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
     const u16* __restrict__ X, const u16* __restrict__ W, const u16* __restrict__ A,
     const u16* __restrict__ B, const uint8_t* __restrict__ keep, u16* __restrict__ Y,
@@ -303,29 +309,75 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
     __syncthreads();
   };
   const int nkb = (k + 63) / 64;
-#pragma unroll
-  for (int pc = 0; pc < 4; ++pc) gload(0, pc);
-#pragma unroll
-  for (int pc = 0; pc < 4; ++pc) swrite(0, pc);
-  __syncthreads();
-  if (nkb > 1) {
-#pragma unroll
-    for (int pc = 0; pc < 4; ++pc) gload(1, pc);
-  }
   using B0 = std::integral_constant<int, 0>;
   using B1 = std::integral_constant<int, 1>;
   using BR = std::integral_constant<int, -1>;
-  int kb = 0;
-  if constexpr (KFULL && BM * BN < 256 * 256) {
-    for (; kb + 3 < nkb; kb += 2) {
-      stage(kb, B0{}, true, true);
-      stage(kb + 1, B1{}, true, true);
+  if constexpr (DMA) {
+    static_assert(KFULL && !DROP && !ROT, "copy pipeline shape");
+    // Copy instruction j of a region covers its rows 8j .. 8j+7: lane l takes
+    // position l % 8 of row 8j + l / 8, i.e. logical chunk (l % 8) ^ kc_swz(row).
+    constexpr int JX = BM / 8, JW = BN / 8, JA = RPS / 8;
+    static_assert(JX % NW == 0 && JW % NW == 0, "copies split evenly");
+    const int dl_row = lane >> 3, dl_cp = lane & 7;
+    auto voff = [&](int j) {
+      const int row = 8 * j + dl_row;
+      return (uint32_t)row * rowbytes + (uint32_t)((dl_cp ^ kc_swz(row)) << 4);
+    };
+    auto dload = [&](int kb, int buf) {
+      const uint32_t k0b = (uint32_t)kb * 128;
+      char* sb = smem + buf * STAGE;
+#pragma unroll
+      for (int i = 0; i < JX / NW; ++i) dma16(rsX, voff(wave + NW * i), k0b, sb + (wave + NW * i) * 1024);
+#pragma unroll
+      for (int i = 0; i < JW / NW; ++i)
+        dma16(rsW, voff(wave + NW * i), k0b, sb + BM * 128 + (wave + NW * i) * 1024);
+#pragma unroll
+      for (int i = 0; i < (JA + NW - 1) / NW; ++i)
+        if (wave + NW * i < JA) dma16(rsA, voff(wave + NW * i), k0b, sb + (BM + BN) * 128 + (wave + NW * i) * 1024);
+    };
+    dload(0, 0);
+    copy_barrier<0>();
+    auto dstage = [&](int kb, auto bufc, bool load_next) {
+      constexpr int BUF = decltype(bufc)::value;
+      if (load_next) dload(kb + 1, BUF ^ 1);   // read in stage kb-1, free since its barrier
+      const char* sb = smem + BUF * STAGE;
+      read_frags(sb, 0, 0);
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+        if (ks < 3) read_frags(sb, ks + 1, (ks + 1) & 1);
+        multiply(ks & 1, ks);
+      }
+      copy_barrier<0>();
+    };
+    int kb = 0;
+    for (; kb + 2 < nkb; kb += 2) {
+      dstage(kb, B0{}, true);
+      dstage(kb + 1, B1{}, true);
     }
+    if (kb < nkb) dstage(kb, B0{}, kb + 1 < nkb);
+    if (kb + 1 < nkb) dstage(kb + 1, B1{}, false);
+  } else {
+#pragma unroll
+    for (int pc = 0; pc < 4; ++pc) gload(0, pc);
+#pragma unroll
+    for (int pc = 0; pc < 4; ++pc) swrite(0, pc);
+    __syncthreads();
+    if (nkb > 1) {
+#pragma unroll
+      for (int pc = 0; pc < 4; ++pc) gload(1, pc);
+    }
+    int kb = 0;
+    if constexpr (KFULL && BM * BN < 256 * 256) {
+      for (; kb + 3 < nkb; kb += 2) {
+        stage(kb, B0{}, true, true);
+        stage(kb + 1, B1{}, true, true);
+      }
+    }
+    for (; kb + 2 < nkb; ++kb) stage(kb, BR{}, true, true);
+    if (kb + 1 < nkb) stage(kb++, BR{}, true, false);
+    stage(kb, BR{}, false, false);
+    if (ROT) multiply(1, 3);
   }
-  for (; kb + 2 < nkb; ++kb) stage(kb, BR{}, true, true);
-  if (kb + 1 < nkb) stage(kb++, BR{}, true, false);
-  stage(kb, BR{}, false, false);
-  if (ROT) multiply(1, 3);
 
   // ---- epilogue ------------------------------------------------------------
   // LDS reuse: Us [NDUP][BM][RP] fp32 partial U (summed in fixed order below),
@@ -958,22 +1010,22 @@ static hipError_t launch_fwd_cfg(const FwdArgs& a, const FwdGroup& grp, int tile
       if (e != hipSuccess) return e;
     }
     if (a.k % 64 == 0)
-      hipLaunchKernelGGL((lora_fwd_kernel<BM, BN, WM, WN, RP, false, false, true, true>), dim3(tiles_m * tiles_n),
-                         dim3(64 * WM * WN), 0, st, a.X, a.W, a.A, a.B, a.keep, a.Y, a.U, (int)a.m, (int)a.n, (int)a.k,
+      hipLaunchKernelGGL((lora_fwd_kernel<BM, BN, WM, WN, RP, false, false, true, true, BM == 256 && BN == 256>),
+                         dim3(tiles_m * tiles_n), dim3(64 * WM * WN), 0, st, a.X, a.W, a.A, a.B, a.keep, a.Y, a.U, (int)a.m, (int)a.n, (int)a.k,
                          (int)a.r, a.s, a.inv_keep, tiles_m, tiles_n, n_begin, grp);
     else
-      hipLaunchKernelGGL((lora_fwd_kernel<BM, BN, WM, WN, RP, false, false, true, false>), dim3(tiles_m * tiles_n),
-                         dim3(64 * WM * WN), 0, st, a.X, a.W, a.A, a.B, a.keep, a.Y, a.U, (int)a.m, (int)a.n, (int)a.k,
+      hipLaunchKernelGGL((lora_fwd_kernel<BM, BN, WM, WN, RP, false, false, true, false, false>),
+                         dim3(tiles_m * tiles_n), dim3(64 * WM * WN), 0, st, a.X, a.W, a.A, a.B, a.keep, a.Y, a.U, (int)a.m, (int)a.n, (int)a.k,
                          (int)a.r, a.s, a.inv_keep, tiles_m, tiles_n, n_begin, grp);
     return hipGetLastError();
   } else {
     if (a.k % 64 == 0)
-      hipLaunchKernelGGL((lora_fwd_kernel<BM, BN, WM, WN, RP, DROP, GRP, false, true>), dim3(tiles_m * tiles_n),
-                         dim3(64 * WM * WN), 0, st, a.X, a.W, a.A, a.B, a.keep, a.Y, a.U, (int)a.m, (int)a.n, (int)a.k,
+      hipLaunchKernelGGL((lora_fwd_kernel<BM, BN, WM, WN, RP, DROP, GRP, false, true, BM == 256 && BN == 256 && !DROP>),
+                         dim3(tiles_m * tiles_n), dim3(64 * WM * WN), 0, st, a.X, a.W, a.A, a.B, a.keep, a.Y, a.U, (int)a.m, (int)a.n, (int)a.k,
                          (int)a.r, a.s, a.inv_keep, tiles_m, tiles_n, n_begin, grp);
     else
-      hipLaunchKernelGGL((lora_fwd_kernel<BM, BN, WM, WN, RP, DROP, GRP, false, false>), dim3(tiles_m * tiles_n),
-                         dim3(64 * WM * WN), 0, st, a.X, a.W, a.A, a.B, a.keep, a.Y, a.U, (int)a.m, (int)a.n, (int)a.k,
+      hipLaunchKernelGGL((lora_fwd_kernel<BM, BN, WM, WN, RP, DROP, GRP, false, false, false>),
+                         dim3(tiles_m * tiles_n), dim3(64 * WM * WN), 0, st, a.X, a.W, a.A, a.B, a.keep, a.Y, a.U, (int)a.m, (int)a.n, (int)a.k,
                          (int)a.r, a.s, a.inv_keep, tiles_m, tiles_n, n_begin, grp);
     return hipGetLastError();
   }
