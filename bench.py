@@ -393,6 +393,9 @@ def main():
     ap.add_argument("--grouped", action="store_true",
                     help="run the projections that read one input (q, k, v; gate, up) as groups "
                          "(workloads with a layer grouping only)")
+    ap.add_argument("--fused-bwd", action="store_true",
+                    help="backward through lora_linear_bwd_fused (dU and dB inside the dX GEMM; "
+                         "rank <= 16, no dropout)")
     ap.add_argument("--summarize-traffic", metavar="DIR", default=None,
                     help="write the HBM-traffic record from counter runs under DIR and exit")
     args = ap.parse_args()
@@ -428,6 +431,8 @@ def main():
         log(f"[bench] {args.steps} copies of {args.copy_mib} MiB done")
         return
     shapes = CONFIGS[args.config]
+    if args.fused_bwd and (args.dropout is not None or args.grouped or any(s.r > 16 for s in shapes)):
+        sys.exit("--fused-bwd: rank <= 16 without dropout or grouping only")
     dev = "cuda"
     stream = torch.cuda.current_stream()
     if args.op == "merge":
@@ -459,7 +464,8 @@ def main():
             "dX": torch.empty((s.m, s.k), dtype=torch.bfloat16, device=dev),
             "dA": torch.empty((s.r, s.k), dtype=torch.float32, device=dev),
             "dB": torch.empty((s.n, s.r), dtype=torch.float32, device=dev),
-            "ws": torch.empty(lora.lora_linear_bwd_workspace_size(s.m, s.n, s.k, s.r),
+            "ws": torch.empty((lora.lora_linear_bwd_fused_workspace_size if args.fused_bwd
+                               else lora.lora_linear_bwd_workspace_size)(s.m, s.n, s.k, s.r),
                               dtype=torch.uint8, device=dev),
         }
         proj.append((s, sets, out))
@@ -479,8 +485,9 @@ def main():
             lora.lora_linear_bwd_dropout(d["dY"], d["X"], d["W"], d["A"], d["B"], out["U"], d["keep"], drop,
                                          out["dX"], out["dA"], out["dB"], out["ws"], s.alpha, stream=stream)
             return
-        lora.lora_linear_bwd(d["dY"], d["X"], d["W"], d["A"], d["B"], out["U"], out["dX"], out["dA"],
-                             out["dB"], out["ws"], s.alpha, stream=stream)
+        (lora.lora_linear_bwd_fused if args.fused_bwd else lora.lora_linear_bwd)(
+            d["dY"], d["X"], d["W"], d["A"], d["B"], out["U"], out["dX"], out["dA"], out["dB"], out["ws"],
+            s.alpha, stream=stream)
 
     def step(i):
         for s, sets, out in proj:
@@ -576,6 +583,7 @@ def main():
                    "projections": [{"name": s.name, "m": s.m, "n": s.n, "k": s.k, "r": s.r,
                                     "alpha": s.alpha} for s in shapes],
                    "input_sets": nsets, "flops_per_step": flops, "lora_dropout": drop,
+                   "backward": "lora_linear_bwd_fused" if args.fused_bwd else "lora_linear_bwd",
                    "operands": "bf16 in, fp32 accumulate; Y, dX bf16; U, dA, dB fp32"},
         "roofline": {"bound": "mfma", "kernel": kernel_label,
                      "achieved": round(achieved, 2),

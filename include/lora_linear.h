@@ -132,6 +132,36 @@ lora_status lora_linear_bwd(const lora_bf16* dY, const lora_bf16* X, const lora_
                             void* stream);
 
 /*
+ * Bytes of device workspace lora_linear_bwd_fused needs for this shape (0 on
+ * an invalid shape or r > 16): dU^T in bf16 high and low parts, the dB
+ * partials of the dX launch (one per 128-token tile row) and the split-K
+ * partials of dA.
+ */
+size_t lora_linear_bwd_fused_workspace_size(int64_t m, int64_t n, int64_t k, int64_t r);
+
+/*
+ * The same backward as lora_linear_bwd (same arguments, outputs and
+ * definitions) with dU and dB formed inside the dX GEMM from the dY tiles it
+ * already stages: the rank-r products dU = s dY B ride as extra matrix-core
+ * products on the GEMM's k loop over n, and the dB = s dY^T U partials of
+ * each 128-token tile row are formed at every tiles_n-th stage; a token
+ * reduction for dA = dU^T X and a fixed-order finalize follow (three
+ * launches, no separate pass over dY).  Results agree with lora_linear_bwd
+ * to rounding (the sums run in a different fixed order) and are
+ * bit-identical from run to run.
+ *
+ * Requires r <= 16 (LORA_ERR_UNSUPPORTED otherwise); the workspace is
+ * lora_linear_bwd_fused_workspace_size(m, n, k, r) bytes, 16-byte aligned.
+ * Other errors as in lora_linear_bwd.
+ */
+lora_status lora_linear_bwd_fused(const lora_bf16* dY, const lora_bf16* X, const lora_bf16* W,
+                                  const lora_bf16* A, const lora_bf16* B, const float* U,
+                                  lora_bf16* dX, float* dA, float* dB,
+                                  void* workspace, size_t workspace_bytes,
+                                  int64_t m, int64_t n, int64_t k, int64_t r, float alpha,
+                                  void* stream);
+
+/*
  * Backward of lora_linear_fwd_dropout for the same keep mask and rate:
  *
  *     dU = s dY B,  dX = dY W + keep * (dU A) / (1 - p),

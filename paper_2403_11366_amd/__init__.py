@@ -16,7 +16,8 @@ from typing import Optional
 
 __all__ = [
     "LoraError", "lib_path", "load_library", "lora_linear_fwd", "lora_linear_bwd",
-    "lora_linear_bwd_workspace_size", "lora_linear_merge", "lora_linear_fwd_dropout", "lora_linear_bwd_dropout",
+    "lora_linear_bwd_workspace_size", "lora_linear_bwd_fused", "lora_linear_bwd_fused_workspace_size",
+    "lora_linear_merge", "lora_linear_fwd_dropout", "lora_linear_bwd_dropout",
     "lora_linear_group_fwd", "lora_linear_group_bwd", "lora_linear_group_bwd_workspace_size",
     "lora_status_string", "STATUS",
 ]
@@ -55,6 +56,10 @@ def load_library() -> ctypes.CDLL:
     lib.lora_linear_bwd_workspace_size.restype = sz
     lib.lora_linear_bwd.argtypes = [p, p, p, p, p, p, p, p, p, p, sz, i64, i64, i64, i64, f32, p]
     lib.lora_linear_bwd.restype = ctypes.c_int
+    lib.lora_linear_bwd_fused_workspace_size.argtypes = [i64, i64, i64, i64]
+    lib.lora_linear_bwd_fused_workspace_size.restype = sz
+    lib.lora_linear_bwd_fused.argtypes = [p, p, p, p, p, p, p, p, p, p, sz, i64, i64, i64, i64, f32, p]
+    lib.lora_linear_bwd_fused.restype = ctypes.c_int
     lib.lora_linear_fwd_dropout.argtypes = [p, p, p, p, p, f32, p, p, i64, i64, i64, i64, f32, p]
     lib.lora_linear_fwd_dropout.restype = ctypes.c_int
     lib.lora_linear_bwd_dropout.argtypes = [p, p, p, p, p, p, p, f32, p, p, p, p, sz, i64, i64, i64, i64, f32, p]
@@ -126,12 +131,26 @@ def lora_linear_fwd(X, W, A, B, Y, U, alpha: float, stream=None) -> None:
         raise LoraError(st, "lora_linear_fwd")
 
 
+def lora_linear_bwd_fused_workspace_size(m: int, n: int, k: int, r: int) -> int:
+    return int(load_library().lora_linear_bwd_fused_workspace_size(m, n, k, r))
+
+
 def lora_linear_bwd(dY, X, W, A, B, U, dX, dA, dB, workspace, alpha: float, stream=None) -> None:
     """dX = dY W + dU A, dA = dU^T X, dB = s dY^T U with dU = s dY B, s = alpha/r.
 
     dY [m,n], X [m,k], W [n,k], A [r,k], B [n,r], dX [m,k]: torch.bfloat16;
     U [m,r], dA [r,k], dB [n,r]: torch.float32; workspace: a device tensor of at
     least lora_linear_bwd_workspace_size(m, n, k, r) bytes."""
+    _bwd_call("lora_linear_bwd", dY, X, W, A, B, U, dX, dA, dB, workspace, alpha, stream)
+
+
+def lora_linear_bwd_fused(dY, X, W, A, B, U, dX, dA, dB, workspace, alpha: float, stream=None) -> None:
+    """lora_linear_bwd with dU and dB formed inside the dX GEMM (r <= 16); the
+    workspace holds at least lora_linear_bwd_fused_workspace_size(m, n, k, r) bytes."""
+    _bwd_call("lora_linear_bwd_fused", dY, X, W, A, B, U, dX, dA, dB, workspace, alpha, stream)
+
+
+def _bwd_call(fn, dY, X, W, A, B, U, dX, dA, dB, workspace, alpha, stream):
     import torch
     m, n = dY.shape
     k, r = X.shape[1], A.shape[0]
@@ -144,11 +163,11 @@ def lora_linear_bwd(dY, X, W, A, B, U, dX, dA, dB, workspace, alpha: float, stre
     if workspace.device.type != "cuda" or not workspace.is_contiguous():
         raise ValueError("workspace: must be a contiguous device tensor")
     ws_bytes = workspace.numel() * workspace.element_size()
-    st = load_library().lora_linear_bwd(_ptr(dY), _ptr(X), _ptr(W), _ptr(A), _ptr(B), _ptr(U),
-                                        _ptr(dX), _ptr(dA), _ptr(dB), _ptr(workspace), ws_bytes,
-                                        m, n, k, r, float(alpha), _stream_handle(stream))
+    st = getattr(load_library(), fn)(_ptr(dY), _ptr(X), _ptr(W), _ptr(A), _ptr(B), _ptr(U),
+                                     _ptr(dX), _ptr(dA), _ptr(dB), _ptr(workspace), ws_bytes,
+                                     m, n, k, r, float(alpha), _stream_handle(stream))
     if st != 0:
-        raise LoraError(st, "lora_linear_bwd")
+        raise LoraError(st, fn)
 
 
 def lora_linear_merge(W, A, B, W_out, alpha: float, sign: int = 1, stream=None) -> None:

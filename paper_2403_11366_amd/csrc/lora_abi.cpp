@@ -176,6 +176,41 @@ lora_status lora_linear_bwd(const lora_bf16* dY, const lora_bf16* X, const lora_
   return e == hipSuccess ? LORA_OK : LORA_ERR_HIP;
 }
 
+size_t lora_linear_bwd_fused_workspace_size(int64_t m, int64_t n, int64_t k, int64_t r) {
+  if (check_shape(m, n, k, r) != LORA_OK || r > 16) return 0;
+  return lora::bwd_fused_layout(m, n, k, r).total;
+}
+
+lora_status lora_linear_bwd_fused(const lora_bf16* dY, const lora_bf16* X, const lora_bf16* W,
+                                  const lora_bf16* A, const lora_bf16* B, const float* U,
+                                  lora_bf16* dX, float* dA, float* dB,
+                                  void* workspace, size_t workspace_bytes,
+                                  int64_t m, int64_t n, int64_t k, int64_t r, float alpha,
+                                  void* stream) {
+  if (!dY || !X || !W || !A || !B || !U || !dX || !dA || !dB) return LORA_ERR_NULL;
+  lora_status st = check_shape(m, n, k, r);
+  if (st != LORA_OK) return st;
+  if (r > 16) return LORA_ERR_UNSUPPORTED;
+  if (!aligned16(dY) || !aligned16(X) || !aligned16(W) || !aligned16(A) || !aligned16(B) ||
+      !aligned16(U) || !aligned16(dX) || !aligned16(dA) || !aligned16(dB))
+    return LORA_ERR_ALIGN;
+  const size_t need = lora::bwd_fused_layout(m, n, k, r).total;
+  if (!workspace || workspace_bytes < need) return LORA_ERR_WORKSPACE;
+  if (!aligned16(workspace)) return LORA_ERR_ALIGN;
+
+  const Range in[6] = {span(dY, m, n, 2), span(X, m, k, 2), span(W, n, k, 2),
+                       span(A, r, k, 2),  span(B, n, r, 2), span(U, m, r, 4)};
+  const Range out[4] = {span(dX, m, k, 2), span(dA, r, k, 4), span(dB, n, r, 4),
+                        Range{reinterpret_cast<uintptr_t>(workspace),
+                              reinterpret_cast<uintptr_t>(workspace) + need}};
+  if (any_alias(out, 4, in, 6)) return LORA_ERR_ALIAS;
+
+  lora::BwdArgs a{dY, X, W, A, B, U, dX, dA, dB, static_cast<char*>(workspace),
+                  m, n, k, r, (float)alpha / (float)r};
+  hipError_t e = lora::launch_bwd_fused(a, reinterpret_cast<hipStream_t>(stream));
+  return e == hipSuccess ? LORA_OK : LORA_ERR_HIP;
+}
+
 lora_status lora_linear_bwd_dropout(const lora_bf16* dY, const lora_bf16* X, const lora_bf16* W,
                                     const lora_bf16* A, const lora_bf16* B, const float* U, const uint8_t* keep,
                                     float p, lora_bf16* dX, float* dA, float* dB, void* workspace,

@@ -776,6 +776,301 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
 }
 
 // ---------------------------------------------------------------------------
+// Fused backward for ranks up to 16 (no dropout): the dX GEMM also forms dU
+// and the dB partials from the dY tiles it stages, so no other launch reads
+// dY.  Tile of 128 tokens x 256 input features, waves and k loop as in
+// lora_bwd_dx_kernel (stages of 64 along n, loads two stages ahead in
+// registers, the products of the last substep after the barrier).
+//   dU^T = B^T dY^T: each stage also stages its 64 B rows ([64][16] bf16,
+//     zero beyond r and n); at substep wn of every stage, wave (wm, wn)
+//     multiplies the transposed B rows (rows t >= 16 of the operand zero)
+//     with its own dY fragments.  After the loop the four partial sums of each
+//     token are added in wn order, s dU is split into bf16 high and low parts
+//     in LDS, and the rank-r term [dU_hi | dU_lo] [A; A] is added to the dX
+//     tile.  The workgroups of column tile 0 also store the parts transposed
+//     (dUt2 [32][mp]) for the dA reduction.
+//   dB^T partials: at the stages st with st % tiles_n == tn, four waves (the
+//     lower or upper four, alternately) each form U^T dY for 16 of the stage's
+//     64 n over the tile's 128 tokens, with U^T as high and low bf16 parts
+//     (staged in LDS in the prologue), and store the tile row's partial
+//     pbt [tm][16][n] (s is applied by the finalize).
+// FULL: n a multiple of 64 and k of 256 (no bound checks on the loads).
+// FASTB: r a multiple of 8 (B rows staged with 16-byte loads).
+template <bool FULL, bool FASTB>
+__global__ __launch_bounds__(512) void lora_bwd_dxf_kernel(
+    const u16* __restrict__ dY, const u16* __restrict__ W, const u16* __restrict__ A, const u16* __restrict__ B,
+    const float* __restrict__ U, u16* __restrict__ dX, u16* __restrict__ dUt2, float* __restrict__ pbt, int m, int n,
+    int k, int r, int mp, float s, int tiles_m, int tiles_n) {
+  constexpr int BM = 128, BN = 256, WM = 2, WN = 4, RP = 16;
+  constexpr int NW = WM * WN, NT = 64 * NW;
+  constexpr int WTI = BM / WM, WTJ = BN / WN;
+  constexpr int FI = WTI / 32, FJ = WTJ / 32;
+  constexpr int YB = BM * 128, WB = 64 * BN * 2, BB = 64 * RP * 2;
+  constexpr int STAGE = YB + WB + BB;
+  constexpr int CPR = BN / 8;                       // 16-byte chunks per W tile row
+  constexpr int CY = BM * 8, CW = 64 * CPR;
+  constexpr int LY = CY / NT, LW = CW / NT, LW1 = LW / 2;
+  constexpr int UTP = BM * 2 + 16;                  // U^T row pitch in bytes
+  constexpr int UT_OFF = 2 * STAGE;
+  static_assert(CY % NT == 0 && CW % NT == 0 && UT_OFF + 2 * RP * UTP <= 160 * 1024, "tile shape and LDS budget");
+  __shared__ __attribute__((aligned(1024))) char smem[UT_OFF + 2 * RP * UTP];
+
+  int tm, tn;
+  tile_coords(tiles_m, tiles_n, 8, (int)blockIdx.x, tm, tn);
+  const int m0 = tm * BM, l0 = tn * BN;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = uniform(tid >> 6);
+  const int wm = wave / WN, wn = wave % WN;
+  const int g = lane >> 5, c32 = lane & 31;
+  const int g16 = lane >> 4, c16 = lane & 15;
+  const uint32_t yrow = (uint32_t)n * 2, wrow = (uint32_t)k * 2;
+  const __amdgpu_buffer_rsrc_t rsY = make_rsrc(dY + (size_t)m0 * n, (uint64_t)min(BM, m - m0) * yrow);
+  const __amdgpu_buffer_rsrc_t rsA = make_rsrc(A, (uint64_t)r * wrow);
+  const __amdgpu_buffer_rsrc_t rsB = make_rsrc(B, (uint64_t)n * r * 2);
+  const int nkb = (n + 63) / 64;
+
+  // U^T of the tile's tokens: high parts in rows 0..15, low parts in rows
+  // 16..31 (zero beyond r and m), for the dB products.
+  char* Uts = smem + UT_OFF;
+  for (int e = tid; e < BM * RP; e += NT) {
+    const int i = e / RP, t = e - i * RP;
+    const float v = (m0 + i < m && t < r) ? U[(size_t)(m0 + i) * r + t] : 0.f;
+    const u16 h = f32_to_bf16(v);
+    *reinterpret_cast<u16*>(Uts + t * UTP + i * 2) = h;
+    *reinterpret_cast<u16*>(Uts + (RP + t) * UTP + i * 2) = f32_to_bf16(v - bf16_to_f32(h));
+  }
+
+  // Staging registers, stored in pieces: 0 = the dY rows and (threads below
+  // 128) one 16-byte half of a B row, 1 and 2 = the two halves of the W rows.
+  int4v gy[LY], gw[LW], gb = int4v{0, 0, 0, 0};
+  auto gload = [&](int st, int piece) {
+    const int n0 = st * 64;
+    if (piece == 0) {
+#pragma unroll
+      for (int i = 0; i < LY; ++i) {
+        const int q = tid + i * NT;
+        const int nn = n0 + 8 * (q & 7);
+        gy[i] = buf_load16(rsY, (FULL || nn < n) ? (uint32_t)(q >> 3) * yrow + (uint32_t)nn * 2 : kOOB);
+      }
+      if (tid < 128) {   // waves 0 and 1: row n0 + tid / 2, ranks 8 (tid % 2) .. +7
+        const int row = n0 + (tid >> 1), t0 = 8 * (tid & 1);
+        if constexpr (FASTB) {
+          gb = buf_load16(rsB, (row < n && t0 < r) ? ((uint32_t)row * r + t0) * 2 : kOOB);
+        } else {
+          uint32_t w[4];
+#pragma unroll
+          for (int x = 0; x < 4; ++x) {
+            const int t = t0 + 2 * x;
+            const uint32_t lo = (row < n && t < r) ? B[(size_t)row * r + t] : 0u;
+            const uint32_t hi = (row < n && t + 1 < r) ? B[(size_t)row * r + t + 1] : 0u;
+            w[x] = lo | (hi << 16);
+          }
+          gb = int4v{(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
+        }
+      }
+    } else if (piece <= 2) {
+      const __amdgpu_buffer_rsrc_t rsW = make_rsrc(W + (size_t)n0 * k, (uint64_t)min(64, n - n0) * wrow);
+#pragma unroll
+      for (int i = piece == 1 ? 0 : LW1; i < (piece == 1 ? LW1 : LW); ++i) {
+        const int q = tid + i * NT;
+        const int ll = l0 + 8 * (q % CPR);
+        gw[i] = buf_load16(rsW, (FULL || ll < k) ? (uint32_t)(q / CPR) * wrow + (uint32_t)ll * 2 : kOOB);
+      }
+    }
+  };
+  auto swrite = [&](int buf, int piece) {
+    char* sb = smem + buf * STAGE;
+    if (piece == 0) {
+#pragma unroll
+      for (int i = 0; i < LY; ++i) {
+        const int q = tid + i * NT;
+        *reinterpret_cast<int4v*>(sb + kc_offset(q >> 3, q & 7)) = gy[i];
+      }
+      if (tid < 128) *reinterpret_cast<int4v*>(sb + YB + WB + tid * 16) = gb;   // Bs [64][16]
+    } else if (piece <= 2) {
+#pragma unroll
+      for (int i = piece == 1 ? 0 : LW1; i < (piece == 1 ? LW1 : LW); ++i) {
+        const int q = tid + i * NT;
+        *reinterpret_cast<int4v*>(sb + YB + mc32_offset<BN>(q / CPR, q % CPR)) = gw[i];
+      }
+    }
+  };
+
+  floatx16 acc[FJ][FI], dacc[FI];
+#pragma unroll
+  for (int a = 0; a < FJ; ++a)
+#pragma unroll
+    for (int b = 0; b < FI; ++b) acc[a][b] = floatx16{};
+#pragma unroll
+  for (int b = 0; b < FI; ++b) dacc[b] = floatx16{};
+
+  // Fragments of substep ks (16 n): W and dY as in lora_bwd_dx_kernel, and at
+  // this wave's substep (ks == wn) the B^T operand: lane (g, c32) row t = c32
+  // (zero for c32 >= 16), k = n 16 ks + 8g .. +7, read transposed from Bs
+  // (rows of 32 bytes, no swizzle: a 16-lane read covers 128 contiguous bytes).
+  short8 fw[2][FJ], fy[2][FI], fb = short8{};
+  auto read_frags = [&](const char* sb, int ks, int p) {
+    const char* Ys = sb;
+    const char* Ws = sb + YB;
+#pragma unroll
+    for (int fj = 0; fj < FJ; ++fj) fw[p][fj] = mc32_read_tr<BN>(Ws, 16 * ks, wn * WTJ + 32 * fj, lane);
+#pragma unroll
+    for (int fi = 0; fi < FI; ++fi) fy[p][fi] = kc_read(Ys, wm * WTI + 32 * fi + c32, 2 * ks + g);
+    if (ks == wn) {
+      const int j = lane & 15;
+      const char* p0 = sb + YB + WB + (16 * ks + 8 * g + (j >> 2)) * (RP * 2) + (j & 3) * 8;
+      const short8 v = join4(__builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4v*)p0),
+                             __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4v*)(p0 + 4 * RP * 2)));
+      fb = ((lane >> 4) & 1) ? short8{} : v;
+    }
+  };
+  auto multiply = [&](int p, int ks) {
+#pragma unroll
+    for (int fi = 0; fi < FI; ++fi)
+#pragma unroll
+      for (int fj = 0; fj < FJ; ++fj) acc[fj][fi] = mfma32x32x16(fw[p][fj], fy[p][fi], acc[fj][fi]);
+    if (ks == wn) {
+#pragma unroll
+      for (int fi = 0; fi < FI; ++fi) dacc[fi] = mfma32x32x16(fb, fy[p][fi], dacc[fi]);
+    }
+  };
+  // dB^T partial of stage st (its buffer sb): wave set (st / tiles_n) % 2,
+  // wave f of the set takes n columns 16 f .. 16 f + 15 of the stage.
+  auto dB_part = [&](const char* sb, int st) {
+    const int f = wave - 4 * ((st / tiles_n) & 1);
+    if (f < 0 || f >= 4) return;
+    floatx4 d = floatx4{0.f, 0.f, 0.f, 0.f};
+    const int j = lane & 15, col = 16 * f + 4 * (j & 3);
+#pragma unroll
+    for (int kt = 0; kt < BM / 32; ++kt) {
+      // B operand: lane (g16, c16) column n 16 f + c16, k = tokens 32 kt + 8 g16 .. +7
+      const int r0 = 32 * kt + 8 * g16 + (j >> 2);
+      const char* p0 = sb + kc_offset(r0, col >> 3) + (col & 7) * 2;
+      const char* p1 = sb + kc_offset(r0 + 4, col >> 3) + (col & 7) * 2;
+      const short8 yb = join4(__builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4v*)p0),
+                              __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4v*)p1));
+      const short8 uh = *reinterpret_cast<const short8*>(Uts + c16 * UTP + (32 * kt + 8 * g16) * 2);
+      const short8 ul = *reinterpret_cast<const short8*>(Uts + (RP + c16) * UTP + (32 * kt + 8 * g16) * 2);
+      d = mfma16x16x32(uh, yb, d);
+      d = mfma16x16x32(ul, yb, d);
+    }
+    const int cn = st * 64 + 16 * f + c16;   // lane: column cn, ranks 4 g16 .. +3
+    if (FULL || cn < n) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) pbt[((size_t)tm * RP + 4 * g16 + q) * n + cn] = d[q];
+    }
+  };
+
+#pragma unroll
+  for (int j = 0; j < FJ; ++j) fw[1][j] = short8{};
+#pragma unroll
+  for (int j = 0; j < FI; ++j) fy[1][j] = short8{};
+  auto stage = [&](int st, auto bufc, bool write_next, bool load_next) {
+    constexpr int BUF = decltype(bufc)::value;
+    const int cur = BUF >= 0 ? BUF : (st & 1);
+    const char* sb = smem + cur * STAGE;
+    read_frags(sb, 0, 0);
+    multiply(1, 3);   // substep 3 of the previous stage (zero operands before stage 0)
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      if (write_next) swrite(cur ^ 1, ks);
+      if (load_next) gload(st + 2, ks);
+      if (ks < 3) {
+        read_frags(sb, ks + 1, (ks + 1) & 1);
+        multiply(ks & 1, ks);
+      }
+    }
+    if (st % tiles_n == tn) dB_part(sb, st);
+    __syncthreads();
+  };
+#pragma unroll
+  for (int pc = 0; pc < 3; ++pc) gload(0, pc);
+#pragma unroll
+  for (int pc = 0; pc < 3; ++pc) swrite(0, pc);
+  __syncthreads();
+  // (stages with run-time buffer parity: the paired loop of lora_bwd_dx_kernel
+  // spills here)
+  using BR = std::integral_constant<int, -1>;
+  int st = 0;
+  if (nkb >= 2) {
+#pragma unroll
+    for (int pc = 0; pc < 3; ++pc) gload(1, pc);
+    for (; st + 2 < nkb; ++st) stage(st, BR{}, true, true);
+    stage(st++, BR{}, true, false);   // st = nkb - 2: stores the last stage
+  }
+  stage(st, BR{}, false, false);
+  multiply(1, 3);
+
+  // ---- epilogue (LDS stage buffers free after the loop's last barrier):
+  // red [NW][FI][8][64] fp32 (rows t < 16 of each wave's dU^T partials), Us2
+  // [BM][UP] bf16 (s dU high | low), As2 [RP][BN] bf16 mn-contiguous (A rows
+  // of the tile, zero beyond r and k).
+  constexpr int RED = NW * FI * 8 * 64 * 4;
+  constexpr int UP = 2 * RP + 8;
+  static_assert(RED + BM * UP * 2 + RP * BN * 2 <= UT_OFF && NW * kYsBytes <= UT_OFF, "epilogue fits the stage LDS");
+  float* red = reinterpret_cast<float*>(smem);
+  u16* Us2 = reinterpret_cast<u16*>(smem + RED);
+  char* As2 = smem + RED + BM * UP * 2;
+#pragma unroll
+  for (int fi = 0; fi < FI; ++fi)
+#pragma unroll
+    for (int q = 0; q < 8; ++q) red[((wave * FI + fi) * 8 + q) * 64 + lane] = dacc[fi][q];
+  for (int q = tid; q < RP * (BN / 8); q += NT) {
+    const int t = q / (BN / 8), c = q % (BN / 8);
+    const int ll = l0 + 8 * c;
+    *reinterpret_cast<int4v*>(As2 + mc32_offset<BN>(t, c)) =
+        buf_load16(rsA, (t < r && ll < k) ? (uint32_t)t * wrow + (uint32_t)ll * 2 : kOOB);
+  }
+  __syncthreads();
+  // entry e: lane ln of (token half wh, fragment fi), result row q: token
+  // wh 64 + 32 fi + ln % 32, rank 8 (q / 4) + 4 (ln / 32) + q % 4
+  for (int e = tid; e < WM * FI * 8 * 64; e += NT) {
+    const int ln = e & 63, q = (e >> 6) & 7, fi = (e >> 9) & 1, wh = e >> 10;
+    float v = 0.f;
+#pragma unroll
+    for (int w4 = 0; w4 < WN; ++w4) v += red[(((wh * WN + w4) * FI + fi) * 8 + q) * 64 + ln];
+    const int i = wh * WTI + 32 * fi + (ln & 31);
+    const int t = 8 * (q >> 2) + 4 * (ln >> 5) + (q & 3);
+    const float d = s * v;
+    const u16 hi = f32_to_bf16(d), lo = f32_to_bf16(d - bf16_to_f32(hi));
+    Us2[i * UP + t] = hi;
+    Us2[i * UP + RP + t] = lo;
+    if (tn == 0 && m0 + i < mp) {
+      dUt2[(size_t)t * mp + m0 + i] = hi;
+      dUt2[(size_t)(RP + t) * mp + m0 + i] = lo;
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int fj = 0; fj < FJ; ++fj) {
+    const short8 af = mc32_read_tr<BN>(As2, 0, wn * WTJ + 32 * fj, lane);
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk)   // k = t of [dU_hi | dU_lo] against [A; A]
+#pragma unroll
+      for (int fi = 0; fi < FI; ++fi) {
+        const short8 bf = *reinterpret_cast<const short8*>(Us2 + (wm * WTI + 32 * fi + c32) * UP + 16 * kk + 8 * g);
+        acc[fj][fi] = mfma32x32x16(af, bf, acc[fj][fi]);
+      }
+  }
+  __syncthreads();
+  {
+    const int j0 = l0 + wn * WTJ;
+#pragma unroll
+    for (int fi = 0; fi < FI; ++fi) {
+      const int i0 = m0 + wm * WTI + 32 * fi;
+      store_block_32x64(acc[0][fi], acc[1][fi], smem + wave * kYsBytes, dX + (size_t)i0 * k + j0, (size_t)k,
+                        m - i0, k - j0, lane);
+    }
+  }
+}
+
+// Fixed-order sum of the dA and dB partials as a launch of its own (the fused
+// backward's token reduction runs after its dX launch).
+__global__ __launch_bounds__(256) void lora_finalize_kernel(FinalizeArgs f) {
+  finalize_partials(f, (int)(blockIdx.x * 256 + threadIdx.x), (int)(gridDim.x * 256));
+}
+
+// ---------------------------------------------------------------------------
 // dX columns [l_begin, l_end) with one tile; the workgroups' tails also
 // finalize the dA and dB partials described by fin (none when fin is empty).
 template <int BM, int BN, int WM, int WN, int RP, bool DROP, bool GRP>
@@ -867,6 +1162,38 @@ static hipError_t launch_bwd_rp(const BwdArgs& a, const BwdLayout& L, hipStream_
   e = tile(p.t1, fin, 0, p.n1);
   if (e != hipSuccess || p.n1 >= a.k) return e;
   return tile(p.t2, FinalizeArgs{}, p.n1, a.k);
+}
+
+// Fused backward: the dX launch (dU, the dB partials, dX), the dA token
+// reduction, then the finalize of dA and dB.
+hipError_t launch_bwd_fused(const BwdArgs& a, hipStream_t st) {
+  const BwdFusedLayout L = bwd_fused_layout(a.m, a.n, a.k, a.r);
+  u16* dUt2 = reinterpret_cast<u16*>(a.ws + L.dut2);
+  float* pb = reinterpret_cast<float*>(a.ws + L.pb);
+  float* pa = reinterpret_cast<float*>(a.ws + L.pa);
+  const int m = (int)a.m, n = (int)a.n, k = (int)a.k, r = (int)a.r, mp = (int)L.mp;
+  const int tiles_m = L.tiles_m, tiles_n = (k + 255) / 256;
+  const dim3 grid(tiles_m * tiles_n), block(512);
+  if (r % 8 != 0)
+    hipLaunchKernelGGL((lora_bwd_dxf_kernel<false, false>), grid, block, 0, st, a.dY, a.W, a.A, a.B, a.U, a.dX, dUt2,
+                       pb, m, n, k, r, mp, a.s, tiles_m, tiles_n);
+  else if (n % 64 == 0 && k % 256 == 0)
+    hipLaunchKernelGGL((lora_bwd_dxf_kernel<true, true>), grid, block, 0, st, a.dY, a.W, a.A, a.B, a.U, a.dX, dUt2,
+                       pb, m, n, k, r, mp, a.s, tiles_m, tiles_n);
+  else
+    hipLaunchKernelGGL((lora_bwd_dxf_kernel<false, true>), grid, block, 0, st, a.dY, a.W, a.A, a.B, a.U, a.dX, dUt2,
+                       pb, m, n, k, r, mp, a.s, tiles_m, tiles_n);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const RedProblem pap{dUt2, a.X, pa, k, (int)L.plan_a.span, L.plan_a.col_tiles, nullptr};
+  const int nb = L.plan_a.col_tiles * L.plan_a.splits;
+  hipLaunchKernelGGL((lora_tokred_kernel<16, false>), dim3(nb), dim3(256), 0, st, pap, pap, nb, m, mp);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  const FinalizeArgs fin{pb, pa, a.dB, a.dA, n, k, r, 16, tiles_m, L.plan_a.splits, a.s, 1.0f};
+  const int total = n * r + r * k;
+  const int blocks = min((total + 255) / 256, 2048);
+  hipLaunchKernelGGL(lora_finalize_kernel, dim3(blocks), dim3(256), 0, st, fin);
+  return hipGetLastError();
 }
 
 hipError_t launch_bwd(const BwdArgs& a, hipStream_t st) {

@@ -127,6 +127,31 @@ inline BwdLayout bwd_layout(int64_t m, int64_t n, int64_t k, int64_t r) {
   return L;
 }
 
+// Workspace of the fused backward (rank <= 16): dUt2 [32][mp] bf16 (dU^T high
+// and low parts, written by the dX launch for the dA reduction), the dB^T
+// partials of the dX launch [tiles_m][16][n] fp32 (one per 128-token tile
+// row) and the dA partials of the token reduction [splits][16][k] fp32.
+struct BwdFusedLayout {
+  size_t dut2, pb, pa, total;
+  RedPlan plan_a;
+  int64_t mp;
+  int tiles_m;
+};
+
+inline BwdFusedLayout bwd_fused_layout(int64_t m, int64_t n, int64_t k, int64_t r) {
+  (void)r;
+  BwdFusedLayout L;
+  L.mp = pad_tokens(m);
+  L.tiles_m = (int)((m + 127) / 128);
+  L.plan_a = plan_reduction(m, k, 16);
+  size_t off = 0;
+  L.dut2 = off; off = align256(off + 2 * 16 * (size_t)L.mp * 2);
+  L.pb = off;   off = align256(off + (size_t)L.tiles_m * 16 * (size_t)n * 4);
+  L.pa = off;   off = align256(off + (size_t)L.plan_a.splits * 16 * (size_t)k * 4);
+  L.total = off;
+  return L;
+}
+
 struct FwdArgs {
   const uint16_t *X, *W, *A, *B;
   uint16_t* Y;
@@ -222,6 +247,7 @@ struct MergeArgs {
 hipError_t launch_fwd(const FwdArgs& a, hipStream_t st);
 hipError_t launch_merge(const MergeArgs& a, hipStream_t st);
 hipError_t launch_bwd(const BwdArgs& a, hipStream_t st);
+hipError_t launch_bwd_fused(const BwdArgs& a, hipStream_t st);   // rank <= 16, no dropout
 hipError_t launch_fwd_group(const GroupFwdArgs& a, hipStream_t st);
 hipError_t launch_bwd_group(const GroupBwdArgs& a, hipStream_t st);
 

@@ -28,8 +28,9 @@ def f64(bits):
     return oracle.bf16_bits_to_f64(bits)
 
 
-def run_gpu(t: dict, shape: Shape, poison: bool = True, stream=None):
-    """Run fwd then bwd on the device; returns host copies of every output."""
+def run_gpu(t: dict, shape: Shape, poison: bool = True, stream=None, fused: bool = False):
+    """Run fwd then bwd on the device (lora_linear_bwd, or lora_linear_bwd_fused
+    with fused=True); returns host copies of every output."""
     import torch
     import paper_2403_11366_amd as lora
     from paper_2403_11366_amd.device_io import bits_to_device, device_to_bits
@@ -41,14 +42,15 @@ def run_gpu(t: dict, shape: Shape, poison: bool = True, stream=None):
     dX = torch.empty((m, k), dtype=torch.bfloat16, device="cuda")
     dA = torch.empty((r, k), dtype=torch.float32, device="cuda")
     dB = torch.empty((n, r), dtype=torch.float32, device="cuda")
-    ws = torch.empty(lora.lora_linear_bwd_workspace_size(m, n, k, r), dtype=torch.uint8, device="cuda")
+    ws_size = (lora.lora_linear_bwd_fused_workspace_size if fused else lora.lora_linear_bwd_workspace_size)
+    ws = torch.empty(ws_size(m, n, k, r), dtype=torch.uint8, device="cuda")
     if poison:
         for x in (Y, U, dX, dA, dB):
             x.fill_(float("nan"))
         ws.fill_(0xFF)  # bf16/fp32 NaN patterns everywhere in the workspace
     lora.lora_linear_fwd(d["X"], d["W"], d["A"], d["B"], Y, U, shape.alpha, stream=stream)
-    lora.lora_linear_bwd(d["dY"], d["X"], d["W"], d["A"], d["B"], U, dX, dA, dB, ws, shape.alpha,
-                         stream=stream)
+    bwd = lora.lora_linear_bwd_fused if fused else lora.lora_linear_bwd
+    bwd(d["dY"], d["X"], d["W"], d["A"], d["B"], U, dX, dA, dB, ws, shape.alpha, stream=stream)
     torch.cuda.synchronize()
     return {"Y": device_to_bits(Y), "U": U.cpu().numpy(), "dX": device_to_bits(dX),
             "dA": dA.cpu().numpy(), "dB": dB.cpu().numpy()}

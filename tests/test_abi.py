@@ -264,3 +264,34 @@ def test_group_validation(lib):
     arr["dA"][1] = base + (5 * 16 + 1) * (1 << 30)
     arr["dY"][0] = 0
     assert group_bwd(lib, ns=ns, arrays=arr) == 1
+
+
+def bwd_fused(lib, ptrs=None, ws_bytes=None, m=64, n=64, k=64, r=8, alpha=16.0):
+    p = [addr(i) for i in range(10)] if ptrs is None else ptrs
+    if ws_bytes is None:
+        ws_bytes = lora.lora_linear_bwd_fused_workspace_size(m, n, k, r)
+    return lib.lora_linear_bwd_fused(*p, ws_bytes, m, n, k, r, alpha, None)
+
+
+def test_bwd_fused_validation(lib):
+    need = lora.lora_linear_bwd_fused_workspace_size(64, 64, 64, 8)
+    assert need > 0 and need % 256 == 0
+    assert lora.lora_linear_bwd_fused_workspace_size(64, 64, 64, 17) == 0   # rank above 16
+    assert lora.lora_linear_bwd_fused_workspace_size(64, 60, 64, 8) == 0
+    assert bwd_fused(lib, ws_bytes=need - 1) == 5
+    assert bwd_fused(lib, ws_bytes=1 << 30, r=17) == 4
+    assert bwd_fused(lib, ws_bytes=1 << 30, r=65) == 4
+    assert bwd_fused(lib, ws_bytes=1 << 30, m=0) == 2
+    for i in range(10):
+        p = [addr(j) for j in range(10)]
+        p[i] = None
+        assert bwd_fused(lib, p) == (5 if i == 9 else 1)
+        p = [addr(j) for j in range(10)]
+        p[i] += 4
+        assert bwd_fused(lib, p) == 3
+    p = [addr(j) for j in range(10)]
+    p[6] = p[0]            # dX on top of dY
+    assert bwd_fused(lib, p) == 6
+    p = [addr(j) for j in range(10)]
+    p[9] = p[2] + 256      # workspace inside W
+    assert bwd_fused(lib, p) == 6
