@@ -16,7 +16,9 @@
 //             n and then over the 2 RP wide slab (high and low part of dU
 //             against the same A rows).  W is read through LDS with the
 //             transposing ds_read_b64_tr_b16, since the product contracts
-//             W over its rows.  After its tile, each workgroup of this launch
+//             W over its rows.  The 128 x 256 tile with whole stages copies
+//             them straight into LDS and issues its fragment reads as inline
+//             assembly with explicit waits.  After its tile, each workgroup of this launch
 //             (the first one of a split) sums a slice of the dB and dA
 //             partials in a fixed order (no atomics, so results are
 //             bit-identical from run to run) and applies s to dB.
@@ -443,8 +445,12 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
   static_assert(WTI % 32 == 0 && WTJ % 32 == 0, "32x32 fragments");
   static_assert(BN == 128 || BN == 256, "W tile rows of 256 or 512 bytes");
   static_assert(NSLAB == 1 || NSLAB == 2, "slab stages of the unrolled tail");
-  static_assert(2 * STAGE <= 160 * 1024, "LDS budget");
-  __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
+  // DMA: the plain 128 x 256 tile with FULL copies its stages straight into
+  // three LDS buffers (see the k loop below).
+  constexpr bool DMA = FULL && BM == 128 && BN == 256 && !DROP && !GRP;
+  constexpr int NBUF = DMA ? 3 : 2;
+  static_assert(NBUF * STAGE <= 160 * 1024, "LDS budget");
+  __shared__ __attribute__((aligned(1024))) char smem[NBUF * STAGE];
 
   int tm, tn;
   tile_coords(tiles_m, tiles_n, 8, (int)blockIdx.x, tm, tn);
@@ -581,6 +587,131 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
       for (int fj = 0; fj < FJ; ++fj) acc[fj][fi] = mfma32x32x16(fw[p][fj], fy[p][fi], acc[fj][fi]);
   };
 
+  if constexpr (DMA) {
+    // Stages 0 .. nkb-1 over n, then the NSLAB slab stages; each stage is
+    // copied from global memory straight into one of three LDS buffers, two
+    // stages ahead, without staging registers: copy instruction j of a wave
+    // fills 1 KB of the buffer (dY region: rows 8j .. 8j+7; W region: rows 2j,
+    // 2j+1), lane l its 16-byte position l, which holds the logical chunk given
+    // by the tile's swizzle (applied to the global address).  The fragment
+    // reads are issued as inline assembly with explicit lgkmcnt waits: the
+    // compiler would otherwise wait for every copy still in flight
+    // (s_waitcnt vmcnt(0)) before each transposing read, which undoes the
+    // prefetch.  Per substep a wave issues 6 LDS reads (4 transposing reads of
+    // W, 2 of dY); the products of substep ks wait until only the 6 reads of
+    // substep ks+1 are outstanding.  Each stage ends with a barrier that waits
+    // only for this wave's copies of the next stage (copy_barrier).
+    const int T = nkb + NSLAB;
+    const int dl_r8 = lane >> 3, dl_c8 = lane & 7, dl_r32 = lane >> 5, dl_c32 = lane & 31;
+    auto dload = [&](int kb, int buf) {
+      char* sb = smem + buf * STAGE;
+      if (kb < nkb) {
+        const __amdgpu_buffer_rsrc_t rsW = make_rsrc(W + (size_t)kb * 64 * k, (uint64_t)64 * wrow);
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+          const int j = wave + 8 * i, row = 8 * j + dl_r8;
+          dma16(rsY, (uint32_t)row * yrow + (uint32_t)((dl_c8 ^ kc_swz(row)) << 4), (uint32_t)kb * 128,
+                sb + j * 1024);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int j = wave + 8 * i, row = 2 * j + dl_r32;
+          const int c = dl_c32 ^ mc32_swz(row);
+          dma16(rsW, (uint32_t)row * wrow + (uint32_t)(l0 + 8 * c) * 2, 0, sb + BM * 128 + j * 1024);
+        }
+      } else {
+        const int kk0 = (kb - nkb) * 64;
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+          const int j = wave + 8 * i, row = 8 * j + dl_r8;
+          const int kk = kk0 + 8 * (dl_c8 ^ kc_swz(row));
+          dma16(rsU, kk < KS2 ? (uint32_t)row * urow + (uint32_t)kk * 2 : kOOB, 0, sb + j * 1024);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int j = wave + 8 * i, row = 2 * j + dl_r32;
+          const int c = dl_c32 ^ mc32_swz(row);
+          const int kk = kk0 + row, t = kk % RP;
+          dma16(rsA, (kk < KS2 && t < r) ? (uint32_t)t * wrow + (uint32_t)(l0 + 8 * c) * 2 : kOOB, 0,
+                sb + BM * 128 + j * 1024);
+        }
+      }
+    };
+    constexpr int NCOPY = 6;   // copies per wave and stage
+    // Lane addresses of the fragment reads in buffer 0, substep 0: W fragment
+    // fj (the second read of a pair is 4 rows = 2048 bytes further; substep ks
+    // adds 16 rows = 8192 bytes, the swizzle depending only on row % 4), dY
+    // fragment fi at substep ks (fi adds 32 rows = 4096 bytes).
+    uint32_t wa[FJ], ya[4];
+    {
+      const int h = (lane >> 4) & 1, j = lane & 15, e = j >> 2, q = j & 3;
+#pragma unroll
+      for (int fj = 0; fj < FJ; ++fj) {
+        const int col = wn * WTJ + 32 * fj + 16 * h + 4 * q;
+        wa[fj] = lds_addr(smem + BM * 128 + mc32_offset<BN>(8 * g + e, col >> 3) + (col & 7) * 2);
+      }
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) ya[ks] = lds_addr(smem + kc_offset(wm * WTI + c32, 2 * ks + g));
+    }
+    short4v fwl[2][FJ], fwh[2][FJ];
+    auto reads = [&](uint32_t boff, int ks, int p) {
+#pragma unroll
+      for (int fj = 0; fj < FJ; ++fj) {
+        const uint32_t a0 = wa[fj] + boff + 8192u * ks;
+        ds_read_tr_b64_asm<0>(fwl[p][fj], a0);
+        ds_read_tr_b64_asm<2048>(fwh[p][fj], a0);
+      }
+      ds_read_b128_asm<0>(fy[p][0], ya[ks] + boff);
+      ds_read_b128_asm<4096>(fy[p][1], ya[ks] + boff);
+    };
+    static_assert(FJ == 2 && FI == 2, "six reads per substep");
+    auto mult = [&](int p, bool last) {
+      if (last)
+        asm volatile("s_waitcnt lgkmcnt(0)"
+                     : "+v"(fwl[p][0]), "+v"(fwh[p][0]), "+v"(fwl[p][1]), "+v"(fwh[p][1]), "+v"(fy[p][0]),
+                       "+v"(fy[p][1]));
+      else
+        asm volatile("s_waitcnt lgkmcnt(6)"
+                     : "+v"(fwl[p][0]), "+v"(fwh[p][0]), "+v"(fwl[p][1]), "+v"(fwh[p][1]), "+v"(fy[p][0]),
+                       "+v"(fy[p][1]));
+#pragma unroll
+      for (int fj = 0; fj < FJ; ++fj) {
+        const short8 w8 = join4(fwl[p][fj], fwh[p][fj]);
+#pragma unroll
+        for (int fi = 0; fi < FI; ++fi) acc[fj][fi] = mfma32x32x16(w8, fy[p][fi], acc[fj][fi]);
+      }
+    };
+    auto dstage = [&](int kb, auto bufc, bool load_next) {
+      constexpr int BUF = decltype(bufc)::value;
+      if (load_next) dload(kb + 2, (BUF + 2) % 3);
+      constexpr uint32_t boff = (uint32_t)BUF * STAGE;
+      reads(boff, 0, 0);
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+        if (ks < 3) reads(boff, ks + 1, (ks + 1) & 1);
+        mult(ks & 1, ks == 3);
+      }
+      if (load_next) copy_barrier<NCOPY>();
+      else copy_barrier<0>();
+    };
+    using D0 = std::integral_constant<int, 0>;
+    using D1 = std::integral_constant<int, 1>;
+    using D2 = std::integral_constant<int, 2>;
+    dload(0, 0);
+    if (T > 1) dload(1, 1);
+    copy_barrier<0>();
+    int kb = 0;
+    for (; kb + 5 < T; kb += 3) {
+      dstage(kb, D0{}, true);
+      dstage(kb + 1, D1{}, true);
+      dstage(kb + 2, D2{}, true);
+    }
+    if (kb < T) dstage(kb, D0{}, kb + 2 < T);
+    if (kb + 1 < T) dstage(kb + 1, D1{}, kb + 3 < T);
+    if (kb + 2 < T) dstage(kb + 2, D2{}, kb + 4 < T);
+    if (kb + 3 < T) dstage(kb + 3, D0{}, false);
+    if (kb + 4 < T) dstage(kb + 4, D1{}, false);
+  } else {
   // Same pipeline as the forward GEMM: at the top of stage st the registers
   // hold stage st+1; piece ks goes to the free LDS buffer at substep ks and
   // its registers then receive the loads of stage st+2.  With ROT the
@@ -644,6 +775,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
   if (NSL > 1) stage(st++, BR{}, true, LD_NONE);                     // writes slab 1
   stage(st, BR{}, false, LD_NONE);
   if (ROT) multiply(1);
+  }
 
   if (GRP) {
     // LDS after the k loop, per projection: Us2 [BM][UP] bf16 (dU_g high |

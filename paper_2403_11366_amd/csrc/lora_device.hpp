@@ -95,6 +95,24 @@ __device__ __forceinline__ void copy_barrier() {
   asm volatile("s_barrier" ::: "memory");
 }
 
+// LDS byte address of a pointer into a __shared__ array.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)p;
+}
+
+// LDS reads issued as inline assembly: the compiler does not see them as LDS
+// accesses, so it neither waits for outstanding global -> LDS copies before
+// them nor for their results; the caller waits (s_waitcnt lgkmcnt) before the
+// first use, in an asm statement that takes the destinations as operands.
+template <int OFF>
+__device__ __forceinline__ void ds_read_tr_b64_asm(short4v& d, uint32_t addr) {
+  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(d) : "v"(addr), "i"(OFF));
+}
+template <int OFF>
+__device__ __forceinline__ void ds_read_b128_asm(short8& d, uint32_t addr) {
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(d) : "v"(addr), "i"(OFF));
+}
+
 // 8-byte load through a buffer resource (byte_off a multiple of 8).
 __device__ __forceinline__ uint2 buf_load8(__amdgpu_buffer_rsrc_t rs, uint32_t byte_off) {
   const auto v = __builtin_amdgcn_raw_buffer_load_b64(rs, byte_off, 0, 0);
