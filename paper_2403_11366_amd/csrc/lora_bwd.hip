@@ -16,9 +16,9 @@
 //             n and then over the 2 RP wide slab (high and low part of dU
 //             against the same A rows).  W is read through LDS with the
 //             transposing ds_read_b64_tr_b16, since the product contracts
-//             W over its rows.  The 128 x 256 tile with whole stages copies
-//             them straight into LDS and issues its fragment reads as inline
-//             assembly with explicit waits.  After its tile, each workgroup of this launch
+//             W over its rows.  The 128 x 256 and 256 x 256 tiles with whole
+//             stages copy them straight into LDS and issue their fragment
+//             reads as inline assembly with explicit waits.  After its tile, each workgroup of this launch
 //             (the first one of a split) sums a slice of the dB and dA
 //             partials in a fixed order (no atomics, so results are
 //             bit-identical from run to run) and applies s to dB.
@@ -445,10 +445,11 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
   static_assert(WTI % 32 == 0 && WTJ % 32 == 0, "32x32 fragments");
   static_assert(BN == 128 || BN == 256, "W tile rows of 256 or 512 bytes");
   static_assert(NSLAB == 1 || NSLAB == 2, "slab stages of the unrolled tail");
-  // DMA: the plain 128 x 256 tile with FULL copies its stages straight into
-  // three LDS buffers (see the k loop below).
-  constexpr bool DMA = FULL && BM == 128 && BN == 256 && !DROP && !GRP;
-  constexpr int NBUF = DMA ? 3 : 2;
+  // DMA: the plain 128 x 256 and 256 x 256 tiles with FULL copy their stages
+  // straight into LDS (three buffers, two stages ahead; two buffers, one stage
+  // ahead for 256 x 256), see the k loop below.
+  constexpr bool DMA = FULL && BN == 256 && !DROP && !GRP;
+  constexpr int NBUF = DMA && BM == 128 ? 3 : 2;
   static_assert(NBUF * STAGE <= 160 * 1024, "LDS budget");
   __shared__ __attribute__((aligned(1024))) char smem[NBUF * STAGE];
 
@@ -589,18 +590,21 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
 
   if constexpr (DMA) {
     // Stages 0 .. nkb-1 over n, then the NSLAB slab stages; each stage is
-    // copied from global memory straight into one of three LDS buffers, two
-    // stages ahead, without staging registers: copy instruction j of a wave
-    // fills 1 KB of the buffer (dY region: rows 8j .. 8j+7; W region: rows 2j,
-    // 2j+1), lane l its 16-byte position l, which holds the logical chunk given
-    // by the tile's swizzle (applied to the global address).  The fragment
-    // reads are issued as inline assembly with explicit lgkmcnt waits: the
-    // compiler would otherwise wait for every copy still in flight
-    // (s_waitcnt vmcnt(0)) before each transposing read, which undoes the
-    // prefetch.  Per substep a wave issues 6 LDS reads (4 transposing reads of
-    // W, 2 of dY); the products of substep ks wait until only the 6 reads of
-    // substep ks+1 are outstanding.  Each stage ends with a barrier that waits
-    // only for this wave's copies of the next stage (copy_barrier).
+    // copied from global memory straight into an LDS buffer without staging
+    // registers (128 x 256: three buffers, two stages ahead; 256 x 256: two
+    // buffers, one stage ahead): copy instruction j of a wave fills 1 KB of the
+    // buffer (dY region: rows 8j .. 8j+7; W region: rows 2j, 2j+1), lane l its
+    // 16-byte position l, which holds the logical chunk given by the tile's
+    // swizzle (applied to the global address).  The fragment reads are issued
+    // as inline assembly with explicit lgkmcnt waits: the compiler would
+    // otherwise wait for every copy still in flight (s_waitcnt vmcnt(0))
+    // before each transposing read, which undoes the prefetch.  Per substep a
+    // wave issues NRD LDS reads (2 FJ transposing reads of W, FI of dY); the
+    // products of substep ks wait until only the reads of substep ks+1 are
+    // outstanding.  Each stage ends with a barrier that waits only for this
+    // wave's copies of the next stage (copy_barrier).
+    constexpr int NRD = 2 * FJ + FI;
+    constexpr int CYW = BM / 64;            // dY-region copies per wave and stage
     const int T = nkb + NSLAB;
     const int dl_r8 = lane >> 3, dl_c8 = lane & 7, dl_r32 = lane >> 5, dl_c32 = lane & 31;
     auto dload = [&](int kb, int buf) {
@@ -608,7 +612,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
       if (kb < nkb) {
         const __amdgpu_buffer_rsrc_t rsW = make_rsrc(W + (size_t)kb * 64 * k, (uint64_t)64 * wrow);
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
+        for (int i = 0; i < CYW; ++i) {
           const int j = wave + 8 * i, row = 8 * j + dl_r8;
           dma16(rsY, (uint32_t)row * yrow + (uint32_t)((dl_c8 ^ kc_swz(row)) << 4), (uint32_t)kb * 128,
                 sb + j * 1024);
@@ -622,7 +626,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
       } else {
         const int kk0 = (kb - nkb) * 64;
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
+        for (int i = 0; i < CYW; ++i) {
           const int j = wave + 8 * i, row = 8 * j + dl_r8;
           const int kk = kk0 + 8 * (dl_c8 ^ kc_swz(row));
           dma16(rsU, kk < KS2 ? (uint32_t)row * urow + (uint32_t)kk * 2 : kOOB, 0, sb + j * 1024);
@@ -637,7 +641,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
         }
       }
     };
-    constexpr int NCOPY = 6;   // copies per wave and stage
+    constexpr int NCOPY = CYW + 4;   // copies per wave and stage
     // Lane addresses of the fragment reads in buffer 0, substep 0: W fragment
     // fj (the second read of a pair is 4 rows = 2048 bytes further; substep ks
     // adds 16 rows = 8192 bytes, the swizzle depending only on row % 4), dY
@@ -661,19 +665,36 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
         ds_read_tr_b64_asm<0>(fwl[p][fj], a0);
         ds_read_tr_b64_asm<2048>(fwh[p][fj], a0);
       }
-      ds_read_b128_asm<0>(fy[p][0], ya[ks] + boff);
-      ds_read_b128_asm<4096>(fy[p][1], ya[ks] + boff);
+      const uint32_t y0 = ya[ks] + boff;
+      ds_read_b128_asm<0>(fy[p][0], y0);
+      ds_read_b128_asm<4096>(fy[p][1], y0);
+      if constexpr (FI == 4) {
+        ds_read_b128_asm<8192>(fy[p][2], y0);
+        ds_read_b128_asm<12288>(fy[p][3], y0);
+      }
     };
-    static_assert(FJ == 2 && FI == 2, "six reads per substep");
+    static_assert(FJ == 2 && (FI == 2 || FI == 4), "reads per substep");
     auto mult = [&](int p, bool last) {
-      if (last)
-        asm volatile("s_waitcnt lgkmcnt(0)"
-                     : "+v"(fwl[p][0]), "+v"(fwh[p][0]), "+v"(fwl[p][1]), "+v"(fwh[p][1]), "+v"(fy[p][0]),
-                       "+v"(fy[p][1]));
-      else
-        asm volatile("s_waitcnt lgkmcnt(6)"
-                     : "+v"(fwl[p][0]), "+v"(fwh[p][0]), "+v"(fwl[p][1]), "+v"(fwh[p][1]), "+v"(fy[p][0]),
-                       "+v"(fy[p][1]));
+      if constexpr (FI == 2) {
+        if (last)
+          asm volatile("s_waitcnt lgkmcnt(0)"
+                       : "+v"(fwl[p][0]), "+v"(fwh[p][0]), "+v"(fwl[p][1]), "+v"(fwh[p][1]), "+v"(fy[p][0]),
+                         "+v"(fy[p][1]));
+        else
+          asm volatile("s_waitcnt lgkmcnt(6)"
+                       : "+v"(fwl[p][0]), "+v"(fwh[p][0]), "+v"(fwl[p][1]), "+v"(fwh[p][1]), "+v"(fy[p][0]),
+                         "+v"(fy[p][1]));
+      } else {
+        if (last)
+          asm volatile("s_waitcnt lgkmcnt(0)"
+                       : "+v"(fwl[p][0]), "+v"(fwh[p][0]), "+v"(fwl[p][1]), "+v"(fwh[p][1]), "+v"(fy[p][0]),
+                         "+v"(fy[p][1]), "+v"(fy[p][2]), "+v"(fy[p][3]));
+        else
+          asm volatile("s_waitcnt lgkmcnt(8)"
+                       : "+v"(fwl[p][0]), "+v"(fwh[p][0]), "+v"(fwl[p][1]), "+v"(fwh[p][1]), "+v"(fy[p][0]),
+                         "+v"(fy[p][1]), "+v"(fy[p][2]), "+v"(fy[p][3]));
+      }
+      static_assert(NRD == (FI == 2 ? 6 : 8), "wait counts above");
 #pragma unroll
       for (int fj = 0; fj < FJ; ++fj) {
         const short8 w8 = join4(fwl[p][fj], fwh[p][fj]);
@@ -681,36 +702,57 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
         for (int fi = 0; fi < FI; ++fi) acc[fj][fi] = mfma32x32x16(w8, fy[p][fi], acc[fj][fi]);
       }
     };
-    auto dstage = [&](int kb, auto bufc, bool load_next) {
-      constexpr int BUF = decltype(bufc)::value;
-      if (load_next) dload(kb + 2, (BUF + 2) % 3);
-      constexpr uint32_t boff = (uint32_t)BUF * STAGE;
+    auto compute = [&](uint32_t boff) {
       reads(boff, 0, 0);
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) {
         if (ks < 3) reads(boff, ks + 1, (ks + 1) & 1);
         mult(ks & 1, ks == 3);
       }
-      if (load_next) copy_barrier<NCOPY>();
-      else copy_barrier<0>();
     };
     using D0 = std::integral_constant<int, 0>;
     using D1 = std::integral_constant<int, 1>;
     using D2 = std::integral_constant<int, 2>;
-    dload(0, 0);
-    if (T > 1) dload(1, 1);
-    copy_barrier<0>();
-    int kb = 0;
-    for (; kb + 5 < T; kb += 3) {
-      dstage(kb, D0{}, true);
-      dstage(kb + 1, D1{}, true);
-      dstage(kb + 2, D2{}, true);
+    if constexpr (NBUF == 3) {
+      auto dstage = [&](int kb, auto bufc, bool load_next) {
+        constexpr int BUF = decltype(bufc)::value;
+        if (load_next) dload(kb + 2, (BUF + 2) % 3);
+        compute((uint32_t)BUF * STAGE);
+        if (load_next) copy_barrier<NCOPY>();
+        else copy_barrier<0>();
+      };
+      dload(0, 0);
+      if (T > 1) dload(1, 1);
+      copy_barrier<0>();
+      int kb = 0;
+      for (; kb + 5 < T; kb += 3) {
+        dstage(kb, D0{}, true);
+        dstage(kb + 1, D1{}, true);
+        dstage(kb + 2, D2{}, true);
+      }
+      if (kb < T) dstage(kb, D0{}, kb + 2 < T);
+      if (kb + 1 < T) dstage(kb + 1, D1{}, kb + 3 < T);
+      if (kb + 2 < T) dstage(kb + 2, D2{}, kb + 4 < T);
+      if (kb + 3 < T) dstage(kb + 3, D0{}, false);
+      if (kb + 4 < T) dstage(kb + 4, D1{}, false);
+    } else {
+      // two buffers: stage kb+1 is copied into the other buffer (read in
+      // stage kb-1, before the last barrier) while stage kb multiplies
+      auto dstage = [&](int kb, auto bufc, bool load_next) {
+        constexpr int BUF = decltype(bufc)::value;
+        if (load_next) dload(kb + 1, BUF ^ 1);
+        compute((uint32_t)BUF * STAGE);
+        copy_barrier<0>();
+      };
+      dload(0, 0);
+      copy_barrier<0>();
+      int kb = 0;
+      for (; kb + 1 < T; kb += 2) {
+        dstage(kb, D0{}, true);
+        dstage(kb + 1, D1{}, kb + 2 < T);
+      }
+      if (kb < T) dstage(kb, D0{}, false);
     }
-    if (kb < T) dstage(kb, D0{}, kb + 2 < T);
-    if (kb + 1 < T) dstage(kb + 1, D1{}, kb + 3 < T);
-    if (kb + 2 < T) dstage(kb + 2, D2{}, kb + 4 < T);
-    if (kb + 3 < T) dstage(kb + 3, D0{}, false);
-    if (kb + 4 < T) dstage(kb + 4, D1{}, false);
   } else {
   // Same pipeline as the forward GEMM: at the top of stage st the registers
   // hold stage st+1; piece ks goes to the free LDS buffer at substep ks and
@@ -1212,9 +1254,10 @@ static hipError_t launch_dx_cfg(const BwdArgs& a, const BwdLayout& L, const Fina
   const int nt = 64 * WM * WN;
   const int lb = (int)l_begin;
   const u16* dU2 = GRP ? nullptr : reinterpret_cast<const u16*>(a.ws + L.du2);
-  // (the 256 x 256 tile measured no faster without the checks, and spilled more)
+  // (FULL on the 256 x 256 tile only with its copying variant: register staging
+  // without the checks measured no faster there and spilled more)
   bool full = false;
-  if constexpr (BM * BN < 256 * 256) {
+  if constexpr (BM * BN < 256 * 256 || !GRP) {   // (256 x 256: only the copying variant)
     full = (l_end - l_begin) % BN == 0 && l_end <= a.k;
     if (GRP) {
       for (int g = 0; g < grp.count; ++g) full = full && grp.n[g] % 64 == 0;
