@@ -445,9 +445,11 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
   static_assert(WTI % 32 == 0 && WTJ % 32 == 0, "32x32 fragments");
   static_assert(BN == 128 || BN == 256, "W tile rows of 256 or 512 bytes");
   static_assert(NSLAB == 1 || NSLAB == 2, "slab stages of the unrolled tail");
-  // DMA: the plain 128 x 256 and 256 x 256 tiles with FULL copy their stages
-  // straight into LDS (three buffers, two stages ahead; two buffers, one stage
-  // ahead for 256 x 256), see the k loop below.
+  // DMA: the plain 256-wide tiles with FULL copy their stages straight into
+  // LDS (128 x 256: three buffers, two stages ahead; 256 x 256: two buffers,
+  // one stage ahead), see the k loop below.  (The 128 x 128 tile with two
+  // buffers measured slower than with register staging: 13B q_proj step
+  // 462 -> 467 us.)
   constexpr bool DMA = FULL && BN == 256 && !DROP && !GRP;
   constexpr int NBUF = DMA && BM == 128 ? 3 : 2;
   static_assert(NBUF * STAGE <= 160 * 1024, "LDS budget");
@@ -591,9 +593,9 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
   if constexpr (DMA) {
     // Stages 0 .. nkb-1 over n, then the NSLAB slab stages; each stage is
     // copied from global memory straight into an LDS buffer without staging
-    // registers (128 x 256: three buffers, two stages ahead; 256 x 256: two
-    // buffers, one stage ahead): copy instruction j of a wave fills 1 KB of the
-    // buffer (dY region: rows 8j .. 8j+7; W region: rows 2j, 2j+1), lane l its
+    // registers (three or two buffers, two stages or one ahead): copy
+    // instruction j of a wave fills 1 KB of the
+    // buffer (dY region: rows 8j .. 8j+7; W region: rows WRK j ..), lane l its
     // 16-byte position l, which holds the logical chunk given by the tile's
     // swizzle (applied to the global address).  The fragment reads are issued
     // as inline assembly with explicit lgkmcnt waits: the compiler would
@@ -604,48 +606,52 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
     // outstanding.  Each stage ends with a barrier that waits only for this
     // wave's copies of the next stage (copy_barrier).
     constexpr int NRD = 2 * FJ + FI;
-    constexpr int CYW = BM / 64;            // dY-region copies per wave and stage
+    constexpr int CYW = BM / 8 / NW;        // dY-region copies per wave and stage
+    constexpr int CWW = BN / 8 / NW;        // W-region copies per wave and stage
+    constexpr int WRK = 512 / BN;           // W rows per 1 KB copy
+    constexpr int WRB = BN * 2;             // bytes of a W tile row
+    static_assert(CYW * NW * 8 == BM && CWW * NW * 8 == BN, "copies per stage");
     const int T = nkb + NSLAB;
-    const int dl_r8 = lane >> 3, dl_c8 = lane & 7, dl_r32 = lane >> 5, dl_c32 = lane & 31;
+    const int dl_r8 = lane >> 3, dl_c8 = lane & 7, dl_rw = lane / (BN / 8), dl_cw = lane % (BN / 8);
     auto dload = [&](int kb, int buf) {
       char* sb = smem + buf * STAGE;
       if (kb < nkb) {
         const __amdgpu_buffer_rsrc_t rsW = make_rsrc(W + (size_t)kb * 64 * k, (uint64_t)64 * wrow);
 #pragma unroll
         for (int i = 0; i < CYW; ++i) {
-          const int j = wave + 8 * i, row = 8 * j + dl_r8;
+          const int j = wave + NW * i, row = 8 * j + dl_r8;
           dma16(rsY, (uint32_t)row * yrow + (uint32_t)((dl_c8 ^ kc_swz(row)) << 4), (uint32_t)kb * 128,
                 sb + j * 1024);
         }
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int j = wave + 8 * i, row = 2 * j + dl_r32;
-          const int c = dl_c32 ^ mc32_swz(row);
+        for (int i = 0; i < CWW; ++i) {
+          const int j = wave + NW * i, row = WRK * j + dl_rw;
+          const int c = dl_cw ^ mc32_swz(row);
           dma16(rsW, (uint32_t)row * wrow + (uint32_t)(l0 + 8 * c) * 2, 0, sb + BM * 128 + j * 1024);
         }
       } else {
         const int kk0 = (kb - nkb) * 64;
 #pragma unroll
         for (int i = 0; i < CYW; ++i) {
-          const int j = wave + 8 * i, row = 8 * j + dl_r8;
+          const int j = wave + NW * i, row = 8 * j + dl_r8;
           const int kk = kk0 + 8 * (dl_c8 ^ kc_swz(row));
           dma16(rsU, kk < KS2 ? (uint32_t)row * urow + (uint32_t)kk * 2 : kOOB, 0, sb + j * 1024);
         }
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int j = wave + 8 * i, row = 2 * j + dl_r32;
-          const int c = dl_c32 ^ mc32_swz(row);
+        for (int i = 0; i < CWW; ++i) {
+          const int j = wave + NW * i, row = WRK * j + dl_rw;
+          const int c = dl_cw ^ mc32_swz(row);
           const int kk = kk0 + row, t = kk % RP;
           dma16(rsA, (kk < KS2 && t < r) ? (uint32_t)t * wrow + (uint32_t)(l0 + 8 * c) * 2 : kOOB, 0,
                 sb + BM * 128 + j * 1024);
         }
       }
     };
-    constexpr int NCOPY = CYW + 4;   // copies per wave and stage
+    constexpr int NCOPY = CYW + CWW;   // copies per wave and stage
     // Lane addresses of the fragment reads in buffer 0, substep 0: W fragment
-    // fj (the second read of a pair is 4 rows = 2048 bytes further; substep ks
-    // adds 16 rows = 8192 bytes, the swizzle depending only on row % 4), dY
-    // fragment fi at substep ks (fi adds 32 rows = 4096 bytes).
+    // fj (the second read of a pair is 4 rows further; substep ks adds 16
+    // rows, the swizzle depending only on row % 4), dY fragment fi at substep
+    // ks (fi adds 32 rows = 4096 bytes).
     uint32_t wa[FJ], ya[4];
     {
       const int h = (lane >> 4) & 1, j = lane & 15, e = j >> 2, q = j & 3;
@@ -661,9 +667,9 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
     auto reads = [&](uint32_t boff, int ks, int p) {
 #pragma unroll
       for (int fj = 0; fj < FJ; ++fj) {
-        const uint32_t a0 = wa[fj] + boff + 8192u * ks;
+        const uint32_t a0 = wa[fj] + boff + (uint32_t)(16 * WRB) * ks;
         ds_read_tr_b64_asm<0>(fwl[p][fj], a0);
-        ds_read_tr_b64_asm<2048>(fwh[p][fj], a0);
+        ds_read_tr_b64_asm<4 * WRB>(fwh[p][fj], a0);
       }
       const uint32_t y0 = ya[ks] + boff;
       ds_read_b128_asm<0>(fy[p][0], y0);
