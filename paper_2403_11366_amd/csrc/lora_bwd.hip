@@ -445,12 +445,12 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
   static_assert(WTI % 32 == 0 && WTJ % 32 == 0, "32x32 fragments");
   static_assert(BN == 128 || BN == 256, "W tile rows of 256 or 512 bytes");
   static_assert(NSLAB == 1 || NSLAB == 2, "slab stages of the unrolled tail");
-  // DMA: the plain 256-wide tiles with FULL copy their stages straight into
+  // DMA: the 256-wide tiles with FULL (no dropout) copy their stages straight into
   // LDS (128 x 256: three buffers, two stages ahead; 256 x 256: two buffers,
   // one stage ahead), see the k loop below.  (The 128 x 128 tile with two
   // buffers measured slower than with register staging: 13B q_proj step
   // 462 -> 467 us.)
-  constexpr bool DMA = FULL && BN == 256 && !DROP && !GRP;
+  constexpr bool DMA = FULL && BN == 256 && !DROP;
   constexpr int NBUF = DMA && BM == 128 ? 3 : 2;
   static_assert(NBUF * STAGE <= 160 * 1024, "LDS budget");
   __shared__ __attribute__((aligned(1024))) char smem[NBUF * STAGE];
@@ -611,16 +611,43 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
     constexpr int WRK = 512 / BN;           // W rows per 1 KB copy
     constexpr int WRB = BN * 2;             // bytes of a W tile row
     static_assert(CYW * NW * 8 == BM && CWW * NW * 8 == BN, "copies per stage");
-    const int T = nkb + NSLAB;
+    const int T = nkb + (GRP ? 0 : NSLAB);
+    // With GRP the copies walk the projections' stages in order (dload is
+    // called once per stage, in stage order): cursor = projection, its stage,
+    // its dY rows.
+    int dc_g = 0, dc_sl = -1, dc_n = GRP ? grp.n[0] : n;
+    const u16* dc_W = GRP ? grp.W[0] : W;
+    uint32_t dc_yr = GRP ? (uint32_t)grp.n[0] * 2 : yrow;
+    __amdgpu_buffer_rsrc_t dc_rsY =
+        GRP ? make_rsrc(grp.dY[0] + (size_t)m0 * grp.n[0], (uint64_t)min(BM, m - m0) * dc_yr) : rsY;
     const int dl_r8 = lane >> 3, dl_c8 = lane & 7, dl_rw = lane / (BN / 8), dl_cw = lane % (BN / 8);
     auto dload = [&](int kb, int buf) {
       char* sb = smem + buf * STAGE;
       if (kb < nkb) {
-        const __amdgpu_buffer_rsrc_t rsW = make_rsrc(W + (size_t)kb * 64 * k, (uint64_t)64 * wrow);
+        const u16* Wp = W;
+        uint32_t yr = yrow;
+        __amdgpu_buffer_rsrc_t rsYs = rsY;
+        int sl = kb;
+        if (GRP) {
+          ++dc_sl;
+          if (dc_sl * 64 >= dc_n) {   // next projection (uniform)
+            ++dc_g;
+            dc_sl = 0;
+            dc_n = pick(grp.n, dc_g);
+            dc_W = pick(grp.W, dc_g);
+            dc_yr = (uint32_t)dc_n * 2;
+            dc_rsY = make_rsrc(pick(grp.dY, dc_g) + (size_t)m0 * dc_n, (uint64_t)min(BM, m - m0) * dc_yr);
+          }
+          Wp = dc_W;
+          yr = dc_yr;
+          rsYs = dc_rsY;
+          sl = dc_sl;
+        }
+        const __amdgpu_buffer_rsrc_t rsW = make_rsrc(Wp + (size_t)sl * 64 * k, (uint64_t)64 * wrow);
 #pragma unroll
         for (int i = 0; i < CYW; ++i) {
           const int j = wave + NW * i, row = 8 * j + dl_r8;
-          dma16(rsY, (uint32_t)row * yrow + (uint32_t)((dl_c8 ^ kc_swz(row)) << 4), (uint32_t)kb * 128,
+          dma16(rsYs, (uint32_t)row * yr + (uint32_t)((dl_c8 ^ kc_swz(row)) << 4), (uint32_t)sl * 128,
                 sb + j * 1024);
         }
 #pragma unroll
@@ -1260,10 +1287,10 @@ static hipError_t launch_dx_cfg(const BwdArgs& a, const BwdLayout& L, const Fina
   const int nt = 64 * WM * WN;
   const int lb = (int)l_begin;
   const u16* dU2 = GRP ? nullptr : reinterpret_cast<const u16*>(a.ws + L.du2);
-  // (FULL on the 256 x 256 tile only with its copying variant: register staging
+  // (FULL on the 256 x 256 tile selects its copying variant; register staging
   // without the checks measured no faster there and spilled more)
   bool full = false;
-  if constexpr (BM * BN < 256 * 256 || !GRP) {   // (256 x 256: only the copying variant)
+  {
     full = (l_end - l_begin) % BN == 0 && l_end <= a.k;
     if (GRP) {
       for (int g = 0; g < grp.count; ++g) full = full && grp.n[g] % 64 == 0;
