@@ -445,12 +445,12 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
   static_assert(WTI % 32 == 0 && WTJ % 32 == 0, "32x32 fragments");
   static_assert(BN == 128 || BN == 256, "W tile rows of 256 or 512 bytes");
   static_assert(NSLAB == 1 || NSLAB == 2, "slab stages of the unrolled tail");
-  // DMA: the 256-wide tiles with FULL (no dropout) copy their stages straight into
+  // DMA: the 256-wide tiles with FULL copy their stages straight into
   // LDS (128 x 256: three buffers, two stages ahead; 256 x 256: two buffers,
   // one stage ahead), see the k loop below.  (The 128 x 128 tile with two
   // buffers measured slower than with register staging: 13B q_proj step
   // 462 -> 467 us.)
-  constexpr bool DMA = FULL && BN == 256 && !DROP;
+  constexpr bool DMA = FULL && BN == 256;
   constexpr int NBUF = DMA && BM == 128 ? 3 : 2;
   static_assert(NBUF * STAGE <= 160 * 1024, "LDS budget");
   __shared__ __attribute__((aligned(1024))) char smem[NBUF * STAGE];
@@ -611,7 +611,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
     constexpr int WRK = 512 / BN;           // W rows per 1 KB copy
     constexpr int WRB = BN * 2;             // bytes of a W tile row
     static_assert(CYW * NW * 8 == BM && CWW * NW * 8 == BN, "copies per stage");
-    const int T = nkb + (GRP ? 0 : NSLAB);
+    const int T = nkb + ((GRP || DROP) ? 0 : NSLAB);   // (group and dropout epilogues add dU A)
     // With GRP the copies walk the projections' stages in order (dload is
     // called once per stage, in stage order): cursor = projection, its stage,
     // its dY rows.
