@@ -423,9 +423,10 @@ struct DxGroup {
 // loop, each stage loading from its own projection's dY_g and W_g; the slab
 // stages are skipped and each dU_g A_g is added after the loop from LDS.
 //
-// FULL (every n a multiple of 64 and k of BN; tiles below 256 x 256): the
-// n-stage loads carry no bound checks and the n stages run in pairs with
-// compile-time LDS buffers.
+// FULL (every n a multiple of 64 and the launch's columns a multiple of BN):
+// the n-stage loads carry no bound checks.  With BN = 256 the stages are then
+// copied straight into LDS (DMA below); on the 128 x 128 tile they keep the
+// register staging and run in pairs with compile-time LDS buffers.
 template <int BM, int BN, int WM, int WN, int RP, bool DROP, bool GRP, bool FULL>
 __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
     const u16* __restrict__ dY, const u16* __restrict__ W, const u16* __restrict__ dU2,
