@@ -406,7 +406,7 @@ def main():
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
+        print("bench.py measures one GPU only: the library has no multi-GPU path "
               "(the LoRA linear would shard over tokens with an all-reduce of dA and dB; "
               "not built here). Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
