@@ -2,16 +2,20 @@
 """LoRA-linear forward + backward throughput on one MI355X.
 
 One step = lora_linear_fwd + lora_linear_bwd (the whole path: fused forward
-GEMM, dU, dB and dA token reductions, dX GEMM, finalize) over one batch of
-synthetic bf16 inputs of a Llama-2 projection shape.  Inputs are resident in
-HBM before timing starts; successive steps rotate over several copies of the
-inputs whose total size exceeds the 256 MB Infinity Cache, so every step reads
-its operands from HBM.
+GEMM, dU, dB and dA token reductions, dX GEMM, finalize) for every projection
+of the workload -- by default the three Llama-2-7B shapes (q_proj 2048 x 4096
+x 4096 r 8, up_proj 4096 x 11008 x 4096 r 16, down_proj 8192 x 4096 x 11008
+r 64) back to back -- on synthetic bf16 inputs.  Inputs are resident in HBM
+before timing starts; when one step's operands fit the 256 MB Infinity Cache,
+successive steps rotate over several copies so every step reads from HBM.
 
 Prints one JSON line: whole-job TFLOP/s (algorithmic flops 4mnk + 6mr(n+k) per
-projection), the fraction of the bf16 dense matrix-core peak, a roofline entry
-for the dominant kernel (the forward GEMM, timed live with HIP events on its
-stream) and the fp64 CPU oracle's throughput on the host as a baseline.
+projection), the fraction of the bf16 dense matrix-core peak, per-projection
+forward and backward call times, the host's enqueue time per step, a roofline
+entry for the dominant kernel (the forward call of the projection with the
+most forward flops, timed live with HIP events on its stream; its kernels come
+from the library's own launch plan) and the fp64 CPU oracle's throughput on
+the host as a baseline.
 """
 from __future__ import annotations
 
@@ -29,70 +33,33 @@ sys.path.insert(0, ROOT)
 PEAK_BF16_TFLOPS = 2500.0    # MI355X dense bf16 matrix-core peak
 PEAK_HBM_GBS = 8000.0        # MI355X HBM3E
 MALL_BYTES = 256 << 20       # Infinity Cache
-KERNEL_SOURCES = ["paper_2403_11366_amd/csrc/lora_fwd.hip", "paper_2403_11366_amd/csrc/lora_device.hpp"]
+KERNEL_SOURCES = ["paper_2403_11366_amd/csrc/lora_fwd.hip", "paper_2403_11366_amd/csrc/lora_device.hpp",
+                  "paper_2403_11366_amd/csrc/lora_plan.hpp", "paper_2403_11366_amd/csrc/lora_launch.hpp"]
+
+
+def forward_plan(s, dropout: bool = False):
+    """The forward launches the library makes for shape s (its own plan query)."""
+    import paper_2403_11366_amd as lora
+    return lora.lora_linear_plan("fwd_dropout" if dropout else "fwd", s.m, s.n, s.k, s.r)
+
+
+def short_kernel(name: str) -> str:
+    """'lora::lora_fwd_kernel<...>' -> 'lora_fwd_kernel'."""
+    return name.split("::")[-1].split("<")[0]
+
+
+def dominant_shape(shapes):
+    """The projection whose forward GEMM has the most flops: its forward call is
+    the roofline entry of a multi-projection step."""
+    return max(shapes, key=lambda s: 2 * s.m * s.n * s.k + 2 * s.m * s.k * s.r + 2 * s.m * s.n * s.r)
+
+
 def traffic_file(workload: str) -> str:
-    """Committed HBM-traffic record of the forward kernel of `workload`."""
+    """Committed HBM-traffic record of the forward call of the dominant shape of `workload`."""
     from lora_synth import CONFIGS
-    s0 = CONFIGS[workload][0]
-    return os.path.join(ROOT, "profiles", f"{forward_kernel_name(s0.m, s0.n, s0.r, False)}_{workload}_traffic.json")
-
-
-_TILES = (("256x256", 256, 256), ("128x256", 128, 256), ("128x128", 128, 128))
-
-
-def _rounds(m: int, n: int, bm: int, bn: int) -> int:
-    return -(-(-(-m // bm) * -(-n // bn)) // 256)
-
-
-def _choose_tile(m: int, n: int) -> str:
-    """The library's single-tile choice: rounds of 256 workgroups times tile
-    area over a per-tile efficiency (1.0, 0.9, 0.75)."""
-    best, cost = None, None
-    for (name, bm, bn), eff in zip(_TILES, (1.0, 0.9, 0.75)):
-        c = _rounds(m, n, bm, bn) * bm * bn / eff
-        if cost is None or c < cost:
-            best, cost = name, c
-    return best
-
-
-def _column_split(m: int, n: int):
-    """The library's column split of an m x n GEMM output (same estimate as
-    its launcher: efficiencies 1.0, 0.95, 0.72, second part at most one
-    round, taken when more than 5% cheaper, ties to the larger n1): returns
-    [(tile, first column, end column), ...]."""
-    eff = {"256x256": 1.0, "128x256": 0.95, "128x128": 0.72}
-    dims = {name: (bm, bn) for name, bm, bn in _TILES}
-    cost = lambda t, cols: _rounds(m, cols, *dims[t]) * dims[t][0] * dims[t][1] / eff[t]
-    t0 = _choose_tile(m, n)
-    best, best_cost, found = [(t0, 0, n)], 0.95 * cost(t0, n), False
-    for t1, _, bn1 in _TILES:
-        for n1 in range(bn1, n, bn1):
-            for t2, bm2, bn2 in _TILES:
-                if -(-m // bm2) * -(-(n - n1) // bn2) > 256:
-                    continue
-                c = cost(t1, n1) + cost(t2, n - n1)
-                if c < best_cost or (found and c == best_cost and n1 > best[0][2]):
-                    best, best_cost, found = [(t1, 0, n1), (t2, n1, n)], c, True
-    return best
-
-
-def forward_launches(m: int, n: int, r: int, dropout: bool):
-    """Forward GEMM launches the library makes for this shape, as (kernel,
-    tile, first column, end column): 128 x 256 in place of 256 x 256 and no
-    column split under dropout; the 128 x 256 tile with rank <= 16 and no
-    dropout runs the k-split kernel."""
-    if dropout:
-        t = _choose_tile(m, n)
-        parts = [("128x256" if t == "256x256" else t, 0, n)]
-    else:
-        parts = _column_split(m, n)
-    return [("lora_fwd_ks_kernel" if t == "128x256" and r <= 16 and not dropout else "lora_fwd_kernel", t, a, b)
-            for t, a, b in parts]
-
-
-def forward_kernel_name(m: int, n: int, r: int, dropout: bool) -> str:
-    """Name of the (first) forward kernel the library launches for this shape."""
-    return forward_launches(m, n, r, dropout)[0][0]
+    s0 = dominant_shape(CONFIGS[workload])
+    kname = short_kernel(forward_plan(s0)[-1]["kernel"])
+    return os.path.join(ROOT, "profiles", f"{kname}_{s0.name}_traffic.json")
 
 
 def log(*a):
@@ -115,20 +82,22 @@ def kernel_source_hash() -> str:
 
 
 def measured_traffic(workload: str):
-    """HBM bytes per forward-kernel launch from the committed rocprofv3 counter
-    runs, if they were taken on the current kernel source; else None."""
+    """HBM bytes per forward call of the dominant shape from the committed
+    rocprofv3 counter runs, if they were taken on the current kernel source;
+    else None."""
     try:
         with open(traffic_file(workload)) as f:
             rec = json.load(f)
     except (OSError, ValueError):
         return None
-    if rec.get("kernel_source_sha") != kernel_source_hash() or rec.get("workload") != workload:
+    if rec.get("kernel_source_sha") != kernel_source_hash():
         return None
     return rec.get("hbm_bytes_per_launch")
 
 
 def summarize_traffic(root: str, workload: str, copy_mib: int):
-    """Turn four rocprofv3 --pmc runs into HBM bytes per forward-kernel launch.
+    """Turn four rocprofv3 --pmc runs into HBM bytes per forward call of the
+    dominant shape of `workload` (the sum over the call's kernels).
 
     root/{fwd_fetch,fwd_write,copy_fetch,copy_write}/ hold the counter CSVs of
     `--only fwd` and `--only copy` runs with FETCH_SIZE and WRITE_SIZE (KiB per
@@ -149,22 +118,27 @@ def summarize_traffic(root: str, workload: str, copy_mib: int):
         return v[len(v) // 2], len(v)
 
     from lora_synth import CONFIGS
-    s0 = CONFIGS[workload][0]
-    kname = forward_kernel_name(s0.m, s0.n, s0.r, False)
-    f_fwd, nf = per_dispatch("fwd_fetch", "FETCH_SIZE", kname + "<")
-    w_fwd, nw = per_dispatch("fwd_write", "WRITE_SIZE", kname + "<")
+    s0 = dominant_shape(CONFIGS[workload])
+    kernels = [x["kernel"] for x in forward_plan(s0)]
+    f_fwd = w_fwd = 0.0
+    counts = []
+    for kname in kernels:
+        fv, nf = per_dispatch("fwd_fetch", "FETCH_SIZE", kname)
+        wv, nw = per_dispatch("fwd_write", "WRITE_SIZE", kname)
+        f_fwd, w_fwd = f_fwd + fv, w_fwd + wv
+        counts.append([nf, nw])
     f_cpy, _ = per_dispatch("copy_fetch", "FETCH_SIZE", "")
     w_cpy, _ = per_dispatch("copy_write", "WRITE_SIZE", "")
     known_kib = copy_mib * 1024.0
     sf, sw = known_kib / f_cpy, known_kib / w_cpy
     fetch_b = f_fwd * sf * 1024.0
     write_b = w_fwd * sw * 1024.0
-    rec = {"workload": workload, "kernel": kname, "kernel_source_sha": kernel_source_hash(),
+    rec = {"workload": workload, "shape": s0.name, "kernels": kernels, "kernel_source_sha": kernel_source_hash(),
            "fetch_kib_raw": f_fwd, "write_kib_raw": w_fwd, "copy_mib": copy_mib,
            "copy_fetch_kib_raw": f_cpy, "copy_write_kib_raw": w_cpy,
            "fetch_scale": sf, "write_scale": sw,
            "hbm_fetch_bytes_per_launch": fetch_b, "hbm_write_bytes_per_launch": write_b,
-           "hbm_bytes_per_launch": fetch_b + write_b, "dispatches": [nf, nw]}
+           "hbm_bytes_per_launch": fetch_b + write_b, "dispatches": counts}
     out = traffic_file(workload)
     os.makedirs(os.path.dirname(out), exist_ok=True)
     with open(out, "w") as f:
@@ -172,47 +146,64 @@ def summarize_traffic(root: str, workload: str, copy_mib: int):
     print(json.dumps(rec))
 
 
+def host_cpu():
+    """(threads this process may use, CPU model) of the host."""
+    cores = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1)
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return cores, model
+
+
 def cpu_baseline(shape, seconds: float, drop=None):
     """Time the fp64 oracle (as it stands) on this host for `shape` (with LoRA
-    dropout at rate `drop` when given)."""
-    import numpy as np
+    dropout at rate `drop` when given), on every core of the process's
+    affinity mask."""
     import oracle
     from lora_synth import gen_inputs, gen_keep_mask
+    cores, model = host_cpu()
     try:
-        from threadpoolctl import threadpool_info
-        threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+        from threadpoolctl import threadpool_limits
+        limiter = threadpool_limits(limits=cores)
     except Exception:
-        threads = os.cpu_count() or 1
+        limiter = None
     t = gen_inputs(shape)
     keep = None if drop is None else gen_keep_mask(shape.m, shape.k, drop, shape.seed + 1)
     runs, t0 = 0, time.perf_counter()
-    while True:
-        if keep is None:
-            oracle.lora_forward(t["X"], t["W"], t["A"], t["B"], shape.alpha)
-            oracle.lora_backward(t["dY"], t["X"], t["W"], t["A"], t["B"], shape.alpha)
-        else:
-            oracle.lora_forward_dropout(t["X"], t["W"], t["A"], t["B"], keep, drop, shape.alpha)
-            oracle.lora_backward_dropout(t["dY"], t["X"], t["W"], t["A"], t["B"], keep, drop, shape.alpha)
-        runs += 1
-        el = time.perf_counter() - t0
-        if el >= seconds or runs >= 50:
-            break
+    try:
+        while True:
+            if keep is None:
+                oracle.lora_forward(t["X"], t["W"], t["A"], t["B"], shape.alpha)
+                oracle.lora_backward(t["dY"], t["X"], t["W"], t["A"], t["B"], shape.alpha)
+            else:
+                oracle.lora_forward_dropout(t["X"], t["W"], t["A"], t["B"], keep, drop, shape.alpha)
+                oracle.lora_backward_dropout(t["dY"], t["X"], t["W"], t["A"], t["B"], keep, drop, shape.alpha)
+            runs += 1
+            el = time.perf_counter() - t0
+            if el >= seconds or runs >= 50:
+                break
+    finally:
+        if limiter is not None:
+            limiter.unregister()
     per = el / runs
-    return {"value": shape.flops_fwd_bwd / per / 1e12, "unit": "TFLOP/s", "cores": int(threads),
-            "kind": "oracle",
+    return {"value": shape.flops_fwd_bwd / per / 1e12, "unit": "TFLOP/s", "cores": int(cores),
+            "kind": "oracle", "cpu_model": model,
             "sample": f"{runs} full fwd+bwd of {shape.name} (m={shape.m} n={shape.n} k={shape.k} "
-                      f"r={shape.r}) in fp64 numpy/OpenBLAS, {el:.1f} s total, {per:.3f} s each"}
+                      f"r={shape.r}) by the fp64 oracle (numpy matmul per formula line), {el:.1f} s total, "
+                      f"{per:.3f} s each"}
 
 
 def cpu_baseline_merge(shape, seconds: float):
     """Time the fp64 oracle's merge (as it stands) on this host for `shape`."""
     import oracle
     from lora_synth import gen_inputs
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
-    except Exception:
-        threads = os.cpu_count() or 1
+    threads, model = host_cpu()
     t = gen_inputs(shape)
     runs, t0 = 0, time.perf_counter()
     while True:
@@ -223,7 +214,7 @@ def cpu_baseline_merge(shape, seconds: float):
             break
     per = el / runs
     nbytes = 2 * 2 * shape.n * shape.k + 2 * shape.r * (shape.n + shape.k)
-    return {"value": nbytes / per / 1e9, "unit": "GB/s", "cores": int(threads), "kind": "oracle",
+    return {"value": nbytes / per / 1e9, "unit": "GB/s", "cores": int(threads), "kind": "oracle", "cpu_model": model,
             "sample": f"{runs} merges of {shape.name} (n={shape.n} k={shape.k} r={shape.r}) in fp64 "
                       f"numpy/OpenBLAS with exact bf16 rounding, {el:.1f} s total, {per:.3f} s each"}
 
@@ -378,7 +369,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=100)
-    ap.add_argument("--config", default="llama2_7b_q_proj")
+    ap.add_argument("--config", default="llama2_7b_shapes")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--only", choices=["fwd", "copy"], default=None,
@@ -494,12 +485,14 @@ def main():
             fwd(i, s, sets, out)
             bwd(i, s, sets, out)
 
-    if args.only == "fwd":
+    if args.only == "fwd":   # counter runs: the dominant shape's forward call only
+        s_dom = dominant_shape(shapes)
         for i in range(args.warmup + args.steps):
             for s_, sets_, out_ in proj:
-                fwd(i, s_, sets_, out_)
+                if s_ is s_dom:
+                    fwd(i, s_, sets_, out_)
         torch.cuda.synchronize()
-        log(f"[bench] {args.warmup + args.steps} forward launches done")
+        log(f"[bench] {args.warmup + args.steps} forward calls of {s_dom.name} done")
         return
 
     # ---- whole path
@@ -508,7 +501,8 @@ def main():
     torch.cuda.synchronize()
     log(f"[bench] warmup {args.warmup} steps done; timing {args.steps} steps")
     # HIP events split the timed steps into 5 repetitions (recorded on the
-    # stream, no synchronisation inside the timed region)
+    # stream, no synchronisation inside the timed region); the host clock also
+    # notes when the last step has been enqueued.
     nrep = 5 if args.steps >= 5 else 1
     marks = [round(j * args.steps / nrep) for j in range(nrep + 1)]
     evs = [torch.cuda.Event(enable_timing=True) for _ in range(nrep + 1)]
@@ -518,51 +512,60 @@ def main():
         step(i)
         if i + 1 in marks:
             evs[marks.index(i + 1)].record(stream)
+    t_enq = time.perf_counter()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     ms_per_step = elapsed / args.steps * 1e3
+    enqueue_us = (t_enq - t0) / args.steps * 1e6
     rep_ms = [evs[j].elapsed_time(evs[j + 1]) / (marks[j + 1] - marks[j]) for j in range(nrep)]
     flops = sum(s.flops_fwd_bwd for s, _, _ in proj)
     tflops = flops / (ms_per_step / 1e3) / 1e12
-    log(f"[bench] {ms_per_step * 1e3:.1f} us/step, {tflops:.1f} TFLOP/s")
+    log(f"[bench] {ms_per_step * 1e3:.1f} us/step, {tflops:.1f} TFLOP/s (host enqueue {enqueue_us:.1f} us/step)")
 
-    # ---- dominant kernel: the forward GEMM (one kernel per lora_linear_fwd call),
-    # timed with HIP events recorded on the stream it is launched on.
-    s0, sets0, out0 = proj[0]
+    # ---- per projection: the forward and the backward call, each timed with
+    # HIP events recorded on the stream they are launched on
     reps = max(20, args.steps)
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    for i in range(5):
-        fwd(i, s0, sets0, out0)
-    ev0.record(stream)
-    for i in range(reps):
-        fwd(i, s0, sets0, out0)
-    ev1.record(stream)
-    torch.cuda.synchronize()
-    fwd_us = ev0.elapsed_time(ev1) / reps * 1e3
-    # backward call (several kernels) for context
-    ev0.record(stream)
-    for i in range(reps):
-        bwd(i, s0, sets0, out0)
-    ev1.record(stream)
-    torch.cuda.synchronize()
-    bwd_us = ev0.elapsed_time(ev1) / reps * 1e3
-    m, n, k, r = s0.m, s0.n, s0.k, s0.r
-    k1_flops = 2 * m * n * k + 2 * m * k * r + 2 * m * n * r
+
+    def timed(fn, s, sets, out):
+        for i in range(3):
+            fn(i, s, sets, out)
+        ev0.record(stream)
+        for i in range(reps):
+            fn(i, s, sets, out)
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        return ev0.elapsed_time(ev1) / reps * 1e3
+
+    per_shape = []
+    for s, sets, out in proj:
+        f_us, b_us = timed(fwd, s, sets, out), timed(bwd, s, sets, out)
+        k1 = 2 * s.m * s.n * s.k + 2 * s.m * s.k * s.r + 2 * s.m * s.n * s.r
+        per_shape.append({"name": s.name, "fwd_us": round(f_us, 2), "bwd_us": round(b_us, 2),
+                          "tflops": round(s.flops_fwd_bwd / ((f_us + b_us) * 1e-6) / 1e12, 2),
+                          "fwd_frac": round(k1 / (f_us * 1e-6) / 1e12 / PEAK_BF16_TFLOPS, 4),
+                          "fwd_kernels": [x["kernel"] for x in forward_plan(s, drop is not None)],
+                          "bwd_kernels": [x["kernel"] for x in lora.lora_linear_plan(
+                              ("bwd_dropout" if drop is not None else "bwd_fused" if args.fused_bwd else "bwd"),
+                              s.m, s.n, s.k, s.r)]})
+        log(f"[bench] {s.name}: forward call {f_us:.1f} us, backward call {b_us:.1f} us")
+
+    # ---- roofline entry: the forward call of the projection with the most
+    # forward flops (one GEMM launch, or a U pass and/or two column ranges,
+    # all inside the timed call, as its plan lists)
+    s0 = dominant_shape([s for s, _, _ in proj])
+    e0 = next(e for e in per_shape if e["name"] == s0.name)
+    fwd_us = e0["fwd_us"]
+    k1_flops = 2 * s0.m * s0.n * s0.k + 2 * s0.m * s0.k * s0.r + 2 * s0.m * s0.n * s0.r
     achieved = k1_flops / (fwd_us * 1e-6) / 1e12
-    # The forward call is one launch at the 7B q_proj shape; elsewhere it may
-    # be a U pass (rank > 16, no dropout) and/or a column split in two launches,
-    # all inside the timed call.
-    launches = forward_launches(m, n, r, drop is not None)
-    kernel_label = " + ".join((["lora_u_kernel"] if r > 16 and drop is None else [])
-                              + [name if len(launches) == 1 else f"{name} {t} columns [{a}, {b})"
-                                 for name, t, a, b in launches])
+    kernel_label = " + ".join(e0["fwd_kernels"])
     traffic = measured_traffic(args.config) if drop is None else None
-    log(f"[bench] forward kernel {fwd_us:.1f} us ({achieved:.1f} TFLOP/s); backward call {bwd_us:.1f} us")
 
     cpu = None
     if not args.no_cpu_baseline:
-        log(f"[bench] timing the fp64 oracle on the host (~{args.cpu_seconds:.0f} s)")
-        cpu = cpu_baseline(s0, args.cpu_seconds, drop)
+        c0 = min((s for s, _, _ in proj), key=lambda s: s.flops_fwd_bwd)
+        log(f"[bench] timing the fp64 oracle on the host (~{args.cpu_seconds:.0f} s, {c0.name})")
+        cpu = cpu_baseline(c0, args.cpu_seconds, drop)
 
     rec = {
         "metric": "LoRA-linear fwd+bwd TFLOP/s + % bf16 MFMA peak, Llama-2-7B shapes, 1 GPU"
@@ -585,11 +588,12 @@ def main():
                    "input_sets": nsets, "flops_per_step": flops, "lora_dropout": drop,
                    "backward": "lora_linear_bwd_fused" if args.fused_bwd else "lora_linear_bwd",
                    "operands": "bf16 in, fp32 accumulate; Y, dX bf16; U, dA, dB fp32"},
-        "roofline": {"bound": "mfma", "kernel": kernel_label,
+        "roofline": {"bound": "mfma", "kernel": kernel_label, "shape": s0.name,
                      "achieved": round(achieved, 2),
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                      "traffic": traffic, "flops_per_launch": k1_flops, "avg_launch_us": round(fwd_us, 2)},
-        "bwd_call_us": round(bwd_us, 2),
+        "per_projection": per_shape,
+        "host_enqueue_us_per_step": round(enqueue_us, 2),
         "repetitions": {"count": nrep, "ms_per_step": [round(x, 4) for x in rep_ms],
                         "median": round(sorted(rep_ms)[nrep // 2], 4),
                         "std": round((sum((x - sum(rep_ms) / nrep) ** 2 for x in rep_ms) / nrep) ** 0.5, 4)},

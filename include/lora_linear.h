@@ -257,6 +257,46 @@ lora_status lora_linear_group_bwd(const lora_bf16* const* dY, const lora_bf16* X
                                   float* const* dA, float* const* dB, void* workspace, size_t workspace_bytes,
                                   int64_t m, int64_t k, int64_t r, float alpha, void* stream);
 
+/*
+ * Launch plan of a call (host only: no GPU, no HIP call, nothing enqueued).
+ * Reports, in launch order, the kernels the entry point named by `op` would
+ * launch for these shapes -- the same plan the entry point itself executes --
+ * so that tools and tests can tell which kernel variant serves a shape.
+ *
+ *   op        which entry point (lora_op below)
+ *   group, n  the output widths: for single-projection ops group = 1 and n
+ *             points to n; for the grouped ops as in lora_linear_group_fwd
+ *   m, k, r   as in the entry point (m is ignored for LORA_OP_MERGE)
+ *   out       HOST array of `capacity` entries (may be NULL when capacity is 0)
+ * Returns the number of launches (entries beyond `capacity` are not written),
+ * or minus the lora_status the entry point would return for these shapes
+ * (shape rules only: no pointer checks).
+ */
+typedef enum {
+  LORA_OP_FWD = 0,          /* lora_linear_fwd */
+  LORA_OP_FWD_DROPOUT = 1,  /* lora_linear_fwd_dropout */
+  LORA_OP_BWD = 2,          /* lora_linear_bwd */
+  LORA_OP_BWD_DROPOUT = 3,  /* lora_linear_bwd_dropout */
+  LORA_OP_BWD_FUSED = 4,    /* lora_linear_bwd_fused */
+  LORA_OP_MERGE = 5,        /* lora_linear_merge */
+  LORA_OP_GROUP_FWD = 6,    /* lora_linear_group_fwd */
+  LORA_OP_GROUP_BWD = 7     /* lora_linear_group_bwd */
+} lora_op;
+
+typedef struct {
+  char kernel[128];         /* the instantiation as profilers print it, e.g.
+                               "lora::lora_bwd_dx_kernel<128, 256, 2, 4, 16, false, false, true>" */
+  int64_t grid;             /* workgroups */
+  int32_t block;            /* threads per workgroup */
+  int32_t tile_m, tile_n;   /* GEMM output tile (tokens x features), 0 for other kernels */
+  int32_t member;           /* grouped backward: projection served by a per-projection launch */
+  int64_t col_begin;        /* GEMM output columns [col_begin, col_end) of a single projection */
+  int64_t col_end;
+} lora_launch_info;
+
+int64_t lora_linear_plan(lora_op op, int64_t group, const int64_t* n, int64_t m, int64_t k, int64_t r,
+                         lora_launch_info* out, int64_t capacity);
+
 /* Static, human-readable name of a status code. */
 const char* lora_status_string(lora_status s);
 

@@ -68,6 +68,10 @@ CONFIGS: Dict[str, List[Shape]] = {
     "llama2_13b_layer": [_cfg(4, f"llama2_13b_{p}", 4096, n, k, 8, 16, proj=i)
                          for i, (p, n, k) in enumerate(_L13)],
 }
+# The three Llama-2-7B projection shapes above as one step (q_proj, up_proj,
+# down_proj back to back), each with its own configuration's seed.
+CONFIGS["llama2_7b_shapes"] = (CONFIGS["llama2_7b_q_proj"] + CONFIGS["llama2_7b_up_proj"]
+                               + CONFIGS["llama2_7b_down_proj"])
 CONFIG_ORDER = ["tiny", "llama2_7b_q_proj", "llama2_7b_up_proj", "llama2_7b_down_proj",
                 "llama2_13b_layer"]
 

@@ -19,12 +19,15 @@ __all__ = [
     "lora_linear_bwd_workspace_size", "lora_linear_bwd_fused", "lora_linear_bwd_fused_workspace_size",
     "lora_linear_merge", "lora_linear_fwd_dropout", "lora_linear_bwd_dropout",
     "lora_linear_group_fwd", "lora_linear_group_bwd", "lora_linear_group_bwd_workspace_size",
-    "lora_status_string", "STATUS",
+    "lora_status_string", "STATUS", "lora_linear_plan", "OPS",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB_NAME = "liblora_linear.so"
 _lib = None
+
+OPS = {"fwd": 0, "fwd_dropout": 1, "bwd": 2, "bwd_dropout": 3, "bwd_fused": 4, "merge": 5,
+       "group_fwd": 6, "group_bwd": 7}
 
 STATUS = {0: "LORA_OK", 1: "LORA_ERR_NULL", 2: "LORA_ERR_SHAPE", 3: "LORA_ERR_ALIGN",
           4: "LORA_ERR_UNSUPPORTED", 5: "LORA_ERR_WORKSPACE", 6: "LORA_ERR_ALIAS", 7: "LORA_ERR_HIP"}
@@ -34,6 +37,12 @@ class LoraError(RuntimeError):
     def __init__(self, status: int, where: str):
         self.status = status
         super().__init__(f"{where}: {STATUS.get(status, status)} ({lora_status_string(status)})")
+
+
+class _LaunchInfo(ctypes.Structure):
+    _fields_ = [("kernel", ctypes.c_char * 128), ("grid", ctypes.c_int64), ("block", ctypes.c_int32),
+                ("tile_m", ctypes.c_int32), ("tile_n", ctypes.c_int32), ("member", ctypes.c_int32),
+                ("col_begin", ctypes.c_int64), ("col_end", ctypes.c_int64)]
 
 
 def lib_path() -> str:
@@ -74,6 +83,8 @@ def load_library() -> ctypes.CDLL:
     lib.lora_linear_group_bwd_workspace_size.restype = sz
     lib.lora_linear_group_bwd.argtypes = [pa, p, i64, pn, pa, pa, pa, pa, p, pa, pa, p, sz, i64, i64, i64, f32, p]
     lib.lora_linear_group_bwd.restype = ctypes.c_int
+    lib.lora_linear_plan.argtypes = [ctypes.c_int, i64, pn, i64, i64, i64, ctypes.POINTER(_LaunchInfo), i64]
+    lib.lora_linear_plan.restype = i64
     lib.lora_status_string.argtypes = [ctypes.c_int]
     lib.lora_status_string.restype = ctypes.c_char_p
     _lib = lib
@@ -296,3 +307,21 @@ def lora_linear_group_bwd(dYs, X, Ws, As, Bs, Us, dX, dAs, dBs, workspace, alpha
                                               m, k, r, float(alpha), _stream_handle(stream))
     if st != 0:
         raise LoraError(st, "lora_linear_group_bwd")
+
+
+def lora_linear_plan(op: str, m: int, n, k: int, r: int) -> list:
+    """The kernels the entry point `op` (a key of OPS) launches for these shapes,
+    in order, as dicts (kernel name as profilers print it, grid, block, GEMM
+    tile and column range, grouped member).  `n` is an int, or a list of
+    output widths for the grouped ops.  Host only; raises LoraError on shapes
+    the entry point would refuse."""
+    ns = [int(n)] if isinstance(n, int) else [int(x) for x in n]
+    lib = load_library()
+    cap = 32
+    buf = (_LaunchInfo * cap)()
+    cnt = lib.lora_linear_plan(OPS[op], len(ns), _n_array(ns), m, k, r, buf, cap)
+    if cnt < 0:
+        raise LoraError(int(-cnt), f"lora_linear_plan({op})")
+    return [{"kernel": buf[i].kernel.decode(), "grid": buf[i].grid, "block": buf[i].block,
+             "tile": (buf[i].tile_m, buf[i].tile_n), "member": buf[i].member,
+             "cols": (buf[i].col_begin, buf[i].col_end)} for i in range(min(cnt, cap))]

@@ -36,7 +36,9 @@ FLAGS = [
 
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, os.path.basename(src) + ".o")
-    lang = ["-x", "hip"] if src.endswith(".hip") else []
+    # HIP sources keep their intermediate files (-save-temps=obj): the device
+    # object is assembled from the saved gfx950 assembly, which asm_check reads.
+    lang = ["-x", "hip", "-save-temps=obj"] if src.endswith(".hip") else []
     cmd = [hipcc()] + FLAGS + ["-I", os.path.join(ROOT, "include"), "-I", CSRC] + lang + \
           ["-c", os.path.join(CSRC, src), "-o", obj]
     res = subprocess.run(cmd, capture_output=True, text=True)
@@ -49,6 +51,16 @@ def build(verbose: bool = False) -> str:
     os.makedirs(BUILD, exist_ok=True)
     with cf.ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
         objs = list(ex.map(_compile, SOURCES))
+    # kernels whose LDS reads are inline assembly: no register of a read may be
+    # touched before its wait, no scratch, no calls (asm_check)
+    from paper_2403_11366_amd import asm_check
+    device_asm = [os.path.join(BUILD, os.path.splitext(s)[0] + "-hip-amdgcn-amd-amdhsa-gfx950.s")
+                  for s in SOURCES if s.endswith(".hip")]
+    problems = asm_check.check_files(device_asm)
+    if problems:
+        raise RuntimeError("inline-assembly LDS reads unsafe in the compiled kernels:\n" + "\n".join(problems[:20]))
+    if verbose:
+        print(f"asm_check: {asm_check.count_checked(device_asm)} kernel(s) with inline-asm LDS reads verified")
     tmp = LIB + ".tmp"
     cmd = [hipcc(), "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp] + objs
     res = subprocess.run(cmd, capture_output=True, text=True)

@@ -7,6 +7,7 @@
 
 #include "lora_linear.h"
 #include "lora_launch.hpp"
+#include "lora_plan.hpp"
 
 namespace {
 
@@ -348,6 +349,58 @@ lora_status lora_linear_group_bwd(const lora_bf16* const* dY, const lora_bf16* X
   a.m = m; a.k = k; a.r = r; a.s = (float)alpha / (float)r;
   hipError_t e = lora::launch_bwd_group(a, reinterpret_cast<hipStream_t>(stream));
   return e == hipSuccess ? LORA_OK : LORA_ERR_HIP;
+}
+
+int64_t lora_linear_plan(lora_op op, int64_t group, const int64_t* n, int64_t m, int64_t k, int64_t r,
+                         lora_launch_info* out, int64_t capacity) {
+  if (!n || (capacity > 0 && !out)) return -(int64_t)LORA_ERR_NULL;
+  lora_status st = LORA_OK;
+  lora::Plan p;
+  switch (op) {
+    case LORA_OP_FWD:
+    case LORA_OP_FWD_DROPOUT:
+    case LORA_OP_BWD:
+    case LORA_OP_BWD_DROPOUT:
+    case LORA_OP_BWD_FUSED: {
+      if (group != 1) return -(int64_t)LORA_ERR_SHAPE;
+      st = check_shape(m, n[0], k, r);
+      const bool drop = op == LORA_OP_FWD_DROPOUT || op == LORA_OP_BWD_DROPOUT;
+      if (st == LORA_OK && drop && k % 64 != 0) st = LORA_ERR_SHAPE;
+      if (st == LORA_OK && op == LORA_OP_BWD_FUSED && r > 16) st = LORA_ERR_UNSUPPORTED;
+      if (st != LORA_OK) break;
+      if (op == LORA_OP_FWD || op == LORA_OP_FWD_DROPOUT) p = lora::plan_fwd(m, n[0], k, r, drop);
+      else if (op == LORA_OP_BWD_FUSED) p = lora::plan_bwd_fused(m, n[0], k, r);
+      else p = lora::plan_bwd(m, n[0], k, r, drop);
+      break;
+    }
+    case LORA_OP_MERGE:
+      if (group != 1) return -(int64_t)LORA_ERR_SHAPE;
+      st = check_shape(1, n[0], k, r);
+      if (st == LORA_OK) p = lora::plan_merge(n[0], k, r);
+      break;
+    case LORA_OP_GROUP_FWD:
+    case LORA_OP_GROUP_BWD:
+      st = check_group(group, n, m, k, r);
+      if (st != LORA_OK) break;
+      p = op == LORA_OP_GROUP_FWD ? lora::plan_group_fwd((int)group, n, m, k, r)
+                                  : lora::plan_group_bwd((int)group, n, m, k, r);
+      break;
+    default: return -(int64_t)LORA_ERR_SHAPE;
+  }
+  if (st != LORA_OK) return -(int64_t)st;
+  for (int i = 0; i < p.count && i < capacity; ++i) {
+    const lora::Launch& L = p.l[i];
+    lora_launch_info& o = out[i];
+    lora::launch_name(L, o.kernel, sizeof(o.kernel));
+    o.grid = L.grid;
+    o.block = L.block;
+    o.tile_m = L.bm;
+    o.tile_n = L.bn;
+    o.member = L.member;
+    o.col_begin = L.col_begin;
+    o.col_end = L.col_end;
+  }
+  return p.count;
 }
 
 }  // extern "C"

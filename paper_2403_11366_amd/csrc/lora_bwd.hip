@@ -26,6 +26,7 @@
 
 #include "lora_device.hpp"
 #include "lora_launch.hpp"
+#include "lora_plan.hpp"
 
 namespace lora {
 
@@ -94,7 +95,7 @@ __global__ __launch_bounds__(512) void lora_bwd_du_kernel(
   // loads of batch b+1 are in flight while batch b multiplies.
   short8 yf[2][UNR];
   int4v bq[2][UNR][BL];
-  auto load = [&](int bt, int p) {
+  auto load = [&](int bt, int p) LORA_INLINE {
 #pragma unroll
     for (int u = 0; u < UNR; ++u) {
       const int j = 32 * wave + 32 * NWV * (UNR * bt + u);
@@ -107,7 +108,7 @@ __global__ __launch_bounds__(512) void lora_bwd_du_kernel(
       }
     }
   };
-  auto process = [&](int p) {
+  auto process = [&](int p) LORA_INLINE {
 #pragma unroll
     for (int u = 0; u < UNR; ++u) {
       char* slot = slots + u * SLOT;
@@ -250,7 +251,7 @@ __global__ __launch_bounds__(256) void lora_tokred_kernel(RedProblem p0, RedProb
   short8 pv[2][FP];
   const uint8_t* keep = KEEP ? pr.keep : nullptr;
   const uint32_t kb8 = (uint32_t)ncols / 8;
-  auto load = [&](int ts, int b) {
+  auto load = [&](int ts, int b) LORA_INLINE {
     const int rows = uniform(max(0, min(32, m - ts)));   // keeps the resource in scalar registers
     const __amdgpu_buffer_rsrc_t rsQ = make_rsrc(Q + (size_t)ts * ncols, (uint64_t)rows * qrow);
 #pragma unroll
@@ -273,7 +274,7 @@ __global__ __launch_bounds__(256) void lora_tokred_kernel(RedProblem p0, RedProb
       pv[b][f] = __builtin_bit_cast(
           short8, buf_load16(rsP, ((uint32_t)(16 * f + c16) * (uint32_t)mp + (uint32_t)(ts + 8 * g)) * 2));
   };
-  auto step = [&](int b) {
+  auto step = [&](int b) LORA_INLINE {
     char* qs = wreg + b * REG;
 #pragma unroll
     for (int u = 0; u < QL; ++u) {
@@ -484,7 +485,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
   uint32_t cur_yr = GRP ? (uint32_t)grp.n[0] * 2 : yrow;
   __amdgpu_buffer_rsrc_t cur_rsY =
       GRP ? make_rsrc(grp.dY[0] + (size_t)m0 * grp.n[0], (uint64_t)min(BM, m - m0) * cur_yr) : rsY;
-  auto gload_w = [&](int st, int piece) {
+  auto gload_w = [&](int st, int piece) LORA_INLINE {
     const u16* Wp = W;
     int ns = n, sl = st;
     if (GRP) {
@@ -525,7 +526,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
       }
     }
   };
-  auto gload_s = [&](int sl, int piece) {
+  auto gload_s = [&](int sl, int piece) LORA_INLINE {
     const int kk0 = sl * 64;
     if (piece == 0) {
 #pragma unroll
@@ -548,7 +549,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
       }
     }
   };
-  auto swrite = [&](int buf, int piece) {
+  auto swrite = [&](int buf, int piece) LORA_INLINE {
     char* sb = smem + buf * STAGE;
     if (piece == 0) {
 #pragma unroll
@@ -576,7 +577,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
   // Fragments of the next 16-wide substep are read while the current one
   // multiplies (two register sets, p = substep parity).
   short8 fw[2][FJ], fy[2][FI];
-  auto read_frags = [&](const char* sb, int ks, int p) {
+  auto read_frags = [&](const char* sb, int ks, int p) LORA_INLINE {
     const char* Ys = sb;
     const char* Ws = sb + BM * 128;
 #pragma unroll
@@ -584,7 +585,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
 #pragma unroll
     for (int fi = 0; fi < FI; ++fi) fy[p][fi] = kc_read(Ys, wm * WTI + 32 * fi + c32, 2 * ks + g);
   };
-  auto multiply = [&](int p) {
+  auto multiply = [&](int p) LORA_INLINE {
 #pragma unroll
     for (int fi = 0; fi < FI; ++fi)
 #pragma unroll
@@ -622,7 +623,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
     __amdgpu_buffer_rsrc_t dc_rsY =
         GRP ? make_rsrc(grp.dY[0] + (size_t)m0 * grp.n[0], (uint64_t)min(BM, m - m0) * dc_yr) : rsY;
     const int dl_r8 = lane >> 3, dl_c8 = lane & 7, dl_rw = lane / (BN / 8), dl_cw = lane % (BN / 8);
-    auto dload = [&](int kb, int buf) {
+    auto dload = [&](int kb, int buf) LORA_INLINE {
       char* sb = smem + buf * STAGE;
       if (kb < nkb) {
         const u16* Wp = W;
@@ -692,7 +693,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
       for (int ks = 0; ks < 4; ++ks) ya[ks] = lds_addr(smem + kc_offset(wm * WTI + c32, 2 * ks + g));
     }
     short4v fwl[2][FJ], fwh[2][FJ];
-    auto reads = [&](uint32_t boff, int ks, int p) {
+    auto reads = [&](uint32_t boff, int ks, int p) LORA_INLINE {
 #pragma unroll
       for (int fj = 0; fj < FJ; ++fj) {
         const uint32_t a0 = wa[fj] + boff + (uint32_t)(16 * WRB) * ks;
@@ -708,7 +709,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
       }
     };
     static_assert(FJ == 2 && (FI == 2 || FI == 4), "reads per substep");
-    auto mult = [&](int p, bool last) {
+    auto mult = [&](int p, bool last) LORA_INLINE {
       if constexpr (FI == 2) {
         if (last)
           asm volatile("s_waitcnt lgkmcnt(0)"
@@ -736,7 +737,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
         for (int fi = 0; fi < FI; ++fi) acc[fj][fi] = mfma32x32x16(w8, fy[p][fi], acc[fj][fi]);
       }
     };
-    auto compute = [&](uint32_t boff) {
+    auto compute = [&](uint32_t boff) LORA_INLINE {
       reads(boff, 0, 0);
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) {
@@ -748,7 +749,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
     using D1 = std::integral_constant<int, 1>;
     using D2 = std::integral_constant<int, 2>;
     if constexpr (NBUF == 3) {
-      auto dstage = [&](int kb, auto bufc, bool load_next) {
+      auto dstage = [&](int kb, auto bufc, bool load_next) LORA_INLINE {
         constexpr int BUF = decltype(bufc)::value;
         if (load_next) dload(kb + 2, (BUF + 2) % 3);
         compute((uint32_t)BUF * STAGE);
@@ -772,7 +773,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
     } else {
       // two buffers: stage kb+1 is copied into the other buffer (read in
       // stage kb-1, before the last barrier) while stage kb multiplies
-      auto dstage = [&](int kb, auto bufc, bool load_next) {
+      auto dstage = [&](int kb, auto bufc, bool load_next) LORA_INLINE {
         constexpr int BUF = decltype(bufc)::value;
         if (load_next) dload(kb + 1, BUF ^ 1);
         compute((uint32_t)BUF * STAGE);
@@ -804,7 +805,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
   enum { LD_NONE, LD_W, LD_S0, LD_S1 };
   // bufc: the stage's LDS buffer as a compile-time constant, or -1 for the
   // parity of st at run time
-  auto stage = [&](int st, auto bufc, bool write_next, int load) {
+  auto stage = [&](int st, auto bufc, bool write_next, int load) LORA_INLINE {
     constexpr int BUF = decltype(bufc)::value;
     const int cur = BUF >= 0 ? BUF : (st & 1);
     const char* sb = smem + cur * STAGE;
@@ -880,9 +881,11 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
             buf_load16(rsAq, (t < r && ll < k) ? (uint32_t)t * wrow + (uint32_t)ll * 2 : kOOB);
       }
       __syncthreads();
+      // (kk unrolled by two only: fully unrolled, the fragment reads of all
+      // 2 RP / 16 steps are issued ahead and spill beside the accumulators)
 #pragma unroll
       for (int fj = 0; fj < FJ; ++fj)
-#pragma unroll
+#pragma unroll 2
         for (int kk = 0; kk < KS2 / 16; ++kk) {
           const short8 af = mc32_read_tr<BN>(As2, (16 * kk) % RP, wn * WTJ + 32 * fj, lane);
 #pragma unroll
@@ -1051,7 +1054,7 @@ __global__ __launch_bounds__(512) void lora_bwd_dxf_kernel(
   // Staging registers, stored in pieces: 0 = the dY rows and (threads below
   // 128) one 16-byte half of a B row, 1 and 2 = the two halves of the W rows.
   int4v gy[LY], gw[LW], gb = int4v{0, 0, 0, 0};
-  auto gload = [&](int st, int piece) {
+  auto gload = [&](int st, int piece) LORA_INLINE {
     const int n0 = st * 64;
     if (piece == 0) {
 #pragma unroll
@@ -1086,7 +1089,7 @@ __global__ __launch_bounds__(512) void lora_bwd_dxf_kernel(
       }
     }
   };
-  auto swrite = [&](int buf, int piece) {
+  auto swrite = [&](int buf, int piece) LORA_INLINE {
     char* sb = smem + buf * STAGE;
     if (piece == 0) {
 #pragma unroll
@@ -1117,7 +1120,7 @@ __global__ __launch_bounds__(512) void lora_bwd_dxf_kernel(
   // (zero for c32 >= 16), k = n 16 ks + 8g .. +7, read transposed from Bs
   // (rows of 32 bytes, no swizzle: a 16-lane read covers 128 contiguous bytes).
   short8 fw[2][FJ], fy[2][FI], fb = short8{};
-  auto read_frags = [&](const char* sb, int ks, int p) {
+  auto read_frags = [&](const char* sb, int ks, int p) LORA_INLINE {
     const char* Ys = sb;
     const char* Ws = sb + YB;
 #pragma unroll
@@ -1132,7 +1135,7 @@ __global__ __launch_bounds__(512) void lora_bwd_dxf_kernel(
       fb = ((lane >> 4) & 1) ? short8{} : v;
     }
   };
-  auto multiply = [&](int p, int ks) {
+  auto multiply = [&](int p, int ks) LORA_INLINE {
 #pragma unroll
     for (int fi = 0; fi < FI; ++fi)
 #pragma unroll
@@ -1144,7 +1147,7 @@ __global__ __launch_bounds__(512) void lora_bwd_dxf_kernel(
   };
   // dB^T partial of stage st (its buffer sb): wave set (st / tiles_n) % 2,
   // wave f of the set takes n columns 16 f .. 16 f + 15 of the stage.
-  auto dB_part = [&](const char* sb, int st) {
+  auto dB_part = [&](const char* sb, int st) LORA_INLINE {
     const int f = wave - 4 * ((st / tiles_n) & 1);
     if (f < 0 || f >= 4) return;
     floatx4 d = floatx4{0.f, 0.f, 0.f, 0.f};
@@ -1173,7 +1176,7 @@ __global__ __launch_bounds__(512) void lora_bwd_dxf_kernel(
   for (int j = 0; j < FJ; ++j) fw[1][j] = short8{};
 #pragma unroll
   for (int j = 0; j < FI; ++j) fy[1][j] = short8{};
-  auto stage = [&](int st, auto bufc, bool write_next, bool load_next) {
+  auto stage = [&](int st, auto bufc, bool write_next, bool load_next) LORA_INLINE {
     constexpr int BUF = decltype(bufc)::value;
     const int cur = BUF >= 0 ? BUF : (st & 1);
     const char* sb = smem + cur * STAGE;
@@ -1279,190 +1282,155 @@ __global__ __launch_bounds__(256) void lora_finalize_kernel(FinalizeArgs f) {
 }
 
 // ---------------------------------------------------------------------------
-// dX columns [l_begin, l_end) with one tile; the workgroups' tails also
-// finalize the dA and dB partials described by fin (none when fin is empty).
-template <int BM, int BN, int WM, int WN, int RP, bool DROP, bool GRP>
-static hipError_t launch_dx_cfg(const BwdArgs& a, const BwdLayout& L, const FinalizeArgs& fin, const DxGroup& grp,
-                                int64_t l_begin, int64_t l_end, hipStream_t st) {
-  const int tiles_m = (int)((a.m + BM - 1) / BM), tiles_n = (int)((l_end - l_begin + BN - 1) / BN);
-  const int nt = 64 * WM * WN;
-  const int lb = (int)l_begin;
-  const u16* dU2 = GRP ? nullptr : reinterpret_cast<const u16*>(a.ws + L.du2);
-  // (FULL on the 256 x 256 tile selects its copying variant; register staging
-  // without the checks measured no faster there and spilled more)
-  bool full = false;
-  {
-    full = (l_end - l_begin) % BN == 0 && l_end <= a.k;
-    if (GRP) {
-      for (int g = 0; g < grp.count; ++g) full = full && grp.n[g] % 64 == 0;
-    } else {
-      full = full && a.n % 64 == 0;
-    }
-    if (full)
-      hipLaunchKernelGGL((lora_bwd_dx_kernel<BM, BN, WM, WN, RP, DROP, GRP, true>), dim3(tiles_m * tiles_n),
-                         dim3(nt), 0, st, a.dY, a.W, dU2, a.A, a.keep, a.dX, (int)a.m, (int)a.n, (int)a.k, (int)a.r,
-                         (int)L.mp, a.inv_keep, tiles_m, tiles_n, lb, fin, grp);
-  }
-  if (!full)
-    hipLaunchKernelGGL((lora_bwd_dx_kernel<BM, BN, WM, WN, RP, DROP, GRP, false>), dim3(tiles_m * tiles_n),
-                       dim3(nt), 0, st, a.dY, a.W, dU2, a.A, a.keep, a.dX, (int)a.m, (int)a.n, (int)a.k, (int)a.r,
-                       (int)L.mp, a.inv_keep, tiles_m, tiles_n, lb, fin, grp);
-  return hipGetLastError();
+// Launchers: execute the plans of lora_plan.hpp.
+
+// dX instantiations a plan can name: no dropout in groups or on the 256 x 256
+// tile, and the 256 x 256 tile only with whole stages (FULL).
+template <int BM, int BN, int RP, bool DROP, bool GRP, bool FULL>
+constexpr bool dx_instantiated() {
+  return !(DROP && GRP) && !(DROP && BM == 256) && !(BM == 256 && !FULL);
 }
 
-// dU (and the U^T, dU^T splits), then the dB and dA partials of one projection.
-template <int RP>
-static hipError_t launch_du_tokred(const BwdArgs& a, const BwdLayout& L, hipStream_t st) {
-  const int m = (int)a.m, n = (int)a.n, r = (int)a.r, mp = (int)L.mp;
-  u16* Ut2 = reinterpret_cast<u16*>(a.ws + L.ut2);
-  u16* dU2 = reinterpret_cast<u16*>(a.ws + L.du2);
-  u16* dUt2 = reinterpret_cast<u16*>(a.ws + L.dut2);
-  float* pb = reinterpret_cast<float*>(a.ws + L.pb);
-  float* pa = reinterpret_cast<float*>(a.ws + L.pa);
-  hipError_t e;
-
-  if (mp / 16 < 256)   // fewer workgroups of 16 tokens than compute units: 8 tokens each
-    hipLaunchKernelGGL((lora_bwd_du_kernel<RP, 8>), dim3(mp / 8), dim3(512), 0, st, a.dY, a.B, a.U, dU2, dUt2, Ut2, m,
-                       n, r, mp, a.s);
-  else
-    hipLaunchKernelGGL((lora_bwd_du_kernel<RP, 16>), dim3(mp / 16), dim3(512), 0, st, a.dY, a.B, a.U, dU2, dUt2, Ut2, m,
-                       n, r, mp, a.s);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
-
-  const RedProblem pbp{Ut2, a.dY, pb, n, (int)L.plan_b.span, L.plan_b.col_tiles, nullptr};
-  const RedProblem pap{dUt2, a.X, pa, (int)a.k, (int)L.plan_a.span, L.plan_a.col_tiles, a.keep};
-  const int nb0 = L.plan_b.col_tiles * L.plan_b.splits;
-  const int nb1 = L.plan_a.col_tiles * L.plan_a.splits;
-  if (a.keep)
-    hipLaunchKernelGGL((lora_tokred_kernel<RP, true>), dim3(nb0 + nb1), dim3(256), 0, st, pbp, pap, nb0, m, mp);
-  else
-    hipLaunchKernelGGL((lora_tokred_kernel<RP, false>), dim3(nb0 + nb1), dim3(256), 0, st, pbp, pap, nb0, m, mp);
-  return hipGetLastError();
+static hipError_t run_dx(const Launch& L, const BwdArgs& a, const u16* dU2, int mp, const FinalizeArgs& fin,
+                         const DxGroup& grp, hipStream_t st) {
+  const dim3 grid((unsigned)L.grid), block((unsigned)L.block);
+  return with_int<0, 1, 2>(tile_code(L), [&](auto tc) {
+    constexpr int T = decltype(tc)::value;
+    constexpr int BM = T == 0 ? 256 : 128, BN = T == 2 ? 128 : 256, WN = T == 2 ? 2 : 4;
+    return with_int<16, 32, 48, 64>(L.rp, [&](auto rc) {
+      return with_bool(L.drop, [&](auto dr) {
+        return with_bool(L.grp, [&](auto gr) {
+          return with_bool(L.full, [&](auto fu) {
+            constexpr int RP = decltype(rc)::value;
+            constexpr bool DROP = decltype(dr)::value, GRP = decltype(gr)::value, FULL = decltype(fu)::value;
+            if constexpr (!dx_instantiated<BM, BN, RP, DROP, GRP, FULL>()) {
+              return hipErrorInvalidValue;
+            } else {
+              hipLaunchKernelGGL((lora_bwd_dx_kernel<BM, BN, 2, WN, RP, DROP, GRP, FULL>), grid, block, 0, st, a.dY,
+                                 a.W, dU2, a.A, a.keep, a.dX, (int)a.m, (int)a.n, (int)a.k, (int)a.r, mp, a.inv_keep,
+                                 L.tiles_m, L.tiles_n, (int)L.col_begin, L.finalize ? fin : FinalizeArgs{}, grp);
+              return hipGetLastError();
+            }
+          });
+        });
+      });
+    });
+  });
 }
 
-template <int RP>
+static hipError_t run_du(const Launch& L, const BwdArgs& a, const BwdLayout& BL, hipStream_t st) {
+  u16* Ut2 = reinterpret_cast<u16*>(a.ws + BL.ut2);
+  u16* dU2 = reinterpret_cast<u16*>(a.ws + BL.du2);
+  u16* dUt2 = reinterpret_cast<u16*>(a.ws + BL.dut2);
+  return with_int<16, 32, 48, 64>(L.rp, [&](auto rc) {
+    return with_int<8, 16>(L.tpw, [&](auto tc) {
+      hipLaunchKernelGGL((lora_bwd_du_kernel<decltype(rc)::value, decltype(tc)::value>), dim3((unsigned)L.grid),
+                         dim3((unsigned)L.block), 0, st, a.dY, a.B, a.U, dU2, dUt2, Ut2, (int)a.m, (int)a.n, (int)a.r,
+                         (int)BL.mp, a.s);
+      return hipGetLastError();
+    });
+  });
+}
+
+// The two token reductions of one projection in one launch: dB^T partials =
+// Ut2 . dY, then dA partials = dUt2 . X (masked X under dropout).
+static hipError_t run_tokred(const Launch& L, const BwdArgs& a, const BwdLayout& BL, hipStream_t st) {
+  const u16* Ut2 = reinterpret_cast<const u16*>(a.ws + BL.ut2);
+  const u16* dUt2 = reinterpret_cast<const u16*>(a.ws + BL.dut2);
+  float* pb = reinterpret_cast<float*>(a.ws + BL.pb);
+  float* pa = reinterpret_cast<float*>(a.ws + BL.pa);
+  const RedProblem pbp{Ut2, a.dY, pb, (int)a.n, (int)BL.plan_b.span, BL.plan_b.col_tiles, nullptr};
+  const RedProblem pap{dUt2, a.X, pa, (int)a.k, (int)BL.plan_a.span, BL.plan_a.col_tiles, a.keep};
+  const int nb0 = BL.plan_b.col_tiles * BL.plan_b.splits;
+  return with_int<16, 32, 48, 64>(L.rp, [&](auto rc) {
+    return with_bool(L.drop, [&](auto kc) {
+      hipLaunchKernelGGL((lora_tokred_kernel<decltype(rc)::value, decltype(kc)::value>), dim3((unsigned)L.grid),
+                         dim3((unsigned)L.block), 0, st, pbp, pap, nb0, (int)a.m, (int)BL.mp);
+      return hipGetLastError();
+    });
+  });
+}
+
 static FinalizeArgs finalize_args(const BwdArgs& a, const BwdLayout& L) {
   return FinalizeArgs{reinterpret_cast<const float*>(a.ws + L.pb), reinterpret_cast<const float*>(a.ws + L.pa),
-                      a.dB, a.dA, (int)a.n, (int)a.k, (int)a.r, RP, L.plan_b.splits, L.plan_a.splits, a.s,
+                      a.dB, a.dA, (int)a.n, (int)a.k, (int)a.r, L.rp, L.plan_b.splits, L.plan_a.splits, a.s,
                       a.keep ? a.inv_keep : 1.0f};
 }
 
-template <int RP>
-static hipError_t launch_bwd_rp(const BwdArgs& a, const BwdLayout& L, hipStream_t st) {
-  hipError_t e = launch_du_tokred<RP>(a, L, st);
-  if (e != hipSuccess) return e;
-  const FinalizeArgs fin = finalize_args<RP>(a, L);
+hipError_t launch_bwd(const BwdArgs& a, hipStream_t st) {
+  const BwdLayout BL = bwd_layout(a.m, a.n, a.k, a.r);
+  const Plan p = plan_bwd(a.m, a.n, a.k, a.r, a.keep != nullptr);
+  const FinalizeArgs fin = finalize_args(a, BL);
   const DxGroup none{};
-  if (a.keep) {   // the 256 x 256 tile has no registers left for the dropout epilogue
-    if (choose_gemm_tile(a.m, a.k) == TILE_128x128)
-      return launch_dx_cfg<128, 128, 2, 2, RP, true, false>(a, L, fin, none, 0, a.k, st);
-    return launch_dx_cfg<128, 256, 2, 4, RP, true, false>(a, L, fin, none, 0, a.k, st);
-  }
-  // Columns of dX split between two launches as for the forward; the first
-  // launch's tails finalize dA and dB.
-  auto tile = [&](GemmTile t, const FinalizeArgs& f, int64_t lb, int64_t le) {
-    switch (t) {
-      case TILE_256x256: return launch_dx_cfg<256, 256, 2, 4, RP, false, false>(a, L, f, none, lb, le, st);
-      case TILE_128x256: return launch_dx_cfg<128, 256, 2, 4, RP, false, false>(a, L, f, none, lb, le, st);
-      default: return launch_dx_cfg<128, 128, 2, 2, RP, false, false>(a, L, f, none, lb, le, st);
+  const u16* dU2 = reinterpret_cast<const u16*>(a.ws + BL.du2);
+  for (int i = 0; i < p.count; ++i) {
+    const Launch& L = p.l[i];
+    hipError_t e = hipErrorInvalidValue;
+    switch (L.id) {
+      case K_DU: e = run_du(L, a, BL, st); break;
+      case K_TOKRED: e = run_tokred(L, a, BL, st); break;
+      case K_DX: e = run_dx(L, a, dU2, (int)BL.mp, fin, none, st); break;
+      default: break;
     }
-  };
-  const GemmSplit p = plan_gemm_split(a.m, a.k);
-  e = tile(p.t1, fin, 0, p.n1);
-  if (e != hipSuccess || p.n1 >= a.k) return e;
-  return tile(p.t2, FinalizeArgs{}, p.n1, a.k);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 // Fused backward: the dX launch (dU, the dB partials, dX), the dA token
 // reduction, then the finalize of dA and dB.
 hipError_t launch_bwd_fused(const BwdArgs& a, hipStream_t st) {
-  const BwdFusedLayout L = bwd_fused_layout(a.m, a.n, a.k, a.r);
-  u16* dUt2 = reinterpret_cast<u16*>(a.ws + L.dut2);
-  float* pb = reinterpret_cast<float*>(a.ws + L.pb);
-  float* pa = reinterpret_cast<float*>(a.ws + L.pa);
-  const int m = (int)a.m, n = (int)a.n, k = (int)a.k, r = (int)a.r, mp = (int)L.mp;
-  const int tiles_m = L.tiles_m, tiles_n = (k + 255) / 256;
-  const dim3 grid(tiles_m * tiles_n), block(512);
-  if (r % 8 != 0)
-    hipLaunchKernelGGL((lora_bwd_dxf_kernel<false, false>), grid, block, 0, st, a.dY, a.W, a.A, a.B, a.U, a.dX, dUt2,
-                       pb, m, n, k, r, mp, a.s, tiles_m, tiles_n);
-  else if (n % 64 == 0 && k % 256 == 0)
-    hipLaunchKernelGGL((lora_bwd_dxf_kernel<true, true>), grid, block, 0, st, a.dY, a.W, a.A, a.B, a.U, a.dX, dUt2,
-                       pb, m, n, k, r, mp, a.s, tiles_m, tiles_n);
-  else
-    hipLaunchKernelGGL((lora_bwd_dxf_kernel<false, true>), grid, block, 0, st, a.dY, a.W, a.A, a.B, a.U, a.dX, dUt2,
-                       pb, m, n, k, r, mp, a.s, tiles_m, tiles_n);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  const RedProblem pap{dUt2, a.X, pa, k, (int)L.plan_a.span, L.plan_a.col_tiles, nullptr};
-  const int nb = L.plan_a.col_tiles * L.plan_a.splits;
-  hipLaunchKernelGGL((lora_tokred_kernel<16, false>), dim3(nb), dim3(256), 0, st, pap, pap, nb, m, mp);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
-  const FinalizeArgs fin{pb, pa, a.dB, a.dA, n, k, r, 16, tiles_m, L.plan_a.splits, a.s, 1.0f};
-  const int total = n * r + r * k;
-  const int blocks = min((total + 255) / 256, 2048);
-  hipLaunchKernelGGL(lora_finalize_kernel, dim3(blocks), dim3(256), 0, st, fin);
-  return hipGetLastError();
-}
-
-hipError_t launch_bwd(const BwdArgs& a, hipStream_t st) {
-  const BwdLayout L = bwd_layout(a.m, a.n, a.k, a.r);
-  switch (L.rp) {
-    case 16: return launch_bwd_rp<16>(a, L, st);
-    case 32: return launch_bwd_rp<32>(a, L, st);
-    case 48: return launch_bwd_rp<48>(a, L, st);
-    default: return launch_bwd_rp<64>(a, L, st);
+  const BwdFusedLayout BL = bwd_fused_layout(a.m, a.n, a.k, a.r);
+  const Plan p = plan_bwd_fused(a.m, a.n, a.k, a.r);
+  u16* dUt2 = reinterpret_cast<u16*>(a.ws + BL.dut2);
+  float* pb = reinterpret_cast<float*>(a.ws + BL.pb);
+  float* pa = reinterpret_cast<float*>(a.ws + BL.pa);
+  const int m = (int)a.m, n = (int)a.n, k = (int)a.k, r = (int)a.r, mp = (int)BL.mp;
+  for (int i = 0; i < p.count; ++i) {
+    const Launch& L = p.l[i];
+    const dim3 grid((unsigned)L.grid), block((unsigned)L.block);
+    if (L.id == K_DXF) {
+      const hipError_t e = with_bool(L.full, [&](auto fc) {
+        return with_bool(L.fastb, [&](auto bc) {
+          constexpr bool F = decltype(fc)::value, FB = decltype(bc)::value;
+          if constexpr (F && !FB) {
+            return hipErrorInvalidValue;
+          } else {
+            hipLaunchKernelGGL((lora_bwd_dxf_kernel<F, FB>), grid, block, 0, st, a.dY, a.W, a.A, a.B, a.U, a.dX, dUt2,
+                               pb, m, n, k, r, mp, a.s, L.tiles_m, L.tiles_n);
+            return hipGetLastError();
+          }
+        });
+      });
+      if (e != hipSuccess) return e;
+    } else if (L.id == K_TOKRED) {
+      const RedProblem pap{dUt2, a.X, pa, k, (int)BL.plan_a.span, BL.plan_a.col_tiles, nullptr};
+      hipLaunchKernelGGL((lora_tokred_kernel<16, false>), grid, block, 0, st, pap, pap, (int)L.grid, m, mp);
+      const hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
+    } else if (L.id == K_FINALIZE) {
+      const FinalizeArgs fin{pb, pa, a.dB, a.dA, n, k, r, 16, BL.tiles_m, BL.plan_a.splits, a.s, 1.0f};
+      hipLaunchKernelGGL(lora_finalize_kernel, grid, block, 0, st, fin);
+      const hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
+    } else {
+      return hipErrorInvalidValue;
+    }
   }
+  return hipSuccess;
 }
 
 // Grouped backward: per projection the dU and token-reduction launches (each
 // in its own workspace region), then one dX launch over the whole group whose
-// tails finalize every projection's dA and dB.
-template <int RP>
-static hipError_t launch_bwd_group_rp(const GroupBwdArgs& a, const GroupBwdLayout& GL, hipStream_t st) {
-  DxGroup grp{};
-  int nkb = 0;
-  for (int g = 0; g < a.count; ++g) {
+// tails (of the first column range) finalize every projection's dA and dB.
+hipError_t launch_bwd_group(const GroupBwdArgs& a, hipStream_t st) {
+  auto member_args = [&](int g, const GroupBwdLayout& GL) {
     BwdArgs b{};
     b.dY = a.dY[g]; b.X = a.X; b.W = a.W[g]; b.A = a.A[g]; b.B = a.B[g]; b.U = a.U[g];
     b.dX = a.dX; b.dA = a.dA[g]; b.dB = a.dB[g]; b.ws = a.ws + GL.off[g];
     b.m = a.m; b.n = a.n[g]; b.k = a.k; b.r = a.r; b.s = a.s;
-    const hipError_t e = launch_du_tokred<RP>(b, GL.L[g], st);
-    if (e != hipSuccess) return e;
-    grp.dY[g] = a.dY[g];
-    grp.W[g] = a.W[g];
-    grp.dU2[g] = reinterpret_cast<const u16*>(b.ws + GL.L[g].du2);
-    grp.A[g] = a.A[g];
-    grp.n[g] = (int)a.n[g];
-    nkb += (int)((a.n[g] + 63) / 64);
-    grp.fin[g] = finalize_args<RP>(b, GL.L[g]);
-  }
-  grp.count = a.count;
-  grp.nkb = nkb;
-  BwdArgs d{};
-  d.X = a.X; d.dX = a.dX; d.ws = a.ws;
-  d.m = a.m; d.n = 0; d.k = a.k; d.r = a.r; d.s = a.s;
-  // Columns of dX may be split between two launches as for one projection;
-  // the first one's tails finalize every projection's dA and dB.  (The
-  // 256 x 256 tile keeps a few values it needs only after the k loop in
-  // scratch across the loop.)
-  const FinalizeArgs none{};
-  auto tile = [&](GemmTile t, const DxGroup& gg, int64_t lb, int64_t le) {
-    switch (t) {
-      case TILE_256x256: return launch_dx_cfg<256, 256, 2, 4, RP, false, true>(d, GL.L[0], none, gg, lb, le, st);
-      case TILE_128x256: return launch_dx_cfg<128, 256, 2, 4, RP, false, true>(d, GL.L[0], none, gg, lb, le, st);
-      default: return launch_dx_cfg<128, 128, 2, 2, RP, false, true>(d, GL.L[0], none, gg, lb, le, st);
-    }
+    return b;
   };
-  const GemmSplit p = plan_gemm_split(a.m, a.k);
-  const hipError_t e = tile(p.t1, grp, 0, p.n1);
-  if (e != hipSuccess || p.n1 >= a.k) return e;
-  DxGroup rest = grp;
-  for (int g = 0; g < kMaxGroup; ++g) rest.fin[g] = FinalizeArgs{};
-  return tile(p.t2, rest, p.n1, a.k);
-}
-
-hipError_t launch_bwd_group(const GroupBwdArgs& a, hipStream_t st) {
   if (a.count == 1) {   // a group of one is the single projection (workspace sizes agree)
     BwdArgs b{};
     b.dY = a.dY[0]; b.X = a.X; b.W = a.W[0]; b.A = a.A[0]; b.B = a.B[0]; b.U = a.U[0];
@@ -1471,12 +1439,38 @@ hipError_t launch_bwd_group(const GroupBwdArgs& a, hipStream_t st) {
     return launch_bwd(b, st);
   }
   const GroupBwdLayout GL = group_bwd_layout(a.count, a.n, a.m, a.k, a.r);
-  switch (GL.L[0].rp) {
-    case 16: return launch_bwd_group_rp<16>(a, GL, st);
-    case 32: return launch_bwd_group_rp<32>(a, GL, st);
-    case 48: return launch_bwd_group_rp<48>(a, GL, st);
-    default: return launch_bwd_group_rp<64>(a, GL, st);
+  const Plan p = plan_group_bwd(a.count, a.n, a.m, a.k, a.r);
+  DxGroup grp{};
+  int nkb = 0;
+  for (int g = 0; g < a.count; ++g) {
+    const BwdArgs b = member_args(g, GL);
+    grp.dY[g] = a.dY[g];
+    grp.W[g] = a.W[g];
+    grp.dU2[g] = reinterpret_cast<const u16*>(b.ws + GL.L[g].du2);
+    grp.A[g] = a.A[g];
+    grp.n[g] = (int)a.n[g];
+    nkb += (int)((a.n[g] + 63) / 64);
+    grp.fin[g] = finalize_args(b, GL.L[g]);
   }
+  grp.count = a.count;
+  grp.nkb = nkb;
+  DxGroup rest = grp;   // later column ranges finalize nothing
+  for (int g = 0; g < kMaxGroup; ++g) rest.fin[g] = FinalizeArgs{};
+  BwdArgs d{};
+  d.X = a.X; d.dX = a.dX; d.ws = a.ws;
+  d.m = a.m; d.n = 0; d.k = a.k; d.r = a.r; d.s = a.s;
+  for (int i = 0; i < p.count; ++i) {
+    const Launch& L = p.l[i];
+    hipError_t e = hipErrorInvalidValue;
+    if (L.id == K_DU || L.id == K_TOKRED) {
+      const BwdArgs b = member_args(L.member, GL);
+      e = L.id == K_DU ? run_du(L, b, GL.L[L.member], st) : run_tokred(L, b, GL.L[L.member], st);
+    } else if (L.id == K_DX) {
+      e = run_dx(L, d, nullptr, (int)GL.L[0].mp, FinalizeArgs{}, L.finalize ? grp : rest, st);
+    }
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 }  // namespace lora

@@ -29,6 +29,12 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+// Lambdas inside kernels are forced inline: the fragment registers written
+// by the inline-assembly LDS reads below must stay in registers between the
+// read and its wait, which an outlined call (its operands passed through
+// scratch) would break.
+#define LORA_INLINE __attribute__((always_inline))
+
 namespace lora {
 
 typedef uint16_t u16;

@@ -36,6 +36,7 @@
 
 #include "lora_device.hpp"
 #include "lora_launch.hpp"
+#include "lora_plan.hpp"
 
 namespace lora {
 
@@ -134,7 +135,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
   constexpr int LW1 = (LW + 1) / 2;
   int4v gx[LX], gw[LW], ga[LA];
   uint2 gk = uint2{0u, 0u};   // keep bits of row tid for this k-block (dropout; tid < BM)
-  auto gload = [&](int kb, int piece) {
+  auto gload = [&](int kb, int piece) LORA_INLINE {
     const int k0 = kb * 64;
     if (DROP && piece == 0 && wave * 64 < BM) gk = buf_load8(rsK, (uint32_t)tid * kb8 + (uint32_t)kb * 8);
     if (piece == 0) {
@@ -163,7 +164,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
       }
     }
   };
-  auto swrite = [&](int buf, int piece) {
+  auto swrite = [&](int buf, int piece) LORA_INLINE {
     char* sb = smem + buf * STAGE;
     if (DROP && piece == 0 && wave * 64 < BM) *reinterpret_cast<uint2*>(sb + KS_OFF + tid * 8) = gk;
     if (piece == 0) {
@@ -217,7 +218,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
   // the same instruction stream.
   short8 fw[2][FJ], fx[2][FI], fa[2][FT], fxu[2][FUW];
   short8 fa16[2], fxu16[2][GPW];
-  auto read_frags = [&](const char* sb, int ks, int p) {
+  auto read_frags = [&](const char* sb, int ks, int p) LORA_INLINE {
     const char* Xs = sb;
     const char* Ws = sb + BM * 128;
     const char* As = sb + (BM + BN) * 128;
@@ -250,7 +251,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
       }
     }
   };
-  auto multiply = [&](int p, int ks) {
+  auto multiply = [&](int p, int ks) LORA_INLINE {
 #pragma unroll
     for (int fi = 0; fi < FI; ++fi)
 #pragma unroll
@@ -293,7 +294,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
   }
   // bufc: the stage's LDS buffer as a compile-time constant, or -1 for the
   // parity of kb at run time
-  auto stage = [&](int kb, auto bufc, bool write_next, bool load_next) {
+  auto stage = [&](int kb, auto bufc, bool write_next, bool load_next) LORA_INLINE {
     constexpr int BUF = decltype(bufc)::value;
     const int cur = BUF >= 0 ? BUF : (kb & 1);
     const char* sb = smem + cur * STAGE;
@@ -319,11 +320,11 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
     constexpr int JX = BM / 8, JW = BN / 8, JA = RPS / 8;
     static_assert(JX % NW == 0 && JW % NW == 0, "copies split evenly");
     const int dl_row = lane >> 3, dl_cp = lane & 7;
-    auto voff = [&](int j) {
+    auto voff = [&](int j) LORA_INLINE {
       const int row = 8 * j + dl_row;
       return (uint32_t)row * rowbytes + (uint32_t)((dl_cp ^ kc_swz(row)) << 4);
     };
-    auto dload = [&](int kb, int buf) {
+    auto dload = [&](int kb, int buf) LORA_INLINE {
       const uint32_t k0b = (uint32_t)kb * 128;
       char* sb = smem + buf * STAGE;
 #pragma unroll
@@ -337,7 +338,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
     };
     dload(0, 0);
     copy_barrier<0>();
-    auto dstage = [&](int kb, auto bufc, bool load_next) {
+    auto dstage = [&](int kb, auto bufc, bool load_next) LORA_INLINE {
       constexpr int BUF = decltype(bufc)::value;
       if (load_next) dload(kb + 1, BUF ^ 1);   // read in stage kb-1, free since its barrier
       const char* sb = smem + BUF * STAGE;
@@ -533,7 +534,7 @@ __global__ __launch_bounds__(512) void lora_u_kernel(const u16* __restrict__ X, 
   // A ring of NB register slots holds one chunk each, NB - 1 chunks ahead
   // (7B down_proj: 78 -> 74 us against two-chunk batches one batch ahead).
   short8 xf[NB][TG], af[NB][FT];
-  auto load = [&](int j, int p) {
+  auto load = [&](int j, int p) LORA_INLINE {
     const int kk = 32 * (wave + NWV * j) + 8 * g;
 #pragma unroll
     for (int tg = 0; tg < TG; ++tg)
@@ -544,7 +545,7 @@ __global__ __launch_bounds__(512) void lora_u_kernel(const u16* __restrict__ X, 
       af[p][ft] = __builtin_bit_cast(
           short8, buf_load16(rsA, kk < k ? (uint32_t)(16 * ft + c16) * rowbytes + (uint32_t)kk * 2 : kOOB));
   };
-  auto process = [&](int p) {
+  auto process = [&](int p) LORA_INLINE {
 #pragma unroll
     for (int ft = 0; ft < FT; ++ft)
 #pragma unroll
@@ -657,7 +658,7 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
   // Register staging of one k-block as in lora_fwd_kernel, stored in two
   // pieces (0 = X and A rows, 1 = W rows), one per substep of the stage.
   int4v gx[LX], gw[LW], ga[LA];
-  auto gload = [&](int kb, int piece) {
+  auto gload = [&](int kb, int piece) LORA_INLINE {
     const int k0 = kb * 64;
     if (piece == 0) {
 #pragma unroll
@@ -682,7 +683,7 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
       }
     }
   };
-  auto swrite = [&](int buf, int piece) {
+  auto swrite = [&](int buf, int piece) LORA_INLINE {
     char* sb = smem + buf * STAGE;
     if (piece == 0) {
 #pragma unroll
@@ -720,7 +721,7 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
   short8 fw[2][FJ], fx[2][FI], fa16, fxu16[GPW];
   // Fragments of the wave's substep j (0, 1), global substep 2 wk + j; the
   // U operands of the wave's 32-wide k half are read with substep 0.
-  auto read_frags = [&](const char* sb, int j, int p) {
+  auto read_frags = [&](const char* sb, int j, int p) LORA_INLINE {
     const char* Xs = sb;
     const char* Ws = sb + BM * 128;
     const char* As = sb + (BM + BN) * 128;
@@ -735,7 +736,7 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
       for (int gg = 0; gg < GPW; ++gg) fxu16[gg] = kc_read(Xs, urow16[gg], 4 * wk + g16);
     }
   };
-  auto multiply = [&](int p, int j) {
+  auto multiply = [&](int p, int j) LORA_INLINE {
 #pragma unroll
     for (int fi = 0; fi < FI; ++fi)
 #pragma unroll
@@ -749,7 +750,7 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
   // top of stage kb the registers hold block kb+1; each piece is stored to the
   // free buffer and reloaded with block kb+2; fragments of substep 1 are read
   // while substep 0 multiplies.
-  auto stage = [&](int kb, auto bufc, bool write_next, bool load_next) {
+  auto stage = [&](int kb, auto bufc, bool write_next, bool load_next) LORA_INLINE {
     constexpr int BUF = decltype(bufc)::value;    // -1: the buffer of kb's parity at run time
     const int cur = BUF >= 0 ? BUF : (kb & 1);
     const char* sb = smem + cur * STAGE;
@@ -774,11 +775,11 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
   // logical chunk (l % 8) ^ kc_swz(row) (the swizzle is applied on the global
   // side).  Per stage a wave issues 2 X, 4 W and (waves 0, 1) 1 A copies.
   const int dl_row = lane >> 3, dl_cp = lane & 7;
-  auto voff = [&](int j) {
+  auto voff = [&](int j) LORA_INLINE {
     const int row = 8 * j + dl_row;
     return (uint32_t)row * rowbytes + (uint32_t)((dl_cp ^ kc_swz(row)) << 4);
   };
-  auto dload = [&](int kb, int buf) {
+  auto dload = [&](int kb, int buf) LORA_INLINE {
     const uint32_t k0b = (uint32_t)kb * 128;
     char* sb = smem + buf * STAGE;
 #pragma unroll
@@ -818,7 +819,7 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
   // Stage kb reads buffer kb % 3; at its top the copies of stage kb+2 go to
   // buffer (kb+2) % 3, which every wave finished reading in stage kb-1; at
   // its end each wave waits for its copies of stage kb+1 before the barrier.
-  auto dstage = [&](int kb, auto bufc, bool load_next) {
+  auto dstage = [&](int kb, auto bufc, bool load_next) LORA_INLINE {
     constexpr int BUF = decltype(bufc)::value;
     if (load_next) dload(kb + 2, (BUF + 2) % 3);
     const char* sb = smem + BUF * STAGE;
@@ -910,7 +911,7 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
   // 2 wk, 2 wk + 1 and sends the other two.
   float4* xb = reinterpret_cast<float4*>(smem);
   const int pair = wm * 2 + wn;
-  auto region = [&](int h) { return xb + (size_t)((pair * 2 + h) * 16) * 64; };
+  auto region = [&](int h) LORA_INLINE { return xb + (size_t)((pair * 2 + h) * 16) * 64; };
   {
     float4* dst = region(1 - wk);
 #pragma unroll
@@ -999,109 +1000,87 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
   else finish(acc[2], acc[3]);
 }
 
-template <int BM, int BN, int WM, int WN, int RP, bool DROP, bool GRP>
-static hipError_t launch_fwd_cfg(const FwdArgs& a, const FwdGroup& grp, int tiles_n, int n_begin, hipStream_t st) {
-  const int tiles_m = (int)((a.m + BM - 1) / BM);
-  if constexpr (RP >= 32 && !DROP && !GRP) {   // U in a pass of its own, then the tile without U columns
-    if (!a.u_ready) {
-      hipLaunchKernelGGL((lora_u_kernel<RP, 32>), dim3((a.m + 31) / 32), dim3(512), 0, st, a.X, a.A, a.U,
-                         (int)a.m, (int)a.k, (int)a.r);
-      const hipError_t e = hipGetLastError();
-      if (e != hipSuccess) return e;
-    }
-    if (a.k % 64 == 0)
-      hipLaunchKernelGGL((lora_fwd_kernel<BM, BN, WM, WN, RP, false, false, true, true, BM == 256 && BN == 256>),
-                         dim3(tiles_m * tiles_n), dim3(64 * WM * WN), 0, st, a.X, a.W, a.A, a.B, a.keep, a.Y, a.U, (int)a.m, (int)a.n, (int)a.k,
-                         (int)a.r, a.s, a.inv_keep, tiles_m, tiles_n, n_begin, grp);
-    else
-      hipLaunchKernelGGL((lora_fwd_kernel<BM, BN, WM, WN, RP, false, false, true, false, false>),
-                         dim3(tiles_m * tiles_n), dim3(64 * WM * WN), 0, st, a.X, a.W, a.A, a.B, a.keep, a.Y, a.U, (int)a.m, (int)a.n, (int)a.k,
-                         (int)a.r, a.s, a.inv_keep, tiles_m, tiles_n, n_begin, grp);
-    return hipGetLastError();
-  } else {
-    if (a.k % 64 == 0)
-      hipLaunchKernelGGL((lora_fwd_kernel<BM, BN, WM, WN, RP, DROP, GRP, false, true, BM == 256 && BN == 256 && !DROP>),
-                         dim3(tiles_m * tiles_n), dim3(64 * WM * WN), 0, st, a.X, a.W, a.A, a.B, a.keep, a.Y, a.U, (int)a.m, (int)a.n, (int)a.k,
-                         (int)a.r, a.s, a.inv_keep, tiles_m, tiles_n, n_begin, grp);
-    else
-      hipLaunchKernelGGL((lora_fwd_kernel<BM, BN, WM, WN, RP, DROP, GRP, false, false, false>),
-                         dim3(tiles_m * tiles_n), dim3(64 * WM * WN), 0, st, a.X, a.W, a.A, a.B, a.keep, a.Y, a.U, (int)a.m, (int)a.n, (int)a.k,
-                         (int)a.r, a.s, a.inv_keep, tiles_m, tiles_n, n_begin, grp);
-    return hipGetLastError();
-  }
+// ---------------------------------------------------------------------------
+// Launchers: execute the plans of lora_plan.hpp.
+
+// Instantiations a plan can name (any other combination is refused).
+// (the 128 x 256 tile at rank 16 without dropout is the k-split kernel's)
+template <int BM, int BN, int RP, bool DROP, bool GRP, bool UPRE, bool KFULL, bool DMA>
+constexpr bool fwd_instantiated() {
+  return !(DROP && GRP) && !(DROP && BM == 256) && !(BM == 128 && BN == 256 && RP == 16 && !DROP) &&
+         UPRE == (RP >= 32 && !DROP && !GRP) && DMA == (KFULL && BM == 256 && BN == 256 && !DROP);
 }
 
-// Single projection: the column tiles of output columns [n_begin, n_end).
-// Group: the column tiles of each projection, back to back (tile0 filled
-// here).  The 128 x 256 tile with rank <= 16 and no dropout runs the k-split
-// kernel.
-template <int BM, int BN, int WM, int WN, bool DROP, bool GRP>
-static hipError_t launch_fwd_rp(const FwdArgs& a, FwdGroup grp, int64_t n_begin, int64_t n_end, hipStream_t st) {
-  int tiles_n = (int)((n_end - n_begin + BN - 1) / BN);
-  if (GRP) {
-    tiles_n = 0;
-    for (int g = 0; g < grp.count; ++g) {
-      grp.tile0[g] = tiles_n;
-      tiles_n += (grp.n[g] + BN - 1) / BN;
-    }
+static hipError_t run_fwd_launch(const Launch& L, const FwdArgs& a, const FwdGroup& grp, hipStream_t st) {
+  const dim3 grid((unsigned)L.grid), block((unsigned)L.block);
+  if (L.id == K_UPASS) {
+    return with_int<32, 64>(L.rp, [&](auto rc) {
+      hipLaunchKernelGGL((lora_u_kernel<decltype(rc)::value, 32>), grid, block, 0, st, a.X, a.A, a.U, (int)a.m,
+                         (int)a.k, (int)a.r);
+      return hipGetLastError();
+    });
   }
-  if (BM == 128 && BN == 256 && !DROP && a.r <= 16) {
-    const int tiles_m = (int)((a.m + BM - 1) / BM);
-    // Single-round launches (at most one tile per compute unit) copy straight
-    // into LDS: measured faster there (7B q_proj forward 83-86 -> 77-79 us),
-    // slightly slower over many rounds (13B gate_proj 630-633 -> 636-639 us).
-    if (a.k % 64 == 0 && !GRP && tiles_m * tiles_n <= 256)
-      hipLaunchKernelGGL((lora_fwd_ks_kernel<false, true, true>), dim3(tiles_m * tiles_n), dim3(512), 0, st, a.X, a.W,
-                         a.A, a.B, a.Y, a.U, (int)a.m, (int)a.n, (int)a.k, (int)a.r, a.s, tiles_m, tiles_n,
-                         (int)n_begin, grp);
-    else if (a.k % 64 == 0)
-      hipLaunchKernelGGL((lora_fwd_ks_kernel<GRP, true, false>), dim3(tiles_m * tiles_n), dim3(512), 0, st, a.X, a.W,
-                         a.A, a.B, a.Y, a.U, (int)a.m, (int)a.n, (int)a.k, (int)a.r, a.s, tiles_m, tiles_n,
-                         (int)n_begin, grp);
-    else
-      hipLaunchKernelGGL((lora_fwd_ks_kernel<GRP, false, false>), dim3(tiles_m * tiles_n), dim3(512), 0, st, a.X, a.W, a.A,
-                         a.B, a.Y, a.U, (int)a.m, (int)a.n, (int)a.k, (int)a.r, a.s, tiles_m, tiles_n, (int)n_begin,
-                         grp);
-    return hipGetLastError();
+  if (L.id == K_FWD_KS) {
+    return with_bool(L.grp, [&](auto gc) {
+      return with_bool(L.full, [&](auto fc) {
+        return with_bool(L.dma, [&](auto dc) {
+          constexpr bool G = decltype(gc)::value, F = decltype(fc)::value, D = decltype(dc)::value;
+          if constexpr (D && (G || !F)) {
+            return hipErrorInvalidValue;
+          } else {
+            hipLaunchKernelGGL((lora_fwd_ks_kernel<G, F, D>), grid, block, 0, st, a.X, a.W, a.A, a.B, a.Y, a.U,
+                               (int)a.m, (int)a.n, (int)a.k, (int)a.r, a.s, L.tiles_m, L.tiles_n, (int)L.col_begin,
+                               grp);
+            return hipGetLastError();
+          }
+        });
+      });
+    });
   }
-  const int nb = (int)n_begin;
-  if (a.r <= 16) return launch_fwd_cfg<BM, BN, WM, WN, 16, DROP, GRP>(a, grp, tiles_n, nb, st);
-  if (a.r <= 32) return launch_fwd_cfg<BM, BN, WM, WN, 32, DROP, GRP>(a, grp, tiles_n, nb, st);
-  return launch_fwd_cfg<BM, BN, WM, WN, 64, DROP, GRP>(a, grp, tiles_n, nb, st);
+  if (L.id != K_FWD) return hipErrorInvalidValue;
+  return with_int<0, 1, 2>(tile_code(L), [&](auto tc) {
+    constexpr int T = decltype(tc)::value;
+    constexpr int BM = T == 0 ? 256 : 128, BN = T == 2 ? 128 : 256, WN = T == 2 ? 2 : 4;
+    return with_int<16, 32, 64>(L.rp, [&](auto rc) {
+      return with_bool(L.drop, [&](auto dr) {
+        return with_bool(L.grp, [&](auto gr) {
+          return with_bool(L.upre, [&](auto up) {
+            return with_bool(L.full, [&](auto kf) {
+              return with_bool(L.dma, [&](auto dm) {
+                constexpr int RP = decltype(rc)::value;
+                constexpr bool DROP = decltype(dr)::value, GRP = decltype(gr)::value, UPRE = decltype(up)::value,
+                               KF = decltype(kf)::value, DMA = decltype(dm)::value;
+                if constexpr (!fwd_instantiated<BM, BN, RP, DROP, GRP, UPRE, KF, DMA>()) {
+                  return hipErrorInvalidValue;
+                } else {
+                  hipLaunchKernelGGL((lora_fwd_kernel<BM, BN, 2, WN, RP, DROP, GRP, UPRE, KF, DMA>), grid, block, 0,
+                                     st, a.X, a.W, a.A, a.B, a.keep, a.Y, a.U, (int)a.m, (int)a.n, (int)a.k,
+                                     (int)a.r, a.s, a.inv_keep, L.tiles_m, L.tiles_n, (int)L.col_begin, grp);
+                  return hipGetLastError();
+                }
+              });
+            });
+          });
+        });
+      });
+    });
+  });
 }
 
-// Output columns [n_begin, n_end) of one projection with tile t.
-static hipError_t launch_fwd_tile(const FwdArgs& a, GemmTile t, int64_t n_begin, int64_t n_end, hipStream_t st) {
-  const FwdGroup none{};
-  switch (t) {
-    case TILE_256x256: return launch_fwd_rp<256, 256, 2, 4, false, false>(a, none, n_begin, n_end, st);
-    case TILE_128x256: return launch_fwd_rp<128, 256, 2, 4, false, false>(a, none, n_begin, n_end, st);
-    default: return launch_fwd_rp<128, 128, 2, 2, false, false>(a, none, n_begin, n_end, st);
-  }
-}
-
-// With dropout the 256 x 256 tile is not used: its registers are already full.
-// Without, the columns may be split between two launches of different tiles
-// (plan_gemm_split); the first launch writes U (its first column tile), the
-// second only reads it where its tile takes U precomputed.
 hipError_t launch_fwd(const FwdArgs& a, hipStream_t st) {
-  if (a.keep) {
-    const FwdGroup none{};
-    if (choose_gemm_tile(a.m, a.n) == TILE_128x128)
-      return launch_fwd_rp<128, 128, 2, 2, true, false>(a, none, 0, a.n, st);
-    return launch_fwd_rp<128, 256, 2, 4, true, false>(a, none, 0, a.n, st);
+  const Plan p = plan_fwd(a.m, a.n, a.k, a.r, a.keep != nullptr);
+  const FwdGroup none{};
+  for (int i = 0; i < p.count; ++i) {
+    const hipError_t e = run_fwd_launch(p.l[i], a, none, st);
+    if (e != hipSuccess) return e;
   }
-  const GemmSplit p = plan_gemm_split(a.m, a.n);
-  const hipError_t e = launch_fwd_tile(a, p.t1, 0, p.n1, st);
-  if (e != hipSuccess || p.n1 >= a.n) return e;
-  FwdArgs b = a;
-  b.u_ready = true;
-  return launch_fwd_tile(b, p.t2, p.n1, a.n, st);
+  return hipSuccess;
 }
 
-// One launch for the whole group; the tile is chosen for the combined output
-// of m x (sum of n) features.
+// One launch for the whole group: each projection owns a run of column tiles
+// (tile0 filled here for the plan's tile width).
 hipError_t launch_fwd_group(const GroupFwdArgs& a, hipStream_t st) {
+  const Plan p = plan_group_fwd(a.count, a.n, a.m, a.k, a.r);
   if (a.count == 1) {   // a group of one is the single projection
     FwdArgs f{};
     f.X = a.X; f.W = a.W[0]; f.A = a.A[0]; f.B = a.B[0]; f.Y = a.Y[0]; f.U = a.U[0];
@@ -1109,21 +1088,25 @@ hipError_t launch_fwd_group(const GroupFwdArgs& a, hipStream_t st) {
     return launch_fwd(f, st);
   }
   FwdGroup grp{};
-  int64_t ntot = 0;
   for (int g = 0; g < a.count; ++g) {
     grp.W[g] = a.W[g]; grp.A[g] = a.A[g]; grp.B[g] = a.B[g]; grp.Y[g] = a.Y[g]; grp.U[g] = a.U[g];
     grp.n[g] = (int)a.n[g];
-    ntot += a.n[g];
   }
   grp.count = a.count;
   FwdArgs f{};
   f.X = a.X;
   f.m = a.m; f.n = 0; f.k = a.k; f.r = a.r; f.s = a.s;
-  switch (choose_gemm_tile(a.m, ntot)) {
-    case TILE_256x256: return launch_fwd_rp<256, 256, 2, 4, false, true>(f, grp, 0, 0, st);
-    case TILE_128x256: return launch_fwd_rp<128, 256, 2, 4, false, true>(f, grp, 0, 0, st);
-    default: return launch_fwd_rp<128, 128, 2, 2, false, true>(f, grp, 0, 0, st);
+  for (int i = 0; i < p.count; ++i) {
+    const Launch& L = p.l[i];
+    int t0 = 0;
+    for (int g = 0; g < a.count; ++g) {
+      grp.tile0[g] = t0;
+      t0 += (grp.n[g] + L.bn - 1) / L.bn;
+    }
+    const hipError_t e = run_fwd_launch(L, f, grp, st);
+    if (e != hipSuccess) return e;
   }
+  return hipSuccess;
 }
 
 }  // namespace lora

@@ -17,6 +17,7 @@
 // HBM traffic is one read and one write of W, so the kernel is HBM-bound.
 #include "lora_device.hpp"
 #include "lora_launch.hpp"
+#include "lora_plan.hpp"
 
 namespace lora {
 
@@ -147,25 +148,15 @@ __global__ __launch_bounds__(256) void lora_merge_kernel(const u16* W, const u16
   }
 }
 
-#ifndef LORA_MERGE_BJ
-#define LORA_MERGE_BJ 64
-#endif
-template <int RP>
-static hipError_t launch_merge_rp(const MergeArgs& a, hipStream_t st) {
-  constexpr int BJ = LORA_MERGE_BJ;
-  const int tiles_j = (int)((a.n + BJ - 1) / BJ), tiles_l = (int)((a.k + 127) / 128);
-  hipLaunchKernelGGL((lora_merge_kernel<RP, BJ>), dim3(tiles_j * tiles_l), dim3(256), 0, st, a.W, a.A, a.B,
-                     a.Wout, (int)a.n, (int)a.k, (int)a.r, a.ss, tiles_j, tiles_l);
-  return hipGetLastError();
-}
-
 hipError_t launch_merge(const MergeArgs& a, hipStream_t st) {
-  switch (pad_rank(a.r)) {
-    case 16: return launch_merge_rp<16>(a, st);
-    case 32: return launch_merge_rp<32>(a, st);
-    case 48: return launch_merge_rp<48>(a, st);
-    default: return launch_merge_rp<64>(a, st);
-  }
+  const Plan p = plan_merge(a.n, a.k, a.r);
+  const Launch& L = p.l[0];
+  return with_int<16, 32, 48, 64>(L.rp, [&](auto rc) {
+    hipLaunchKernelGGL((lora_merge_kernel<decltype(rc)::value, kMergeRows>), dim3((unsigned)L.grid),
+                       dim3((unsigned)L.block), 0, st, a.W, a.A, a.B, a.Wout, (int)a.n, (int)a.k, (int)a.r, a.ss,
+                       L.tiles_m, L.tiles_n);
+    return hipGetLastError();
+  });
 }
 
 }  // namespace lora

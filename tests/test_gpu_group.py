@@ -94,12 +94,16 @@ def test_group_of_one_matches_plain():
     check(t, alpha, got)
 
 
-@pytest.mark.parametrize("m,k,ns", [(264, 1024, [512, 1024, 256]), (4096, 5120, [256, 512])],
-                         ids=["m264k1024", "m4096k5120-dx-split"])
-def test_group_integer_exact(m, k, ns):
+# (m, k, ns, r): the last plans the grouped 128 x 256 dX that copies its
+# stages straight into LDS (every n a multiple of 64, whole column tiles)
+EXACT_CASES = [(264, 1024, [512, 1024, 256], 8), (4096, 5120, [256, 512], 8), (2000, 2304, [256, 512, 192], 8)]
+
+
+@pytest.mark.parametrize("m,k,ns,r", EXACT_CASES, ids=["m264k1024", "m4096k5120-dx-split", "m2000k2304-dx128x256"])
+def test_group_integer_exact(m, k, ns, r):
     """Sparse {-1, 0, 1} inputs and s = 2: every sum is a small integer, so
     the GPU matches the oracle bit for bit whatever the summation order."""
-    r, alpha = 8, 16.0
+    alpha = 2.0 * r
     per = [gen_ternary_inputs(m, n, k, r, 50 + g, density=0.01) for g, n in enumerate(ns)]
     t = {"X": per[0]["X"], "W": [p["W"] for p in per], "A": [p["A"] for p in per],
          "B": [p["B"] for p in per], "dY": [p["dY"] for p in per]}
@@ -122,3 +126,17 @@ def test_group_full_size_13b(members):
     print(f"group {[s.name for s in shapes]}", flush=True)
     t = gen_group_inputs(shapes)
     check(t, s0.alpha, run_group(t, s0.m, s0.k, s0.r, s0.alpha), sample_rows(s0.m, s0.seed))
+
+
+# Other full-size groups (ns, m, k, r): the q, k, v projections of a Llama-2-7B
+# attention block over 2048 tokens (its dX takes the grouped 128 x 256 tile
+# that copies its stages straight into LDS).
+FULL_GROUPS = [([4096, 4096, 4096], 2048, 4096, 8)]
+
+
+@pytest.mark.parametrize("ns,m,k,r", FULL_GROUPS, ids=["7b_qkv"])
+def test_group_full_size_other(ns, m, k, r):
+    alpha = 2.0 * r
+    print(f"group ns={ns} m={m} k={k} r={r}", flush=True)
+    t = _group(ns, m, k, r, alpha, 61, b_std=0.02)
+    check(t, alpha, run_group(t, m, k, r, alpha), sample_rows(m, 61))

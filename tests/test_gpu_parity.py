@@ -80,18 +80,6 @@ def test_full_size_configs(shape):
     assert_within(errs, _shape_id(shape))
 
 
-def _mirror_tile(M, N):
-    """Mirror of the library's GEMM tile heuristic (used only to check coverage)."""
-    best, best_cost = None, None
-    for name, bm, bn, eff in (("256x256", 256, 256, 1.0), ("128x256", 128, 256, 0.9),
-                              ("128x128", 128, 128, 0.75)):
-        tiles = -(-M // bm) * -(-N // bn)
-        cost = -(-tiles // 256) * bm * bn / eff
-        if best_cost is None or cost < best_cost:
-            best, best_cost = name, cost
-    return best
-
-
 EXACT = [
     Shape("exact", 257, 1024, 4096, 8, 16.0, 201),
     Shape("exact", 2040, 4096, 4096, 16, 32.0, 202),
@@ -102,8 +90,28 @@ EXACT = [
     Shape("exact", 4096, 5120, 256, 40, 80.0, 207),      # the same with U from its own pass
 ]
 
+# dX plans at the edges of the tile choice: n not a multiple of 64 where the
+# dX would otherwise take the 256 x 256 tile (the 128 x 256 tile with bound
+# checks serves it), and the 256 x 256 direct-to-LDS dX at padded ranks 32
+# and 48.  Run at tolerance on seeded inputs and bit for bit on integer ones.
+SPLIT_EDGE = [
+    Shape("edge", 4096, 4000, 4096, 8, 16.0, 501),
+    Shape("edge", 4096, 4000, 4096, 64, 128.0, 502),
+    Shape("edge", 4096, 1024, 4096, 24, 48.0, 503),
+    Shape("edge", 4096, 1024, 4096, 40, 80.0, 504),
+]
 
-@pytest.mark.parametrize("shape", EXACT, ids=_shape_id)
+
+@pytest.mark.parametrize("shape", SPLIT_EDGE, ids=_shape_id)
+def test_split_edge_shapes(shape):
+    t = gen_inputs(shape, b_std=0.5)
+    out = run_gpu(t, shape)
+    errs = compare(t, shape, out, sample_rows(shape.m, shape.seed))
+    print(_shape_id(shape), errs)
+    assert_within(errs, _shape_id(shape))
+
+
+@pytest.mark.parametrize("shape", EXACT + SPLIT_EDGE, ids=_shape_id)
 def test_integer_inputs_bit_exact(shape):
     """Sparse {-1,0,1} inputs and s = 2: every sum is a small integer, exact in
     bf16 and fp32 whatever the summation order, so GPU == oracle bit for bit."""

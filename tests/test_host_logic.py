@@ -1,11 +1,116 @@
-"""Host-side logic that needs no GPU."""
-from test_gpu_parity import EXACT, RAGGED, _mirror_tile
+"""Host-side logic that needs no GPU: the launch plans the library reports
+(lora_linear_plan, the plan its entry points execute) for every shape of the
+parity suites, and properties of the suites themselves."""
+import pytest
+
+from lora_synth import CONFIGS
+from test_gpu_parity import DEPTH, EXACT, FULL, RAGGED, SPLIT_EDGE
+from test_gpu_group import CASES as GROUP_CASES, EXACT_CASES as GROUP_EXACT, FULL_GROUPS
 
 
-def test_exact_shapes_cover_every_tile():
-    fwd = {_mirror_tile(s.m, s.n) for s in EXACT}
-    dx = {_mirror_tile(s.m, s.k) for s in EXACT}
-    assert fwd == dx == {"256x256", "128x256", "128x128"}, (fwd, dx)
+@pytest.fixture(scope="module")
+def lora():
+    import paper_2403_11366_amd as lora
+    try:
+        lora.load_library()
+    except (RuntimeError, OSError) as e:
+        pytest.skip(f"library not built: {e}")
+    return lora
+
+
+def _gemms(plan):
+    return [x for x in plan if x["tile"] != (0, 0)]
+
+
+def _check_columns(gemm_launches, N):
+    """The GEMM launches of a call cover output columns [0, N) once, in order,
+    each with whole tiles except at the end."""
+    pos = 0
+    for x in gemm_launches:
+        a, b = x["cols"]
+        assert a == pos and b > a, (x, pos)
+        assert x["grid"] >= 1
+        pos = b
+    assert pos == N, (gemm_launches, N)
+
+
+SINGLE = RAGGED + FULL + EXACT + DEPTH + SPLIT_EDGE
+
+
+@pytest.mark.parametrize("s", SINGLE, ids=lambda s: f"{s.name}-m{s.m}n{s.n}k{s.k}r{s.r}")
+def test_single_projection_plans(lora, s):
+    fwd = lora.lora_linear_plan("fwd", s.m, s.n, s.k, s.r)
+    bwd = lora.lora_linear_plan("bwd", s.m, s.n, s.k, s.r)
+    _check_columns(_gemms(fwd), s.n)
+    _check_columns([x for x in bwd if "dx_kernel" in x["kernel"]], s.k)
+    names = [x["kernel"] for x in bwd]
+    assert names[0].startswith("lora::lora_bwd_du_kernel<") and names[1].startswith("lora::lora_tokred_kernel<")
+    # the U pass precedes the first forward GEMM exactly when the rank is above 16
+    assert any("lora_u_kernel" in x["kernel"] for x in fwd) == (s.r > 16)
+    for x in bwd:
+        if "dx_kernel<256, 256" in x["kernel"]:   # the 256 x 256 dX tile runs only with whole stages
+            assert x["kernel"].endswith("true>"), x
+        if "dx_kernel" in x["kernel"]:
+            tm = -(-s.m // x["tile"][0])
+            tn = -(-(x["cols"][1] - x["cols"][0]) // x["tile"][1])
+            assert x["grid"] == tm * tn
+
+
+def test_exact_shapes_cover_every_tile(lora):
+    fwd = {x["tile"] for s in EXACT for x in _gemms(lora.lora_linear_plan("fwd", s.m, s.n, s.k, s.r))}
+    dx = {x["tile"] for s in EXACT for x in lora.lora_linear_plan("bwd", s.m, s.n, s.k, s.r) if x["tile"] != (0, 0)}
+    assert fwd == dx == {(256, 256), (128, 256), (128, 128)}, (fwd, dx)
+
+
+def test_bench_workload_kernels(lora):
+    """The 7B q_proj step is the k-split forward copying its stages straight
+    into LDS, and the 128 x 256 direct-to-LDS dX."""
+    s = CONFIGS["llama2_7b_q_proj"][0]
+    assert [x["kernel"] for x in lora.lora_linear_plan("fwd", s.m, s.n, s.k, s.r)] == \
+        ["lora::lora_fwd_ks_kernel<false, true, true>"]
+    assert lora.lora_linear_plan("bwd", s.m, s.n, s.k, s.r)[-1]["kernel"] == \
+        "lora::lora_bwd_dx_kernel<128, 256, 2, 4, 16, false, false, true>"
+
+
+def test_ragged_n_avoids_the_register_staged_256_tile(lora):
+    """n not a multiple of 64 on a shape whose dX would take the 256 x 256 tile:
+    the 128 x 256 tile without the FULL loads serves it."""
+    for r in (8, 64):
+        plan = lora.lora_linear_plan("bwd", 4096, 4000, 4096, r)
+        dx = [x["kernel"] for x in plan if "dx_kernel" in x["kernel"]]
+        assert dx and all(k.startswith("lora::lora_bwd_dx_kernel<128, 256,") and k.endswith("false>") for k in dx), dx
+
+
+def _group_dx(lora, ns, m, k, r):
+    return [x["kernel"] for x in lora.lora_linear_plan("group_bwd", m, ns, k, r) if "dx_kernel" in x["kernel"]]
+
+
+def test_group_suites_reach_every_grouped_dx_variant(lora):
+    """Every grouped dX variant a plan can name for these suites is run by a
+    GPU test, including the 128 x 256 direct-to-LDS one (7B q/k/v)."""
+    seen = set()
+    for ns, m, k, r, _ in GROUP_CASES:
+        seen |= set(_group_dx(lora, ns, m, k, r))
+    for m, k, ns, r in GROUP_EXACT:
+        seen |= set(_group_dx(lora, ns, m, k, r))
+    for ns, m, k, r in FULL_GROUPS:
+        seen |= set(_group_dx(lora, ns, m, k, r))
+    for want in ("lora::lora_bwd_dx_kernel<128, 256, 2, 4, 16, false, true, true>",
+                 "lora::lora_bwd_dx_kernel<256, 256, 2, 4, 16, false, true, true>",
+                 "lora::lora_bwd_dx_kernel<128, 128, 2, 2, 16, false, true, true>"):
+        assert want in seen, (want, sorted(seen))
+
+
+def test_plan_refuses_what_the_entry_point_refuses(lora):
+    from paper_2403_11366_amd import LoraError
+    with pytest.raises(LoraError):
+        lora.lora_linear_plan("fwd", 16, 100, 64, 8)        # n not a multiple of 8
+    with pytest.raises(LoraError):
+        lora.lora_linear_plan("bwd", 16, 64, 64, 65)        # r > 64
+    with pytest.raises(LoraError):
+        lora.lora_linear_plan("bwd_fused", 16, 64, 64, 32)  # fused: r <= 16
+    with pytest.raises(LoraError):
+        lora.lora_linear_plan("fwd_dropout", 16, 64, 72, 8)  # dropout: k % 64 == 0
 
 
 def test_ragged_shapes_have_tails():

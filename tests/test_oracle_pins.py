@@ -323,3 +323,79 @@ def test_f64_to_bf16_bits_rounding():
     vals = np.array([0.0, 1.0, -3.0, 256.0, 255.0, 1 + 2 ** -8, 1 + 3 * 2 ** -8], dtype=np.float64)
     got = oracle.bf16_bits_to_f64(oracle.f64_to_bf16_bits(vals))
     assert got.tolist() == [0.0, 1.0, -3.0, 256.0, 255.0, 1.0, 1 + 2 ** -6]
+
+
+# ----------------------------------------------------------------------------
+# the rank-r activation U = X A^T on its own (oracle.lora_rank_activation, the
+# U reference of the GPU tests), pinned by checks parameterised by the function
+
+def check_u_golden(u_fn):
+    """The hand-worked U of tests/golden (computed by hand from Eq. 1's A x term)."""
+    for ex in load_golden():
+        t = ex["t"]
+        assert np.array_equal(np.asarray(u_fn(t["X"], t["A"])), t["U"]), ex["name"]
+
+
+def check_u_brute(u_fn):
+    """Scalar loops over the index definition U[i][t] = sum_l X[i][l] A[t][l]."""
+    t = _small_inputs(4, 3, 6, 3, 6.0, 12)
+    X, A = t["X"].tolist(), t["A"].tolist()
+    ref = [[sum(X[i][l] * A[q][l] for l in range(6)) for q in range(3)] for i in range(4)]
+    assert rel(u_fn(t["X"], t["A"]), ref) <= 1e-14
+
+
+def check_u_through_forward(u_fn):
+    """Another route: with W = 0 and B the identity (n = r), Eq. 1 gives
+    Y = s U, so U = Y / s from the (separately pinned) forward."""
+    m, k, r, alpha = 9, 11, 4, 12.0
+    t = _small_inputs(m, r, k, r, alpha, 13)
+    _, Y = oracle.lora_forward(t["X"], np.zeros((r, k)), t["A"], np.eye(r), alpha)
+    assert rel(u_fn(t["X"], t["A"]), Y / (alpha / r)) <= 1e-14
+
+
+def check_u_linear_in_x(u_fn):
+    """U is linear in each row of X: the change of U[i] for a unit change of
+    X[i][l] is column l of A, and other rows do not move."""
+    t = _small_inputs(5, 3, 7, 3, 6.0, 14)
+    base = np.asarray(u_fn(t["X"], t["A"]), dtype=np.float64)
+    for i, l in ((0, 0), (2, 5), (4, 6)):
+        X2 = t["X"].copy()
+        X2[i, l] += 1.0
+        d = np.asarray(u_fn(X2, t["A"]), dtype=np.float64) - base
+        expect = np.zeros_like(base)
+        expect[i] = t["A"][:, l]
+        assert np.allclose(d, expect, rtol=0, atol=1e-12), (i, l)
+
+
+U_CHECKS = [check_u_golden, check_u_brute, check_u_through_forward, check_u_linear_in_x]
+
+
+@pytest.mark.parametrize("check", U_CHECKS, ids=lambda c: c.__name__)
+def test_rank_activation_pin(check):
+    check(oracle.lora_rank_activation)
+
+
+def test_rank_activation_is_the_forward_u():
+    t = gen_inputs(Shape("u", 70, 48, 136, 13, 26.0, 15))
+    assert np.array_equal(oracle.lora_rank_activation(t["X"], t["A"]),
+                          oracle.lora_forward(t["X"], t["W"], t["A"], t["B"], 26.0)[0])
+
+
+U_MUTANTS = [
+    ("u_a_rows_rolled", lambda X, A: oracle.lora_rank_activation(X, np.roll(np.asarray(A), 1, axis=0))),
+    ("u_x_rows_reversed", lambda X, A: oracle.lora_rank_activation(np.asarray(X)[::-1], A)),
+    ("u_a_columns_reversed", lambda X, A: oracle.lora_rank_activation(X, np.asarray(A)[:, ::-1])),
+    ("u_scaled", lambda X, A: 2.0 * oracle.lora_rank_activation(X, A)),
+    ("u_sign", lambda X, A: -oracle.lora_rank_activation(X, A)),
+]
+
+
+@pytest.mark.parametrize("name,fn", U_MUTANTS, ids=[m[0] for m in U_MUTANTS])
+def test_rank_activation_pins_catch_planted_mistake(name, fn):
+    failed = []
+    for check in U_CHECKS:
+        try:
+            check(fn)
+        except AssertionError:
+            failed.append(check.__name__)
+    assert failed, f"planted mistake {name} passed every U pin"
