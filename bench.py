@@ -146,6 +146,103 @@ def summarize_traffic(root: str, workload: str, copy_mib: int):
     print(json.dumps(rec))
 
 
+def algorithmic_units(s, launch):
+    """(unit, amount) of one launch of shape s: flops for the matrix-core GEMMs,
+    bytes for the HBM-bound kernels (the algorithmic minimum: each operand read
+    once, each output written once; split-K partial traffic not credited)."""
+    m, n, k, r = s.m, s.n, s.k, s.r
+    name = launch["kernel"]
+    c0, c1 = launch["cols"]
+    if "lora_fwd_kernel" in name or "lora_fwd_ks_kernel" in name:
+        cols = c1 - c0
+        upre = name.startswith("lora::lora_fwd_kernel") and name.split(",")[7].strip() == "true"
+        u = 0 if (upre or c0 > 0) else 2 * m * k * r
+        return "flop", 2 * m * cols * k + 2 * m * cols * r + u
+    if "lora_bwd_dx_kernel" in name:
+        return "flop", 2 * m * (n + r) * (c1 - c0)
+    if "lora_u_kernel" in name:
+        return "byte", 2 * m * k + 2 * r * k + 4 * m * r
+    if "lora_bwd_du_kernel" in name:
+        return "byte", 2 * m * n + 2 * n * r + 4 * m * r
+    if "lora_tokred_kernel" in name:
+        return "byte", (2 * m * n + 4 * m * r + 4 * n * r) + (2 * m * k + 4 * m * r + 4 * r * k)
+    return None, None
+
+
+def summarize_counters(root: str, workload: str, copy_mib: int):
+    """Per-kernel table from rocprofv3 runs of one single-projection workload
+    under root/: trace/ (--kernel-trace --stats), fetch/ and write/ (--pmc
+    FETCH_SIZE, WRITE_SIZE), mfma/ (--pmc SQ_VALU_MFMA_BUSY_CYCLES
+    SQ_BUSY_CYCLES GRBM_GUI_ACTIVE SQ_INSTS_MFMA), lds/ (--pmc SQ_INSTS_LDS
+    SQ_LDS_BANK_CONFLICT SQ_LDS_IDX_ACTIVE), copy_fetch/ and copy_write/ (the
+    copy of copy_mib MiB that calibrates FETCH_SIZE and WRITE_SIZE).  Prints
+    markdown: per kernel of the workload's plan, its average duration, the
+    algorithmic rate against its roofline, the counter-measured HBM bytes and
+    rate, and matrix-core and LDS figures."""
+    import csv
+    import glob
+    from lora_synth import CONFIGS
+    (s,) = CONFIGS[workload]
+
+    def rows(sub, pattern):
+        out = []
+        for f in glob.glob(os.path.join(root, sub, "**", pattern), recursive=True):
+            out += list(csv.DictReader(open(f)))
+        return out
+
+    def counter(sub, name, kname):
+        per = {}
+        for r_ in rows(sub, "*counter_collection.csv"):
+            if r_["Counter_Name"] == name and kname in r_["Kernel_Name"]:
+                per[r_["Dispatch_Id"]] = per.get(r_["Dispatch_Id"], 0.0) + float(r_["Counter_Value"])
+        if not per:
+            return None
+        v = sorted(per.values())
+        return v[len(v) // 2]
+
+    durations = {}
+    for r_ in rows("trace", "*kernel_stats.csv"):
+        durations[r_["Name"]] = (int(r_["Calls"]), float(r_["AverageNs"]) / 1e3)
+
+    def duration(kname):
+        hits = [(c, d) for nm, (c, d) in durations.items() if nm.startswith(kname + "(") or nm == kname]
+        return hits[0] if hits else (0, None)
+
+    f_cpy, w_cpy = counter("copy_fetch", "FETCH_SIZE", ""), counter("copy_write", "WRITE_SIZE", "")
+    sf = copy_mib * 1024.0 / f_cpy if f_cpy else None
+    sw = copy_mib * 1024.0 / w_cpy if w_cpy else None
+    import paper_2403_11366_amd as lora
+    launches = lora.lora_linear_plan("fwd", s.m, s.n, s.k, s.r) + lora.lora_linear_plan("bwd", s.m, s.n, s.k, s.r)
+    print(f"| kernel | calls | avg us | algorithmic | rate | of peak | HBM bytes (counters) | HBM GB/s "
+          f"| MFMA busy | LDS bank conflicts / LDS instr |")
+    print("|---|---|---|---|---|---|---|---|---|---|")
+    for x in launches:
+        kname = x["kernel"]
+        calls, us = duration(kname)
+        unit, amount = algorithmic_units(s, x)
+        rate = frac = None
+        if us and unit == "flop":
+            rate = amount / (us * 1e-6) / 1e12
+            frac = rate / PEAK_BF16_TFLOPS
+        elif us and unit == "byte":
+            rate = amount / (us * 1e-6) / 1e9
+            frac = rate / PEAK_HBM_GBS
+        fb, wb = counter("fetch", "FETCH_SIZE", kname), counter("write", "WRITE_SIZE", kname)
+        hbm = (fb * sf + wb * sw) * 1024.0 if (fb is not None and wb is not None and sf and sw) else None
+        mfma = counter("mfma", "SQ_VALU_MFMA_BUSY_CYCLES", kname)
+        busy = counter("mfma", "GRBM_GUI_ACTIVE", kname)
+        lds_i, lds_c = counter("lds", "SQ_INSTS_LDS", kname), counter("lds", "SQ_LDS_BANK_CONFLICT", kname)
+        # SQ_VALU_MFMA_BUSY_CYCLES summed over the chip's 256 CUs x 4 SIMDs against
+        # the GPU-busy clock of the dispatch
+        mfma_pct = 100.0 * mfma / (busy * 256 * 4) if (mfma and busy) else None
+        cols = "" if x["tile"] == (0, 0) else f" cols [{x['cols'][0]}, {x['cols'][1]})"
+        fmt = lambda v, p: "-" if v is None else f"{v:.{p}f}"
+        print(f"| `{kname}`{cols} | {calls} | {fmt(us, 2)} | {amount / 1e9:.2f} G{unit} "
+              f"| {fmt(rate, 1)} {'TFLOP/s' if unit == 'flop' else 'GB/s'} | {fmt(frac, 3)} "
+              f"| {fmt(None if hbm is None else hbm / 1e6, 1)} MB | {fmt(None if (hbm is None or not us) else hbm / (us * 1e-6) / 1e9, 0)} "
+              f"| {fmt(mfma_pct, 1)}% | {fmt(None if not lds_i else lds_c / lds_i, 3)} |")
+
+
 def host_cpu():
     """(threads this process may use, CPU model) of the host."""
     cores = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1)
@@ -162,41 +259,42 @@ def host_cpu():
 
 
 def cpu_baseline(shape, seconds: float, drop=None):
-    """Time the fp64 oracle (as it stands) on this host for `shape` (with LoRA
-    dropout at rate `drop` when given), on every core of the process's
-    affinity mask."""
+    """Time the fp64 oracle (as it stands) on this host for `shape`, on every
+    core of the process's affinity mask: its plain-loop form (float64 loops
+    over the index definitions, OpenMP over output rows), or with LoRA dropout
+    at rate `drop` its numpy form (the loop form has no dropout variant).
+    Whole forward + backward passes are repeated until `seconds` have passed."""
     import oracle
     from lora_synth import gen_inputs, gen_keep_mask
     cores, model = host_cpu()
-    try:
-        from threadpoolctl import threadpool_limits
-        limiter = threadpool_limits(limits=cores)
-    except Exception:
-        limiter = None
     t = gen_inputs(shape)
-    keep = None if drop is None else gen_keep_mask(shape.m, shape.k, drop, shape.seed + 1)
+    if drop is None:
+        from oracle import loops
+        loops.build()
+        kind = "plain fp64 loops (oracle/lora_loops.c, OpenMP over output rows)"
+
+        def one():
+            loops.lora_forward_loops(t["X"], t["W"], t["A"], t["B"], shape.alpha, threads=cores)
+            loops.lora_backward_loops(t["dY"], t["X"], t["W"], t["A"], t["B"], shape.alpha, threads=cores)
+    else:
+        keep = gen_keep_mask(shape.m, shape.k, drop, shape.seed + 1)
+        kind = "numpy fp64 (one matmul per formula line)"
+
+        def one():
+            oracle.lora_forward_dropout(t["X"], t["W"], t["A"], t["B"], keep, drop, shape.alpha)
+            oracle.lora_backward_dropout(t["dY"], t["X"], t["W"], t["A"], t["B"], keep, drop, shape.alpha)
     runs, t0 = 0, time.perf_counter()
-    try:
-        while True:
-            if keep is None:
-                oracle.lora_forward(t["X"], t["W"], t["A"], t["B"], shape.alpha)
-                oracle.lora_backward(t["dY"], t["X"], t["W"], t["A"], t["B"], shape.alpha)
-            else:
-                oracle.lora_forward_dropout(t["X"], t["W"], t["A"], t["B"], keep, drop, shape.alpha)
-                oracle.lora_backward_dropout(t["dY"], t["X"], t["W"], t["A"], t["B"], keep, drop, shape.alpha)
-            runs += 1
-            el = time.perf_counter() - t0
-            if el >= seconds or runs >= 50:
-                break
-    finally:
-        if limiter is not None:
-            limiter.unregister()
+    while True:
+        one()
+        runs += 1
+        el = time.perf_counter() - t0
+        if el >= seconds or runs >= 50:
+            break
     per = el / runs
     return {"value": shape.flops_fwd_bwd / per / 1e12, "unit": "TFLOP/s", "cores": int(cores),
             "kind": "oracle", "cpu_model": model,
             "sample": f"{runs} full fwd+bwd of {shape.name} (m={shape.m} n={shape.n} k={shape.k} "
-                      f"r={shape.r}) by the fp64 oracle (numpy matmul per formula line), {el:.1f} s total, "
-                      f"{per:.3f} s each"}
+                      f"r={shape.r}) by the oracle's {kind}, {el:.1f} s total, {per:.2f} s each"}
 
 
 def cpu_baseline_merge(shape, seconds: float):
@@ -370,7 +468,7 @@ def main():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=100)
     ap.add_argument("--config", default="llama2_7b_shapes")
-    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--cpu-seconds", type=float, default=5.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--only", choices=["fwd", "copy"], default=None,
                     help="run only forward launches, or only a plain device copy (for counter runs)")
@@ -387,10 +485,15 @@ def main():
     ap.add_argument("--fused-bwd", action="store_true",
                     help="backward through lora_linear_bwd_fused (dU and dB inside the dX GEMM; "
                          "rank <= 16, no dropout)")
+    ap.add_argument("--summarize-counters", metavar="DIR", default=None,
+                    help="print the per-kernel counter table of the rocprofv3 runs under DIR and exit")
     ap.add_argument("--summarize-traffic", metavar="DIR", default=None,
                     help="write the HBM-traffic record from counter runs under DIR and exit")
     args = ap.parse_args()
 
+    if args.summarize_counters:
+        summarize_counters(args.summarize_counters, args.config, args.copy_mib)
+        return
     if args.summarize_traffic:
         summarize_traffic(args.summarize_traffic, args.config, args.copy_mib)
         return
@@ -564,7 +667,7 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         c0 = min((s for s, _, _ in proj), key=lambda s: s.flops_fwd_bwd)
-        log(f"[bench] timing the fp64 oracle on the host (~{args.cpu_seconds:.0f} s, {c0.name})")
+        log(f"[bench] timing the fp64 oracle on the host ({c0.name}, at least {args.cpu_seconds:.0f} s)")
         cpu = cpu_baseline(c0, args.cpu_seconds, drop)
 
     rec = {

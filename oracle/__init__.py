@@ -36,7 +36,10 @@ W0 x + B A x = (W0 + B A) x) is W + sign s B A, rounded once to bfloat16
 (nearest-even) for the stored result.
 
 Each step is one numpy float64 matrix product; there is no blocking, fusion or
-reordering beyond the definition.  Pins that tie this to the paper and to the
+reordering beyond the definition.  The forward and backward are also written
+as plain float64 loops over the index definitions in C (lora_loops.c, loaded
+by loops.py; its shared library is built by loops.build()): pinned by the same
+checks, it is the form the benchmark times as the CPU baseline.  Pins that tie this to the paper and to the
 mathematics (merge identity, B = 0 and A = 0 invariants, finite differences,
 a hand-worked example, brute-force loops, closed forms) live in
 tests/test_oracle_pins.py.
