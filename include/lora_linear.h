@@ -132,6 +132,31 @@ lora_status lora_linear_bwd(const lora_bf16* dY, const lora_bf16* X, const lora_
                             void* stream);
 
 /*
+ * lora_linear_bwd without a workspace argument, for callers that cannot
+ * allocate device memory: code being captured into a HIP graph, tight
+ * serving loops, harnesses that forbid allocation.  Same arguments (minus the
+ * workspace), outputs, definitions and errors as lora_linear_bwd.
+ *
+ * The workspace is a fixed array of LORA_NOALLOC_SCRATCH_BYTES bytes inside
+ * this library, one per GPU, kept until the process ends; its device address
+ * is looked up on the first call on each device (with that device current).
+ * The call allocates and frees nothing.  Shapes whose workspace
+ * (lora_linear_bwd_workspace_size) exceeds LORA_NOALLOC_SCRATCH_BYTES return
+ * LORA_ERR_WORKSPACE before anything is enqueued; every Llama-2 projection
+ * shape of up to 8192 tokens fits.  All calls on one GPU share its array:
+ * calls whose kernels may overlap in time on one GPU (other streams, other
+ * threads) race on it and must be ordered by the caller; a call's result
+ * depends only on its own arguments (no part of the array needs clearing).
+ */
+#define LORA_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+
+lora_status lora_linear_bwd_noalloc(const lora_bf16* dY, const lora_bf16* X, const lora_bf16* W,
+                                    const lora_bf16* A, const lora_bf16* B, const float* U,
+                                    lora_bf16* dX, float* dA, float* dB,
+                                    int64_t m, int64_t n, int64_t k, int64_t r, float alpha,
+                                    void* stream);
+
+/*
  * Bytes of device workspace lora_linear_bwd_fused needs for this shape (0 on
  * an invalid shape or r > 16): dU^T in bf16 high and low parts, the dB
  * partials of the dX launch (one per 128-token tile row) and the split-K

@@ -16,7 +16,7 @@ from typing import Optional
 
 __all__ = [
     "LoraError", "lib_path", "load_library", "lora_linear_fwd", "lora_linear_bwd",
-    "lora_linear_bwd_workspace_size", "lora_linear_bwd_fused", "lora_linear_bwd_fused_workspace_size",
+    "lora_linear_bwd_workspace_size", "lora_linear_bwd_noalloc", "NOALLOC_SCRATCH_BYTES", "lora_linear_bwd_fused", "lora_linear_bwd_fused_workspace_size",
     "lora_linear_merge", "lora_linear_fwd_dropout", "lora_linear_bwd_dropout",
     "lora_linear_group_fwd", "lora_linear_group_bwd", "lora_linear_group_bwd_workspace_size",
     "lora_status_string", "STATUS", "lora_linear_plan", "OPS",
@@ -65,6 +65,8 @@ def load_library() -> ctypes.CDLL:
     lib.lora_linear_bwd_workspace_size.restype = sz
     lib.lora_linear_bwd.argtypes = [p, p, p, p, p, p, p, p, p, p, sz, i64, i64, i64, i64, f32, p]
     lib.lora_linear_bwd.restype = ctypes.c_int
+    lib.lora_linear_bwd_noalloc.argtypes = [p, p, p, p, p, p, p, p, p, i64, i64, i64, i64, f32, p]
+    lib.lora_linear_bwd_noalloc.restype = ctypes.c_int
     lib.lora_linear_bwd_fused_workspace_size.argtypes = [i64, i64, i64, i64]
     lib.lora_linear_bwd_fused_workspace_size.restype = sz
     lib.lora_linear_bwd_fused.argtypes = [p, p, p, p, p, p, p, p, p, p, sz, i64, i64, i64, i64, f32, p]
@@ -153,6 +155,28 @@ def lora_linear_bwd(dY, X, W, A, B, U, dX, dA, dB, workspace, alpha: float, stre
     U [m,r], dA [r,k], dB [n,r]: torch.float32; workspace: a device tensor of at
     least lora_linear_bwd_workspace_size(m, n, k, r) bytes."""
     _bwd_call("lora_linear_bwd", dY, X, W, A, B, U, dX, dA, dB, workspace, alpha, stream)
+
+
+NOALLOC_SCRATCH_BYTES = 32 << 20   # LORA_NOALLOC_SCRATCH_BYTES of include/lora_linear.h
+
+
+def lora_linear_bwd_noalloc(dY, X, W, A, B, U, dX, dA, dB, alpha: float, stream=None) -> None:
+    """lora_linear_bwd with the library's own per-GPU scratch array as the
+    workspace (no allocation; calls that overlap on one GPU race on it)."""
+    import torch
+    m, n = dY.shape
+    k, r = X.shape[1], A.shape[0]
+    for t, name, dt, shp in ((dY, "dY", torch.bfloat16, (m, n)), (X, "X", torch.bfloat16, (m, k)),
+                             (W, "W", torch.bfloat16, (n, k)), (A, "A", torch.bfloat16, (r, k)),
+                             (B, "B", torch.bfloat16, (n, r)), (U, "U", torch.float32, (m, r)),
+                             (dX, "dX", torch.bfloat16, (m, k)), (dA, "dA", torch.float32, (r, k)),
+                             (dB, "dB", torch.float32, (n, r))):
+        _check(t, name, dt, shp)
+    st = load_library().lora_linear_bwd_noalloc(_ptr(dY), _ptr(X), _ptr(W), _ptr(A), _ptr(B), _ptr(U),
+                                                _ptr(dX), _ptr(dA), _ptr(dB), m, n, k, r, float(alpha),
+                                                _stream_handle(stream))
+    if st != 0:
+        raise LoraError(st, "lora_linear_bwd_noalloc")
 
 
 def lora_linear_bwd_fused(dY, X, W, A, B, U, dX, dA, dB, workspace, alpha: float, stream=None) -> None:

@@ -177,6 +177,27 @@ lora_status lora_linear_bwd(const lora_bf16* dY, const lora_bf16* X, const lora_
   return e == hipSuccess ? LORA_OK : LORA_ERR_HIP;
 }
 
+lora_status lora_linear_bwd_noalloc(const lora_bf16* dY, const lora_bf16* X, const lora_bf16* W,
+                                    const lora_bf16* A, const lora_bf16* B, const float* U,
+                                    lora_bf16* dX, float* dA, float* dB,
+                                    int64_t m, int64_t n, int64_t k, int64_t r, float alpha, void* stream) {
+  if (!dY || !X || !W || !A || !B || !U || !dX || !dA || !dB) return LORA_ERR_NULL;
+  lora_status st = check_shape(m, n, k, r);
+  if (st != LORA_OK) return st;
+  if (!aligned16(dY) || !aligned16(X) || !aligned16(W) || !aligned16(A) || !aligned16(B) ||
+      !aligned16(U) || !aligned16(dX) || !aligned16(dA) || !aligned16(dB))
+    return LORA_ERR_ALIGN;
+  if (lora::bwd_layout(m, n, k, r).total > lora::kNoAllocScratchBytes) return LORA_ERR_WORKSPACE;
+  const Range in[6] = {span(dY, m, n, 2), span(X, m, k, 2), span(W, n, k, 2),
+                       span(A, r, k, 2),  span(B, n, r, 2), span(U, m, r, 4)};
+  const Range out[3] = {span(dX, m, k, 2), span(dA, r, k, 4), span(dB, n, r, 4)};
+  if (any_alias(out, 3, in, 6)) return LORA_ERR_ALIAS;
+
+  lora::BwdArgs a{dY, X, W, A, B, U, dX, dA, dB, nullptr, m, n, k, r, (float)alpha / (float)r};
+  hipError_t e = lora::launch_bwd_noalloc(a, reinterpret_cast<hipStream_t>(stream));
+  return e == hipSuccess ? LORA_OK : LORA_ERR_HIP;
+}
+
 size_t lora_linear_bwd_fused_workspace_size(int64_t m, int64_t n, int64_t k, int64_t r) {
   if (check_shape(m, n, k, r) != LORA_OK || r > 16) return 0;
   return lora::bwd_fused_layout(m, n, k, r).total;

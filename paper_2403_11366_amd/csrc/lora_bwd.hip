@@ -22,6 +22,7 @@
 //             (the first one of a split) sums a slice of the dB and dA
 //             partials in a fixed order (no atomics, so results are
 //             bit-identical from run to run) and applies s to dB.
+#include <mutex>
 #include <type_traits>
 
 #include "lora_device.hpp"
@@ -1418,6 +1419,47 @@ hipError_t launch_bwd_fused(const BwdArgs& a, hipStream_t st) {
     }
   }
   return hipSuccess;
+}
+
+// ---------------------------------------------------------------------------
+// Backward without a caller-provided workspace: the workspace regions live in
+// a fixed device array of this library, one per GPU, whose address is looked
+// up once per device (with that device current) on the first call there.
+// Host code never passes the array's name itself to a kernel or a copy: in
+// host code it stands for a host-side shadow, not the device address.
+static __device__ __align__(256) char scratch[kNoAllocScratchBytes];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+hipError_t noalloc_scratch(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
+}
+
+hipError_t launch_bwd_noalloc(const BwdArgs& a, hipStream_t st) {
+  if (bwd_layout(a.m, a.n, a.k, a.r).total > kNoAllocScratchBytes) return hipErrorInvalidValue;
+  void* ws = nullptr;
+  const hipError_t e = noalloc_scratch(&ws);
+  if (e != hipSuccess) return e;
+  BwdArgs b = a;
+  b.ws = static_cast<char*>(ws);
+  return launch_bwd(b, st);
 }
 
 // Grouped backward: per projection the dU and token-reduction launches (each

@@ -244,7 +244,12 @@ struct MergeArgs {
   float ss;                // sign * alpha / r
 };
 
+// Scratch of lora_linear_bwd_noalloc: a fixed device array per GPU holding
+// the backward workspace (the largest Llama-2 projection shapes need 21 MiB).
+constexpr size_t kNoAllocScratchBytes = size_t(32) << 20;
+
 hipError_t launch_fwd(const FwdArgs& a, hipStream_t st);
+hipError_t launch_bwd_noalloc(const BwdArgs& a, hipStream_t st);   // workspace: the library's scratch array
 hipError_t launch_merge(const MergeArgs& a, hipStream_t st);
 hipError_t launch_bwd(const BwdArgs& a, hipStream_t st);
 hipError_t launch_bwd_fused(const BwdArgs& a, hipStream_t st);   // rank <= 16, no dropout
