@@ -202,7 +202,8 @@ def summarize_counters(root: str, workload: str, copy_mib: int):
 
     durations = {}
     for r_ in rows("trace", "*kernel_stats.csv"):
-        durations[r_["Name"]] = (int(r_["Calls"]), float(r_["AverageNs"]) / 1e3)
+        nm = r_["Name"][5:] if r_["Name"].startswith("void ") else r_["Name"]
+        durations[nm] = (int(r_["Calls"]), float(r_["AverageNs"]) / 1e3)
 
     def duration(kname):
         hits = [(c, d) for nm, (c, d) in durations.items() if nm.startswith(kname + "(") or nm == kname]
@@ -214,8 +215,8 @@ def summarize_counters(root: str, workload: str, copy_mib: int):
     import paper_2403_11366_amd as lora
     launches = lora.lora_linear_plan("fwd", s.m, s.n, s.k, s.r) + lora.lora_linear_plan("bwd", s.m, s.n, s.k, s.r)
     print(f"| kernel | calls | avg us | algorithmic | rate | of peak | HBM bytes (counters) | HBM GB/s "
-          f"| MFMA busy | LDS bank conflicts / LDS instr |")
-    print("|---|---|---|---|---|---|---|---|---|---|")
+          f"| MFMA flops executed / algorithmic | MFMA busy | shader clock | LDS bank conflicts / LDS instr |")
+    print("|---|---|---|---|---|---|---|---|---|---|---|---|")
     for x in launches:
         kname = x["kernel"]
         calls, us = duration(kname)
@@ -230,17 +231,24 @@ def summarize_counters(root: str, workload: str, copy_mib: int):
         fb, wb = counter("fetch", "FETCH_SIZE", kname), counter("write", "WRITE_SIZE", kname)
         hbm = (fb * sf + wb * sw) * 1024.0 if (fb is not None and wb is not None and sf and sw) else None
         mfma = counter("mfma", "SQ_VALU_MFMA_BUSY_CYCLES", kname)
+        mops = counter("mfma", "SQ_INSTS_VALU_MFMA_MOPS_BF16", kname)
         busy = counter("mfma", "GRBM_GUI_ACTIVE", kname)
         lds_i, lds_c = counter("lds", "SQ_INSTS_LDS", kname), counter("lds", "SQ_LDS_BANK_CONFLICT", kname)
-        # SQ_VALU_MFMA_BUSY_CYCLES summed over the chip's 256 CUs x 4 SIMDs against
-        # the GPU-busy clock of the dispatch
-        mfma_pct = 100.0 * mfma / (busy * 256 * 4) if (mfma and busy) else None
+        # GRBM_GUI_ACTIVE reads as the sum over the 8 XCDs of their busy cycles;
+        # SQ_VALU_MFMA_BUSY_CYCLES as the sum over all 1024 SIMDs of the cycles
+        # their matrix pipe is busy (32 per 32x32x16 bf16 instruction).  Busy
+        # fraction: per-SIMD matrix-pipe cycles over the per-XCD busy cycles.
+        mfma_pct = 100.0 * mfma / (busy / 8 * 1024) if (mfma and busy) else None
+        # (GRBM_GUI_ACTIVE also counts the dispatch's ramp: a clock only for long kernels)
+        clock = busy / 8 / (us * 1e-6) / 1e9 if (busy and us and us > 100) else None
+        executed = mops * 512 / amount if (mops and unit == "flop") else None
         cols = "" if x["tile"] == (0, 0) else f" cols [{x['cols'][0]}, {x['cols'][1]})"
         fmt = lambda v, p: "-" if v is None else f"{v:.{p}f}"
         print(f"| `{kname}`{cols} | {calls} | {fmt(us, 2)} | {amount / 1e9:.2f} G{unit} "
               f"| {fmt(rate, 1)} {'TFLOP/s' if unit == 'flop' else 'GB/s'} | {fmt(frac, 3)} "
               f"| {fmt(None if hbm is None else hbm / 1e6, 1)} MB | {fmt(None if (hbm is None or not us) else hbm / (us * 1e-6) / 1e9, 0)} "
-              f"| {fmt(mfma_pct, 1)}% | {fmt(None if not lds_i else lds_c / lds_i, 3)} |")
+              f"| {fmt(executed, 3)} | {fmt(mfma_pct, 1)}% | {fmt(clock, 2)} GHz "
+              f"| {fmt(None if not lds_i else lds_c / lds_i, 3)} |")
 
 
 def host_cpu():
