@@ -6,9 +6,8 @@
 // split between two tiles; each launch costs a few microseconds on its own,
 // so small steps share launches):
 //   du        dU = s dY B, reducing over n.  Writes dU2 (token-major, high |
-//             low) for the dX GEMM and dUt2 (its transpose) for dA, and Ut2
-//             = U^T split into a bf16 high part and a bf16 low part (tokens
-//             padded to mp) for dB.
+//             low) for the dX GEMM, dUt2 (dU^T rounded to bf16) for dA and
+//             Ut2 (U^T rounded to bf16, tokens padded to mp) for dB.
 //   tokred    one launch, two token reductions split over token ranges:
 //             dB^T partials = Ut2 . dY and dA partials = dUt2 . X; the
 //             waves of a workgroup split its tokens.
@@ -44,36 +43,43 @@ __device__ __forceinline__ short8 tr16_read(const char* tile, int pitch, int col
 }
 
 // ---------------------------------------------------------------------------
-// dU = s dY B for TPW (16 or 8) tokens per workgroup, reducing over all of
-// n, plus the U^T high/low split of the same tokens.  TPW = 8 doubles the
-// workgroups for token counts that would leave compute units idle (the
-// matrix-core B operand then carries 8 zero token columns).  The 8 waves take interleaved
-// 32-wide chunks of n, UNR chunks per batch with all of a batch's loads
-// issued together.  A chunk's B rows (32 x r, contiguous in B) are staged in a
-// wave-private LDS slot as [32][RP] (columns t >= r stay zero) and read back
-// transposed into matrix-core A operands; dY rows go straight into B
+// dU = s dY B for TPW (8, 16 or 32) tokens per workgroup, reducing over all
+// of n, plus the U^T high/low split of the same tokens.  The launch takes the
+// largest TPW that still gives every compute unit a workgroup: each
+// workgroup reads all of B (n x r), so more tokens per workgroup means less B
+// traffic per token (at rank 64 B is 4 times the dY bytes of 16 tokens).
+// TPW = 8 carries 8 zero token columns in the matrix-core B operand.  The 8
+// waves take interleaved 32-wide chunks of n, UNR chunks per batch with all
+// of a batch's loads issued together.  A chunk's B rows (32 x r, contiguous
+// in B) are staged in a wave-private LDS slot as [32][RP] (columns t >= r
+// stay zero) and read back transposed into matrix-core A operands, each used
+// for the TG = TPW / 16 groups of 16 tokens; dY rows go straight into B
 // operands.  The waves' sums are added in wave order through LDS, so the
 // result is bit-identical from run to run.  (A split of n over workgroups
 // would need a cross-workgroup reduction, whose device-scope fences write
 // back the per-XCD L2s -- far dearer than the work.)  Writes dU2 (token-major,
-// high | low parts), dUt2 (its transpose) and Ut2 (U^T, high rows then low
-// rows).  Index math is 32-bit: validation bounds every index below 2^30.
+// high | low parts), dUt2 (dU^T rounded to bf16, rows of mp tokens; for a
+// group whose members share one dA reduction, the member's rows of the
+// stacked dU^T) and Ut2 (U^T rounded to bf16).  Index math is 32-bit:
+// validation bounds every index below 2^30.
 template <int RP, int TPW>
 __global__ __launch_bounds__(512) void lora_bwd_du_kernel(
     const u16* __restrict__ dY, const u16* __restrict__ B, const float* __restrict__ U,
     u16* __restrict__ dU2, u16* __restrict__ dUt2, u16* __restrict__ Ut2,
     int m, int n, int r, int mp, float s) {
   constexpr int FT = RP / 16;
+  constexpr int TG = TPW >= 16 ? TPW / 16 : 1;      // 16-token groups
   constexpr int NWV = 8;
   // Chunks per batch: deep batches pay off only for the short n runs of the
-  // 8-token workgroups; with 16 tokens, batches of one or two chunks keep
-  // more of them in flight across the loop (7B up_proj dU 29.8 -> 24.0 us).
-  constexpr int UNR = TPW == 8 ? (RP <= 16 ? 8 : (RP <= 32 ? 4 : 2)) : (RP <= 32 ? 2 : 1);
+  // 8-token workgroups; with 16 or more tokens, batches of one or two chunks
+  // keep more of them in flight across the loop (7B up_proj dU 29.8 -> 24.0 us).
+  constexpr int UNR = TPW == 8 ? (RP <= 16 ? 8 : (RP <= 32 ? 4 : 2)) : (RP <= 32 && TG == 1 ? 2 : 1);
   constexpr int SLOT = 32 * RP * 2;                 // bytes of one staged chunk of B
   constexpr int BL = RP / 16;                       // 16-byte B loads per lane per chunk (4r <= 4 RP)
-  static_assert(NWV * FT * 64 * 16 <= NWV * UNR * SLOT, "reduction fits the staging LDS");
-  __shared__ __attribute__((aligned(1024))) char sm[NWV * UNR * SLOT];
-  static_assert(TPW == 16 || TPW == 8, "tokens per workgroup");
+  constexpr int STAGE_BYTES = NWV * UNR * SLOT, RED_BYTES = NWV * TG * FT * 64 * 16;
+  __shared__ __attribute__((aligned(1024))) char sm[STAGE_BYTES > RED_BYTES ? STAGE_BYTES : RED_BYTES];
+  static_assert(TPW == 32 || TPW == 16 || TPW == 8, "tokens per workgroup");
+  static_assert(TG * FT <= NWV, "one wave per output fragment in the epilogue");
   const int i0 = blockIdx.x * TPW;
   const int tid = threadIdx.x, lane = tid & 63, wave = uniform(tid >> 6);
   const int g = lane >> 4, c16 = lane & 15;
@@ -85,23 +91,28 @@ __global__ __launch_bounds__(512) void lora_bwd_du_kernel(
 
   for (int e = lane; e < UNR * SLOT / 16; e += 64) reinterpret_cast<int4v*>(slots)[e] = int4v{0, 0, 0, 0};
 
-  floatx4 acc[FT];
+  floatx4 acc[TG][FT];
 #pragma unroll
-  for (int ft = 0; ft < FT; ++ft) acc[ft] = floatx4{0.f, 0.f, 0.f, 0.f};
+  for (int tg = 0; tg < TG; ++tg)
+#pragma unroll
+    for (int ft = 0; ft < FT; ++ft) acc[tg][ft] = floatx4{0.f, 0.f, 0.f, 0.f};
 
   const int nbch = 4 * r;                           // 16-byte chunks in 32 rows of B
   const bool fast = (r & 7) == 0;                   // a chunk then lies inside one row of B
   const float rinv = 1.0f / (float)r;
   // Batch b of this wave covers chunks j = 32 wave + 32 NWV (UNR b + u); the
   // loads of batch b+1 are in flight while batch b multiplies.
-  short8 yf[2][UNR];
+  short8 yf[2][UNR][TG];
   int4v bq[2][UNR][BL];
   auto load = [&](int bt, int p) LORA_INLINE {
 #pragma unroll
     for (int u = 0; u < UNR; ++u) {
       const int j = 32 * wave + 32 * NWV * (UNR * bt + u);
       const int jy = j + 8 * g;
-      yf[p][u] = __builtin_bit_cast(short8, buf_load16(rsY, jy < n ? (uint32_t)c16 * rowbytes + (uint32_t)jy * 2 : kOOB));
+#pragma unroll
+      for (int tg = 0; tg < TG; ++tg)
+        yf[p][u][tg] = __builtin_bit_cast(
+            short8, buf_load16(rsY, jy < n ? (uint32_t)(16 * tg + c16) * rowbytes + (uint32_t)jy * 2 : kOOB));
 #pragma unroll
       for (int v = 0; v < BL; ++v) {
         const int c = lane + 64 * v;
@@ -132,7 +143,11 @@ __global__ __launch_bounds__(512) void lora_bwd_du_kernel(
         }
       }
 #pragma unroll
-      for (int ft = 0; ft < FT; ++ft) acc[ft] = mfma16x16x32(tr16_read(slot, RP * 2, 16 * ft, lane), yf[p][u], acc[ft]);
+      for (int ft = 0; ft < FT; ++ft) {
+        const short8 bt = tr16_read(slot, RP * 2, 16 * ft, lane);
+#pragma unroll
+        for (int tg = 0; tg < TG; ++tg) acc[tg][ft] = mfma16x16x32(bt, yf[p][u][tg], acc[tg][ft]);
+      }
     }
   };
   const int nbt = uniform(32 * wave < n ? (n - 32 * wave + 32 * NWV * UNR - 1) / (32 * NWV * UNR) : 0);
@@ -145,27 +160,26 @@ __global__ __launch_bounds__(512) void lora_bwd_du_kernel(
     process(1);
   }
 
-  // U^T high/low split of this workgroup's tokens (tokens >= m are zero).
-  for (int e = tid; e < 2 * RP * TPW; e += 64 * NWV) {
-    const int tt = e / TPW, i = i0 + e % TPW;
-    const int t = tt < RP ? tt : tt - RP;
-    const float v = (i < m && t < r) ? U[(size_t)i * r + t] : 0.f;
-    const u16 h = f32_to_bf16(v);
-    Ut2[(size_t)tt * mp + i] = tt < RP ? h : f32_to_bf16(v - bf16_to_f32(h));
+  // U^T of this workgroup's tokens in bf16 (tokens >= m are zero).
+  for (int e = tid; e < RP * TPW; e += 64 * NWV) {
+    const int t = e / TPW, i = i0 + e % TPW;
+    Ut2[(size_t)t * mp + i] = f32_to_bf16((i < m && t < r) ? U[(size_t)i * r + t] : 0.f);
   }
 
   __syncthreads();
-  floatx4* red = reinterpret_cast<floatx4*>(sm);   // [NWV][FT][64]
+  floatx4* red = reinterpret_cast<floatx4*>(sm);   // [NWV][TG][FT][64]
 #pragma unroll
-  for (int ft = 0; ft < FT; ++ft) red[(wave * FT + ft) * 64 + lane] = acc[ft];
+  for (int tg = 0; tg < TG; ++tg)
+#pragma unroll
+    for (int ft = 0; ft < FT; ++ft) red[((wave * TG + tg) * FT + ft) * 64 + lane] = acc[tg][ft];
   __syncthreads();
-  if (wave >= FT) return;
-  const int ft = wave;  // one wave per 16-row fragment of dU^T
-  floatx4 v = red[ft * 64 + lane];
+  if (wave >= TG * FT) return;
+  const int tg = wave / FT, ft = wave - tg * FT;   // one wave per 16 x 16 fragment of dU^T
+  floatx4 v = red[(tg * FT + ft) * 64 + lane];
 #pragma unroll
-  for (int w = 1; w < NWV; ++w) v += red[(w * FT + ft) * 64 + lane];
-  if (c16 >= TPW) return;   // the zero token columns of TPW = 8
-  const int i = i0 + c16;  // < mp: the grid covers exactly mp tokens
+  for (int w = 1; w < NWV; ++w) v += red[((w * TG + tg) * FT + ft) * 64 + lane];
+  if (16 * tg + c16 >= TPW) return;   // the zero token columns of TPW = 8
+  const int i = i0 + 16 * tg + c16;   // < mp: the grid covers exactly mp tokens
   u16 hi[4], lo[4];
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
@@ -180,22 +194,20 @@ __global__ __launch_bounds__(512) void lora_bwd_du_kernel(
   *reinterpret_cast<uint2*>(row + RP + t) =
       uint2{(uint32_t)lo[0] | ((uint32_t)lo[1] << 16), (uint32_t)lo[2] | ((uint32_t)lo[3] << 16)};
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    dUt2[(size_t)(t + q) * mp + i] = hi[q];
-    dUt2[(size_t)(RP + t + q) * mp + i] = lo[q];
-  }
+  for (int q = 0; q < 4; ++q) dUt2[(size_t)(t + q) * mp + i] = hi[q];
 }
 
 // ---------------------------------------------------------------------------
 // Token reduction part[sp][t][c] = sum over the tokens i of split sp of
-// P[t][i] * Q[i][c], t < RP (the high rows t and low rows RP + t of P are
-// summed), for a tile of kRedCols = 128 columns.  One launch serves two such
-// problems (dB^T from Ut2 and dY, dA from dUt2 and X): workgroups [0, nb0)
-// take the first.
+// P[t][i] * Q[i][c], t < RP, for a tile of kRedCols = 128 columns.  P is the
+// rank-r operand rounded to bf16 (U^T or s dU^T, [RP][mp]); its rounding
+// error (relative 2^-9 per element) averages out in the sums to about 1e-3 of
+// dA and dB.  One launch serves two such problems (dB^T from Ut2 and dY, dA
+// from dUt2 and X): workgroups [0, nb0) take the first.
 //
 // The four waves of a workgroup take interleaved 32-token slices of the
 // split.  Each reads its P fragments straight from the token-contiguous P
-// ([2RP][mp]) into matrix-core A operands and stages its 32 x 128 slice of Q
+// into matrix-core A operands and stages its 32 x 128 slice of Q
 // ([m][cols]) in a private LDS region that it reads back transposed, so the
 // token loop has no barriers; the next slice is loaded while the current one
 // multiplies.  At the end the four waves' sums are added in wave order
@@ -214,11 +226,14 @@ template <int RP, bool KEEP>
 __global__ __launch_bounds__(256) void lora_tokred_kernel(RedProblem p0, RedProblem p1, int nb0, int m, int mp) {
   constexpr int CB = kRedCols;                // columns per workgroup
   constexpr int FC = CB / 16;                 // column fragments
-  constexpr int FH = RP / 16, FP = 2 * FH;    // high-part row fragments; low part follows
+  constexpr int FP = RP / 16;                 // row fragments
   constexpr int CPR = CB / 8;                 // 16-byte chunks per Q row
   constexpr int QL = 32 * CPR / 64;           // Q loads per lane per slice
   constexpr int REG = 32 * CB * 2;            // bytes of one staged Q slice
-  constexpr int FCP = 16 / FP > FC ? FC : (16 / FP > 0 ? 16 / FP : 1);   // fragments per reduction pass
+  // column fragments per reduction pass: the largest power of two dividing FC
+  // whose partial sums (4 waves x FP x FCP fragments) fit the staging LDS
+  constexpr int FCP = 16 / FP >= 8 ? 8 : (16 / FP >= 4 ? 4 : (16 / FP >= 2 ? 2 : 1));
+  static_assert(FC % FCP == 0, "reduction passes cover the column fragments");
   static_assert(CB == 128 && QL * 64 == 32 * CPR, "slice shape");
   static_assert(4 * FP * FCP * 64 * 16 <= 4 * 2 * REG, "reduction fits the staging LDS");
   __shared__ __attribute__((aligned(1024))) char smem[4 * 2 * REG];
@@ -236,7 +251,7 @@ __global__ __launch_bounds__(256) void lora_tokred_kernel(RedProblem p0, RedProb
   const int tid = threadIdx.x, lane = tid & 63, wave = uniform(tid >> 6);
   const int g = lane >> 4, c16 = lane & 15;
   const uint32_t qrow = (uint32_t)ncols * 2;
-  const __amdgpu_buffer_rsrc_t rsP = make_rsrc(P, (uint64_t)2 * RP * mp * 2);
+  const __amdgpu_buffer_rsrc_t rsP = make_rsrc(P, (uint64_t)RP * mp * 2);
   char* wreg = smem + wave * 2 * REG;
 
   floatx4 acc[FP][FC];
@@ -317,19 +332,17 @@ __global__ __launch_bounds__(256) void lora_tokred_kernel(RedProblem p0, RedProb
 #pragma unroll
     for (int f = 0; f < FP; ++f)
 #pragma unroll
-      for (int j = 0; j < FCP; ++j) red[((wave * FP + f) * FCP + j) * 64 + lane] = acc[f][f0 + j];
+      for (int q = 0; q < FCP; ++q) red[((wave * FP + f) * FCP + q) * 64 + lane] = acc[f][f0 + q];
     __syncthreads();
-    for (int e = wave; e < FH * FCP; e += 4) {
-      const int fh = e / FCP, j = e - fh * FCP;
-      floatx4 v = red[((0 * FP + fh) * FCP + j) * 64 + lane];
+    for (int e = wave; e < FP * FCP; e += 4) {
+      const int f = e / FCP, q = e - f * FCP;
+      floatx4 v = red[((0 * FP + f) * FCP + q) * 64 + lane];
 #pragma unroll
-      for (int w = 1; w < 4; ++w) v += red[((w * FP + fh) * FCP + j) * 64 + lane];
-#pragma unroll
-      for (int w = 0; w < 4; ++w) v += red[((w * FP + FH + fh) * FCP + j) * 64 + lane];
-      const int col = c0 + 16 * (f0 + j) + c16;
+      for (int w = 1; w < 4; ++w) v += red[((w * FP + f) * FCP + q) * 64 + lane];
+      const int col = c0 + 16 * (f0 + q) + c16;
       if (col < ncols) {
 #pragma unroll
-        for (int q = 0; q < 4; ++q) part[((size_t)sp * RP + 16 * fh + 4 * g + q) * ncols + col] = v[q];
+        for (int qq = 0; qq < 4; ++qq) part[((size_t)sp * RP + 16 * f + 4 * g + qq) * ncols + col] = v[qq];
       }
     }
   }
@@ -347,6 +360,7 @@ struct FinalizeArgs {
   int n, k, r, rp, sb, sa;
   float s;
   float sa_scale;   // 1, or 1 / (1 - p) with dropout (dA = dU^T keep X / (1 - p))
+  int rpa;          // rows of one split's dA partial block (rp, or a group's stacked rank)
 };
 
 // Sum of `count` partials spaced `step` floats apart, in index order; the
@@ -374,7 +388,7 @@ __device__ __forceinline__ void finalize_partials(const FinalizeArgs& f, int fir
     } else {
       const int g = e - nb;
       const int t = g / f.k, l = g - t * f.k;
-      f.dA[g] = f.sa_scale * sum_partials(f.pa + (size_t)t * f.k + l, (size_t)f.rp * f.k, f.sa);
+      f.dA[g] = f.sa_scale * sum_partials(f.pa + (size_t)t * f.k + l, (size_t)f.rpa * f.k, f.sa);
     }
   }
 }
@@ -1000,7 +1014,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_bwd_dx_kernel(
 //     token are added in wn order, s dU is split into bf16 high and low parts
 //     in LDS, and the rank-r term [dU_hi | dU_lo] [A; A] is added to the dX
 //     tile.  The workgroups of column tile 0 also store the parts transposed
-//     (dUt2 [32][mp]) for the dA reduction.
+//     (dUt2 [16][mp], the bf16 high part) for the dA reduction.
 //   dB^T partials: at the stages st with st % tiles_n == tn, four waves (the
 //     lower or upper four, alternately) each form U^T dY for 16 of the stage's
 //     64 n over the tile's 128 tokens, with U^T as high and low bf16 parts
@@ -1247,10 +1261,7 @@ __global__ __launch_bounds__(512) void lora_bwd_dxf_kernel(
     const u16 hi = f32_to_bf16(d), lo = f32_to_bf16(d - bf16_to_f32(hi));
     Us2[i * UP + t] = hi;
     Us2[i * UP + RP + t] = lo;
-    if (tn == 0 && m0 + i < mp) {
-      dUt2[(size_t)t * mp + m0 + i] = hi;
-      dUt2[(size_t)(RP + t) * mp + m0 + i] = lo;
-    }
+    if (tn == 0 && m0 + i < mp) dUt2[(size_t)t * mp + m0 + i] = hi;
   }
   __syncthreads();
 #pragma unroll
@@ -1319,12 +1330,15 @@ static hipError_t run_dx(const Launch& L, const BwdArgs& a, const u16* dU2, int 
   });
 }
 
-static hipError_t run_du(const Launch& L, const BwdArgs& a, const BwdLayout& BL, hipStream_t st) {
+// dUt2: where dU^T goes (the projection's own region, or its rows of a
+// group's stacked region).
+static hipError_t run_du(const Launch& L, const BwdArgs& a, const BwdLayout& BL, hipStream_t st,
+                         u16* dUt2 = nullptr) {
   u16* Ut2 = reinterpret_cast<u16*>(a.ws + BL.ut2);
   u16* dU2 = reinterpret_cast<u16*>(a.ws + BL.du2);
-  u16* dUt2 = reinterpret_cast<u16*>(a.ws + BL.dut2);
+  if (!dUt2) dUt2 = reinterpret_cast<u16*>(a.ws + BL.dut2);
   return with_int<16, 32, 48, 64>(L.rp, [&](auto rc) {
-    return with_int<8, 16>(L.tpw, [&](auto tc) {
+    return with_int<8, 16, 32>(L.tpw, [&](auto tc) {
       hipLaunchKernelGGL((lora_bwd_du_kernel<decltype(rc)::value, decltype(tc)::value>), dim3((unsigned)L.grid),
                          dim3((unsigned)L.block), 0, st, a.dY, a.B, a.U, dU2, dUt2, Ut2, (int)a.m, (int)a.n, (int)a.r,
                          (int)BL.mp, a.s);
@@ -1335,14 +1349,19 @@ static hipError_t run_du(const Launch& L, const BwdArgs& a, const BwdLayout& BL,
 
 // The two token reductions of one projection in one launch: dB^T partials =
 // Ut2 . dY, then dA partials = dUt2 . X (masked X under dropout).
-static hipError_t run_tokred(const Launch& L, const BwdArgs& a, const BwdLayout& BL, hipStream_t st) {
+// L.part: 0 both reductions, 1 dB only (a group member whose dA is reduced
+// with the group's), 2 the group's stacked dA (pap given by the caller).
+static hipError_t run_tokred(const Launch& L, const BwdArgs& a, const BwdLayout& BL, hipStream_t st,
+                             const RedProblem* stacked = nullptr) {
   const u16* Ut2 = reinterpret_cast<const u16*>(a.ws + BL.ut2);
   const u16* dUt2 = reinterpret_cast<const u16*>(a.ws + BL.dut2);
   float* pb = reinterpret_cast<float*>(a.ws + BL.pb);
   float* pa = reinterpret_cast<float*>(a.ws + BL.pa);
-  const RedProblem pbp{Ut2, a.dY, pb, (int)a.n, (int)BL.plan_b.span, BL.plan_b.col_tiles, nullptr};
-  const RedProblem pap{dUt2, a.X, pa, (int)a.k, (int)BL.plan_a.span, BL.plan_a.col_tiles, a.keep};
-  const int nb0 = BL.plan_b.col_tiles * BL.plan_b.splits;
+  const RedProblem pbp0{Ut2, a.dY, pb, (int)a.n, (int)BL.plan_b.span, BL.plan_b.col_tiles, nullptr};
+  const RedProblem pap0{dUt2, a.X, pa, (int)a.k, (int)BL.plan_a.span, BL.plan_a.col_tiles, a.keep};
+  const RedProblem pbp = L.part == 2 ? *stacked : pbp0;
+  const RedProblem pap = L.part == 0 ? pap0 : pbp;
+  const int nb0 = L.part == 0 ? BL.plan_b.col_tiles * BL.plan_b.splits : (int)L.grid;
   return with_int<16, 32, 48, 64>(L.rp, [&](auto rc) {
     return with_bool(L.drop, [&](auto kc) {
       hipLaunchKernelGGL((lora_tokred_kernel<decltype(rc)::value, decltype(kc)::value>), dim3((unsigned)L.grid),
@@ -1355,7 +1374,7 @@ static hipError_t run_tokred(const Launch& L, const BwdArgs& a, const BwdLayout&
 static FinalizeArgs finalize_args(const BwdArgs& a, const BwdLayout& L) {
   return FinalizeArgs{reinterpret_cast<const float*>(a.ws + L.pb), reinterpret_cast<const float*>(a.ws + L.pa),
                       a.dB, a.dA, (int)a.n, (int)a.k, (int)a.r, L.rp, L.plan_b.splits, L.plan_a.splits, a.s,
-                      a.keep ? a.inv_keep : 1.0f};
+                      a.keep ? a.inv_keep : 1.0f, L.rp};
 }
 
 hipError_t launch_bwd(const BwdArgs& a, hipStream_t st) {
@@ -1410,7 +1429,7 @@ hipError_t launch_bwd_fused(const BwdArgs& a, hipStream_t st) {
       const hipError_t e = hipGetLastError();
       if (e != hipSuccess) return e;
     } else if (L.id == K_FINALIZE) {
-      const FinalizeArgs fin{pb, pa, a.dB, a.dA, n, k, r, 16, BL.tiles_m, BL.plan_a.splits, a.s, 1.0f};
+      const FinalizeArgs fin{pb, pa, a.dB, a.dA, n, k, r, 16, BL.tiles_m, BL.plan_a.splits, a.s, 1.0f, 16};
       hipLaunchKernelGGL(lora_finalize_kernel, grid, block, 0, st, fin);
       const hipError_t e = hipGetLastError();
       if (e != hipSuccess) return e;
@@ -1482,6 +1501,9 @@ hipError_t launch_bwd_group(const GroupBwdArgs& a, hipStream_t st) {
   }
   const GroupBwdLayout GL = group_bwd_layout(a.count, a.n, a.m, a.k, a.r);
   const Plan p = plan_group_bwd(a.count, a.n, a.m, a.k, a.r);
+  const int rp = GL.L[0].rp;
+  u16* dut_stack = GL.stacked ? reinterpret_cast<u16*>(a.ws + GL.dut_stack) : nullptr;
+  float* pa_stack = GL.stacked ? reinterpret_cast<float*>(a.ws + GL.pa_stack) : nullptr;
   DxGroup grp{};
   int nkb = 0;
   for (int g = 0; g < a.count; ++g) {
@@ -1493,6 +1515,11 @@ hipError_t launch_bwd_group(const GroupBwdArgs& a, hipStream_t st) {
     grp.n[g] = (int)a.n[g];
     nkb += (int)((a.n[g] + 63) / 64);
     grp.fin[g] = finalize_args(b, GL.L[g]);
+    if (GL.stacked) {   // member g's dA rows of the stacked reduction
+      grp.fin[g].pa = pa_stack + (size_t)g * rp * a.k;
+      grp.fin[g].rpa = GL.rpt;
+      grp.fin[g].sa = GL.plan_a.splits;
+    }
   }
   grp.count = a.count;
   grp.nkb = nkb;
@@ -1504,9 +1531,21 @@ hipError_t launch_bwd_group(const GroupBwdArgs& a, hipStream_t st) {
   for (int i = 0; i < p.count; ++i) {
     const Launch& L = p.l[i];
     hipError_t e = hipErrorInvalidValue;
-    if (L.id == K_DU || L.id == K_TOKRED) {
+    if (L.id == K_TOKRED && L.part == 2) {   // the stacked dA reduction over X
+      const RedProblem pap{dut_stack, a.X, pa_stack, (int)a.k, (int)GL.plan_a.span, GL.plan_a.col_tiles, nullptr};
+      const BwdArgs b = member_args(0, GL);
+      e = with_int<32, 48, 64>(L.rp, [&](auto rc) {
+        hipLaunchKernelGGL((lora_tokred_kernel<decltype(rc)::value, false>), dim3((unsigned)L.grid),
+                           dim3((unsigned)L.block), 0, st, pap, pap, (int)L.grid, (int)b.m, (int)GL.L[0].mp);
+        return hipGetLastError();
+      });
+    } else if (L.id == K_DU) {
       const BwdArgs b = member_args(L.member, GL);
-      e = L.id == K_DU ? run_du(L, b, GL.L[L.member], st) : run_tokred(L, b, GL.L[L.member], st);
+      e = GL.stacked ? run_du(L, b, GL.L[L.member], st, dut_stack + (size_t)L.member * rp * GL.L[0].mp)
+                     : run_du(L, b, GL.L[L.member], st);
+    } else if (L.id == K_TOKRED) {
+      const BwdArgs b = member_args(L.member, GL);
+      e = run_tokred(L, b, GL.L[L.member], st);
     } else if (L.id == K_DX) {
       e = run_dx(L, d, nullptr, (int)GL.L[0].mp, FinalizeArgs{}, L.finalize ? grp : rest, st);
     }

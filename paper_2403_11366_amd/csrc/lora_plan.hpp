@@ -39,6 +39,7 @@ struct Launch {
   int block;                   // threads per workgroup
   bool finalize;               // dX: the workgroups' tails finalize dA and dB
   int member;                  // grouped calls: the projection a per-member launch serves
+  int part;                    // token reductions: 0 dB and dA, 1 dB only, 2 a group's stacked dA
 };
 
 constexpr int kMaxLaunches = 4 + 2 * kMaxGroup;
@@ -173,20 +174,27 @@ inline void plan_dx_part(Plan& p, GemmTile t, int64_t m, int rp, int64_t cb, int
 inline Launch du_launch(const BwdLayout& L, int member) {
   Launch x = blank_launch(K_DU);
   x.rp = L.rp;
-  x.tpw = L.mp / 16 < 256 ? 8 : 16;   // fewer 16-token workgroups than compute units: 8 tokens each
+  // the most tokens per workgroup (each reads all of B) that still leaves no
+  // compute unit idle; 32 tokens from padded rank 32 on, where B is at least
+  // as many bytes per workgroup as 16 tokens of dY
+  x.tpw = L.mp / 16 < 256 ? 8 : (L.rp >= 32 && L.mp / 32 >= 256 ? 32 : 16);
   x.grid = L.mp / x.tpw;
   x.block = 512;
   x.member = member;
   return x;
 }
 
-inline Launch tokred_launch(const BwdLayout& L, bool keep, int member) {
+// Token reductions run four waves per workgroup.
+inline int tokred_threads(int) { return 256; }
+
+inline Launch tokred_launch(const BwdLayout& L, bool keep, int member, int part = 0) {
   Launch x = blank_launch(K_TOKRED);
   x.rp = L.rp;
   x.drop = keep;
-  x.grid = (int64_t)L.plan_b.col_tiles * L.plan_b.splits + (int64_t)L.plan_a.col_tiles * L.plan_a.splits;
-  x.block = 256;
+  x.grid = (int64_t)L.plan_b.col_tiles * L.plan_b.splits + (part == 0 ? (int64_t)L.plan_a.col_tiles * L.plan_a.splits : 0);
+  x.block = tokred_threads(x.rp);
   x.member = member;
+  x.part = part;
   return x;
 }
 
@@ -211,19 +219,30 @@ inline Plan plan_bwd(int64_t m, int64_t n, int64_t k, int64_t r, bool drop) {
 }
 
 // lora_linear_group_bwd: per member dU and the token reductions, then one dX
-// launch over the concatenated contraction (split like the single one).
+// launch over the concatenated contraction (split like the single one).  For
+// groups of three or more whose padded ranks add up to at most 64 the dA
+// reductions of all members run as one (a stacked rank over one pass of X)
+// after the members' dB reductions.
 inline Plan plan_group_bwd(int count, const int64_t* n, int64_t m, int64_t k, int64_t r) {
   if (count == 1) return plan_bwd(m, n[0], k, r, false);
+  const GroupBwdLayout G = group_bwd_layout(count, n, m, k, r);
   Plan p;
   bool n_whole = true;
-  int rp = 16;
   for (int g = 0; g < count; ++g) {
-    const BwdLayout L = bwd_layout(m, n[g], k, r);
-    rp = L.rp;
-    p.add(du_launch(L, g));
-    p.add(tokred_launch(L, false, g));
+    p.add(du_launch(G.L[g], g));
+    p.add(tokred_launch(G.L[g], false, g, G.stacked ? 1 : 0));
     n_whole = n_whole && n[g] % 64 == 0;
   }
+  if (G.stacked) {
+    Launch x = blank_launch(K_TOKRED);
+    x.rp = G.rpt;
+    x.grid = (int64_t)G.plan_a.col_tiles * G.plan_a.splits;
+    x.block = tokred_threads(x.rp);
+    x.member = -1;
+    x.part = 2;
+    p.add(x);
+  }
+  const int rp = G.L[0].rp;
   const GemmSplit s = plan_gemm_split(m, k);
   plan_dx_part(p, s.t1, m, rp, 0, s.n1, n_whole, false, true, true);
   if (s.n1 < k) plan_dx_part(p, s.t2, m, rp, s.n1, k, n_whole, false, true, false);
@@ -243,7 +262,7 @@ inline Plan plan_bwd_fused(int64_t m, int64_t n, int64_t k, int64_t r) {
   Launch t = blank_launch(K_TOKRED);
   t.rp = 16;
   t.grid = (int64_t)L.plan_a.col_tiles * L.plan_a.splits;
-  t.block = 256;
+  t.block = tokred_threads(t.rp);
   p.add(t);
   Launch f = blank_launch(K_FINALIZE);
   const int64_t total = n * r + r * k;

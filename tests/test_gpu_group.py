@@ -3,9 +3,12 @@ q, k, v) through the C ABI against the fp64 oracle's grouped forward and
 backward (per projection Y_g, U_g, dA_g, dB_g; the summed dX).
 
 Tolerances are those of the single projection (Y, dX 5e-3; dA, dB 1e-2; U
-1e-5).  Edge cases: a group of one (bit-identical to the plain entry points), ragged widths per projection, every padded rank, the largest
-group (8), integer inputs (bit for bit), and the 13B layer's q/k/v and
-gate/up groups at full size with sampled dX rows.
+1e-5).  Edge cases: a group of one (bit-identical to the plain entry points),
+ragged widths per projection, every padded rank, the largest group (8),
+groups whose dA reductions run as one pass over X (padded ranks adding up to
+at most 64) and groups that keep one per member, integer inputs (bit for
+bit), and the 13B layer's q/k/v and gate/up groups and the 7B q/k/v group at
+full size with sampled dX rows.
 """
 import numpy as np
 import pytest
@@ -72,6 +75,7 @@ CASES = [  # (ns, m, k, r, alpha)
     ([1368, 1368, 1360], 2000, 1024, 8, 16.0),    # the k-split forward tile, ragged members
     ([264, 392], 2000, 5120, 8, 16.0),             # 2.5 rounds of 128x256 dX tiles
     ([264, 392], 4096, 4096, 8, 16.0),             # the 256x256 dX tile for a group
+    ([264, 520, 136, 72], 300, 448, 13, 26.0),     # four members share one dA reduction (stacked rank 64)
 ]
 
 
@@ -96,10 +100,14 @@ def test_group_of_one_matches_plain():
 
 # (m, k, ns, r): the last plans the grouped 128 x 256 dX that copies its
 # stages straight into LDS (every n a multiple of 64, whole column tiles)
-EXACT_CASES = [(264, 1024, [512, 1024, 256], 8), (4096, 5120, [256, 512], 8), (2000, 2304, [256, 512, 192], 8)]
+# (the first and third take the one dA reduction of the whole group at
+# stacked rank 48, the fourth at stacked rank 64, four members of rank 16)
+EXACT_CASES = [(264, 1024, [512, 1024, 256], 8), (4096, 5120, [256, 512], 8), (2000, 2304, [256, 512, 192], 8),
+               (1000, 1032, [256, 136, 384, 520], 16)]
 
 
-@pytest.mark.parametrize("m,k,ns,r", EXACT_CASES, ids=["m264k1024", "m4096k5120-dx-split", "m2000k2304-dx128x256"])
+@pytest.mark.parametrize("m,k,ns,r", EXACT_CASES,
+                         ids=["m264k1024", "m4096k5120-dx-split", "m2000k2304-dx128x256", "m1000k1032-G4r16"])
 def test_group_integer_exact(m, k, ns, r):
     """Sparse {-1, 0, 1} inputs and s = 2: every sum is a small integer, so
     the GPU matches the oracle bit for bit whatever the summation order."""

@@ -88,6 +88,8 @@ EXACT = [
     Shape("exact", 4096, 512, 11008, 8, 16.0, 205),
     Shape("exact", 4096, 5120, 256, 8, 16.0, 206),       # forward columns split: 256x256, then 128x128
     Shape("exact", 4096, 5120, 256, 40, 80.0, 207),      # the same with U from its own pass
+    Shape("exact", 8192, 512, 1024, 64, 128.0, 208),     # dU with 32 tokens per workgroup
+    Shape("exact", 8200, 520, 1032, 40, 80.0, 209),      # the same at padded rank 48, ragged tokens
 ]
 
 # dX plans at the edges of the tile choice: n not a multiple of 64 where the

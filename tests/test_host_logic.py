@@ -116,3 +116,19 @@ def test_plan_refuses_what_the_entry_point_refuses(lora):
 def test_ragged_shapes_have_tails():
     assert any(s.m % 64 for s in RAGGED) and any(s.k % 64 for s in RAGGED)
     assert any(s.n % 64 for s in RAGGED) and {1, 64} <= {s.r for s in RAGGED}
+
+
+def test_group_da_reductions_share_one_pass_over_x(lora):
+    """Groups of three or more whose padded ranks add up to at most 64 share
+    one dA token reduction (a stacked rank) after their own dB reductions;
+    pairs and larger ranks keep one dA reduction per member."""
+    plan = lora.lora_linear_plan("group_bwd", 4096, [5120] * 3, 5120, 8)     # 13B q, k, v
+    red = [x for x in plan if "tokred" in x["kernel"]]
+    assert [x["member"] for x in red] == [0, 1, 2, -1]
+    assert red[-1]["kernel"] == "lora::lora_tokred_kernel<48, false>"
+    plan = lora.lora_linear_plan("group_bwd", 264, [392, 128, 520], 448, 64)  # 3 x 64 > 64: per member
+    assert [x["member"] for x in plan if "tokred" in x["kernel"]] == [0, 1, 2]
+    for ns, m, k, r, _ in GROUP_CASES:
+        stacked = len(ns) >= 3 and len(ns) * (-(-r // 16) * 16) <= 64
+        members = [x["member"] for x in lora.lora_linear_plan("group_bwd", m, ns, k, r) if "tokred" in x["kernel"]]
+        assert (members[-1] == -1) == stacked, (ns, r, members)
