@@ -11,7 +11,9 @@ successive steps rotate over several copies so every step reads from HBM.
 
 Prints one JSON line: whole-job TFLOP/s (algorithmic flops 4mnk + 6mr(n+k) per
 projection), the fraction of the bf16 dense matrix-core peak, per-projection
-forward and backward call times, the host's enqueue time per step, a roofline
+forward and backward call times, the host's enqueue time per step (one step
+into an idle stream; and over the timed loop, where a full launch queue makes
+it follow the GPU time), a roofline
 entry for the dominant kernel (the forward call of the projection with the
 most forward flops, timed live with HIP events on its stream; its kernels come
 from the library's own launch plan) and the fp64 CPU oracle's throughput on
@@ -164,7 +166,7 @@ def algorithmic_units(s, launch):
         return "byte", 2 * m * k + 2 * r * k + 4 * m * r
     if "lora_bwd_du_kernel" in name:
         return "byte", 2 * m * n + 2 * n * r + 4 * m * r
-    if "lora_tokred_kernel" in name:
+    if "lora_tokred_kernel" in name or "lora_tokred_dma_kernel" in name:
         return "byte", (2 * m * n + 4 * m * r + 4 * n * r) + (2 * m * k + 4 * m * r + 4 * r * k)
     return None, None
 
@@ -610,6 +612,18 @@ def main():
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
+    # host cost of enqueueing one step into an idle stream (the launches
+    # return before the GPU work ends): median over 10 steps, each begun after
+    # a synchronisation, so a full launch queue cannot hold the host back
+    host_us = []
+    for i in range(10):
+        torch.cuda.synchronize()
+        t_h = time.perf_counter()
+        step(i)
+        host_us.append((time.perf_counter() - t_h) * 1e6)
+    torch.cuda.synchronize()
+    host_us.sort()
+    enqueue_idle_us = host_us[len(host_us) // 2]
     log(f"[bench] warmup {args.warmup} steps done; timing {args.steps} steps")
     # HIP events split the timed steps into 5 repetitions (recorded on the
     # stream, no synchronisation inside the timed region); the host clock also
@@ -704,7 +718,8 @@ def main():
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                      "traffic": traffic, "flops_per_launch": k1_flops, "avg_launch_us": round(fwd_us, 2)},
         "per_projection": per_shape,
-        "host_enqueue_us_per_step": round(enqueue_us, 2),
+        "host_enqueue_us_per_step": round(enqueue_idle_us, 2),
+        "host_enqueue_timed_us_per_step": round(enqueue_us, 2),
         "repetitions": {"count": nrep, "ms_per_step": [round(x, 4) for x in rep_ms],
                         "median": round(sorted(rep_ms)[nrep // 2], 4),
                         "std": round((sum((x - sum(rep_ms) / nrep) ** 2 for x in rep_ms) / nrep) ** 0.5, 4)},

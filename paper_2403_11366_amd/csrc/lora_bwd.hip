@@ -220,8 +220,9 @@ struct RedProblem {
   const uint8_t* keep;   // dropout keep bits of Q ([m][ncols/8]) or null: masked Q elements count as 0
 };
 
-// KEEP instantiates the masked-Q path (LoRA dropout); without it the keep
-// pointers are ignored and the kernel carries none of the mask registers.
+// Launched with KEEP, for the masked-Q path of LoRA dropout: the mask is
+// applied to the Q chunks in registers before they are staged.  Without a
+// mask the launch takes lora_tokred_dma_kernel below.
 template <int RP, bool KEEP>
 __global__ __launch_bounds__(256) void lora_tokred_kernel(RedProblem p0, RedProblem p1, int nb0, int m, int mp) {
   constexpr int CB = kRedCols;                // columns per workgroup
@@ -344,6 +345,201 @@ __global__ __launch_bounds__(256) void lora_tokred_kernel(RedProblem p0, RedProb
 #pragma unroll
         for (int qq = 0; qq < 4; ++qq) part[((size_t)sp * RP + 16 * f + 4 * g + qq) * ncols + col] = v[qq];
       }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// The same token reduction without a keep mask, fed by copies straight into
+// LDS.  Stages of 64 tokens: the stage's P block (RP rows x 64 tokens, 128
+// bytes a row, kc_offset swizzle) and Q block (64 tokens x 128 columns, 256
+// bytes a row, mc16_offset swizzle) are copied from global memory into a ring
+// of NS LDS stages, NS - 1 stages ahead, in whole row pieces (8 rows of P or 4
+// rows of Q per copy instruction; the swizzles applied to the global
+// addresses), one barrier per stage.  (Register loads of 16 rows x 64 bytes
+// per instruction kept the L1 busy translating addresses.)  The four waves
+// split the columns, two 16-column fragments each, over all tokens of the
+// split, so no cross-wave sum is needed.  The fragment reads are issued as
+// inline assembly with explicit lgkmcnt waits: the compiler would otherwise
+// wait for every copy still in flight before each transposing read of Q.
+// At most 80 KB of LDS, so two workgroups share a compute unit.
+template <int RP>
+__global__ __launch_bounds__(256) void lora_tokred_dma_kernel(RedProblem p0, RedProblem p1, int nb0, int m,
+                                                              int mp) {
+  constexpr int CB = kRedCols, NWV = 4, TS = 64;
+  constexpr int FP = RP / 16;
+  constexpr int PB = RP * 128;                // P block bytes
+  constexpr int QB = TS * CB * 2;             // Q block bytes
+  constexpr int STAGE = PB + QB;
+  constexpr int NS = (80 * 1024) / STAGE;     // ring stages
+  constexpr int NP = RP / 8, NQ = TS / 4;     // 1 KB copies per stage: P rows / 8, Q rows / 4
+  constexpr int QPW = NQ / NWV;               // Q copies per wave
+  constexpr int NRD = FP + 4;                 // LDS reads per wave and substep
+  static_assert(CB == 128 && NQ % NWV == 0 && NS >= 3, "stage shape");
+  static_assert((NS - 2) * (NP / NWV + 1 + QPW) < 64, "copies in flight fit the wait counter");
+  __shared__ __attribute__((aligned(1024))) char smem[NS * STAGE];
+
+  const bool first = (int)blockIdx.x < nb0;
+  const RedProblem& pr = first ? p0 : p1;
+  const int bid = first ? (int)blockIdx.x : (int)blockIdx.x - nb0;
+  const u16* __restrict__ P = pr.P;
+  const u16* __restrict__ Q = pr.Q;
+  const int ncols = pr.ncols;
+  const int c0 = (bid % pr.col_tiles) * CB;
+  const int sp = bid / pr.col_tiles;
+  const int tb = sp * pr.span;
+  const int te = min(mp, tb + pr.span);       // te - tb is a multiple of 64
+  const int nst = (te - tb) / TS;
+  const int tid = threadIdx.x, lane = tid & 63, wave = uniform(tid >> 6);
+  const int g = lane >> 4, c16 = lane & 15;
+  const uint32_t qrow = (uint32_t)ncols * 2;
+  const __amdgpu_buffer_rsrc_t rsP = make_rsrc(P, (uint64_t)RP * mp * 2);
+
+  // Copies of stage st into buffer buf.  P copy j (j = wave mod 4): rows
+  // 8j + lane/8 at physical chunk lane%8; Q copy j = wave + 4i: rows
+  // 4j + lane/16 at physical chunk lane%16.  Each position holds the logical
+  // chunk given by the swizzle.  Tokens at or past m, columns past ncols and
+  // stages past the split read zero.
+  int pcol[NP / NWV + 1];
+  uint32_t qoff[QPW];
+  int qcol[QPW];
+#pragma unroll
+  for (int i = 0; i * NWV < NP; ++i) {
+    const int row = 8 * (wave + NWV * i) + (lane >> 3);
+    pcol[i] = 8 * ((lane & 7) ^ kc_swz(row));
+  }
+#pragma unroll
+  for (int i = 0; i < QPW; ++i) {
+    const int row = 4 * (wave + NWV * i) + (lane >> 4);
+    const int c = (lane & 15) ^ mc16_swz(row);
+    qcol[i] = c0 + 8 * c;
+    qoff[i] = (uint32_t)row * qrow + (uint32_t)qcol[i] * 2;
+  }
+  auto issue = [&](int st, int buf) LORA_INLINE {
+    const int ts = tb + TS * st;
+    const bool live = st < nst;
+    char* sb = smem + buf * STAGE;
+#pragma unroll
+    for (int i = 0; i * NWV < NP; ++i) {
+      const int j = wave + NWV * i;
+      if (j < NP) {   // wave-uniform
+        const int row = 8 * j + (lane >> 3);
+        dma16(rsP, live ? ((uint32_t)row * (uint32_t)mp + (uint32_t)(ts + pcol[i])) * 2 : kOOB, 0, sb + j * 1024);
+      }
+    }
+    const int rows = uniform(live ? max(0, min(TS, m - ts)) : 0);
+    const __amdgpu_buffer_rsrc_t rsQ = make_rsrc(Q + (size_t)ts * ncols, (uint64_t)rows * qrow);
+#pragma unroll
+    for (int i = 0; i < QPW; ++i)
+      dma16(rsQ, qcol[i] < ncols ? qoff[i] : kOOB, 0, sb + PB + (wave + NWV * i) * 1024);
+  };
+  auto stage_barrier = [&]() LORA_INLINE {   // this wave's copies of the stage waited for: NS - 2 stages stay in flight
+    if (wave < NP % NWV) copy_barrier<(NS - 2) * (NP / NWV + 1 + QPW)>();
+    else copy_barrier<(NS - 2) * (NP / NWV + QPW)>();
+  };
+
+  // Lane addresses in buffer 0.  P fragment f (A operand, 16 rank rows x 32
+  // tokens) of substep kk: row 16 f + c16, chunk 4 kk + g (f adds 2048 bytes;
+  // the swizzle of kk depends on the lane).  Q fragment j of this wave
+  // (column tile 2 wave + j; B operand, 32 tokens x 16 columns) as in
+  // mc16_read_tr: two transposing reads 4 rows apart (+1024 bytes), substep kk
+  // 32 rows further (+8192 bytes).
+  uint32_t pa[2], qa[2];
+#pragma unroll
+  for (int kk = 0; kk < 2; ++kk) pa[kk] = lds_addr(smem + kc_offset(c16, 4 * kk + g));
+  {
+    const int j = lane & 15, e = j >> 2, q = j & 3;
+#pragma unroll
+    for (int jf = 0; jf < 2; ++jf) {
+      const int col = 16 * (2 * wave + jf) + 4 * q;
+      qa[jf] = lds_addr(smem + PB + mc16_offset<CB>(8 * g + e, col >> 3) + (col & 7) * 2);
+    }
+  }
+  floatx4 acc[FP][2];
+#pragma unroll
+  for (int f = 0; f < FP; ++f) acc[f][0] = acc[f][1] = floatx4{0.f, 0.f, 0.f, 0.f};
+  short8 fp[2][FP];
+  short4v fql[2][2], fqh[2][2];
+  auto reads = [&](uint32_t boff, int kk) LORA_INLINE {
+    const uint32_t a = pa[kk] + boff;
+    ds_read_b128_asm<0>(fp[kk][0], a);
+    if constexpr (FP > 1) ds_read_b128_asm<2048>(fp[kk][1], a);
+    if constexpr (FP > 2) ds_read_b128_asm<4096>(fp[kk][2], a);
+    if constexpr (FP > 3) ds_read_b128_asm<6144>(fp[kk][3], a);
+#pragma unroll
+    for (int jf = 0; jf < 2; ++jf) {
+      const uint32_t b = qa[jf] + boff;
+      if (kk == 0) {
+        ds_read_tr_b64_asm<0>(fql[kk][jf], b);
+        ds_read_tr_b64_asm<1024>(fqh[kk][jf], b);
+      } else {
+        ds_read_tr_b64_asm<8192>(fql[kk][jf], b);
+        ds_read_tr_b64_asm<9216>(fqh[kk][jf], b);
+      }
+    }
+  };
+  static_assert(FP <= 4, "rank rows per stage");
+  auto mult = [&](int kk) LORA_INLINE {
+#pragma unroll
+    for (int jf = 0; jf < 2; ++jf) {
+      const short8 qf = join4(fql[kk][jf], fqh[kk][jf]);
+#pragma unroll
+      for (int f = 0; f < FP; ++f) acc[f][jf] = mfma16x16x32(fp[kk][f], qf, acc[f][jf]);
+    }
+  };
+  auto compute = [&](int buf) LORA_INLINE {
+    const uint32_t boff = (uint32_t)buf * STAGE;
+    reads(boff, 0);
+    reads(boff, 1);
+    // substep 0 once only the NRD reads of substep 1 are outstanding
+    if constexpr (FP == 1)
+      asm volatile("s_waitcnt lgkmcnt(5)" : "+v"(fp[0][0]), "+v"(fql[0][0]), "+v"(fqh[0][0]), "+v"(fql[0][1]),
+                   "+v"(fqh[0][1]));
+    else if constexpr (FP == 2)
+      asm volatile("s_waitcnt lgkmcnt(6)" : "+v"(fp[0][0]), "+v"(fp[0][1]), "+v"(fql[0][0]), "+v"(fqh[0][0]),
+                   "+v"(fql[0][1]), "+v"(fqh[0][1]));
+    else if constexpr (FP == 3)
+      asm volatile("s_waitcnt lgkmcnt(7)" : "+v"(fp[0][0]), "+v"(fp[0][1]), "+v"(fp[0][2]), "+v"(fql[0][0]),
+                   "+v"(fqh[0][0]), "+v"(fql[0][1]), "+v"(fqh[0][1]));
+    else
+      asm volatile("s_waitcnt lgkmcnt(8)" : "+v"(fp[0][0]), "+v"(fp[0][1]), "+v"(fp[0][2]), "+v"(fp[0][3]),
+                   "+v"(fql[0][0]), "+v"(fqh[0][0]), "+v"(fql[0][1]), "+v"(fqh[0][1]));
+    static_assert(NRD == FP + 4, "wait counts above");
+    mult(0);
+    if constexpr (FP == 1)
+      asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(fp[1][0]), "+v"(fql[1][0]), "+v"(fqh[1][0]), "+v"(fql[1][1]),
+                   "+v"(fqh[1][1]));
+    else if constexpr (FP == 2)
+      asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(fp[1][0]), "+v"(fp[1][1]), "+v"(fql[1][0]), "+v"(fqh[1][0]),
+                   "+v"(fql[1][1]), "+v"(fqh[1][1]));
+    else if constexpr (FP == 3)
+      asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(fp[1][0]), "+v"(fp[1][1]), "+v"(fp[1][2]), "+v"(fql[1][0]),
+                   "+v"(fqh[1][0]), "+v"(fql[1][1]), "+v"(fqh[1][1]));
+    else
+      asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(fp[1][0]), "+v"(fp[1][1]), "+v"(fp[1][2]), "+v"(fp[1][3]),
+                   "+v"(fql[1][0]), "+v"(fqh[1][0]), "+v"(fql[1][1]), "+v"(fqh[1][1]));
+    mult(1);
+  };
+
+#pragma unroll
+  for (int st = 0; st < NS - 1; ++st) issue(st, st);
+  for (int st = 0; st < nst; ++st) {
+    stage_barrier();   // stage st has landed; every wave is done with stage st - 1
+    issue(st + NS - 1, (st + NS - 1) % NS);
+    compute(st % NS);
+  }
+  copy_barrier<0>();   // the trailing copies land before the workgroup ends
+
+  // lane of (f, jf): rank rows 16 f + 4 g .. +3 of column c0 + 16 (2 wave + jf) + c16
+  float* part = pr.part;
+#pragma unroll
+  for (int jf = 0; jf < 2; ++jf) {
+    const int col = c0 + 16 * (2 * wave + jf) + c16;
+    if (col < ncols) {
+#pragma unroll
+      for (int f = 0; f < FP; ++f)
+#pragma unroll
+        for (int qq = 0; qq < 4; ++qq) part[((size_t)sp * RP + 16 * f + 4 * g + qq) * ncols + col] = acc[f][jf][qq];
     }
   }
 }
@@ -1363,11 +1559,14 @@ static hipError_t run_tokred(const Launch& L, const BwdArgs& a, const BwdLayout&
   const RedProblem pap = L.part == 0 ? pap0 : pbp;
   const int nb0 = L.part == 0 ? BL.plan_b.col_tiles * BL.plan_b.splits : (int)L.grid;
   return with_int<16, 32, 48, 64>(L.rp, [&](auto rc) {
-    return with_bool(L.drop, [&](auto kc) {
-      hipLaunchKernelGGL((lora_tokred_kernel<decltype(rc)::value, decltype(kc)::value>), dim3((unsigned)L.grid),
-                         dim3((unsigned)L.block), 0, st, pbp, pap, nb0, (int)a.m, (int)BL.mp);
-      return hipGetLastError();
-    });
+    constexpr int RP = decltype(rc)::value;
+    if (L.drop)
+      hipLaunchKernelGGL((lora_tokred_kernel<RP, true>), dim3((unsigned)L.grid), dim3((unsigned)L.block), 0, st, pbp,
+                         pap, nb0, (int)a.m, (int)BL.mp);
+    else
+      hipLaunchKernelGGL((lora_tokred_dma_kernel<RP>), dim3((unsigned)L.grid), dim3((unsigned)L.block), 0, st, pbp,
+                         pap, nb0, (int)a.m, (int)BL.mp);
+    return hipGetLastError();
   });
 }
 

@@ -506,16 +506,28 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
 // U = X A^T on its own, for ranks above 16.  In the fused tile every output
 // tile recomputes all RP U columns of its tokens, RP / BN more matrix-core
 // work (a quarter at RP = 64 on the 256-wide tile); this pass computes them
-// once.  TPW tokens per workgroup; the 8 waves take interleaved 32-wide chunks
-// of k, seven chunks ahead in a ring of registers, loading X and A
-// straight into v_mfma_f32_16x16x32_bf16 operands (A rows as the A operand,
-// 16 tokens as the B operand).  The waves' sums are added in wave order
-// through LDS (bit-identical from run to run) and written as fp32 U [m][r].
-template <int RP, int TPW>
-__global__ __launch_bounds__(512) void lora_u_kernel(const u16* __restrict__ X, const u16* __restrict__ A,
+// once.  32 tokens per workgroup, four waves.  The k loop runs in stages of
+// 64: a stage's 32 X rows and RP A rows (128 bytes each) are copied from
+// global memory straight into a ring of NS LDS stages, NS - 1 stages ahead,
+// eight whole 128-byte row pieces per copy instruction (the swizzle of
+// kc_offset applied to the global addresses); one barrier per stage.  (Loads
+// of 16 rows x 64 bytes per instruction straight into matrix-core operands
+// kept the L1 busy translating addresses, about 2.6 TB/s of X at 7B
+// down_proj.)  Wave w owns U fragments of 16 rank rows x 16 tokens over all
+// of k (16x16x32 products), so no cross-wave sum is needed; U [m][r] fp32.
+template <int RP>
+__global__ __launch_bounds__(256) void lora_u_kernel(const u16* __restrict__ X, const u16* __restrict__ A,
                                                      float* __restrict__ U, int m, int k, int r) {
-  constexpr int FT = RP / 16, TG = TPW / 16, NWV = 8, NB = 8;
-  __shared__ __attribute__((aligned(16))) floatx4 red[NWV][FT][TG][64];
+  constexpr int TPW = 32, NWV = 4;
+  constexpr int ROWS = TPW + RP;                 // 128-byte rows per stage: X rows, then A rows
+  constexpr int STAGE = ROWS * 128;
+  constexpr int CPS = ROWS / 8, CPW = CPS / NWV;   // 1 KB copies per stage, per wave
+  constexpr int NS = (96 * 1024) / STAGE;        // ring stages (96 KB)
+  constexpr int FT = RP / 16, TG = TPW / 16;
+  constexpr int TW = FT * TG / NWV;              // fragments per wave (same rank rows, TW token groups)
+  static_assert(CPS % NWV == 0 && TW >= 1 && TG % TW == 0, "even split");
+  static_assert(CPW * (NS - 2) < 64, "copies in flight fit the wait counter");
+  __shared__ __attribute__((aligned(1024))) char smem[NS * STAGE];
   const int i0 = blockIdx.x * TPW;
   const int tid = threadIdx.x, lane = tid & 63, wave = uniform(tid >> 6);
   const int g = lane >> 4, c16 = lane & 15;
@@ -524,62 +536,65 @@ __global__ __launch_bounds__(512) void lora_u_kernel(const u16* __restrict__ X, 
   const __amdgpu_buffer_rsrc_t rsX = make_rsrc(X + (size_t)i0 * k, (uint64_t)rows * rowbytes);
   const __amdgpu_buffer_rsrc_t rsA = make_rsrc(A, (uint64_t)r * rowbytes);
 
-  floatx4 acc[FT][TG];
+  // Copy c = wave + NWV i of a stage fills its rows 8c .. 8c+7: this lane's
+  // row 8c + lane/8 at physical chunk lane%8, which holds logical chunk
+  // (lane%8) ^ kc_swz(row).  Rows past m or r, and k past the end, read zero.
+  uint32_t base[CPW];
+  int kc[CPW];
 #pragma unroll
-  for (int ft = 0; ft < FT; ++ft)
-#pragma unroll
-    for (int tg = 0; tg < TG; ++tg) acc[ft][tg] = floatx4{0.f, 0.f, 0.f, 0.f};
-  // chunk j of this wave: k columns 32 (wave + NWV j) .. +31; lane (g, c16)
-  // loads k 8g .. 8g+7 of token row 16 tg + c16 and of A row 16 ft + c16.
-  // A ring of NB register slots holds one chunk each, NB - 1 chunks ahead
-  // (7B down_proj: 78 -> 74 us against two-chunk batches one batch ahead).
-  short8 xf[NB][TG], af[NB][FT];
-  auto load = [&](int j, int p) LORA_INLINE {
-    const int kk = 32 * (wave + NWV * j) + 8 * g;
-#pragma unroll
-    for (int tg = 0; tg < TG; ++tg)
-      xf[p][tg] = __builtin_bit_cast(
-          short8, buf_load16(rsX, kk < k ? (uint32_t)(16 * tg + c16) * rowbytes + (uint32_t)kk * 2 : kOOB));
-#pragma unroll
-    for (int ft = 0; ft < FT; ++ft)
-      af[p][ft] = __builtin_bit_cast(
-          short8, buf_load16(rsA, kk < k ? (uint32_t)(16 * ft + c16) * rowbytes + (uint32_t)kk * 2 : kOOB));
-  };
-  auto process = [&](int p) LORA_INLINE {
-#pragma unroll
-    for (int ft = 0; ft < FT; ++ft)
-#pragma unroll
-      for (int tg = 0; tg < TG; ++tg) acc[ft][tg] = mfma16x16x32(af[p][ft], xf[p][tg], acc[ft][tg]);
-  };
-  const int nch = uniform(32 * wave < k ? (k - 32 * wave + 32 * NWV - 1) / (32 * NWV) : 0);
-#pragma unroll
-  for (int q = 0; q < NB - 1; ++q)
-    if (q < nch) load(q, q);
-  for (int j0 = 0; j0 < nch; j0 += NB) {   // chunk j0 + q sits in slot q
-#pragma unroll
-    for (int q = 0; q < NB; ++q) {
-      if (j0 + q >= nch) break;
-      if (j0 + q + NB - 1 < nch) load(j0 + q + NB - 1, (q + NB - 1) % NB);
-      process(q);
-    }
+  for (int i = 0; i < CPW; ++i) {
+    const int row = 8 * (wave + NWV * i) + (lane >> 3);
+    const int c = (lane & 7) ^ kc_swz(row);
+    const int grow = row < TPW ? row : row - TPW;
+    base[i] = (uint32_t)grow * rowbytes + (uint32_t)c * 16;
+    kc[i] = 8 * c;
   }
+  auto issue = [&](int st, int buf) LORA_INLINE {
+    const int k0 = st * 64;
+    char* sb = smem + buf * STAGE;
 #pragma unroll
-  for (int ft = 0; ft < FT; ++ft)
+    for (int i = 0; i < CPW; ++i) {
+      const bool isx = 8 * (wave + NWV * i) < TPW;   // wave-uniform
+      const uint32_t off = k0 + kc[i] < k ? base[i] + (uint32_t)k0 * 2 : kOOB;
+      dma16(isx ? rsX : rsA, off, 0, sb + (wave + NWV * i) * 1024);
+    }
+  };
+  // wave w: rank rows 16 ft .. +15 with ft = w TW / TG, token groups
+  // tg0 .. tg0 + TW - 1
+  const int ft = wave * TW / TG, tg0 = (wave * TW) % TG;
+  floatx4 acc[TW];
 #pragma unroll
-    for (int tg = 0; tg < TG; ++tg) red[wave][ft][tg][lane] = acc[ft][tg];
-  __syncthreads();
-  // lane of (ft, tg): token 16 tg + c16, rank rows 16 ft + 4 g .. +3
-  for (int e = wave; e < FT * TG; e += NWV) {
-    const int ft = e / TG, tg = e - ft * TG;
-    floatx4 v = red[0][ft][tg][lane];
+  for (int q = 0; q < TW; ++q) acc[q] = floatx4{0.f, 0.f, 0.f, 0.f};
+  auto compute = [&](int buf) LORA_INLINE {
+    const char* sb = smem + buf * STAGE;
 #pragma unroll
-    for (int w = 1; w < NWV; ++w) v += red[w][ft][tg][lane];
-    const int i = i0 + 16 * tg + c16;
+    for (int kk = 0; kk < 2; ++kk) {
+      const int ch = 4 * kk + g;
+      const short8 af = kc_read(sb, TPW + 16 * ft + c16, ch);
+#pragma unroll
+      for (int q = 0; q < TW; ++q) acc[q] = mfma16x16x32(af, kc_read(sb, 16 * (tg0 + q) + c16, ch), acc[q]);
+    }
+  };
+
+  const int nst = (k + 63) / 64;
+#pragma unroll
+  for (int st = 0; st < NS - 1; ++st) issue(st, st);
+  for (int st = 0; st < nst; ++st) {
+    copy_barrier<CPW * (NS - 2)>();   // stage st has landed; every wave is done with stage st - 1
+    issue(st + NS - 1, (st + NS - 1) % NS);
+    compute(st % NS);
+  }
+  copy_barrier<0>();   // the trailing copies (zeros past k) land before the workgroup ends
+
+  // lane of fragment q: rank rows 16 ft + 4 g .. +3 of token 16 (tg0 + q) + c16
+#pragma unroll
+  for (int q = 0; q < TW; ++q) {
+    const int i = i0 + 16 * (tg0 + q) + c16;
     if (i < m) {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int t = 16 * ft + 4 * g + q;
-        if (t < r) U[(size_t)i * r + t] = v[q];
+      for (int j = 0; j < 4; ++j) {
+        const int t = 16 * ft + 4 * g + j;
+        if (t < r) U[(size_t)i * r + t] = acc[q][j];
       }
     }
   }
@@ -1015,7 +1030,7 @@ static hipError_t run_fwd_launch(const Launch& L, const FwdArgs& a, const FwdGro
   const dim3 grid((unsigned)L.grid), block((unsigned)L.block);
   if (L.id == K_UPASS) {
     return with_int<32, 64>(L.rp, [&](auto rc) {
-      hipLaunchKernelGGL((lora_u_kernel<decltype(rc)::value, 32>), grid, block, 0, st, a.X, a.A, a.U, (int)a.m,
+      hipLaunchKernelGGL((lora_u_kernel<decltype(rc)::value>), grid, block, 0, st, a.X, a.A, a.U, (int)a.m,
                          (int)a.k, (int)a.r);
       return hipGetLastError();
     });

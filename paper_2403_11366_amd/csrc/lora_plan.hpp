@@ -15,11 +15,11 @@
 namespace lora {
 
 enum KernelId : int {
-  K_UPASS = 0,     // lora_u_kernel<RP, TPW>: U = X A^T on its own (rank > 16)
+  K_UPASS = 0,     // lora_u_kernel<RP>: U = X A^T on its own (rank > 16)
   K_FWD = 1,       // lora_fwd_kernel<BM, BN, WM, WN, RP, DROP, GRP, UPRE, KFULL, DMA>
   K_FWD_KS = 2,    // lora_fwd_ks_kernel<GRP, KFULL, DMA>
   K_DU = 3,        // lora_bwd_du_kernel<RP, TPW>
-  K_TOKRED = 4,    // lora_tokred_kernel<RP, KEEP>
+  K_TOKRED = 4,    // lora_tokred_dma_kernel<RP>, or lora_tokred_kernel<RP, true> with a keep mask
   K_DX = 5,        // lora_bwd_dx_kernel<BM, BN, WM, WN, RP, DROP, GRP, FULL>
   K_DXF = 6,       // lora_bwd_dxf_kernel<FULL, FASTB>
   K_FINALIZE = 7,  // lora_finalize_kernel
@@ -109,7 +109,7 @@ inline void plan_fwd_part(Plan& p, GemmTile t, int64_t m, int64_t k, int64_t r, 
     u.rp = x.rp;
     u.tpw = 32;
     u.grid = (m + 31) / 32;
-    u.block = 512;
+    u.block = 256;
     p.add(u);
   }
   p.add(x);
@@ -291,14 +291,17 @@ inline Plan plan_merge(int64_t n, int64_t k, int64_t r) {
 inline void launch_name(const Launch& x, char* buf, size_t len) {
   auto b = [](bool v) { return v ? "true" : "false"; };
   switch (x.id) {
-    case K_UPASS: snprintf(buf, len, "lora::lora_u_kernel<%d, %d>", x.rp, x.tpw); break;
+    case K_UPASS: snprintf(buf, len, "lora::lora_u_kernel<%d>", x.rp); break;
     case K_FWD:
       snprintf(buf, len, "lora::lora_fwd_kernel<%d, %d, %d, %d, %d, %s, %s, %s, %s, %s>", x.bm, x.bn, x.wm, x.wn,
                x.rp, b(x.drop), b(x.grp), b(x.upre), b(x.full), b(x.dma));
       break;
     case K_FWD_KS: snprintf(buf, len, "lora::lora_fwd_ks_kernel<%s, %s, %s>", b(x.grp), b(x.full), b(x.dma)); break;
     case K_DU: snprintf(buf, len, "lora::lora_bwd_du_kernel<%d, %d>", x.rp, x.tpw); break;
-    case K_TOKRED: snprintf(buf, len, "lora::lora_tokred_kernel<%d, %s>", x.rp, b(x.drop)); break;
+    case K_TOKRED:
+      if (x.drop) snprintf(buf, len, "lora::lora_tokred_kernel<%d, true>", x.rp);
+      else snprintf(buf, len, "lora::lora_tokred_dma_kernel<%d>", x.rp);
+      break;
     case K_DX:
       snprintf(buf, len, "lora::lora_bwd_dx_kernel<%d, %d, %d, %d, %d, %s, %s, %s>", x.bm, x.bn, x.wm, x.wn, x.rp,
                b(x.drop), b(x.grp), b(x.full));

@@ -73,8 +73,12 @@ def test_dropout_keep_all_matches_plain_path():
     keep = np.full((shape.m, shape.k // 8), 0xFF, dtype=np.uint8)
     got = run_dropout(t, shape, keep, 0.0)
     plain = run_gpu(t, shape)
-    for x in ("Y", "U", "dA", "dB"):
+    for x in ("Y", "U"):
         assert np.array_equal(got[x], plain[x]), x
+    # the two paths reduce dA and dB with different kernels (the masked one
+    # stages X through registers), so their fp32 sums differ in order only
+    for x in ("dA", "dB"):
+        assert rel(got[x], plain[x]) <= 1e-6, x
     assert rel(f64(got["dX"]), f64(plain["dX"])) <= 1e-3
     check(t, shape, keep, 0.0, got)
 

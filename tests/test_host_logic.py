@@ -44,7 +44,7 @@ def test_single_projection_plans(lora, s):
     _check_columns(_gemms(fwd), s.n)
     _check_columns([x for x in bwd if "dx_kernel" in x["kernel"]], s.k)
     names = [x["kernel"] for x in bwd]
-    assert names[0].startswith("lora::lora_bwd_du_kernel<") and names[1].startswith("lora::lora_tokred_kernel<")
+    assert names[0].startswith("lora::lora_bwd_du_kernel<") and names[1].startswith("lora::lora_tokred_dma_kernel<")
     # the U pass precedes the first forward GEMM exactly when the rank is above 16
     assert any("lora_u_kernel" in x["kernel"] for x in fwd) == (s.r > 16)
     for x in bwd:
@@ -125,7 +125,7 @@ def test_group_da_reductions_share_one_pass_over_x(lora):
     plan = lora.lora_linear_plan("group_bwd", 4096, [5120] * 3, 5120, 8)     # 13B q, k, v
     red = [x for x in plan if "tokred" in x["kernel"]]
     assert [x["member"] for x in red] == [0, 1, 2, -1]
-    assert red[-1]["kernel"] == "lora::lora_tokred_kernel<48, false>"
+    assert red[-1]["kernel"] == "lora::lora_tokred_dma_kernel<48>"
     plan = lora.lora_linear_plan("group_bwd", 264, [392, 128, 520], 448, 64)  # 3 x 64 > 64: per member
     assert [x["member"] for x in plan if "tokred" in x["kernel"]] == [0, 1, 2]
     for ns, m, k, r, _ in GROUP_CASES:
