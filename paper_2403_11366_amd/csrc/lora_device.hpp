@@ -79,6 +79,12 @@ __device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t rs, uint32_t voff, 
                                            0);
 }
 
+// The same with 4 bytes per lane: lane l's bytes land at lds_base + 4 l.
+__device__ __forceinline__ void dma4(__amdgpu_buffer_rsrc_t rs, uint32_t voff, uint32_t soff, void* lds_base) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void*)lds_base, 4, voff, soff, 0,
+                                           0);
+}
+
 // s_waitcnt on the vector-memory count only: wait until at most N of this
 // wave's vector-memory operations (global -> LDS copies included) are
 // outstanding.  gfx9 encoding: vmcnt[3:0] in bits 3:0, vmcnt[5:4] in bits

@@ -503,31 +503,43 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// U = X A^T on its own, for ranks above 16.  In the fused tile every output
+// U = X A^T on its own: for ranks above 16 (in the fused tile every output
 // tile recomputes all RP U columns of its tokens, RP / BN more matrix-core
-// work (a quarter at RP = 64 on the 256-wide tile); this pass computes them
-// once.  32 tokens per workgroup, four waves.  The k loop runs in stages of
-// 64: a stage's 32 X rows and RP A rows (128 bytes each) are copied from
-// global memory straight into a ring of NS LDS stages, NS - 1 stages ahead,
-// eight whole 128-byte row pieces per copy instruction (the swizzle of
-// kc_offset applied to the global addresses); one barrier per stage.  (Loads
-// of 16 rows x 64 bytes per instruction straight into matrix-core operands
-// kept the L1 busy translating addresses, about 2.6 TB/s of X at 7B
-// down_proj.)  Wave w owns U fragments of 16 rank rows x 16 tokens over all
-// of k (16x16x32 products), so no cross-wave sum is needed; U [m][r] fp32.
-template <int RP>
+// work, a quarter at RP = 64 on the 256-wide tile; this pass computes them
+// once), and under LoRA dropout (KEEP: U = (keep X) A^T / (1 - p), so the
+// GEMM that follows needs no mask).  TPW (16 or 32) tokens per workgroup,
+// four waves.  The k loop runs in stages of 64; wave w takes stages w, w + 4,
+// ... and copies each of them (its TPW X rows and RP A rows, 128 bytes a row,
+// eight whole row pieces per copy instruction with the swizzle of kc_offset
+// applied to the global addresses; under KEEP also the stage's keep bits, 8
+// bytes a token, 4 bytes a lane) from global memory straight into a private
+// ring of NSW LDS stages, NSW - 1 stages ahead.  No barrier in the loop: the
+// wave waits only for its own copies.  (Loads of 16 rows x 64 bytes per
+// instruction straight into matrix-core operands kept the L1 busy
+// translating addresses; a shared ring with a barrier per stage was bound by
+// each stage's short compute chain.)  Each wave accumulates all RP x TPW of U
+// over its stages (16x16x32 products; under KEEP each X fragment of 8 k is
+// masked with its keep byte first); the four partial sums are added in wave
+// order through LDS at the end (bit-identical from run to run) and written
+// as fp32 U [m][r], scaled by inv_keep under KEEP.
+template <int RP, int TPW, bool KEEP>
 __global__ __launch_bounds__(256) void lora_u_kernel(const u16* __restrict__ X, const u16* __restrict__ A,
-                                                     float* __restrict__ U, int m, int k, int r) {
-  constexpr int TPW = 32, NWV = 4;
+                                                     const uint8_t* __restrict__ keep, float* __restrict__ U, int m,
+                                                     int k, int r, float inv_keep) {
+  constexpr int NWV = 4;
   constexpr int ROWS = TPW + RP;                 // 128-byte rows per stage: X rows, then A rows
-  constexpr int STAGE = ROWS * 128;
-  constexpr int CPS = ROWS / 8, CPW = CPS / NWV;   // 1 KB copies per stage, per wave
-  constexpr int NS = (96 * 1024) / STAGE;        // ring stages (96 KB)
+  constexpr int MOFF = ROWS * 128;               // keep bytes of the stage: [TPW][8]
+  constexpr int STAGE = MOFF + (KEEP ? 256 : 0);
+  constexpr int CPS = ROWS / 8;                  // 1 KB copies per stage
+  constexpr int CPW = CPS + (KEEP ? 1 : 0);      // copy instructions per stage (the wave's own)
+  constexpr int NSW = (156 * 1024) / (NWV * STAGE) < 6 ? (156 * 1024) / (NWV * STAGE) : 6;   // ring stages per wave
   constexpr int FT = RP / 16, TG = TPW / 16;
-  constexpr int TW = FT * TG / NWV;              // fragments per wave (same rank rows, TW token groups)
-  static_assert(CPS % NWV == 0 && TW >= 1 && TG % TW == 0, "even split");
-  static_assert(CPW * (NS - 2) < 64, "copies in flight fit the wait counter");
-  __shared__ __attribute__((aligned(1024))) char smem[NS * STAGE];
+  constexpr int RED = NWV * FT * TG * 64 * 16;   // cross-wave sum: [NWV][FT][TG][64] float4
+  constexpr int SMEM = NWV * NSW * STAGE > RED ? NWV * NSW * STAGE : RED;
+  static_assert(TPW == 16 || TPW == 32, "tokens per workgroup");
+  static_assert(NSW >= 3 && CPW * (NSW - 2) < 64, "copies in flight fit the wait counter");
+  static_assert(FT * TG <= 8, "fragments per wave");
+  __shared__ __attribute__((aligned(1024))) char smem[SMEM];
   const int i0 = blockIdx.x * TPW;
   const int tid = threadIdx.x, lane = tid & 63, wave = uniform(tid >> 6);
   const int g = lane >> 4, c16 = lane & 15;
@@ -535,66 +547,89 @@ __global__ __launch_bounds__(256) void lora_u_kernel(const u16* __restrict__ X, 
   const int rows = uniform(max(0, min(TPW, m - i0)));
   const __amdgpu_buffer_rsrc_t rsX = make_rsrc(X + (size_t)i0 * k, (uint64_t)rows * rowbytes);
   const __amdgpu_buffer_rsrc_t rsA = make_rsrc(A, (uint64_t)r * rowbytes);
+  const uint32_t kb8 = (uint32_t)k / 8;          // keep bytes per token (k % 64 == 0 with dropout)
+  const __amdgpu_buffer_rsrc_t rsK =
+      make_rsrc(KEEP ? (const void*)(keep + (size_t)i0 * kb8) : (const void*)X, KEEP ? (uint64_t)rows * kb8 : 0);
+  char* ring = smem + wave * NSW * STAGE;
 
-  // Copy c = wave + NWV i of a stage fills its rows 8c .. 8c+7: this lane's
-  // row 8c + lane/8 at physical chunk lane%8, which holds logical chunk
-  // (lane%8) ^ kc_swz(row).  Rows past m or r, and k past the end, read zero.
-  uint32_t base[CPW];
-  int kc[CPW];
-#pragma unroll
-  for (int i = 0; i < CPW; ++i) {
-    const int row = 8 * (wave + NWV * i) + (lane >> 3);
-    const int c = (lane & 7) ^ kc_swz(row);
-    const int grow = row < TPW ? row : row - TPW;
-    base[i] = (uint32_t)grow * rowbytes + (uint32_t)c * 16;
-    kc[i] = 8 * c;
-  }
-  auto issue = [&](int st, int buf) LORA_INLINE {
+  // Copy c of a stage fills its rows 8c .. 8c+7: this lane's row 8c + lane/8
+  // at physical chunk lane%8, which holds logical chunk (lane%8) ^ kc_swz(row).
+  // Rows past m or r, k past the end and stages past the wave's last read zero.
+  const int c8 = lane & 7, r8 = lane >> 3;
+  const int nst = (k + 63) / 64;
+  auto issue = [&](int j, int buf) LORA_INLINE {   // the wave's j-th stage
+    const int st = wave + NWV * j;
     const int k0 = st * 64;
-    char* sb = smem + buf * STAGE;
+    const bool live = st < nst;
+    char* sb = ring + buf * STAGE;
 #pragma unroll
-    for (int i = 0; i < CPW; ++i) {
-      const bool isx = 8 * (wave + NWV * i) < TPW;   // wave-uniform
-      const uint32_t off = k0 + kc[i] < k ? base[i] + (uint32_t)k0 * 2 : kOOB;
-      dma16(isx ? rsX : rsA, off, 0, sb + (wave + NWV * i) * 1024);
+    for (int c = 0; c < CPS; ++c) {
+      const int row = 8 * c + r8;
+      const int lc = c8 ^ kc_swz(row);
+      const bool isx = 8 * c < TPW;   // uniform
+      const int grow = isx ? row : row - TPW;
+      const uint32_t off = live && k0 + 8 * lc < k ? (uint32_t)grow * rowbytes + (uint32_t)(k0 + 8 * lc) * 2 : kOOB;
+      dma16(isx ? rsX : rsA, off, 0, sb + c * 1024);
     }
+    if (KEEP)   // lane l: bytes 4 (l % 2) .. +3 of token l / 2's stage bits (lanes past TPW tokens: zero)
+      dma4(rsK, live && (lane >> 1) < TPW ? (uint32_t)(lane >> 1) * kb8 + (uint32_t)k0 / 8 + 4 * (lane & 1) : kOOB,
+           0, sb + MOFF);
   };
-  // wave w: rank rows 16 ft .. +15 with ft = w TW / TG, token groups
-  // tg0 .. tg0 + TW - 1
-  const int ft = wave * TW / TG, tg0 = (wave * TW) % TG;
-  floatx4 acc[TW];
+  floatx4 acc[FT][TG];
 #pragma unroll
-  for (int q = 0; q < TW; ++q) acc[q] = floatx4{0.f, 0.f, 0.f, 0.f};
+  for (int ft = 0; ft < FT; ++ft)
+#pragma unroll
+    for (int tg = 0; tg < TG; ++tg) acc[ft][tg] = floatx4{0.f, 0.f, 0.f, 0.f};
   auto compute = [&](int buf) LORA_INLINE {
-    const char* sb = smem + buf * STAGE;
+    const char* sb = ring + buf * STAGE;
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
       const int ch = 4 * kk + g;
-      const short8 af = kc_read(sb, TPW + 16 * ft + c16, ch);
+      short8 xf[TG], af[FT];
 #pragma unroll
-      for (int q = 0; q < TW; ++q) acc[q] = mfma16x16x32(af, kc_read(sb, 16 * (tg0 + q) + c16, ch), acc[q]);
+      for (int tg = 0; tg < TG; ++tg) {
+        xf[tg] = kc_read(sb, 16 * tg + c16, ch);
+        if constexpr (KEEP) xf[tg] = keep_mask8(xf[tg], (uint32_t)(uint8_t)sb[MOFF + (16 * tg + c16) * 8 + ch]);
+      }
+#pragma unroll
+      for (int ft = 0; ft < FT; ++ft) af[ft] = kc_read(sb, TPW + 16 * ft + c16, ch);
+#pragma unroll
+      for (int ft = 0; ft < FT; ++ft)
+#pragma unroll
+        for (int tg = 0; tg < TG; ++tg) acc[ft][tg] = mfma16x16x32(af[ft], xf[tg], acc[ft][tg]);
     }
   };
 
-  const int nst = (k + 63) / 64;
+  const int nsw = wave < nst ? (nst - wave + NWV - 1) / NWV : 0;   // this wave's stages
 #pragma unroll
-  for (int st = 0; st < NS - 1; ++st) issue(st, st);
-  for (int st = 0; st < nst; ++st) {
-    copy_barrier<CPW * (NS - 2)>();   // stage st has landed; every wave is done with stage st - 1
-    issue(st + NS - 1, (st + NS - 1) % NS);
-    compute(st % NS);
+  for (int j = 0; j < NSW - 1; ++j) issue(j, j);
+  for (int j = 0; j < nsw; ++j) {
+    wait_vmcnt<CPW * (NSW - 2)>();   // the wave's stage j has landed
+    issue(j + NSW - 1, (j + NSW - 1) % NSW);   // into the buffer of stage j - 1, read already
+    compute(j % NSW);
   }
-  copy_barrier<0>();   // the trailing copies (zeros past k) land before the workgroup ends
+  wait_vmcnt<0>();   // the trailing copies (zeros) land before the LDS is reused
 
-  // lane of fragment q: rank rows 16 ft + 4 g .. +3 of token 16 (tg0 + q) + c16
+  // Cross-wave sum in wave order; lane of (ft, tg): rank rows 16 ft + 4 g ..
+  // +3 of token 16 tg + c16.
+  floatx4* red = reinterpret_cast<floatx4*>(smem);
+  __syncthreads();
 #pragma unroll
-  for (int q = 0; q < TW; ++q) {
-    const int i = i0 + 16 * (tg0 + q) + c16;
+  for (int ft = 0; ft < FT; ++ft)
+#pragma unroll
+    for (int tg = 0; tg < TG; ++tg) red[((wave * FT + ft) * TG + tg) * 64 + lane] = acc[ft][tg];
+  __syncthreads();
+  for (int e = wave; e < FT * TG; e += NWV) {
+    const int ft = e / TG, tg = e - ft * TG;
+    floatx4 v = red[((0 * FT + ft) * TG + tg) * 64 + lane];
+#pragma unroll
+    for (int w = 1; w < NWV; ++w) v += red[((w * FT + ft) * TG + tg) * 64 + lane];
+    const int i = i0 + 16 * tg + c16;
     if (i < m) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int t = 16 * ft + 4 * g + j;
-        if (t < r) U[(size_t)i * r + t] = acc[q][j];
+        if (t < r) U[(size_t)i * r + t] = KEEP ? inv_keep * v[j] : v[j];
       }
     }
   }
@@ -623,7 +658,10 @@ __global__ __launch_bounds__(256) void lora_u_kernel(const u16* __restrict__ X, 
 // global addresses), two stages ahead and without staging registers; each
 // stage ends with a barrier that waits only for this wave's copies of the
 // next stage (copy_barrier).
-template <bool GRP, bool KFULL, bool DMA>
+//
+// UPRE (LoRA dropout: U from the masked U pass): the stages hold no A rows,
+// the loop runs no U products, and the epilogue reads U back.
+template <bool GRP, bool KFULL, bool DMA, bool UPRE>
 __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
     const u16* __restrict__ X, const u16* __restrict__ W, const u16* __restrict__ A,
     const u16* __restrict__ B, u16* __restrict__ Y, float* __restrict__ U, int m, int n, int k, int r, float s,
@@ -631,10 +669,12 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
   constexpr int BM = 128, BN = 256, NT = 512, RP = 16;
   constexpr int WTI = 64, WTJ = 128, FI = 2, FJ = 4;
   constexpr int GPW = 2;                          // 16-token U groups per wave
-  constexpr int ROWS = BM + BN + RP;
+  constexpr int RPS = UPRE ? 0 : RP;              // A rows staged per stage
+  constexpr int ROWS = BM + BN + RPS;
   constexpr int STAGE = ROWS * 128;
-  constexpr int CX = BM * 8, CW = BN * 8, CA = RP * 8;
-  constexpr int LX = CX / NT, LW = CW / NT, LA = (CA + NT - 1) / NT;
+  constexpr int CX = BM * 8, CW = BN * 8, CA = RPS * 8;
+  constexpr int LX = CX / NT, LW = CW / NT, LA = UPRE ? 1 : (CA + NT - 1) / NT;
+  static_assert(!(UPRE && GRP), "U from the U pass only for single projections");
   constexpr int XCH = 8 * 16 * 1024;              // exchange: 8 waves x 32 fragments x 64 lanes x 4 B
   static_assert(!DMA || KFULL, "the copies carry no k-bound checks");
   constexpr int NBUF = DMA ? 3 : 2;                       // LDS stage buffers
@@ -684,6 +724,7 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
       }
 #pragma unroll
       for (int i = 0; i < LA; ++i) {
+        if (UPRE) break;
         const int q = tid + i * NT;
         if (CA % NT != 0 && wave * 64 + i * NT >= CA) break;
         const int kk = k0 + 8 * (q & 7);
@@ -708,6 +749,7 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
       }
 #pragma unroll
       for (int i = 0; i < LA; ++i) {
+        if (UPRE) break;
         const int q = tid + i * NT;
         if (CA % NT != 0 && wave * 64 + i * NT >= CA) break;
         *reinterpret_cast<int4v*>(sb + (BM + BN) * 128 + kc_offset(q >> 3, q & 7)) = ga[i];
@@ -745,7 +787,7 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
     for (int fj = 0; fj < FJ; ++fj) fw[p][fj] = kc_read(Ws, wn * WTJ + 32 * fj + c32, ch);
 #pragma unroll
     for (int fi = 0; fi < FI; ++fi) fx[p][fi] = kc_read(Xs, wm * WTI + 32 * fi + c32, ch);
-    if (j == 0) {   // the wave's 32-wide half: chunks 4 wk + g16
+    if (!UPRE && j == 0) {   // the wave's 32-wide half: chunks 4 wk + g16
       fa16 = kc_read(As, c16, 4 * wk + g16);
 #pragma unroll
       for (int gg = 0; gg < GPW; ++gg) fxu16[gg] = kc_read(Xs, urow16[gg], 4 * wk + g16);
@@ -756,7 +798,7 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
     for (int fi = 0; fi < FI; ++fi)
 #pragma unroll
       for (int fj = 0; fj < FJ; ++fj) acc[fj][fi] = mfma32x32x16(fw[p][fj], fx[p][fi], acc[fj][fi]);
-    if (j == 0) {
+    if (!UPRE && j == 0) {
 #pragma unroll
       for (int gg = 0; gg < GPW; ++gg) uacc16[gg] = mfma16x16x32(fa16, fxu16[gg], uacc16[gg]);
     }
@@ -801,7 +843,7 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
     for (int i = 0; i < 2; ++i) dma16(rsX, voff(wave + 8 * i), k0b, sb + (wave + 8 * i) * 1024);
 #pragma unroll
     for (int i = 0; i < 4; ++i) dma16(rsW, voff(wave + 8 * i), k0b, sb + BM * 128 + (wave + 8 * i) * 1024);
-    if (wave < 2) dma16(rsA, voff(wave), k0b, sb + (BM + BN) * 128 + wave * 1024);
+    if (!UPRE && wave < 2) dma16(rsA, voff(wave), k0b, sb + (BM + BN) * 128 + wave * 1024);
   };
   constexpr int NDMA_MIN = 6;   // fewest copies any wave issues per stage
   dload(0, 0);
@@ -939,10 +981,12 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
           dst[((fjl * FI + fi) * 4 + q4) * 64 + lane] = float4{v[4 * q4], v[4 * q4 + 1], v[4 * q4 + 2], v[4 * q4 + 3]};
       }
   }
+  if (!UPRE) {
 #pragma unroll
-  for (int gg = 0; gg < GPW; ++gg)
+    for (int gg = 0; gg < GPW; ++gg)
 #pragma unroll
-    for (int q = 0; q < 4; ++q) Us[(wk * BM + urow16[gg]) * RP + 4 * g16 + q] = uacc16[gg][q];
+      for (int q = 0; q < 4; ++q) Us[(wk * BM + urow16[gg]) * RP + 4 * g16 + q] = uacc16[gg][q];
+  }
   __syncthreads();
   {
     const float4* src = region(wk);
@@ -962,10 +1006,17 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
           }
         }
   }
-  // (the partial of half 1 is read here and written before the barrier above)
-  for (int e = tid; e < BM * RP; e += NT) Us[e] = Us[e] + Us[BM * RP + e];
+  if (UPRE) {   // U of the tile's tokens from the U pass (zero beyond r and m)
+    for (int e = tid; e < BM * RP; e += NT) {
+      const int il = e / RP, t = e - il * RP;
+      Us[e] = (m0 + il < m && t < r) ? U[(size_t)(m0 + il) * r + t] : 0.f;
+    }
+  } else {
+    // (the partial of half 1 is read here and written before the barrier above)
+    for (int e = tid; e < BM * RP; e += NT) Us[e] = Us[e] + Us[BM * RP + e];
+  }
   __syncthreads();
-  if (n0 == 0) {
+  if (n0 == 0 && !UPRE) {
     for (int e = tid; e < BM * RP; e += NT) {
       const int il = e / RP, t = e - il * RP;
       if (m0 + il < m && t < r) U[(size_t)(m0 + il) * r + t] = Us[e];
@@ -1018,36 +1069,51 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
 // ---------------------------------------------------------------------------
 // Launchers: execute the plans of lora_plan.hpp.
 
-// Instantiations a plan can name (any other combination is refused).
-// (the 128 x 256 tile at rank 16 without dropout is the k-split kernel's)
+// Instantiations a plan can name (any other combination is refused): U from
+// the U pass for single projections of rank above 16 and under dropout
+// (where the pass applies the keep mask), in the tile for groups and rank 16;
+// the 128 x 256 tile at rank 16 is the k-split kernel's.
 template <int BM, int BN, int RP, bool DROP, bool GRP, bool UPRE, bool KFULL, bool DMA>
 constexpr bool fwd_instantiated() {
-  return !(DROP && GRP) && !(DROP && BM == 256) && !(BM == 128 && BN == 256 && RP == 16 && !DROP) &&
-         UPRE == (RP >= 32 && !DROP && !GRP) && DMA == (KFULL && BM == 256 && BN == 256 && !DROP);
+  return !DROP && !(BM == 128 && BN == 256 && RP == 16) && (UPRE ? !GRP : (RP == 16 || GRP)) &&
+         DMA == (KFULL && BM == 256 && BN == 256);
 }
 
 static hipError_t run_fwd_launch(const Launch& L, const FwdArgs& a, const FwdGroup& grp, hipStream_t st) {
   const dim3 grid((unsigned)L.grid), block((unsigned)L.block);
   if (L.id == K_UPASS) {
-    return with_int<32, 64>(L.rp, [&](auto rc) {
-      hipLaunchKernelGGL((lora_u_kernel<decltype(rc)::value>), grid, block, 0, st, a.X, a.A, a.U, (int)a.m,
-                         (int)a.k, (int)a.r);
-      return hipGetLastError();
+    return with_int<16, 32, 64>(L.rp, [&](auto rc) {
+      return with_int<16, 32>(L.tpw, [&](auto tc) {
+        return with_bool(L.drop, [&](auto kc) {
+          constexpr int RP = decltype(rc)::value;
+          constexpr bool KEEP = decltype(kc)::value;
+          if constexpr (RP == 16 && !KEEP) {   // rank 16 without dropout: U in the tile
+            return hipErrorInvalidValue;
+          } else {
+            hipLaunchKernelGGL((lora_u_kernel<RP, decltype(tc)::value, KEEP>), grid, block, 0, st, a.X, a.A, a.keep,
+                               a.U, (int)a.m, (int)a.k, (int)a.r, a.inv_keep);
+            return hipGetLastError();
+          }
+        });
+      });
     });
   }
   if (L.id == K_FWD_KS) {
     return with_bool(L.grp, [&](auto gc) {
       return with_bool(L.full, [&](auto fc) {
         return with_bool(L.dma, [&](auto dc) {
-          constexpr bool G = decltype(gc)::value, F = decltype(fc)::value, D = decltype(dc)::value;
-          if constexpr (D && (G || !F)) {
-            return hipErrorInvalidValue;
-          } else {
-            hipLaunchKernelGGL((lora_fwd_ks_kernel<G, F, D>), grid, block, 0, st, a.X, a.W, a.A, a.B, a.Y, a.U,
-                               (int)a.m, (int)a.n, (int)a.k, (int)a.r, a.s, L.tiles_m, L.tiles_n, (int)L.col_begin,
-                               grp);
-            return hipGetLastError();
-          }
+          return with_bool(L.upre, [&](auto uc) {
+            constexpr bool G = decltype(gc)::value, F = decltype(fc)::value, D = decltype(dc)::value,
+                           UP = decltype(uc)::value;
+            if constexpr ((D && (G || !F)) || (UP && (G || !F))) {   // (dropout: k a multiple of 64)
+              return hipErrorInvalidValue;
+            } else {
+              hipLaunchKernelGGL((lora_fwd_ks_kernel<G, F, D, UP>), grid, block, 0, st, a.X, a.W, a.A, a.B, a.Y,
+                                 a.U, (int)a.m, (int)a.n, (int)a.k, (int)a.r, a.s, L.tiles_m, L.tiles_n,
+                                 (int)L.col_begin, grp);
+              return hipGetLastError();
+            }
+          });
         });
       });
     });

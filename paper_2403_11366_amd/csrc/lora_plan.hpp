@@ -15,9 +15,9 @@
 namespace lora {
 
 enum KernelId : int {
-  K_UPASS = 0,     // lora_u_kernel<RP>: U = X A^T on its own (rank > 16)
+  K_UPASS = 0,     // lora_u_kernel<RP, TPW, KEEP>: U = X A^T on its own (rank > 16, and under dropout)
   K_FWD = 1,       // lora_fwd_kernel<BM, BN, WM, WN, RP, DROP, GRP, UPRE, KFULL, DMA>
-  K_FWD_KS = 2,    // lora_fwd_ks_kernel<GRP, KFULL, DMA>
+  K_FWD_KS = 2,    // lora_fwd_ks_kernel<GRP, KFULL, DMA, UPRE>
   K_DU = 3,        // lora_bwd_du_kernel<RP, TPW>
   K_TOKRED = 4,    // lora_tokred_dma_kernel<RP>, or lora_tokred_kernel<RP, true> with a keep mask
   K_DX = 5,        // lora_bwd_dx_kernel<BM, BN, WM, WN, RP, DROP, GRP, FULL>
@@ -83,50 +83,50 @@ inline Launch gemm_launch(KernelId id, GemmTile t, int64_t M, int64_t col_begin,
 }
 
 // Forward GEMM launch(es) for output columns [cb, ce) with tile t.  `first`:
-// the launch whose range starts at column 0 (it writes U; for rank > 16 the U
-// pass runs before it).  For a group, tiles_n is the summed column tiles.
+// the launch whose range starts at column 0 (it writes U, or the U pass runs
+// before it).  U comes from the U pass for single projections of rank above
+// 16 and under dropout (drop: the pass applies the keep mask, and the GEMM
+// then runs exactly as without dropout); otherwise the tile computes it.  For
+// a group, tiles_n is the summed column tiles.
 inline void plan_fwd_part(Plan& p, GemmTile t, int64_t m, int64_t k, int64_t r, int64_t cb, int64_t ce,
                           bool first, bool drop, bool grp, int tiles_n) {
   const bool kfull = k % 64 == 0;
+  const bool upre = !grp && (drop || fwd_rank(r) >= 32);
+  if (upre && first) {
+    Launch u = blank_launch(K_UPASS);
+    u.rp = fwd_rank(r);
+    u.drop = drop;
+    // 32 tokens per workgroup (A read half as often) unless that leaves
+    // compute units idle
+    u.tpw = (m + 31) / 32 >= 256 ? 32 : 16;
+    u.grid = (m + u.tpw - 1) / u.tpw;
+    u.block = 256;
+    p.add(u);
+  }
   Launch x = gemm_launch(K_FWD, t, m, cb, ce, tiles_n);
-  x.drop = drop;
   x.grp = grp;
-  if (t == TILE_128x256 && !drop && r <= 16) {
+  x.upre = upre;
+  x.full = kfull;
+  if (t == TILE_128x256 && r <= 16) {
     // k-split tile; single-round launches copy their stages straight into LDS
     x.id = K_FWD_KS;
     x.rp = 16;
-    x.full = kfull;
     x.dma = kfull && !grp && x.grid <= 256;
     p.add(x);
     return;
   }
   x.rp = fwd_rank(r);
-  x.full = kfull;
-  x.upre = x.rp >= 32 && !drop && !grp;
-  x.dma = t == TILE_256x256 && kfull && !drop;
-  if (x.upre && first) {
-    Launch u = blank_launch(K_UPASS);
-    u.rp = x.rp;
-    u.tpw = 32;
-    u.grid = (m + 31) / 32;
-    u.block = 256;
-    p.add(u);
-  }
+  x.dma = t == TILE_256x256 && kfull;
   p.add(x);
 }
 
-// lora_linear_fwd / lora_linear_fwd_dropout.  Under dropout no 256 x 256 tile
-// (its registers are full) and no column split.
+// lora_linear_fwd / lora_linear_fwd_dropout (the same tiles and column split;
+// under dropout the U pass applies the mask).
 inline Plan plan_fwd(int64_t m, int64_t n, int64_t k, int64_t r, bool drop) {
   Plan p;
-  if (drop) {
-    const GemmTile t = choose_gemm_tile(m, n) == TILE_128x128 ? TILE_128x128 : TILE_128x256;
-    plan_fwd_part(p, t, m, k, r, 0, n, true, true, false, -1);
-    return p;
-  }
   const GemmSplit s = plan_gemm_split(m, n);
-  plan_fwd_part(p, s.t1, m, k, r, 0, s.n1, true, false, false, -1);
-  if (s.n1 < n) plan_fwd_part(p, s.t2, m, k, r, s.n1, n, false, false, false, -1);
+  plan_fwd_part(p, s.t1, m, k, r, 0, s.n1, true, drop, false, -1);
+  if (s.n1 < n) plan_fwd_part(p, s.t2, m, k, r, s.n1, n, false, drop, false, -1);
   return p;
 }
 
@@ -291,12 +291,14 @@ inline Plan plan_merge(int64_t n, int64_t k, int64_t r) {
 inline void launch_name(const Launch& x, char* buf, size_t len) {
   auto b = [](bool v) { return v ? "true" : "false"; };
   switch (x.id) {
-    case K_UPASS: snprintf(buf, len, "lora::lora_u_kernel<%d>", x.rp); break;
+    case K_UPASS: snprintf(buf, len, "lora::lora_u_kernel<%d, %d, %s>", x.rp, x.tpw, b(x.drop)); break;
     case K_FWD:
       snprintf(buf, len, "lora::lora_fwd_kernel<%d, %d, %d, %d, %d, %s, %s, %s, %s, %s>", x.bm, x.bn, x.wm, x.wn,
                x.rp, b(x.drop), b(x.grp), b(x.upre), b(x.full), b(x.dma));
       break;
-    case K_FWD_KS: snprintf(buf, len, "lora::lora_fwd_ks_kernel<%s, %s, %s>", b(x.grp), b(x.full), b(x.dma)); break;
+    case K_FWD_KS:
+      snprintf(buf, len, "lora::lora_fwd_ks_kernel<%s, %s, %s, %s>", b(x.grp), b(x.full), b(x.dma), b(x.upre));
+      break;
     case K_DU: snprintf(buf, len, "lora::lora_bwd_du_kernel<%d, %d>", x.rp, x.tpw); break;
     case K_TOKRED:
       if (x.drop) snprintf(buf, len, "lora::lora_tokred_kernel<%d, true>", x.rp);

@@ -49,7 +49,13 @@ def check(t, shape, keep, p, out):
 SHAPES = [Shape("drop_tiny", 256, 512, 512, 8, 16.0, 21), Shape("drop_ragged", 200, 264, 320, 5, 10.0, 22),
           Shape("drop_128x256", 2000, 4000, 1024, 5, 10.0, 28),  # the 128 x 256 tile, ragged m and n
           Shape("drop_r33", 130, 136, 192, 33, 66.0, 23), Shape("drop_r64", 264, 392, 448, 64, 128.0, 24),
-          Shape("drop_r16", 520, 1032, 640, 16, 32.0, 25)]
+          Shape("drop_r16", 520, 1032, 640, 16, 32.0, 25),
+          Shape("drop_256x256", 1536, 8192, 256, 8, 16.0, 29),    # the 256 x 256 tile reading U back
+          Shape("drop_ks_rounds", 2560, 8192, 256, 13, 26.0, 30),  # k-split tile over several rounds
+          # the masked U pass with 32 tokens per workgroup (8192 tokens and more) at padded ranks 16, 32, 64,
+          # and with 16 at rank 32
+          Shape("drop_m8192", 8200, 264, 256, 8, 16.0, 31), Shape("drop_m8192_r24", 8192, 136, 128, 24, 48.0, 32),
+          Shape("drop_m8192_r64", 8192, 128, 192, 64, 128.0, 33), Shape("drop_r24", 300, 264, 192, 24, 48.0, 34)]
 
 
 @pytest.mark.parametrize("shape", SHAPES, ids=lambda s: s.name)
@@ -73,13 +79,14 @@ def test_dropout_keep_all_matches_plain_path():
     keep = np.full((shape.m, shape.k // 8), 0xFF, dtype=np.uint8)
     got = run_dropout(t, shape, keep, 0.0)
     plain = run_gpu(t, shape)
-    for x in ("Y", "U"):
-        assert np.array_equal(got[x], plain[x]), x
-    # the two paths reduce dA and dB with different kernels (the masked one
-    # stages X through registers), so their fp32 sums differ in order only
-    for x in ("dA", "dB"):
-        assert rel(got[x], plain[x]) <= 1e-6, x
-    assert rel(f64(got["dX"]), f64(plain["dX"])) <= 1e-3
+    # the two paths form U (the U pass against the tile) and reduce dA and dB
+    # (the masked reduction stages X through registers) with different
+    # kernels, so their fp32 sums differ in order only; Y and dX then differ
+    # by at most the odd flipped bf16 rounding
+    for x in ("U", "dA", "dB"):
+        assert rel(got[x], plain[x]) <= 1e-5, x
+    for x in ("Y", "dX"):
+        assert rel(f64(got[x]), f64(plain[x])) <= 1e-3, x
     check(t, shape, keep, 0.0, got)
 
 

@@ -52,6 +52,7 @@ RAGGED = [
     Shape("ragged", 1500, 3000, 2056, 13, 26.0, 111),
     Shape("ragged", 3900, 4864, 5056, 13, 26.0, 112),    # forward and dX columns split between two tiles
     Shape("ragged", 4000, 5000, 264, 5, 10.0, 113),      # forward split, ragged second part
+    Shape("ragged", 8200, 136, 200, 24, 48.0, 114),      # U pass with 32 tokens per workgroup at padded rank 32
 ]
 
 

@@ -5,6 +5,7 @@ import pytest
 
 from lora_synth import CONFIGS
 from test_gpu_parity import DEPTH, EXACT, FULL, RAGGED, SPLIT_EDGE
+from test_gpu_dropout import SHAPES as DROP_SHAPES
 from test_gpu_group import CASES as GROUP_CASES, EXACT_CASES as GROUP_EXACT, FULL_GROUPS
 
 
@@ -67,9 +68,45 @@ def test_bench_workload_kernels(lora):
     into LDS, and the 128 x 256 direct-to-LDS dX."""
     s = CONFIGS["llama2_7b_q_proj"][0]
     assert [x["kernel"] for x in lora.lora_linear_plan("fwd", s.m, s.n, s.k, s.r)] == \
-        ["lora::lora_fwd_ks_kernel<false, true, true>"]
+        ["lora::lora_fwd_ks_kernel<false, true, true, false>"]
     assert lora.lora_linear_plan("bwd", s.m, s.n, s.k, s.r)[-1]["kernel"] == \
         "lora::lora_bwd_dx_kernel<128, 256, 2, 4, 16, false, false, true>"
+
+
+@pytest.mark.parametrize("s", SINGLE, ids=lambda s: f"{s.name}-m{s.m}n{s.n}k{s.k}r{s.r}")
+def test_dropout_forward_is_masked_u_pass_then_plain_tiles(lora, s):
+    """Under dropout the forward is the U pass with the keep mask, then the
+    tiles the plain forward takes (each reading U back)."""
+    if s.k % 64:
+        return
+    plain = lora.lora_linear_plan("fwd", s.m, s.n, s.k, s.r)
+    drop = lora.lora_linear_plan("fwd_dropout", s.m, s.n, s.k, s.r)
+    rp = 16 if s.r <= 16 else (32 if s.r <= 32 else 64)
+    assert drop[0]["kernel"].startswith(f"lora::lora_u_kernel<{rp}, ") and drop[0]["kernel"].endswith(", true>")
+    assert [x["tile"] for x in _gemms(drop)] == [x["tile"] for x in _gemms(plain)]
+    assert [x["cols"] for x in _gemms(drop)] == [x["cols"] for x in _gemms(plain)]
+    for x in _gemms(drop):   # every GEMM of the dropout forward reads U back
+        k = x["kernel"]
+        assert k.endswith("true>") if "ks_kernel" in k else k.split(",")[7].strip() == "true", k
+
+
+def test_dropout_suite_reaches_every_dropout_forward_variant(lora):
+    seen = {x["kernel"] for s in DROP_SHAPES for x in lora.lora_linear_plan("fwd_dropout", s.m, s.n, s.k, s.r)}
+    for want in ("lora::lora_u_kernel<16, 16, true>", "lora::lora_u_kernel<16, 32, true>",
+                 "lora::lora_u_kernel<32, 16, true>", "lora::lora_u_kernel<32, 32, true>",
+                 "lora::lora_u_kernel<64, 16, true>", "lora::lora_u_kernel<64, 32, true>",
+                 "lora::lora_fwd_ks_kernel<false, true, true, true>",
+                 "lora::lora_fwd_ks_kernel<false, true, false, true>",
+                 "lora::lora_fwd_kernel<256, 256, 2, 4, 16, false, false, true, true, true>",
+                 "lora::lora_fwd_kernel<128, 128, 2, 2, 16, false, false, true, true, false>"):
+        assert want in seen, (want, sorted(seen))
+
+
+def test_parity_suites_reach_every_plain_u_pass(lora):
+    seen = {x["kernel"] for s in SINGLE for x in lora.lora_linear_plan("fwd", s.m, s.n, s.k, s.r)}
+    for want in ("lora::lora_u_kernel<32, 16, false>", "lora::lora_u_kernel<32, 32, false>",
+                 "lora::lora_u_kernel<64, 16, false>", "lora::lora_u_kernel<64, 32, false>"):
+        assert want in seen, (want, sorted(x for x in seen if "u_kernel" in x))
 
 
 def test_ragged_n_avoids_the_register_staged_256_tile(lora):
