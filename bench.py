@@ -157,7 +157,7 @@ def algorithmic_units(s, launch):
     c0, c1 = launch["cols"]
     if "lora_fwd_kernel" in name or "lora_fwd_ks_kernel" in name:
         cols = c1 - c0
-        upre = name.startswith("lora::lora_fwd_kernel") and name.split(",")[7].strip() == "true"
+        upre = name.startswith("lora::lora_fwd_kernel") and name.split(",")[6].strip() == "true"
         u = 0 if (upre or c0 > 0) else 2 * m * k * r
         return "flop", 2 * m * cols * k + 2 * m * cols * r + u
     if "lora_bwd_dx_kernel" in name:

@@ -1,15 +1,17 @@
 // Forward of the LoRA-adapted linear layer (Eq. 1 of JORA, Section 3):
 //   U = X A^T,   Y = X W^T + s U B^T,   s = alpha / r.
 //
-// Kernels (one launch per call; a U pass before it for rank > 16, and a
-// second GEMM launch when the columns are split between two tiles):
-//   lora_fwd_ks_kernel  the 128 x 256 tile for rank <= 16 without dropout
-//                       (the 7B q_proj shape): wave pairs split the k
-//                       substeps of each stage, see its own comment.
-//   lora_fwd_kernel     the other tiles (256 x 256, 128 x 256, 128 x 128),
-//                       dropout and grouped launches; described below.
-//   lora_u_kernel       U = X A^T on its own for rank > 16, followed by
-//                       lora_fwd_kernel without U columns.
+// Kernels (one launch per call; a U pass before it for rank > 16 and under
+// dropout, and a second GEMM launch when the columns are split between two
+// tiles):
+//   lora_fwd_ks_kernel  the 128 x 256 tile for rank <= 16 (the 7B q_proj
+//                       shape): wave pairs split the k substeps of each
+//                       stage, see its own comment.
+//   lora_fwd_kernel     the other tiles (256 x 256, 128 x 256, 128 x 128)
+//                       and grouped launches; described below.
+//   lora_u_kernel       U = X A^T on its own (under dropout with the keep
+//                       mask applied), followed by a GEMM tile without U
+//                       columns.
 // A launch covers the output columns from n_begin on (plan_gemm_split);
 // the launch whose range starts at column 0 writes U.
 //
@@ -50,16 +52,16 @@ namespace lora {
 // KFULL (k a multiple of 64): the loads carry no k-bound checks, and below the
 // 256 x 256 tile the stages run in pairs with compile-time LDS buffers.
 //
-// DMA (the 256 x 256 tile with KFULL, no dropout): each stage is copied from
+// DMA (the 256 x 256 tile with KFULL): each stage is copied from
 // global memory straight into the free LDS buffer at the top of the stage
 // before it (one 16-byte chunk per lane per copy instruction, the swizzle
 // applied to the global addresses), with no staging registers; the stage's
 // closing barrier waits for those copies (copy_barrier).
-template <int BM, int BN, int WM, int WN, int RP, bool DROP, bool GRP, bool UPRE, bool KFULL, bool DMA>
+template <int BM, int BN, int WM, int WN, int RP, bool GRP, bool UPRE, bool KFULL, bool DMA>
 __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
     const u16* __restrict__ X, const u16* __restrict__ W, const u16* __restrict__ A,
-    const u16* __restrict__ B, const uint8_t* __restrict__ keep, u16* __restrict__ Y,
-    float* __restrict__ U, int m, int n, int k, int r, float s, float inv_keep, int tiles_m, int tiles_n,
+    const u16* __restrict__ B, u16* __restrict__ Y,
+    float* __restrict__ U, int m, int n, int k, int r, float s, int tiles_m, int tiles_n,
     int n_begin, FwdGroup grp) {
   constexpr int NW = WM * WN;
   constexpr int NT = 64 * NW;
@@ -80,10 +82,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
   constexpr int GPW = U16 ? (WTI / 16) / WN : 1;
   constexpr int RPS = UPRE ? 0 : RP;             // A rows staged per stage
   constexpr int ROWS = BM + BN + RPS;            // 128-byte rows per 64-wide stage
-  // With dropout the stage also holds the keep bits of its X rows: 8 bytes
-  // (64 k) per row.
-  constexpr int KS_OFF = ROWS * 128;
-  constexpr int STAGE = KS_OFF + (DROP ? BM * 8 : 0);
+  constexpr int STAGE = ROWS * 128;
   constexpr int CX = BM * 8, CW = BN * 8, CA = RPS * 8;  // 16-byte chunks per region
   constexpr int LX = (CX + NT - 1) / NT, LW = (CW + NT - 1) / NT, LA = UPRE ? 1 : (CA + NT - 1) / NT;
   static_assert(WTI % 32 == 0 && WTJ % 32 == 0 && (U16 || RP % 32 == 0), "32x32 fragments");
@@ -123,9 +122,6 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
   const __amdgpu_buffer_rsrc_t rsX = make_rsrc(X + (size_t)m0 * k, (uint64_t)min(BM, m - m0) * rowbytes);
   const __amdgpu_buffer_rsrc_t rsW = make_rsrc(W + (size_t)n0 * k, (uint64_t)min(BN, n - n0) * rowbytes);
   const __amdgpu_buffer_rsrc_t rsA = make_rsrc(A, (uint64_t)r * rowbytes);
-  const uint32_t kb8 = (uint32_t)k / 8;          // keep-mask bytes per row (k % 64 == 0 with dropout)
-  const __amdgpu_buffer_rsrc_t rsK = make_rsrc(DROP ? (const void*)(keep + (size_t)m0 * kb8) : (const void*)X,
-                                                DROP ? (uint64_t)min(BM, m - m0) * kb8 : 0);
 
   // Register staging of one k-block of the three regions: thread chunk
   // q = tid + i NT of a region is row q/8, k-chunk q%8 (coalesced 128-byte
@@ -134,10 +130,8 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
   // 3 = A rows.
   constexpr int LW1 = (LW + 1) / 2;
   int4v gx[LX], gw[LW], ga[LA];
-  uint2 gk = uint2{0u, 0u};   // keep bits of row tid for this k-block (dropout; tid < BM)
   auto gload = [&](int kb, int piece) LORA_INLINE {
     const int k0 = kb * 64;
-    if (DROP && piece == 0 && wave * 64 < BM) gk = buf_load8(rsK, (uint32_t)tid * kb8 + (uint32_t)kb * 8);
     if (piece == 0) {
 #pragma unroll
       for (int i = 0; i < LX; ++i) {
@@ -166,7 +160,6 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
   };
   auto swrite = [&](int buf, int piece) LORA_INLINE {
     char* sb = smem + buf * STAGE;
-    if (DROP && piece == 0 && wave * 64 < BM) *reinterpret_cast<uint2*>(sb + KS_OFF + tid * 8) = gk;
     if (piece == 0) {
 #pragma unroll
       for (int i = 0; i < LX; ++i) {
@@ -227,28 +220,19 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
     for (int fj = 0; fj < FJ; ++fj) fw[p][fj] = kc_read(Ws, wn * WTJ + 32 * fj + c32, ch);
 #pragma unroll
     for (int fi = 0; fi < FI; ++fi) fx[p][fi] = kc_read(Xs, wm * WTI + 32 * fi + c32, ch);
-    // Dropout acts on the U operand only (the W path reads X unmasked): each
-    // 8-k chunk of a row has one keep byte in the stage.
-    const uint8_t* Ks = reinterpret_cast<const uint8_t*>(sb + KS_OFF);
     if (UPRE) {
     } else if (U16) {
       if (ks % 2 == 0) {   // the 32-wide half starting at substep ks: chunks 2 ks + g16
         fa16[p] = kc_read(As, c16, 2 * ks + g16);
 #pragma unroll
-        for (int gg = 0; gg < GPW; ++gg) {
-          fxu16[p][gg] = kc_read(Xs, urow16[gg], 2 * ks + g16);
-          if (DROP) fxu16[p][gg] = keep_mask8(fxu16[p][gg], Ks[urow16[gg] * 8 + 2 * ks + g16]);
-        }
+        for (int gg = 0; gg < GPW; ++gg) fxu16[p][gg] = kc_read(Xs, urow16[gg], 2 * ks + g16);
       }
     } else if (ks % NDUP == 0) {
       const int uch = ch + 2 * udup;
 #pragma unroll
       for (int ft = 0; ft < FT; ++ft) fa[p][ft] = kc_read(As, 32 * ft + c32, uch);
 #pragma unroll
-      for (int fu = 0; fu < FUW; ++fu) {
-        fxu[p][fu] = kc_read(Xs, urow[fu], uch);
-        if (DROP) fxu[p][fu] = keep_mask8(fxu[p][fu], Ks[urow[fu] * 8 + uch]);
-      }
+      for (int fu = 0; fu < FUW; ++fu) fxu[p][fu] = kc_read(Xs, urow[fu], uch);
     }
   };
   auto multiply = [&](int p, int ks) LORA_INLINE {
@@ -314,7 +298,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
   using B1 = std::integral_constant<int, 1>;
   using BR = std::integral_constant<int, -1>;
   if constexpr (DMA) {
-    static_assert(KFULL && !DROP && !ROT, "copy pipeline shape");
+    static_assert(KFULL && !ROT, "copy pipeline shape");
     // Copy instruction j of a region covers its rows 8j .. 8j+7: lane l takes
     // position l % 8 of row 8j + l / 8, i.e. logical chunk (l % 8) ^ kc_swz(row).
     constexpr int JX = BM / 8, JW = BN / 8, JA = RPS / 8;
@@ -397,8 +381,6 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
     const int q = tid + i * NT;
     bv[i] = buf_load16(rsB, q < nch ? (uint32_t)q * 16 : kOOB);
   }
-  // (with dropout the accumulated products are scaled by 1 / (1 - p) here)
-  const float uscale = DROP ? inv_keep : 1.0f;
   if (UPRE) {   // U of the tile's tokens from the U pass (zero beyond r and m)
     for (int e = tid; e < BM * RP; e += NT) {
       const int il = e / RP, t = e - il * RP;
@@ -408,7 +390,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
 #pragma unroll
     for (int gg = 0; gg < GPW; ++gg)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) Us[urow16[gg] * RP + 4 * g16 + q] = uscale * uacc16[gg][q];
+      for (int q = 0; q < 4; ++q) Us[urow16[gg] * RP + 4 * g16 + q] = uacc16[gg][q];
   } else {
 #pragma unroll
     for (int fu = 0; fu < FUW; ++fu) {
@@ -418,7 +400,7 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
 #pragma unroll
         for (int q = 0; q < 16; ++q) {
           const int t = 32 * ft + 8 * (q >> 2) + 4 * g + (q & 3);
-          Us[(udup * BM + il) * RP + t] = uscale * uacc[ft][fu][q];
+          Us[(udup * BM + il) * RP + t] = uacc[ft][fu][q];
         }
     }
   }
@@ -1073,9 +1055,9 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
 // the U pass for single projections of rank above 16 and under dropout
 // (where the pass applies the keep mask), in the tile for groups and rank 16;
 // the 128 x 256 tile at rank 16 is the k-split kernel's.
-template <int BM, int BN, int RP, bool DROP, bool GRP, bool UPRE, bool KFULL, bool DMA>
+template <int BM, int BN, int RP, bool GRP, bool UPRE, bool KFULL, bool DMA>
 constexpr bool fwd_instantiated() {
-  return !DROP && !(BM == 128 && BN == 256 && RP == 16) && (UPRE ? !GRP : (RP == 16 || GRP)) &&
+  return !(BM == 128 && BN == 256 && RP == 16) && (UPRE ? !GRP : (RP == 16 || GRP)) &&
          DMA == (KFULL && BM == 256 && BN == 256);
 }
 
@@ -1123,23 +1105,21 @@ static hipError_t run_fwd_launch(const Launch& L, const FwdArgs& a, const FwdGro
     constexpr int T = decltype(tc)::value;
     constexpr int BM = T == 0 ? 256 : 128, BN = T == 2 ? 128 : 256, WN = T == 2 ? 2 : 4;
     return with_int<16, 32, 64>(L.rp, [&](auto rc) {
-      return with_bool(L.drop, [&](auto dr) {
-        return with_bool(L.grp, [&](auto gr) {
-          return with_bool(L.upre, [&](auto up) {
-            return with_bool(L.full, [&](auto kf) {
-              return with_bool(L.dma, [&](auto dm) {
-                constexpr int RP = decltype(rc)::value;
-                constexpr bool DROP = decltype(dr)::value, GRP = decltype(gr)::value, UPRE = decltype(up)::value,
-                               KF = decltype(kf)::value, DMA = decltype(dm)::value;
-                if constexpr (!fwd_instantiated<BM, BN, RP, DROP, GRP, UPRE, KF, DMA>()) {
-                  return hipErrorInvalidValue;
-                } else {
-                  hipLaunchKernelGGL((lora_fwd_kernel<BM, BN, 2, WN, RP, DROP, GRP, UPRE, KF, DMA>), grid, block, 0,
-                                     st, a.X, a.W, a.A, a.B, a.keep, a.Y, a.U, (int)a.m, (int)a.n, (int)a.k,
-                                     (int)a.r, a.s, a.inv_keep, L.tiles_m, L.tiles_n, (int)L.col_begin, grp);
-                  return hipGetLastError();
-                }
-              });
+      return with_bool(L.grp, [&](auto gr) {
+        return with_bool(L.upre, [&](auto up) {
+          return with_bool(L.full, [&](auto kf) {
+            return with_bool(L.dma, [&](auto dm) {
+              constexpr int RP = decltype(rc)::value;
+              constexpr bool GRP = decltype(gr)::value, UPRE = decltype(up)::value, KF = decltype(kf)::value,
+                             DMA = decltype(dm)::value;
+              if constexpr (!fwd_instantiated<BM, BN, RP, GRP, UPRE, KF, DMA>()) {
+                return hipErrorInvalidValue;
+              } else {
+                hipLaunchKernelGGL((lora_fwd_kernel<BM, BN, 2, WN, RP, GRP, UPRE, KF, DMA>), grid, block, 0, st,
+                                   a.X, a.W, a.A, a.B, a.Y, a.U, (int)a.m, (int)a.n, (int)a.k, (int)a.r, a.s,
+                                   L.tiles_m, L.tiles_n, (int)L.col_begin, grp);
+                return hipGetLastError();
+              }
             });
           });
         });

@@ -16,7 +16,7 @@ namespace lora {
 
 enum KernelId : int {
   K_UPASS = 0,     // lora_u_kernel<RP, TPW, KEEP>: U = X A^T on its own (rank > 16, and under dropout)
-  K_FWD = 1,       // lora_fwd_kernel<BM, BN, WM, WN, RP, DROP, GRP, UPRE, KFULL, DMA>
+  K_FWD = 1,       // lora_fwd_kernel<BM, BN, WM, WN, RP, GRP, UPRE, KFULL, DMA>
   K_FWD_KS = 2,    // lora_fwd_ks_kernel<GRP, KFULL, DMA, UPRE>
   K_DU = 3,        // lora_bwd_du_kernel<RP, TPW>
   K_TOKRED = 4,    // lora_tokred_dma_kernel<RP>, or lora_tokred_kernel<RP, true> with a keep mask
@@ -293,8 +293,8 @@ inline void launch_name(const Launch& x, char* buf, size_t len) {
   switch (x.id) {
     case K_UPASS: snprintf(buf, len, "lora::lora_u_kernel<%d, %d, %s>", x.rp, x.tpw, b(x.drop)); break;
     case K_FWD:
-      snprintf(buf, len, "lora::lora_fwd_kernel<%d, %d, %d, %d, %d, %s, %s, %s, %s, %s>", x.bm, x.bn, x.wm, x.wn,
-               x.rp, b(x.drop), b(x.grp), b(x.upre), b(x.full), b(x.dma));
+      snprintf(buf, len, "lora::lora_fwd_kernel<%d, %d, %d, %d, %d, %s, %s, %s, %s>", x.bm, x.bn, x.wm, x.wn, x.rp,
+               b(x.grp), b(x.upre), b(x.full), b(x.dma));
       break;
     case K_FWD_KS:
       snprintf(buf, len, "lora::lora_fwd_ks_kernel<%s, %s, %s, %s>", b(x.grp), b(x.full), b(x.dma), b(x.upre));

@@ -87,7 +87,7 @@ def test_dropout_forward_is_masked_u_pass_then_plain_tiles(lora, s):
     assert [x["cols"] for x in _gemms(drop)] == [x["cols"] for x in _gemms(plain)]
     for x in _gemms(drop):   # every GEMM of the dropout forward reads U back
         k = x["kernel"]
-        assert k.endswith("true>") if "ks_kernel" in k else k.split(",")[7].strip() == "true", k
+        assert k.endswith("true>") if "ks_kernel" in k else k.split(",")[6].strip() == "true", k
 
 
 def test_dropout_suite_reaches_every_dropout_forward_variant(lora):
@@ -97,8 +97,8 @@ def test_dropout_suite_reaches_every_dropout_forward_variant(lora):
                  "lora::lora_u_kernel<64, 16, true>", "lora::lora_u_kernel<64, 32, true>",
                  "lora::lora_fwd_ks_kernel<false, true, true, true>",
                  "lora::lora_fwd_ks_kernel<false, true, false, true>",
-                 "lora::lora_fwd_kernel<256, 256, 2, 4, 16, false, false, true, true, true>",
-                 "lora::lora_fwd_kernel<128, 128, 2, 2, 16, false, false, true, true, false>"):
+                 "lora::lora_fwd_kernel<256, 256, 2, 4, 16, false, true, true, true>",
+                 "lora::lora_fwd_kernel<128, 128, 2, 2, 16, false, true, true, false>"):
         assert want in seen, (want, sorted(seen))
 
 
