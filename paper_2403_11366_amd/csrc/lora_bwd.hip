@@ -1624,7 +1624,7 @@ hipError_t launch_bwd_fused(const BwdArgs& a, hipStream_t st) {
       if (e != hipSuccess) return e;
     } else if (L.id == K_TOKRED) {
       const RedProblem pap{dUt2, a.X, pa, k, (int)BL.plan_a.span, BL.plan_a.col_tiles, nullptr};
-      hipLaunchKernelGGL((lora_tokred_kernel<16, false>), grid, block, 0, st, pap, pap, (int)L.grid, m, mp);
+      hipLaunchKernelGGL((lora_tokred_dma_kernel<16>), grid, block, 0, st, pap, pap, (int)L.grid, m, mp);
       const hipError_t e = hipGetLastError();
       if (e != hipSuccess) return e;
     } else if (L.id == K_FINALIZE) {
@@ -1734,7 +1734,7 @@ hipError_t launch_bwd_group(const GroupBwdArgs& a, hipStream_t st) {
       const RedProblem pap{dut_stack, a.X, pa_stack, (int)a.k, (int)GL.plan_a.span, GL.plan_a.col_tiles, nullptr};
       const BwdArgs b = member_args(0, GL);
       e = with_int<32, 48, 64>(L.rp, [&](auto rc) {
-        hipLaunchKernelGGL((lora_tokred_kernel<decltype(rc)::value, false>), dim3((unsigned)L.grid),
+        hipLaunchKernelGGL((lora_tokred_dma_kernel<decltype(rc)::value>), dim3((unsigned)L.grid),
                            dim3((unsigned)L.block), 0, st, pap, pap, (int)L.grid, (int)b.m, (int)GL.L[0].mp);
         return hipGetLastError();
       });
