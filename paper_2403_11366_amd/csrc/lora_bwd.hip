@@ -198,6 +198,223 @@ __global__ __launch_bounds__(512) void lora_bwd_du_kernel(
 }
 
 // ---------------------------------------------------------------------------
+// Wait until at most N LDS operations of this wave are outstanding, in an asm
+// statement that takes a substep's fragment registers as operands (so no use
+// of them can move above it): TG dY fragments, FT pairs of B^T halves.
+template <int N, int FT, int TG>
+__device__ __forceinline__ void du_frag_wait(short8 (&y)[TG], short4v (&bl)[FT], short4v (&bh)[FT]) {
+  static_assert(N >= 0 && N <= 15, "lgkmcnt range");
+#define LORA_DU_WAIT(...) asm volatile("s_waitcnt lgkmcnt(%[cnt])" : __VA_ARGS__ : [cnt] "i"(N))
+  if constexpr (FT == 1 && TG == 1) LORA_DU_WAIT("+v"(y[0]), "+v"(bl[0]), "+v"(bh[0]));
+  else if constexpr (FT == 1 && TG == 2) LORA_DU_WAIT("+v"(y[0]), "+v"(y[1]), "+v"(bl[0]), "+v"(bh[0]));
+  else if constexpr (FT == 2 && TG == 1) LORA_DU_WAIT("+v"(y[0]), "+v"(bl[0]), "+v"(bh[0]), "+v"(bl[1]), "+v"(bh[1]));
+  else if constexpr (FT == 2 && TG == 2)
+    LORA_DU_WAIT("+v"(y[0]), "+v"(y[1]), "+v"(bl[0]), "+v"(bh[0]), "+v"(bl[1]), "+v"(bh[1]));
+  else if constexpr (FT == 3 && TG == 1)
+    LORA_DU_WAIT("+v"(y[0]), "+v"(bl[0]), "+v"(bh[0]), "+v"(bl[1]), "+v"(bh[1]), "+v"(bl[2]), "+v"(bh[2]));
+  else if constexpr (FT == 3 && TG == 2)
+    LORA_DU_WAIT("+v"(y[0]), "+v"(y[1]), "+v"(bl[0]), "+v"(bh[0]), "+v"(bl[1]), "+v"(bh[1]), "+v"(bl[2]),
+                 "+v"(bh[2]));
+  else if constexpr (FT == 4 && TG == 1)
+    LORA_DU_WAIT("+v"(y[0]), "+v"(bl[0]), "+v"(bh[0]), "+v"(bl[1]), "+v"(bh[1]), "+v"(bl[2]), "+v"(bh[2]),
+                 "+v"(bl[3]), "+v"(bh[3]));
+  else {
+    static_assert(FT == 4 && TG == 2, "fragment shapes");
+    LORA_DU_WAIT("+v"(y[0]), "+v"(y[1]), "+v"(bl[0]), "+v"(bh[0]), "+v"(bl[1]), "+v"(bh[1]), "+v"(bl[2]),
+                 "+v"(bh[2]), "+v"(bl[3]), "+v"(bh[3]));
+  }
+#undef LORA_DU_WAIT
+}
+
+// ---------------------------------------------------------------------------
+// dU = s dY B for ranks that are multiples of 8 (each 16-byte piece of B then
+// lies inside one row), fed by copies straight into LDS.  TPW (8, 16 or 32)
+// tokens per workgroup, four waves; the n loop runs in stages of 64: wave w
+// takes stages w, w + 4, ... and copies each of them (its TPW dY rows, 8 rows
+// of 128 bytes per copy instruction with the swizzle of kc_offset applied to
+// the global addresses, and the stage's 64 rows of B as a [64][RP] block,
+// zero past r) straight into a private ring of NSW LDS stages, NSW - 1
+// stages ahead, waiting only for its own copies (no barrier in the loop).
+// (The register-loading kernel above reads 16 rows x 64 bytes of dY per
+// instruction, which keeps the L1 busy translating addresses.)  Each wave
+// accumulates all of dU^T for its stages on 16x16x32 products: B^T fragments
+// by transposing reads of the B block, dY fragments as the second operand
+// (TPW = 8 leaves token columns 8..15 zero); the fragment reads are issued as
+// inline assembly with counted waits, since the compiler would otherwise wait
+// for every copy in flight before each transposing read.  The four partial
+// sums are added in wave order through LDS, then written as the register
+// kernel does (dU2, dUt2, Ut2).
+template <int RP, int TPW>
+__global__ __launch_bounds__(256) void lora_bwd_du_dma_kernel(
+    const u16* __restrict__ dY, const u16* __restrict__ B, const float* __restrict__ U,
+    u16* __restrict__ dU2, u16* __restrict__ dUt2, u16* __restrict__ Ut2,
+    int m, int n, int r, int mp, float s) {
+  constexpr int NWV = 4;
+  constexpr int FT = RP / 16;
+  constexpr int TG = TPW >= 16 ? TPW / 16 : 1;
+  constexpr int YR = TG * 16;                    // dY rows per stage in LDS (TPW = 8: rows 8..15 stay zero)
+  constexpr int BOFF = YR * 128;                 // the B block [64][RP] after the dY rows
+  constexpr int STAGE = BOFF + 64 * RP * 2;
+  constexpr int CY = TPW / 8, CB = RP / 8;       // 1 KB copies per stage: dY rows, B block
+  constexpr int CPW = CY + CB;
+  constexpr int NSW = (156 * 1024) / (NWV * STAGE) < 6 ? (156 * 1024) / (NWV * STAGE) : 6;
+  constexpr int RED = NWV * TG * FT * 64 * 16;   // cross-wave sum [NWV][TG][FT][64] float4
+  constexpr int SMEM = NWV * NSW * STAGE > RED ? NWV * NSW * STAGE : RED;
+  constexpr int NRD = TG + 2 * FT;               // LDS reads per wave and 32-wide substep
+  static_assert(TPW == 8 || TPW == 16 || TPW == 32, "tokens per workgroup");
+  static_assert(NSW >= 3 && CPW * (NSW - 2) < 64, "copies in flight fit the wait counter");
+  static_assert(NRD <= 15, "reads of one substep fit the LDS wait counter");
+  __shared__ __attribute__((aligned(1024))) char sm[SMEM];
+  const int i0 = blockIdx.x * TPW;
+  const int tid = threadIdx.x, lane = tid & 63, wave = uniform(tid >> 6);
+  const int g = lane >> 4, c16 = lane & 15;
+  const uint32_t rowbytes = (uint32_t)n * 2;
+  const int rows = uniform(max(0, min(TPW, m - i0)));
+  const __amdgpu_buffer_rsrc_t rsY = make_rsrc(dY + (size_t)i0 * n, (uint64_t)rows * rowbytes);
+  const __amdgpu_buffer_rsrc_t rsB = make_rsrc(B, (uint64_t)n * r * 2);
+  char* ring = sm + wave * NSW * STAGE;
+  if (YR > TPW) {   // the zero token rows of TPW = 8, in every stage of the ring
+    for (int e = lane; e < NSW * (YR - TPW) * 8; e += 64) {
+      const int st = e / ((YR - TPW) * 8), q = e % ((YR - TPW) * 8);
+      reinterpret_cast<int4v*>(ring + st * STAGE + TPW * 128)[q] = int4v{0, 0, 0, 0};
+    }
+  }
+
+  // Copy c of the dY rows: rows 8c + lane/8 at physical chunk lane%8, which
+  // holds logical chunk (lane%8) ^ kc_swz(row).  Copy c of the B block: its
+  // bytes 1024c + 16 lane, i.e. row (1024c + 16 lane) / (2 RP) of the stage
+  // and 8-element chunk ((1024c + 16 lane) % (2 RP)) / 16.
+  const int nst = (n + 63) / 64;
+  auto issue = [&](int j, int buf) LORA_INLINE {
+    const int st = wave + NWV * j;
+    const int j0 = st * 64;
+    const bool live = st < nst;
+    char* sb = ring + buf * STAGE;
+#pragma unroll
+    for (int c = 0; c < CY; ++c) {
+      const int row = 8 * c + (lane >> 3);
+      const int jj = j0 + 8 * ((lane & 7) ^ kc_swz(row));
+      dma16(rsY, live && jj < n ? (uint32_t)row * rowbytes + (uint32_t)jj * 2 : kOOB, 0, sb + c * 1024);
+    }
+#pragma unroll
+    for (int c = 0; c < CB; ++c) {
+      const int byte = 1024 * c + 16 * lane;
+      const int row = byte / (2 * RP), t0 = (byte % (2 * RP)) / 2;
+      const int jb = j0 + row;
+      dma16(rsB, live && jb < n && t0 < r ? ((uint32_t)jb * (uint32_t)r + (uint32_t)t0) * 2 : kOOB, 0,
+            sb + BOFF + c * 1024);
+    }
+  };
+
+  // Lane addresses in stage 0 of the wave's ring.  dY fragment (second
+  // operand, 32 n x 16 tokens) of substep kk: row c16 (+ 2048 bytes per token
+  // group), chunk 4 kk + g.  B^T fragment (first operand, 16 t x 32 n) as in
+  // tr16_read: rows 8 g + e (+ 4 rows for the second read, + 32 rows for kk),
+  // columns 16 ft + 4 q.
+  uint32_t ya[2], ba;
+#pragma unroll
+  for (int kk = 0; kk < 2; ++kk) ya[kk] = lds_addr(ring + kc_offset(c16, 4 * kk + g));
+  {
+    const int j = lane & 15, e = j >> 2, q = j & 3;
+    ba = lds_addr(ring + BOFF + (8 * g + e) * (2 * RP) + 4 * q * 2);
+  }
+  floatx4 acc[TG][FT];
+#pragma unroll
+  for (int tg = 0; tg < TG; ++tg)
+#pragma unroll
+    for (int ft = 0; ft < FT; ++ft) acc[tg][ft] = floatx4{0.f, 0.f, 0.f, 0.f};
+  short8 fy[2][TG];
+  short4v fbl[2][FT], fbh[2][FT];
+  auto reads = [&](uint32_t boff, auto kkc) LORA_INLINE {
+    constexpr int kk = decltype(kkc)::value;
+    ds_read_b128_asm<0>(fy[kk][0], ya[kk] + boff);
+    if constexpr (TG > 1) ds_read_b128_asm<2048>(fy[kk][1], ya[kk] + boff);
+#pragma unroll
+    for (int ft = 0; ft < FT; ++ft) {
+      // (ft, kk) immediates: 32 ft bytes of columns, 32 rows of 2 RP bytes per kk
+      const uint32_t a = ba + boff + (uint32_t)(32 * ft);
+      ds_read_tr_b64_asm<kk * 32 * 2 * RP>(fbl[kk][ft], a);
+      ds_read_tr_b64_asm<kk * 32 * 2 * RP + 4 * 2 * RP>(fbh[kk][ft], a);
+    }
+  };
+  auto mult = [&](int kk) LORA_INLINE {
+#pragma unroll
+    for (int ft = 0; ft < FT; ++ft) {
+      const short8 bt = join4(fbl[kk][ft], fbh[kk][ft]);
+#pragma unroll
+      for (int tg = 0; tg < TG; ++tg) acc[tg][ft] = mfma16x16x32(bt, fy[kk][tg], acc[tg][ft]);
+    }
+  };
+  using K0 = std::integral_constant<int, 0>;
+  using K1 = std::integral_constant<int, 1>;
+  auto compute = [&](int buf) LORA_INLINE {
+    const uint32_t boff = (uint32_t)buf * STAGE;
+    if constexpr (2 * NRD <= 15) {   // both substeps' reads in flight, then the products
+      reads(boff, K0{});
+      reads(boff, K1{});
+      du_frag_wait<NRD, FT, TG>(fy[0], fbl[0], fbh[0]);   // only substep 1's reads outstanding
+      mult(0);
+      du_frag_wait<0, FT, TG>(fy[1], fbl[1], fbh[1]);
+      mult(1);
+    } else {
+      reads(boff, K0{});
+      du_frag_wait<0, FT, TG>(fy[0], fbl[0], fbh[0]);
+      mult(0);
+      reads(boff, K1{});
+      du_frag_wait<0, FT, TG>(fy[1], fbl[1], fbh[1]);
+      mult(1);
+    }
+  };
+
+  const int nsw = wave < nst ? (nst - wave + NWV - 1) / NWV : 0;   // this wave's stages
+#pragma unroll
+  for (int j = 0; j < NSW - 1; ++j) issue(j, j);
+  for (int j = 0; j < nsw; ++j) {
+    wait_vmcnt<CPW * (NSW - 2)>();   // the wave's stage j has landed
+    issue(j + NSW - 1, (j + NSW - 1) % NSW);   // into the buffer of stage j - 1, read already
+    compute(j % NSW);
+  }
+  wait_vmcnt<0>();   // the trailing copies (zeros) land before the LDS is reused
+
+  // U^T of this workgroup's tokens in bf16 (tokens >= m are zero).
+  for (int e = tid; e < RP * TPW; e += 64 * NWV) {
+    const int t = e / TPW, i = i0 + e % TPW;
+    Ut2[(size_t)t * mp + i] = f32_to_bf16((i < m && t < r) ? U[(size_t)i * r + t] : 0.f);
+  }
+
+  __syncthreads();
+  floatx4* red = reinterpret_cast<floatx4*>(sm);   // [NWV][TG][FT][64]
+#pragma unroll
+  for (int tg = 0; tg < TG; ++tg)
+#pragma unroll
+    for (int ft = 0; ft < FT; ++ft) red[((wave * TG + tg) * FT + ft) * 64 + lane] = acc[tg][ft];
+  __syncthreads();
+  for (int e = wave; e < TG * FT; e += NWV) {   // fragment e of dU^T, summed in wave order
+    const int tg = e / FT, ft = e - tg * FT;
+    floatx4 v = red[(tg * FT + ft) * 64 + lane];
+#pragma unroll
+    for (int w = 1; w < NWV; ++w) v += red[((w * TG + tg) * FT + ft) * 64 + lane];
+    if (16 * tg + c16 >= TPW) continue;   // the zero token columns of TPW = 8
+    const int i = i0 + 16 * tg + c16;     // < mp: the grid covers exactly mp tokens
+    u16 hi[4], lo[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float d = s * v[q];
+      hi[q] = f32_to_bf16(d);
+      lo[q] = f32_to_bf16(d - bf16_to_f32(hi[q]));
+    }
+    const int t = 16 * ft + 4 * g;
+    u16* row = dU2 + (size_t)i * (2 * RP);
+    *reinterpret_cast<uint2*>(row + t) =
+        uint2{(uint32_t)hi[0] | ((uint32_t)hi[1] << 16), (uint32_t)hi[2] | ((uint32_t)hi[3] << 16)};
+    *reinterpret_cast<uint2*>(row + RP + t) =
+        uint2{(uint32_t)lo[0] | ((uint32_t)lo[1] << 16), (uint32_t)lo[2] | ((uint32_t)lo[3] << 16)};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) dUt2[(size_t)(t + q) * mp + i] = hi[q];
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Token reduction part[sp][t][c] = sum over the tokens i of split sp of
 // P[t][i] * Q[i][c], t < RP, for a tile of kRedCols = 128 columns.  P is the
 // rank-r operand rounded to bf16 (U^T or s dU^T, [RP][mp]); its rounding
@@ -1535,9 +1752,13 @@ static hipError_t run_du(const Launch& L, const BwdArgs& a, const BwdLayout& BL,
   if (!dUt2) dUt2 = reinterpret_cast<u16*>(a.ws + BL.dut2);
   return with_int<16, 32, 48, 64>(L.rp, [&](auto rc) {
     return with_int<8, 16, 32>(L.tpw, [&](auto tc) {
-      hipLaunchKernelGGL((lora_bwd_du_kernel<decltype(rc)::value, decltype(tc)::value>), dim3((unsigned)L.grid),
-                         dim3((unsigned)L.block), 0, st, a.dY, a.B, a.U, dU2, dUt2, Ut2, (int)a.m, (int)a.n, (int)a.r,
-                         (int)BL.mp, a.s);
+      constexpr int RP = decltype(rc)::value, TPW = decltype(tc)::value;
+      if (L.fastb)
+        hipLaunchKernelGGL((lora_bwd_du_dma_kernel<RP, TPW>), dim3((unsigned)L.grid), dim3((unsigned)L.block), 0, st,
+                           a.dY, a.B, a.U, dU2, dUt2, Ut2, (int)a.m, (int)a.n, (int)a.r, (int)BL.mp, a.s);
+      else
+        hipLaunchKernelGGL((lora_bwd_du_kernel<RP, TPW>), dim3((unsigned)L.grid), dim3((unsigned)L.block), 0, st,
+                           a.dY, a.B, a.U, dU2, dUt2, Ut2, (int)a.m, (int)a.n, (int)a.r, (int)BL.mp, a.s);
       return hipGetLastError();
     });
   });

@@ -18,7 +18,7 @@ enum KernelId : int {
   K_UPASS = 0,     // lora_u_kernel<RP, TPW, KEEP>: U = X A^T on its own (rank > 16, and under dropout)
   K_FWD = 1,       // lora_fwd_kernel<BM, BN, WM, WN, RP, GRP, UPRE, KFULL, DMA>
   K_FWD_KS = 2,    // lora_fwd_ks_kernel<GRP, KFULL, DMA, UPRE>
-  K_DU = 3,        // lora_bwd_du_kernel<RP, TPW>
+  K_DU = 3,        // lora_bwd_du_dma_kernel<RP, TPW> (r a multiple of 8), else lora_bwd_du_kernel<RP, TPW>
   K_TOKRED = 4,    // lora_tokred_dma_kernel<RP>, or lora_tokred_kernel<RP, true> with a keep mask
   K_DX = 5,        // lora_bwd_dx_kernel<BM, BN, WM, WN, RP, DROP, GRP, FULL>
   K_DXF = 6,       // lora_bwd_dxf_kernel<FULL, FASTB>
@@ -171,15 +171,16 @@ inline void plan_dx_part(Plan& p, GemmTile t, int64_t m, int rp, int64_t cb, int
   p.add(x);
 }
 
-inline Launch du_launch(const BwdLayout& L, int member) {
+inline Launch du_launch(const BwdLayout& L, int64_t r, int member) {
   Launch x = blank_launch(K_DU);
   x.rp = L.rp;
+  x.fastb = r % 8 == 0;   // 16-byte pieces of B then lie inside one row: the direct-to-LDS kernel
   // the most tokens per workgroup (each reads all of B) that still leaves no
   // compute unit idle; 32 tokens from padded rank 32 on, where B is at least
   // as many bytes per workgroup as 16 tokens of dY
   x.tpw = L.mp / 16 < 256 ? 8 : (L.rp >= 32 && L.mp / 32 >= 256 ? 32 : 16);
   x.grid = L.mp / x.tpw;
-  x.block = 512;
+  x.block = x.fastb ? 256 : 512;
   x.member = member;
   return x;
 }
@@ -204,7 +205,7 @@ inline Launch tokred_launch(const BwdLayout& L, bool keep, int member, int part 
 inline Plan plan_bwd(int64_t m, int64_t n, int64_t k, int64_t r, bool drop) {
   const BwdLayout L = bwd_layout(m, n, k, r);
   Plan p;
-  p.add(du_launch(L, 0));
+  p.add(du_launch(L, r, 0));
   p.add(tokred_launch(L, drop, 0));
   const bool n_whole = n % 64 == 0;
   if (drop) {
@@ -229,7 +230,7 @@ inline Plan plan_group_bwd(int count, const int64_t* n, int64_t m, int64_t k, in
   Plan p;
   bool n_whole = true;
   for (int g = 0; g < count; ++g) {
-    p.add(du_launch(G.L[g], g));
+    p.add(du_launch(G.L[g], r, g));
     p.add(tokred_launch(G.L[g], false, g, G.stacked ? 1 : 0));
     n_whole = n_whole && n[g] % 64 == 0;
   }
@@ -299,7 +300,10 @@ inline void launch_name(const Launch& x, char* buf, size_t len) {
     case K_FWD_KS:
       snprintf(buf, len, "lora::lora_fwd_ks_kernel<%s, %s, %s, %s>", b(x.grp), b(x.full), b(x.dma), b(x.upre));
       break;
-    case K_DU: snprintf(buf, len, "lora::lora_bwd_du_kernel<%d, %d>", x.rp, x.tpw); break;
+    case K_DU:
+      snprintf(buf, len, x.fastb ? "lora::lora_bwd_du_dma_kernel<%d, %d>" : "lora::lora_bwd_du_kernel<%d, %d>", x.rp,
+               x.tpw);
+      break;
     case K_TOKRED:
       if (x.drop) snprintf(buf, len, "lora::lora_tokred_kernel<%d, true>", x.rp);
       else snprintf(buf, len, "lora::lora_tokred_dma_kernel<%d>", x.rp);

@@ -53,6 +53,12 @@ RAGGED = [
     Shape("ragged", 3900, 4864, 5056, 13, 26.0, 112),    # forward and dX columns split between two tiles
     Shape("ragged", 4000, 5000, 264, 5, 10.0, 113),      # forward split, ragged second part
     Shape("ragged", 8200, 136, 200, 24, 48.0, 114),      # U pass with 32 tokens per workgroup at padded rank 32
+    # dU of ranks that are not multiples of 8 (the register-loading kernel) at 16 and 32 tokens per workgroup
+    Shape("ragged", 4100, 520, 264, 13, 26.0, 115), Shape("ragged", 8200, 136, 200, 33, 66.0, 116),
+    Shape("ragged", 4096, 264, 136, 21, 42.0, 117), Shape("ragged", 2048, 264, 136, 61, 122.0, 118),
+    Shape("ragged", 8200, 72, 64, 29, 58.0, 119), Shape("ragged", 600, 136, 72, 27, 54.0, 120),
+    Shape("ragged", 4096, 136, 72, 45, 90.0, 121), Shape("ragged", 4100, 72, 136, 57, 114.0, 122),
+    Shape("ragged", 8192, 64, 72, 63, 126.0, 123),
 ]
 
 

@@ -45,7 +45,8 @@ def test_single_projection_plans(lora, s):
     _check_columns(_gemms(fwd), s.n)
     _check_columns([x for x in bwd if "dx_kernel" in x["kernel"]], s.k)
     names = [x["kernel"] for x in bwd]
-    assert names[0].startswith("lora::lora_bwd_du_kernel<") and names[1].startswith("lora::lora_tokred_dma_kernel<")
+    assert names[0].startswith("lora::lora_bwd_du_dma_kernel<" if s.r % 8 == 0 else "lora::lora_bwd_du_kernel<")
+    assert names[1].startswith("lora::lora_tokred_dma_kernel<")
     # the U pass precedes the first forward GEMM exactly when the rank is above 16
     assert any("lora_u_kernel" in x["kernel"] for x in fwd) == (s.r > 16)
     for x in bwd:
@@ -107,6 +108,25 @@ def test_parity_suites_reach_every_plain_u_pass(lora):
     for want in ("lora::lora_u_kernel<32, 16, false>", "lora::lora_u_kernel<32, 32, false>",
                  "lora::lora_u_kernel<64, 16, false>", "lora::lora_u_kernel<64, 32, false>"):
         assert want in seen, (want, sorted(x for x in seen if "u_kernel" in x))
+
+
+def test_parity_suites_reach_every_plannable_du_and_u_pass(lora):
+    """Every dU kernel and U pass a plan can name, over token counts and ranks
+    that cover each choice of tokens per workgroup and padded rank, runs in a
+    GPU parity case."""
+    suites = {x["kernel"] for s in SINGLE for x in lora.lora_linear_plan("bwd", s.m, s.n, s.k, s.r)}
+    suites |= {x["kernel"] for s in SINGLE for x in lora.lora_linear_plan("fwd", s.m, s.n, s.k, s.r)}
+    suites |= {x["kernel"] for s in DROP_SHAPES for x in lora.lora_linear_plan("fwd_dropout", s.m, s.n, s.k, s.r)}
+    suites |= {x["kernel"] for s in DROP_SHAPES for x in lora.lora_linear_plan("bwd_dropout", s.m, s.n, s.k, s.r)}
+    plannable = set()
+    for m in (7, 2048, 4096, 8200):
+        for r in range(1, 65):
+            plannable |= {x["kernel"] for x in lora.lora_linear_plan("bwd", m, 128, 128, r) if "du_" in x["kernel"]}
+            plannable |= {x["kernel"] for x in lora.lora_linear_plan("fwd", m, 128, 128, r) if "u_kernel" in x["kernel"]}
+            plannable |= {x["kernel"] for x in lora.lora_linear_plan("fwd_dropout", m, 128, 128, r)
+                          if "u_kernel" in x["kernel"]}
+    missing = sorted(plannable - suites)
+    assert not missing, missing
 
 
 def test_ragged_n_avoids_the_register_staged_256_tile(lora):
