@@ -1,9 +1,9 @@
 // Forward of the LoRA-adapted linear layer (Eq. 1 of JORA, Section 3):
 //   U = X A^T,   Y = X W^T + s U B^T,   s = alpha / r.
 //
-// Kernels (one launch per call; a U pass before it for rank > 16 and under
-// dropout, and a second GEMM launch when the columns are split between two
-// tiles):
+// Kernels (one launch per call; a U pass before it for rank > 16, on the
+// 256 x 256 tile and under dropout, and a second GEMM launch when the columns
+// are split between two tiles):
 //   lora_fwd_ks_kernel  the 128 x 256 tile for rank <= 16 (the 7B q_proj
 //                       shape): wave pairs split the k substeps of each
 //                       stage, see its own comment.
@@ -1052,9 +1052,10 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
 // Launchers: execute the plans of lora_plan.hpp.
 
 // Instantiations a plan can name (any other combination is refused): U from
-// the U pass for single projections of rank above 16 and under dropout
-// (where the pass applies the keep mask), in the tile for groups and rank 16;
-// the 128 x 256 tile at rank 16 is the k-split kernel's.
+// the U pass for single projections of rank above 16, on the 256 x 256 tile
+// and under dropout (where the pass applies the keep mask), in the tile for
+// groups and rank 16 otherwise; the 128 x 256 tile at rank 16 is the k-split
+// kernel's.
 template <int BM, int BN, int RP, bool GRP, bool UPRE, bool KFULL, bool DMA>
 constexpr bool fwd_instantiated() {
   return !(BM == 128 && BN == 256 && RP == 16) && (UPRE ? !GRP : (RP == 16 || GRP)) &&
@@ -1067,15 +1068,9 @@ static hipError_t run_fwd_launch(const Launch& L, const FwdArgs& a, const FwdGro
     return with_int<16, 32, 64>(L.rp, [&](auto rc) {
       return with_int<16, 32>(L.tpw, [&](auto tc) {
         return with_bool(L.drop, [&](auto kc) {
-          constexpr int RP = decltype(rc)::value;
-          constexpr bool KEEP = decltype(kc)::value;
-          if constexpr (RP == 16 && !KEEP) {   // rank 16 without dropout: U in the tile
-            return hipErrorInvalidValue;
-          } else {
-            hipLaunchKernelGGL((lora_u_kernel<RP, decltype(tc)::value, KEEP>), grid, block, 0, st, a.X, a.A, a.keep,
-                               a.U, (int)a.m, (int)a.k, (int)a.r, a.inv_keep);
-            return hipGetLastError();
-          }
+          hipLaunchKernelGGL((lora_u_kernel<decltype(rc)::value, decltype(tc)::value, decltype(kc)::value>), grid,
+                             block, 0, st, a.X, a.A, a.keep, a.U, (int)a.m, (int)a.k, (int)a.r, a.inv_keep);
+          return hipGetLastError();
         });
       });
     });

@@ -59,6 +59,7 @@ RAGGED = [
     Shape("ragged", 8200, 72, 64, 29, 58.0, 119), Shape("ragged", 600, 136, 72, 27, 54.0, 120),
     Shape("ragged", 4096, 136, 72, 45, 90.0, 121), Shape("ragged", 4100, 72, 136, 57, 114.0, 122),
     Shape("ragged", 8192, 64, 72, 63, 126.0, 123),
+    Shape("ragged", 8200, 4096, 128, 8, 16.0, 124),     # U pass with 32 tokens per workgroup before the 256 x 256 tile
 ]
 
 

@@ -47,8 +47,9 @@ def test_single_projection_plans(lora, s):
     names = [x["kernel"] for x in bwd]
     assert names[0].startswith("lora::lora_bwd_du_dma_kernel<" if s.r % 8 == 0 else "lora::lora_bwd_du_kernel<")
     assert names[1].startswith("lora::lora_tokred_dma_kernel<")
-    # the U pass precedes the first forward GEMM exactly when the rank is above 16
-    assert any("lora_u_kernel" in x["kernel"] for x in fwd) == (s.r > 16)
+    # the U pass precedes the first forward GEMM exactly when the rank is above
+    # 16 or that GEMM is the 256 x 256 tile
+    assert any("lora_u_kernel" in x["kernel"] for x in fwd) == (s.r > 16 or _gemms(fwd)[0]["tile"] == (256, 256))
     for x in bwd:
         if "dx_kernel<256, 256" in x["kernel"]:   # the 256 x 256 dX tile runs only with whole stages
             assert x["kernel"].endswith("true>"), x
@@ -122,9 +123,9 @@ def test_parity_suites_reach_every_plannable_du_and_u_pass(lora):
     for m in (7, 2048, 4096, 8200):
         for r in range(1, 65):
             plannable |= {x["kernel"] for x in lora.lora_linear_plan("bwd", m, 128, 128, r) if "du_" in x["kernel"]}
-            plannable |= {x["kernel"] for x in lora.lora_linear_plan("fwd", m, 128, 128, r) if "u_kernel" in x["kernel"]}
-            plannable |= {x["kernel"] for x in lora.lora_linear_plan("fwd_dropout", m, 128, 128, r)
-                          if "u_kernel" in x["kernel"]}
+            for n in (128, 4096):   # (4096 columns: the 256 x 256 tile, which reads U from the pass)
+                for op in ("fwd", "fwd_dropout"):
+                    plannable |= {x["kernel"] for x in lora.lora_linear_plan(op, m, n, 128, r) if "u_kernel" in x["kernel"]}
     missing = sorted(plannable - suites)
     assert not missing, missing
 
