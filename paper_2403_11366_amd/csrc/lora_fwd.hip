@@ -91,7 +91,9 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
   static_assert(U16 || (FI >= WN ? FI % WN == 0 : WN % FI == 0), "U fragments split evenly");
   static_assert(4 % NDUP == 0, "U substeps split evenly");
   static_assert(2 * STAGE <= 160 * 1024, "LDS budget");
-  static_assert(NDUP * BM * RP * 4 + BN * RP * 2 <= 2 * STAGE, "epilogue LDS reuse");
+  constexpr int RPU = RP + 4, RPB = RP + 8;     // padded row lengths of the epilogue's U and B copies
+  constexpr int NUS = UPRE ? 1 : NDUP;           // U copies in the epilogue
+  static_assert(NUS * BM * RPU * 4 + BN * RPB * 2 <= 2 * STAGE, "epilogue LDS reuse");
 
   __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
 
@@ -365,12 +367,14 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
   }
 
   // ---- epilogue ------------------------------------------------------------
-  // LDS reuse: Us [NDUP][BM][RP] fp32 partial U (summed in fixed order below),
-  // then Bs [BN][RP] bf16 (B rows of this tile, zero beyond r and n).  Rows
-  // n0 .. n0+jn-1 of B are contiguous, so they are fetched as 16-byte chunks
-  // of 8 elements, all issued before the first wait, and scattered into Bs.
+  // LDS reuse: Us [NUS][BM][RPU] fp32 partial U (summed in fixed order below),
+  // then Bs [BN][RPB] bf16 (B rows of this tile, zero beyond r and n).  The
+  // rows are padded by 16 bytes so that the 16 lanes of a read group, which
+  // read 16 consecutive rows, fall in different banks.  Rows n0 .. n0+jn-1 of
+  // B are contiguous, so they are fetched as 16-byte chunks of 8 elements, all
+  // issued before the first wait, and scattered into Bs.
   float* Us = reinterpret_cast<float*>(smem);
-  u16* Bs = reinterpret_cast<u16*>(smem + NDUP * BM * RP * 4);
+  u16* Bs = reinterpret_cast<u16*>(smem + NUS * BM * RPU * 4);
   constexpr int BCH = (BN * RP / 8 + NT - 1) / NT;   // chunks per thread (r <= RP)
   const int jn = min(BN, n - n0);
   const int nch = jn * r / 8;                       // exact: n and n0 are multiples of 8
@@ -384,13 +388,13 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
   if (UPRE) {   // U of the tile's tokens from the U pass (zero beyond r and m)
     for (int e = tid; e < BM * RP; e += NT) {
       const int il = e / RP, t = e - il * RP;
-      Us[e] = (m0 + il < m && t < r) ? U[(size_t)(m0 + il) * r + t] : 0.f;
+      Us[il * RPU + t] = (m0 + il < m && t < r) ? U[(size_t)(m0 + il) * r + t] : 0.f;
     }
   } else if (U16) {   // lane holds token column c16 of its group, U rows t = 4 g16 .. +3
 #pragma unroll
     for (int gg = 0; gg < GPW; ++gg)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) Us[urow16[gg] * RP + 4 * g16 + q] = uacc16[gg][q];
+      for (int q = 0; q < 4; ++q) Us[urow16[gg] * RPU + 4 * g16 + q] = uacc16[gg][q];
   } else {
 #pragma unroll
     for (int fu = 0; fu < FUW; ++fu) {
@@ -400,11 +404,11 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
 #pragma unroll
         for (int q = 0; q < 16; ++q) {
           const int t = 32 * ft + 8 * (q >> 2) + 4 * g + (q & 3);
-          Us[(udup * BM + il) * RP + t] = uacc[ft][fu][q];
+          Us[(udup * BM + il) * RPU + t] = uacc[ft][fu][q];
         }
     }
   }
-  for (int e = tid; e < BN * RP / 8; e += NT) reinterpret_cast<int4v*>(Bs)[e] = int4v{0, 0, 0, 0};
+  for (int e = tid; e < BN * RPB / 8; e += NT) reinterpret_cast<int4v*>(Bs)[e] = int4v{0, 0, 0, 0};
   __syncthreads();
   {
     // element idx of the chunks is B row idx / r, column idx % r; the quotient
@@ -419,24 +423,25 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
           const int idx = 8 * q + e;
           const int j = (int)(((float)idx + 0.5f) * rinv);
           const int t = idx - j * r;
-          Bs[j * RP + t] = (u16)((uint32_t)bv[i][e >> 1] >> (16 * (e & 1)));
+          Bs[j * RPB + t] = (u16)((uint32_t)bv[i][e >> 1] >> (16 * (e & 1)));
         }
       }
     }
   }
   if (NDUP > 1 && !UPRE) {  // fold the partial U sums into copy 0 (fixed order)
     for (int e = tid; e < BM * RP; e += NT) {
-      float v = Us[e];
+      const int o = (e / RP) * RPU + e % RP;
+      float v = Us[o];
 #pragma unroll
-      for (int d = 1; d < NDUP; ++d) v += Us[d * BM * RP + e];
-      Us[e] = v;
+      for (int d = 1; d < NDUP; ++d) v += Us[d * BM * RPU + o];
+      Us[o] = v;
     }
   }
   __syncthreads();
   if (n0 == 0 && !UPRE) {   // U output: the first tile column writes it
     for (int e = tid; e < BM * RP; e += NT) {
       const int il = e / RP, t = e - il * RP;
-      if (m0 + il < m && t < r) U[(size_t)(m0 + il) * r + t] = Us[e];
+      if (m0 + il < m && t < r) U[(size_t)(m0 + il) * r + t] = Us[il * RPU + t];
     }
   }
 
@@ -449,12 +454,12 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
 #pragma unroll
     for (int fj = 0; fj < FJ; ++fj) {
       const int jl = wn * WTJ + 32 * fj + c32;
-      bfr[fj] = *reinterpret_cast<const short8*>(Bs + jl * RP + t0);
+      bfr[fj] = *reinterpret_cast<const short8*>(Bs + jl * RPB + t0);
     }
 #pragma unroll
     for (int fi = 0; fi < FI; ++fi) {
       const int il = wm * WTI + 32 * fi + c32;
-      const float* up = Us + il * RP + t0;
+      const float* up = Us + il * RPU + t0;
       short8 uh, ul;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
