@@ -164,7 +164,7 @@ def algorithmic_units(s, launch):
         return "flop", 2 * m * (n + r) * (c1 - c0)
     if "lora_u_kernel" in name:
         return "byte", 2 * m * k + 2 * r * k + 4 * m * r
-    if "lora_bwd_du_kernel" in name:
+    if "lora_bwd_du_kernel" in name or "lora_bwd_du_dma_kernel" in name:
         return "byte", 2 * m * n + 2 * n * r + 4 * m * r
     if "lora_tokred_kernel" in name or "lora_tokred_dma_kernel" in name:
         return "byte", (2 * m * n + 4 * m * r + 4 * n * r) + (2 * m * k + 4 * m * r + 4 * r * k)

@@ -190,3 +190,23 @@ def test_group_da_reductions_share_one_pass_over_x(lora):
         stacked = len(ns) >= 3 and len(ns) * (-(-r // 16) * 16) <= 64
         members = [x["member"] for x in lora.lora_linear_plan("group_bwd", m, ns, k, r) if "tokred" in x["kernel"]]
         assert (members[-1] == -1) == stacked, (ns, r, members)
+
+
+def test_bench_prices_every_kernel_of_the_single_projection_plans(lora):
+    """bench.py's algorithmic units (flops of the GEMMs, minimum bytes of the
+    HBM-bound kernels) name every kernel the forward and backward plans of the
+    Llama-2 shapes launch, except the dA/dB finalize (split-K partial traffic
+    is not credited)."""
+    import os
+    import sys
+    sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+    import bench
+    for name in ("llama2_7b_q_proj", "llama2_7b_up_proj", "llama2_7b_down_proj", "llama2_13b_layer"):
+        for s in CONFIGS[name]:
+            for op in ("fwd", "bwd", "fwd_dropout", "bwd_dropout"):
+                for x in lora.lora_linear_plan(op, s.m, s.n, s.k, s.r):
+                    unit, amount = bench.algorithmic_units(s, x)
+                    if x["kernel"] == "lora::lora_finalize_kernel":
+                        assert unit is None
+                    else:
+                        assert unit in ("flop", "byte") and amount > 0, (op, s.name, x["kernel"])
