@@ -28,8 +28,9 @@
  *     synchronised.  Calls that share buffers must be ordered by the caller.
  *   - Outputs are overwritten (no accumulation into existing contents).
  *   - All arguments are validated before anything is enqueued.  On an error
- *     nothing is launched and every output is left untouched.  No C++ exception
- *     crosses this interface.
+ *     nothing is launched and every output is left untouched, except when a
+ *     launch itself fails (LORA_ERR_HIP): kernels of the call enqueued before
+ *     it may run.  No C++ exception crosses this interface.
  *   - Arithmetic: bf16 operands, fp32 accumulation on the matrix cores, bf16
  *     outputs rounded to nearest-even.  The rank-r intermediates U and dU enter
  *     the matrix cores as a bf16 high part plus a bf16 low part, so they keep
@@ -56,7 +57,9 @@ typedef enum {
   LORA_ERR_UNSUPPORTED = 4, /* r > 64, or a dimension beyond the supported range */
   LORA_ERR_WORKSPACE = 5,   /* workspace missing or smaller than lora_linear_bwd_workspace_size() */
   LORA_ERR_ALIAS = 6,       /* an output overlaps an input or another output */
-  LORA_ERR_HIP = 7          /* the HIP runtime reported an error at launch */
+  LORA_ERR_HIP = 7          /* the HIP runtime reported an error at launch; also returned, before anything
+                               is enqueued, while an error of an earlier HIP call is pending on the calling
+                               thread (hipPeekAtLastError; it is left for the caller to read) */
 } lora_status;
 
 /*

@@ -96,6 +96,13 @@ const char* lora_status_string(lora_status s) {
   return "unknown status";
 }
 
+// HIP keeps the last runtime error of the calling thread until it is read,
+// and the launchers read it after each launch.  An error left pending by an
+// earlier call would be reported by a call's first launch after that kernel
+// was enqueued, so it is reported before anything is enqueued instead (and
+// left pending for the caller to read).
+static bool hip_error_pending() { return hipPeekAtLastError() != hipSuccess; }
+
 lora_status lora_linear_fwd(const lora_bf16* X, const lora_bf16* W, const lora_bf16* A,
                             const lora_bf16* B, lora_bf16* Y, float* U,
                             int64_t m, int64_t n, int64_t k, int64_t r, float alpha,
@@ -112,6 +119,7 @@ lora_status lora_linear_fwd(const lora_bf16* X, const lora_bf16* W, const lora_b
   if (overlap(ry, ru)) return LORA_ERR_ALIAS;
 
   lora::FwdArgs a{X, W, A, B, Y, U, m, n, k, r, (float)alpha / (float)r};
+  if (hip_error_pending()) return LORA_ERR_HIP;
   hipError_t e = lora::launch_fwd(a, reinterpret_cast<hipStream_t>(stream));
   return e == hipSuccess ? LORA_OK : LORA_ERR_HIP;
 }
@@ -134,6 +142,7 @@ lora_status lora_linear_fwd_dropout(const lora_bf16* X, const lora_bf16* W, cons
   if (overlap(ry, ru)) return LORA_ERR_ALIAS;
 
   lora::FwdArgs a{X, W, A, B, Y, U, m, n, k, r, (float)alpha / (float)r, keep, 1.0f / (1.0f - p)};
+  if (hip_error_pending()) return LORA_ERR_HIP;
   hipError_t e = lora::launch_fwd(a, reinterpret_cast<hipStream_t>(stream));
   return e == hipSuccess ? LORA_OK : LORA_ERR_HIP;
 }
@@ -173,6 +182,7 @@ lora_status lora_linear_bwd(const lora_bf16* dY, const lora_bf16* X, const lora_
 
   lora::BwdArgs a{dY, X, W, A, B, U, dX, dA, dB, static_cast<char*>(workspace),
                   m, n, k, r, (float)alpha / (float)r};
+  if (hip_error_pending()) return LORA_ERR_HIP;
   hipError_t e = lora::launch_bwd(a, reinterpret_cast<hipStream_t>(stream));
   return e == hipSuccess ? LORA_OK : LORA_ERR_HIP;
 }
@@ -194,6 +204,7 @@ lora_status lora_linear_bwd_noalloc(const lora_bf16* dY, const lora_bf16* X, con
   if (any_alias(out, 3, in, 6)) return LORA_ERR_ALIAS;
 
   lora::BwdArgs a{dY, X, W, A, B, U, dX, dA, dB, nullptr, m, n, k, r, (float)alpha / (float)r};
+  if (hip_error_pending()) return LORA_ERR_HIP;
   hipError_t e = lora::launch_bwd_noalloc(a, reinterpret_cast<hipStream_t>(stream));
   return e == hipSuccess ? LORA_OK : LORA_ERR_HIP;
 }
@@ -229,6 +240,7 @@ lora_status lora_linear_bwd_fused(const lora_bf16* dY, const lora_bf16* X, const
 
   lora::BwdArgs a{dY, X, W, A, B, U, dX, dA, dB, static_cast<char*>(workspace),
                   m, n, k, r, (float)alpha / (float)r};
+  if (hip_error_pending()) return LORA_ERR_HIP;
   hipError_t e = lora::launch_bwd_fused(a, reinterpret_cast<hipStream_t>(stream));
   return e == hipSuccess ? LORA_OK : LORA_ERR_HIP;
 }
@@ -263,6 +275,7 @@ lora_status lora_linear_bwd_dropout(const lora_bf16* dY, const lora_bf16* X, con
 
   lora::BwdArgs a{dY, X, W, A, B, U, dX, dA, dB, static_cast<char*>(workspace),
                   m, n, k, r, (float)alpha / (float)r, keep, 1.0f / (1.0f - p)};
+  if (hip_error_pending()) return LORA_ERR_HIP;
   hipError_t e = lora::launch_bwd(a, reinterpret_cast<hipStream_t>(stream));
   return e == hipSuccess ? LORA_OK : LORA_ERR_HIP;
 }
@@ -279,6 +292,7 @@ lora_status lora_linear_merge(const lora_bf16* W, const lora_bf16* A, const lora
   if (overlap(ro, rw) && W_out != W) return LORA_ERR_ALIAS;   // in place is allowed, a shifted overlap is not
 
   lora::MergeArgs a{W, A, B, W_out, n, k, r, (float)sign * ((float)alpha / (float)r)};
+  if (hip_error_pending()) return LORA_ERR_HIP;
   hipError_t e = lora::launch_merge(a, reinterpret_cast<hipStream_t>(stream));
   return e == hipSuccess ? LORA_OK : LORA_ERR_HIP;
 }
@@ -314,6 +328,7 @@ lora_status lora_linear_group_fwd(const lora_bf16* X, int64_t group, const int64
     a.n[g] = n[g]; a.W[g] = W[g]; a.A[g] = A[g]; a.B[g] = B[g]; a.Y[g] = Y[g]; a.U[g] = U[g];
   }
   a.m = m; a.k = k; a.r = r; a.s = (float)alpha / (float)r;
+  if (hip_error_pending()) return LORA_ERR_HIP;
   hipError_t e = lora::launch_fwd_group(a, reinterpret_cast<hipStream_t>(stream));
   return e == hipSuccess ? LORA_OK : LORA_ERR_HIP;
 }
@@ -368,6 +383,7 @@ lora_status lora_linear_group_bwd(const lora_bf16* const* dY, const lora_bf16* X
   a.dX = dX;
   a.ws = static_cast<char*>(workspace);
   a.m = m; a.k = k; a.r = r; a.s = (float)alpha / (float)r;
+  if (hip_error_pending()) return LORA_ERR_HIP;
   hipError_t e = lora::launch_bwd_group(a, reinterpret_cast<hipStream_t>(stream));
   return e == hipSuccess ? LORA_OK : LORA_ERR_HIP;
 }

@@ -71,6 +71,13 @@ __device__ __forceinline__ floatx16 mfma32x32x16(short8 a, short8 b, floatx16 c)
 
 __device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
 
+// The lane's index in its wave from the mbcnt instructions (no input
+// registers): for code after a long loop to recompute lane-derived values
+// instead of keeping threadIdx-derived ones live across the loop.
+__device__ __forceinline__ int lane_fresh() {
+  return (int)__builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
+}
+
 // Global -> LDS copy of 16 bytes per lane through a buffer resource (offset
 // voff + soff): lane l's bytes land at lds_base + 16 l (lds_base wave-uniform).
 // Out-of-range offsets write zeros.  Completion is counted by vmcnt.

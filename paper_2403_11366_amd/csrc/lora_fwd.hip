@@ -943,6 +943,16 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
   }
 
   }
+  // The epilogue's lane-derived values are recomputed from the lane index
+  // rather than kept live across the k loop (which runs at the register limit).
+  const int lane_e = lane_fresh();
+  {
+  const int lane = lane_e, tid = wave * 64 + lane_e;
+  const int g = lane >> 5, c32 = lane & 31;
+  const int g16 = lane >> 4, c16 = lane & 15;
+  int urow16[GPW];
+#pragma unroll
+  for (int gg = 0; gg < GPW; ++gg) urow16[gg] = wm * WTI + 16 * (wn * GPW + gg) + c16;
   // ---- epilogue (LDS is free after the loop's last barrier).  Regions:
   // [0, XCH) the exchange of the k-half partial sums, later the per-wave
   // staging of the bf16 output block; then Us [2][BM][RP] fp32 (the two
@@ -1051,6 +1061,7 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
   static_assert(8 * kYsBytes <= XCH, "output staging fits the exchange region");
   if (wk == 0) finish(acc[0], acc[1]);
   else finish(acc[2], acc[3]);
+  }
 }
 
 // ---------------------------------------------------------------------------

@@ -96,3 +96,59 @@ def test_graph_replays_match_eager():
     g.replay()
     torch.cuda.synchronize()
     assert _same(_host(o), eager2)
+
+
+def _loaded_hip_runtime():
+    """The HIP runtime this process already has loaded (the one the library's
+    launches go through), opened by its own path."""
+    import ctypes
+    import os
+    import re
+    maps = open(f"/proc/{os.getpid()}/maps").read()
+    paths = sorted(set(re.findall(r"(/\S*libamdhip64\.so\S*)", maps)))
+    assert len(paths) == 1, paths
+    hip = ctypes.CDLL(paths[0])
+    hip.hipMalloc.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_size_t]
+    hip.hipMalloc.restype = ctypes.c_int
+    hip.hipPeekAtLastError.restype = ctypes.c_int
+    hip.hipGetLastError.restype = ctypes.c_int
+    return hip
+
+
+def test_pending_hip_error_is_reported_before_anything_is_enqueued():
+    """LORA_ERR_HIP for an error an earlier HIP call left pending on this
+    thread (here a refused allocation): returned before any launch, outputs
+    untouched, the error left for the caller; once it is read the same call
+    succeeds.  The call goes straight through the C ABI so that nothing runs
+    between the failed allocation and the call."""
+    import ctypes
+    import torch
+    import paper_2403_11366_amd as lora
+    from paper_2403_11366_amd.device_io import bits_to_device
+    s = Shape("pending", 200, 264, 320, 40, 80.0, 63)   # rank 40: U pass, then the tile
+    t = gen_inputs(s)
+    d = {key: bits_to_device(v) for key, v in t.items()}
+    Y = torch.full((s.m, s.n), 3.0, dtype=torch.bfloat16, device="cuda")
+    U = torch.full((s.m, s.r), -7.0, dtype=torch.float32, device="cuda")
+    torch.cuda.synchronize()
+    lib = lora.load_library()
+    args = (d["X"].data_ptr(), d["W"].data_ptr(), d["A"].data_ptr(), d["B"].data_ptr(), Y.data_ptr(),
+            U.data_ptr(), s.m, s.n, s.k, s.r, s.alpha, torch.cuda.current_stream().cuda_stream)
+    hip = _loaded_hip_runtime()
+    assert hip.hipPeekAtLastError() == 0
+    p = ctypes.c_void_p()
+    try:
+        assert hip.hipMalloc(ctypes.byref(p), ctypes.c_size_t(1 << 62)) != 0   # 4 EiB: refused
+        pending = hip.hipPeekAtLastError()
+        st = lib.lora_linear_fwd(*args) if pending else None
+        still = hip.hipPeekAtLastError()
+    finally:
+        hip.hipGetLastError()
+    if not pending:
+        pytest.skip("this HIP runtime keeps no pending error after a refused allocation")
+    assert st == 7 and still == pending, (st, still, pending)
+    torch.cuda.synchronize()
+    assert bool((Y == 3.0).all()) and bool((U == -7.0).all())
+    assert lib.lora_linear_fwd(*args) == 0
+    torch.cuda.synchronize()
+    assert not bool((U == -7.0).any())
