@@ -43,15 +43,18 @@ inline GemmTile choose_gemm_tile(int64_t M, int64_t N) {
 // tile t1, then columns [n1, N) with tile t2 in a second launch.  Taken when
 // the split, whose second part is at most one round of 256 workgroups, is
 // estimated more than 5% faster than the single tiling (estimate: rounds x
-// tile area / relative efficiency, 1.0, 0.95 and 0.72 for 256x256, 128x256
-// and 128x128 as measured at 4096 x 5120 x 5120).  Typical case: 4096 x 5120,
-// where 640 tiles of 128x256 take three rounds and 256 tiles of 256x256 plus
-// 256 tiles of 128x128 take two.  Among equal estimates the largest n1 wins.
+// tile area / relative efficiency, 1.0, 0.9 and 0.72 for 256x256, 128x256
+// and 128x128, measured at 4096 x 5120 x 5120 and 4096 x 13824 x 5120).
+// Typical cases: 4096 x 5120, where 640 tiles of 128x256 take three rounds
+// and 256 tiles of 256x256 plus 256 tiles of 128x128 take two; 4096 x 13824,
+// where 1728 tiles of 128x256 take seven rounds and 768 tiles of 256x256 plus
+// 192 of 128x256 take four (forward 607-616 -> 537 us).  Among equal
+// estimates the largest n1 wins.
 // n1 == N: no split.
 struct GemmSplit { GemmTile t1, t2; int64_t n1; };
 inline GemmSplit plan_gemm_split(int64_t M, int64_t N) {
   struct C { GemmTile t; int bm, bn; double eff; };
-  const C cands[3] = {{TILE_256x256, 256, 256, 1.0}, {TILE_128x256, 128, 256, 0.95},
+  const C cands[3] = {{TILE_256x256, 256, 256, 1.0}, {TILE_128x256, 128, 256, 0.9},
                       {TILE_128x128, 128, 128, 0.72}};
   auto tiles = [&](const C& c, int64_t n) { return ((M + c.bm - 1) / c.bm) * ((n + c.bn - 1) / c.bn); };
   auto cost = [&](const C& c, int64_t n) { return (double)((tiles(c, n) + 255) / 256) * c.bm * c.bn / c.eff; };

@@ -51,7 +51,8 @@ SHAPES = [Shape("drop_tiny", 256, 512, 512, 8, 16.0, 21), Shape("drop_ragged", 2
           Shape("drop_r33", 130, 136, 192, 33, 66.0, 23), Shape("drop_r64", 264, 392, 448, 64, 128.0, 24),
           Shape("drop_r16", 520, 1032, 640, 16, 32.0, 25),
           Shape("drop_256x256", 1536, 8192, 256, 8, 16.0, 29),    # the 256 x 256 tile reading U back
-          Shape("drop_ks_rounds", 2560, 8192, 256, 13, 26.0, 30),  # k-split tile over several rounds
+          Shape("drop_ks_rounds", 2431, 6656, 256, 13, 26.0, 30),  # k-split tile over several rounds
+          Shape("drop_split", 2560, 8192, 256, 13, 26.0, 39),      # 256 x 256 columns, then one k-split round
           # the masked U pass with 32 tokens per workgroup (8192 tokens and more) at padded ranks 16, 32, 64,
           # and with 16 at rank 32
           Shape("drop_m8192", 8200, 264, 256, 8, 16.0, 31), Shape("drop_m8192_r24", 8192, 136, 128, 24, 48.0, 32),
