@@ -56,7 +56,18 @@ SHAPES = [Shape("drop_tiny", 256, 512, 512, 8, 16.0, 21), Shape("drop_ragged", 2
           # the masked U pass with 32 tokens per workgroup (8192 tokens and more) at padded ranks 16, 32, 64,
           # and with 16 at rank 32
           Shape("drop_m8192", 8200, 264, 256, 8, 16.0, 31), Shape("drop_m8192_r24", 8192, 136, 128, 24, 48.0, 32),
-          Shape("drop_m8192_r64", 8192, 128, 192, 64, 128.0, 33), Shape("drop_r24", 300, 264, 192, 24, 48.0, 34)]
+          Shape("drop_m8192_r64", 8192, 128, 192, 64, 128.0, 33), Shape("drop_r24", 300, 264, 192, 24, 48.0, 34),
+          # the masked dX tiles of every padded rank: 128 x 128 at 32, 48, 64; 128 x 256 at 16 .. 64 with and
+          # without whole stages (n a multiple of 64 or not)
+          Shape("drop_dx128_r24", 7, 64, 1024, 24, 48.0, 40), Shape("drop_dx128_r33", 7, 64, 1024, 33, 66.0, 41),
+          Shape("drop_dx128_r64", 7, 64, 1024, 64, 128.0, 42),
+          Shape("drop_dx256_r1", 300, 136, 11008, 1, 2.0, 43), Shape("drop_dx256f_r1", 300, 64, 11008, 1, 2.0, 44),
+          Shape("drop_dx256_r24", 300, 136, 11008, 24, 48.0, 45),
+          Shape("drop_dx256f_r24", 300, 64, 11008, 24, 48.0, 46),
+          Shape("drop_dx256_r33", 300, 136, 11008, 33, 66.0, 47),
+          Shape("drop_dx256f_r33", 300, 64, 11008, 33, 66.0, 48),
+          Shape("drop_dx256_r64", 300, 136, 11008, 64, 128.0, 49),
+          Shape("drop_dx256f_r64", 300, 64, 11008, 64, 128.0, 50)]
 
 
 @pytest.mark.parametrize("shape", SHAPES, ids=lambda s: s.name)

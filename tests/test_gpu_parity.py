@@ -60,6 +60,14 @@ RAGGED = [
     Shape("ragged", 4096, 136, 72, 45, 90.0, 121), Shape("ragged", 4100, 72, 136, 57, 114.0, 122),
     Shape("ragged", 8192, 64, 72, 63, 126.0, 123),
     Shape("ragged", 8200, 4096, 128, 8, 16.0, 124),     # U pass with 32 tokens per workgroup before the 256 x 256 tile
+    # the remaining tiles a plan can name: 128 x 128 dX at padded ranks 32 and 64, 128 x 256 dX at 32 and 48
+    # (with and without whole stages), and forward tiles reading U from the pass at padded ranks 32 and 64
+    # with and without whole stages
+    Shape("ragged", 7, 64, 1024, 24, 48.0, 130), Shape("ragged", 7, 64, 1024, 64, 128.0, 131),
+    Shape("ragged", 300, 136, 11008, 24, 48.0, 132), Shape("ragged", 300, 64, 11008, 33, 66.0, 133),
+    Shape("ragged", 300, 11008, 72, 24, 48.0, 134), Shape("ragged", 300, 11008, 64, 33, 66.0, 135),
+    Shape("ragged", 2048, 11008, 72, 24, 48.0, 136), Shape("ragged", 2048, 11008, 64, 24, 48.0, 137),
+    Shape("ragged", 2048, 11008, 72, 33, 66.0, 138),
 ]
 
 

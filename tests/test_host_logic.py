@@ -130,6 +130,30 @@ def test_parity_suites_reach_every_plannable_du_and_u_pass(lora):
     assert not missing, missing
 
 
+def test_parity_suites_reach_every_plannable_kernel(lora):
+    """Every kernel instantiation the forward and backward plans (plain and
+    dropout) can name over a sweep of token counts, widths, depths and ranks
+    runs in a GPU parity case."""
+    suites = set()
+    for s in SINGLE:
+        for op in ("fwd", "bwd"):
+            suites |= {x["kernel"] for x in lora.lora_linear_plan(op, s.m, s.n, s.k, s.r)}
+    for s in DROP_SHAPES:
+        for op in ("fwd_dropout", "bwd_dropout"):
+            suites |= {x["kernel"] for x in lora.lora_linear_plan(op, s.m, s.n, s.k, s.r)}
+    plannable = {}
+    for m in (7, 300, 2048, 4096, 8200):
+        for n in (64, 136, 1024, 4000, 4096, 5120, 11008, 13824):
+            for k in (64, 72, 1024, 4096, 4104, 5120, 11008):
+                for r in (1, 8, 16, 24, 33, 40, 64):
+                    ops = ("fwd", "bwd") + (("fwd_dropout", "bwd_dropout") if k % 64 == 0 else ())
+                    for op in ops:
+                        for x in lora.lora_linear_plan(op, m, n, k, r):
+                            plannable.setdefault(x["kernel"], (op, m, n, k, r))
+    missing = {kname: plannable[kname] for kname in sorted(set(plannable) - suites)}
+    assert not missing, missing
+
+
 def test_ragged_n_avoids_the_register_staged_256_tile(lora):
     """n not a multiple of 64 on a shape whose dX would take the 256 x 256 tile:
     the 128 x 256 tile without the FULL loads serves it."""
