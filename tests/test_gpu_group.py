@@ -76,6 +76,21 @@ CASES = [  # (ns, m, k, r, alpha)
     ([264, 392], 2000, 5120, 8, 16.0),             # 2.5 rounds of 128x256 dX tiles
     ([264, 392], 4096, 4096, 8, 16.0),             # the 256x256 dX tile for a group
     ([264, 520, 136, 72], 300, 448, 13, 26.0),     # four members share one dA reduction (stacked rank 64)
+] + [
+    # the remaining grouped tiles a plan can name, at padded ranks 16 .. 64 with and without whole k stages:
+    # the 128 x 128 forward and dX (few tokens), the 128 x 256 forward and k-split forward (130 tokens over
+    # two 13824-wide members), the 256 x 256 forward (520 tokens), the 128 x 256 dX with and without whole n
+    # stages, and the 256 x 256 dX
+    (ns, m, k, r, 2.0 * r) for ns, m, k, r in (
+        ([64, 64], 7, 64, 24), ([64, 64], 7, 72, 24), ([64, 64], 7, 72, 33), ([64, 64], 7, 1024, 24),
+        ([64, 64], 7, 1024, 33), ([64, 64], 7, 1024, 64),
+        ([13824, 13824], 130, 64, 24), ([13824, 13824], 130, 64, 33), ([13824, 13824], 130, 72, 1),
+        ([13824, 13824], 130, 72, 24), ([13824, 13824], 130, 72, 33),
+        ([6912, 6912], 520, 64, 24), ([6912, 6912], 520, 64, 33), ([6912, 6912], 520, 72, 1),
+        ([6912, 6912], 520, 72, 24), ([6912, 6912], 520, 72, 33),
+        ([64, 64], 2048, 2304, 24), ([64, 64], 2048, 2304, 33), ([64, 64], 2048, 2304, 64),
+        ([136, 264, 72], 2048, 2304, 24), ([136, 264, 72], 2048, 2304, 33), ([136, 264, 72], 2048, 2304, 64),
+        ([64, 64], 3000, 4096, 24), ([64, 64], 3000, 4096, 33), ([64, 64], 3000, 4096, 64))
 ]
 
 

@@ -154,6 +154,35 @@ def test_parity_suites_reach_every_plannable_kernel(lora):
     assert not missing, missing
 
 
+def test_group_suites_reach_every_plannable_kernel(lora):
+    """Every kernel instantiation the grouped forward and backward plans can
+    name over a sweep of token counts, depths, ranks and member widths runs in
+    a GPU case (a grouped one, or for the launches of a group of one, a
+    single-projection one)."""
+    groups = [(ns, m, k, r) for ns, m, k, r, _ in GROUP_CASES] + [(ns, m, k, r) for m, k, ns, r in GROUP_EXACT]
+    groups += list(FULL_GROUPS)
+    layer = CONFIGS["llama2_13b_layer"]
+    groups += [([layer[i].n for i in mem], layer[0].m, layer[0].k, layer[0].r) for mem in ([0, 1, 2], [4, 5])]
+    suites = set()
+    for ns, m, k, r in groups:
+        for op in ("group_fwd", "group_bwd"):
+            suites |= {x["kernel"] for x in lora.lora_linear_plan(op, m, ns, k, r)}
+    for s in SINGLE:
+        for op in ("fwd", "bwd"):
+            suites |= {x["kernel"] for x in lora.lora_linear_plan(op, s.m, s.n, s.k, s.r)}
+    plannable = {}
+    for m in (7, 300, 2048, 4096, 8200):
+        for k in (64, 72, 1024, 4096, 4104, 5120, 13824):
+            for r in (1, 8, 16, 24, 33, 64):
+                for ns in ([64, 64], [136, 264, 72], [4096] * 3, [5120] * 3, [13824] * 2,
+                           [64, 72, 80, 88, 96, 104, 112, 120], [5120]):
+                    for op in ("group_fwd", "group_bwd"):
+                        for x in lora.lora_linear_plan(op, m, ns, k, r):
+                            plannable.setdefault(x["kernel"], (op, m, ns, k, r))
+    missing = {kname: plannable[kname] for kname in sorted(set(plannable) - suites)}
+    assert not missing, missing
+
+
 def test_ragged_n_avoids_the_register_staged_256_tile(lora):
     """n not a multiple of 64 on a shape whose dX would take the 256 x 256 tile:
     the 128 x 256 tile without the FULL loads serves it."""
