@@ -17,7 +17,9 @@ it follow the GPU time), a roofline
 entry for the dominant kernel (the forward call of the projection with the
 most forward flops, timed live with HIP events on its stream; its kernels come
 from the library's own launch plan) and the fp64 CPU oracle's throughput on
-the host as a baseline.
+the host as a baseline.  With --dropout P a step is the *_dropout entry
+points instead, each projection's keep mask drawn afresh on the device
+(lora_dropout_keep_mask) at the top of the step, inside the timed region.
 """
 from __future__ import annotations
 
@@ -488,7 +490,8 @@ def main():
                          "merge W + s B A of each projection's adapter into its weight")
     ap.add_argument("--dropout", type=float, default=None, metavar="P",
                     help="train with LoRA dropout at rate P on the adapter input (the *_dropout "
-                         "entry points, a seeded keep mask per input set)")
+                         "entry points; each step draws a fresh keep mask on the device with "
+                         "lora_dropout_keep_mask, inside the timed step)")
     ap.add_argument("--grouped", action="store_true",
                     help="run the projections that read one input (q, k, v; gate, up) as groups "
                          "(workloads with a layer grouping only)")
@@ -518,9 +521,8 @@ def main():
     import numpy as np
     import torch
     import paper_2403_11366_amd as lora
-    from lora_synth import CONFIGS
+    from lora_synth import CONFIGS, gen_inputs
     from paper_2403_11366_amd.device_io import bits_to_device
-    from lora_synth import gen_inputs, gen_keep_mask
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     lora.load_library()
@@ -551,16 +553,13 @@ def main():
 
     # ---- inputs resident in HBM, rotated over enough copies to exceed the MALL
     drop = args.dropout
-    per_set = sum(2 * (s.m * s.k + s.n * s.k + s.r * s.k + s.n * s.r + s.m * s.n)
-                  + (s.m * s.k // 8 if drop is not None else 0) for s in shapes)
+    per_set = sum(2 * (s.m * s.k + s.n * s.k + s.r * s.k + s.n * s.r + s.m * s.n) for s in shapes)
     nsets = max(1, math.ceil(2 * MALL_BYTES / per_set))
     log(f"[bench] {args.config}: {len(shapes)} projection(s), {nsets} input set(s) of {per_set / 2**20:.0f} MiB")
     proj = []
     for s in shapes:
         t = gen_inputs(s)
         base = {key: bits_to_device(v, dev) for key, v in t.items()}
-        if drop is not None:
-            base["keep"] = torch.from_numpy(gen_keep_mask(s.m, s.k, drop, s.seed + 1)).to(dev)
         sets = [base] + [{key: v.clone() for key, v in base.items()} for _ in range(nsets - 1)]
         out = {
             "Y": torch.empty((s.m, s.n), dtype=torch.bfloat16, device=dev),
@@ -572,13 +571,16 @@ def main():
                                else lora.lora_linear_bwd_workspace_size)(s.m, s.n, s.k, s.r),
                               dtype=torch.uint8, device=dev),
         }
+        if drop is not None:   # the step's keep mask, drawn on the device at the top of each step
+            out["keep"] = torch.empty((s.m, s.k // 8), dtype=torch.uint8, device=dev)
+            lora.lora_dropout_keep_mask(s.seed, 0, drop, out["keep"])
         proj.append((s, sets, out))
     torch.cuda.synchronize()
 
     def fwd(i, s, sets, out):
         d = sets[i % len(sets)]
         if drop is not None:
-            lora.lora_linear_fwd_dropout(d["X"], d["W"], d["A"], d["B"], d["keep"], drop, out["Y"], out["U"],
+            lora.lora_linear_fwd_dropout(d["X"], d["W"], d["A"], d["B"], out["keep"], drop, out["Y"], out["U"],
                                          s.alpha, stream=stream)
             return
         lora.lora_linear_fwd(d["X"], d["W"], d["A"], d["B"], out["Y"], out["U"], s.alpha, stream=stream)
@@ -586,7 +588,7 @@ def main():
     def bwd(i, s, sets, out):
         d = sets[i % len(sets)]
         if drop is not None:
-            lora.lora_linear_bwd_dropout(d["dY"], d["X"], d["W"], d["A"], d["B"], out["U"], d["keep"], drop,
+            lora.lora_linear_bwd_dropout(d["dY"], d["X"], d["W"], d["A"], d["B"], out["U"], out["keep"], drop,
                                          out["dX"], out["dA"], out["dB"], out["ws"], s.alpha, stream=stream)
             return
         (lora.lora_linear_bwd_fused if args.fused_bwd else lora.lora_linear_bwd)(
@@ -595,6 +597,8 @@ def main():
 
     def step(i):
         for s, sets, out in proj:
+            if drop is not None:   # a fresh mask per step: the next m k / 8 counters of the projection's seed
+                lora.lora_dropout_keep_mask(s.seed, (i + 1) * (s.m * s.k // 8), drop, out["keep"], stream=stream)
             fwd(i, s, sets, out)
             bwd(i, s, sets, out)
 

@@ -106,6 +106,34 @@ lora_status lora_linear_fwd_dropout(const lora_bf16* X, const lora_bf16* W, cons
                                     int64_t m, int64_t n, int64_t k, int64_t r, float alpha, void* stream);
 
 /*
+ * Keep mask for the *_dropout entry points, drawn on the device (Listing 3
+ * carries LORA_DROPOUT; the mask is what the dropout of the adapter input
+ * draws).  Writes keep [m, k/8] in the layout those entry points read: bit
+ * (l % 8) of byte (i, l / 8) set keeps X[i][l].
+ *
+ * Generator: the counter-based Philox4x64-10 (Salmon, Moraes, Dror, Shaw,
+ * "Parallel random numbers: as easy as 1, 2, 3", SC 2011), key (seed, 0).
+ * Bytes 2t and 2t + 1 of the mask (byte b = i (k/8) + l/8 holds the bits of
+ * elements l .. l + 7 of row i, l a multiple of 8) come from one generator
+ * block at the 256-bit counter (offset + t as a 128-bit integer, 0, 0); its
+ * four 64-bit output words give sixteen 16-bit values u_e (u_{4h+j} = bits
+ * 16j .. 16j + 15 of word h), and bit e of the byte pair (e = 0..7 in byte
+ * 2t, 8..15 in byte 2t + 1) is set iff u_e < floor((1 - p) 2^16 + 1/2)
+ * (computed in double from the float p).  Every element is kept independently
+ * with probability 1 - p up to that rounding (2^-16), exactly for p = 0.  The
+ * call uses the counters offset .. offset + ceil(m k / 16) - 1: for a fresh
+ * mask per step, advance offset by that count (or change the seed).
+ *
+ *   seed, offset  generator key word and first counter
+ *   p             dropout rate, 0 <= p < 1 (else LORA_ERR_SHAPE)
+ *   keep          DEVICE buffer of m * k / 8 bytes, 16-byte aligned, written
+ *   m, k          rows and columns of the X the mask is for (k a multiple of 8)
+ * The result depends only on (seed, offset, p, m, k).
+ */
+lora_status lora_dropout_keep_mask(uint64_t seed, uint64_t offset, float p, uint8_t* keep, int64_t m, int64_t k,
+                                   void* stream);
+
+/*
  * Bytes of device workspace lora_linear_bwd needs for this shape (0 on an
  * invalid shape).  The workspace holds transposed and split copies of the
  * rank-r operands and the fixed-order split-K partial sums of dA and dB.
@@ -308,7 +336,8 @@ typedef enum {
   LORA_OP_BWD_FUSED = 4,    /* lora_linear_bwd_fused */
   LORA_OP_MERGE = 5,        /* lora_linear_merge */
   LORA_OP_GROUP_FWD = 6,    /* lora_linear_group_fwd */
-  LORA_OP_GROUP_BWD = 7     /* lora_linear_group_bwd */
+  LORA_OP_GROUP_BWD = 7,    /* lora_linear_group_bwd */
+  LORA_OP_KEEP_MASK = 8     /* lora_dropout_keep_mask (m, k; n and r ignored) */
 } lora_op;
 
 typedef struct {

@@ -35,6 +35,9 @@ The merge of the adapter into the frozen weight (Eq. 1's second form,
 W0 x + B A x = (W0 + B A) x) is W + sign s B A, rounded once to bfloat16
 (nearest-even) for the stored result.
 
+The dropout keep mask the library can draw on the device (Philox4x64-10)
+is evaluated from the generator's published definition in dropout_rng.py.
+
 Each step is one numpy float64 matrix product; there is no blocking, fusion or
 reordering beyond the definition.  The forward and backward are also written
 as plain float64 loops over the index definitions in C (lora_loops.c, loaded
@@ -49,9 +52,11 @@ from .lora_oracle import (bf16_bits_to_f64, lora_scale, lora_rank_activation, lo
                           f64_to_bf16_rne, lora_merged_weight, lora_merge_bf16, dropout_keep,
                           dropped_input, lora_forward_dropout, lora_backward_dropout,
                           lora_group_forward, lora_group_backward)
+from .dropout_rng import philox4x64_10, keep_threshold, dropout_keep_philox
 
 __all__ = ["bf16_bits_to_f64", "lora_scale", "lora_rank_activation", "lora_forward",
            "lora_backward", "lora_forward_rows", "lora_backward_rows", "f64_to_bf16_bits",
            "f64_to_bf16_rne", "lora_merged_weight", "lora_merge_bf16", "dropout_keep",
            "dropped_input", "lora_forward_dropout", "lora_backward_dropout",
-           "lora_group_forward", "lora_group_backward"]
+           "lora_group_forward", "lora_group_backward", "philox4x64_10", "keep_threshold",
+           "dropout_keep_philox"]

@@ -27,7 +27,7 @@ _LIB_NAME = "liblora_linear.so"
 _lib = None
 
 OPS = {"fwd": 0, "fwd_dropout": 1, "bwd": 2, "bwd_dropout": 3, "bwd_fused": 4, "merge": 5,
-       "group_fwd": 6, "group_bwd": 7}
+       "group_fwd": 6, "group_bwd": 7, "keep_mask": 8}
 
 STATUS = {0: "LORA_OK", 1: "LORA_ERR_NULL", 2: "LORA_ERR_SHAPE", 3: "LORA_ERR_ALIGN",
           4: "LORA_ERR_UNSUPPORTED", 5: "LORA_ERR_WORKSPACE", 6: "LORA_ERR_ALIAS", 7: "LORA_ERR_HIP"}
@@ -73,6 +73,9 @@ def load_library() -> ctypes.CDLL:
     lib.lora_linear_bwd_fused.restype = ctypes.c_int
     lib.lora_linear_fwd_dropout.argtypes = [p, p, p, p, p, f32, p, p, i64, i64, i64, i64, f32, p]
     lib.lora_linear_fwd_dropout.restype = ctypes.c_int
+    u64 = ctypes.c_uint64
+    lib.lora_dropout_keep_mask.argtypes = [u64, u64, f32, p, i64, i64, p]
+    lib.lora_dropout_keep_mask.restype = ctypes.c_int
     lib.lora_linear_bwd_dropout.argtypes = [p, p, p, p, p, p, p, f32, p, p, p, p, sz, i64, i64, i64, i64, f32, p]
     lib.lora_linear_bwd_dropout.restype = ctypes.c_int
     lib.lora_linear_merge.argtypes = [p, p, p, p, i64, i64, i64, f32, ctypes.c_int, p]
@@ -226,6 +229,20 @@ def _check_keep(keep, m, k):
     if keep.dtype != torch.uint8 or tuple(keep.shape) != (m, k // 8) or not keep.is_contiguous() \
             or keep.device.type != "cuda":
         raise ValueError(f"keep: expected a contiguous uint8 device tensor of shape {(m, k // 8)}")
+
+
+def lora_dropout_keep_mask(seed: int, offset: int, p: float, keep, stream=None) -> None:
+    """Draw the dropout keep mask on the device (Philox4x64-10, key (seed, 0),
+    counters offset .. offset + keep.numel() - 1; see include/lora_linear.h).
+    keep: contiguous uint8 device tensor [m, k/8], written."""
+    import torch
+    if keep.dtype != torch.uint8 or keep.dim() != 2 or not keep.is_contiguous() or keep.device.type != "cuda":
+        raise ValueError("keep: expected a contiguous uint8 device tensor [m, k/8]")
+    m, k = keep.shape[0], keep.shape[1] * 8
+    st = load_library().lora_dropout_keep_mask(int(seed), int(offset), float(p), _ptr(keep), m, k,
+                                               _stream_handle(stream))
+    if st != 0:
+        raise LoraError(st, "lora_dropout_keep_mask")
 
 
 def lora_linear_fwd_dropout(X, W, A, B, keep, p: float, Y, U, alpha: float, stream=None) -> None:

@@ -17,7 +17,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "liblora_linear.so")
-SOURCES = ["lora_abi.cpp", "lora_fwd.hip", "lora_bwd.hip", "lora_merge.hip"]
+SOURCES = ["lora_abi.cpp", "lora_fwd.hip", "lora_bwd.hip", "lora_merge.hip", "lora_mask.hip"]
 
 
 def hipcc() -> str:

@@ -1,6 +1,7 @@
 // C ABI of the LoRA-linear library: argument validation, workspace sizing and
 // dispatch to the kernel launchers.  Every check runs before the first HIP
 // call, so an invalid call launches nothing and leaves its outputs untouched.
+#include <cmath>
 #include <stdint.h>
 
 #include <new>
@@ -388,6 +389,19 @@ lora_status lora_linear_group_bwd(const lora_bf16* const* dY, const lora_bf16* X
   return e == hipSuccess ? LORA_OK : LORA_ERR_HIP;
 }
 
+lora_status lora_dropout_keep_mask(uint64_t seed, uint64_t offset, float p, uint8_t* keep, int64_t m, int64_t k,
+                                   void* stream) {
+  if (!keep) return LORA_ERR_NULL;
+  lora_status st = check_shape(m, 8, k, 1);
+  if (st != LORA_OK) return st;
+  if (!(p >= 0.0f && p < 1.0f)) return LORA_ERR_SHAPE;
+  if (!aligned16(keep)) return LORA_ERR_ALIGN;
+  lora::MaskArgs a{seed, offset, (uint32_t)std::floor((1.0 - (double)p) * 65536.0 + 0.5), keep, m, k};
+  if (hip_error_pending()) return LORA_ERR_HIP;
+  hipError_t e = lora::launch_keep_mask(a, reinterpret_cast<hipStream_t>(stream));
+  return e == hipSuccess ? LORA_OK : LORA_ERR_HIP;
+}
+
 int64_t lora_linear_plan(lora_op op, int64_t group, const int64_t* n, int64_t m, int64_t k, int64_t r,
                          lora_launch_info* out, int64_t capacity) {
   if (!n || (capacity > 0 && !out)) return -(int64_t)LORA_ERR_NULL;
@@ -414,6 +428,10 @@ int64_t lora_linear_plan(lora_op op, int64_t group, const int64_t* n, int64_t m,
       if (group != 1) return -(int64_t)LORA_ERR_SHAPE;
       st = check_shape(1, n[0], k, r);
       if (st == LORA_OK) p = lora::plan_merge(n[0], k, r);
+      break;
+    case LORA_OP_KEEP_MASK:
+      st = check_shape(m, 8, k, 1);
+      if (st == LORA_OK) p = lora::plan_keep_mask(m, k);
       break;
     case LORA_OP_GROUP_FWD:
     case LORA_OP_GROUP_BWD:

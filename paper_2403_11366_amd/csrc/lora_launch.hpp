@@ -263,6 +263,16 @@ inline GroupBwdLayout group_bwd_layout(int count, const int64_t* n, int64_t m, i
   return G;
 }
 
+// Dropout keep mask drawn on the device (lora_mask.hip).
+struct MaskArgs {
+  uint64_t seed, offset;   // Philox key word 0 and the first counter
+  uint32_t thr;            // keep iff the 16-bit draw is below thr (thr <= 2^16)
+  uint8_t* keep;           // [m, k/8] packed bits
+  int64_t m, k;
+};
+
+hipError_t launch_keep_mask(const MaskArgs& a, hipStream_t st);
+
 struct MergeArgs {
   const uint16_t* W;       // [n, k]
   const uint16_t *A, *B;   // [r, k], [n, r]

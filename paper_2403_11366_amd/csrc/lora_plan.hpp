@@ -24,6 +24,7 @@ enum KernelId : int {
   K_DXF = 6,       // lora_bwd_dxf_kernel<FULL, FASTB>
   K_FINALIZE = 7,  // lora_finalize_kernel
   K_MERGE = 8,     // lora_merge_kernel<RP, 64>
+  K_MASK = 9,      // lora_keep_mask_kernel: the dropout keep mask from the counter-based generator
 };
 
 // One kernel launch.  Fields a kernel does not use stay zero / false.
@@ -289,6 +290,18 @@ inline Plan plan_merge(int64_t n, int64_t k, int64_t r) {
   return p;
 }
 
+// lora_dropout_keep_mask: kMaskBytesPerThread mask bytes (two per generator
+// block) per thread.
+constexpr int kMaskBytesPerThread = 4;
+inline Plan plan_keep_mask(int64_t m, int64_t k) {
+  Plan p;
+  Launch x = blank_launch(K_MASK);
+  x.grid = (m * (k / 8) + kMaskBytesPerThread * 256 - 1) / (kMaskBytesPerThread * 256);
+  x.block = 256;
+  p.add(x);
+  return p;
+}
+
 // The instantiation's name as profilers print it (demangled, without the
 // argument list).
 inline void launch_name(const Launch& x, char* buf, size_t len) {
@@ -317,6 +330,7 @@ inline void launch_name(const Launch& x, char* buf, size_t len) {
     case K_DXF: snprintf(buf, len, "lora::lora_bwd_dxf_kernel<%s, %s>", b(x.full), b(x.fastb)); break;
     case K_FINALIZE: snprintf(buf, len, "lora::lora_finalize_kernel"); break;
     case K_MERGE: snprintf(buf, len, "lora::lora_merge_kernel<%d, %d>", x.rp, kMergeRows); break;
+    case K_MASK: snprintf(buf, len, "lora::lora_keep_mask_kernel"); break;
   }
 }
 

@@ -295,3 +295,21 @@ def test_bwd_fused_validation(lib):
     p = [addr(j) for j in range(10)]
     p[9] = p[2] + 256      # workspace inside W
     assert bwd_fused(lib, p) == 6
+
+
+def test_keep_mask_validation(lib):
+    f = lib.lora_dropout_keep_mask
+    assert f(1, 0, 0.05, None, 64, 64, None) == 1
+    for p in (-0.1, 1.0, 2.0, float("nan")):
+        assert f(1, 0, p, addr(0), 64, 64, None) == 2
+    for m, k in ((0, 64), (64, 0), (64, 12), (-1, 64)):
+        assert f(1, 0, 0.05, addr(0), m, k, None) == 2
+    assert f(1, 0, 0.05, addr(0) + 8, 64, 64, None) == 3   # misaligned
+
+
+def test_keep_mask_plan(lib):
+    plan = lora.lora_linear_plan("keep_mask", 300, 64, 1024, 1)
+    assert [x["kernel"] for x in plan] == ["lora::lora_keep_mask_kernel"]
+    assert plan[0]["grid"] == -(-300 * 128 // (4 * 256)) and plan[0]["block"] == 256
+    with pytest.raises(lora.LoraError):
+        lora.lora_linear_plan("keep_mask", 300, 64, 12, 1)

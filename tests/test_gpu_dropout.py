@@ -16,13 +16,13 @@ from gpu_harness import TOL_DA, TOL_DB, TOL_DX, TOL_U, TOL_Y, f64, rel, run_gpu
 pytestmark = pytest.mark.gpu
 
 
-def run_dropout(t, shape, keep, p):
+def run_dropout(t, shape, keep, p, device_keep=None):
     import torch
     import paper_2403_11366_amd as lora
     from paper_2403_11366_amd.device_io import bits_to_device, device_to_bits
     m, n, k, r = shape.m, shape.n, shape.k, shape.r
     d = {key: bits_to_device(v) for key, v in t.items()}
-    kd = torch.from_numpy(np.ascontiguousarray(keep)).cuda()
+    kd = torch.from_numpy(np.ascontiguousarray(keep)).cuda() if device_keep is None else device_keep
     Y = torch.full((m, n), float("nan"), dtype=torch.bfloat16, device="cuda")
     U = torch.full((m, r), float("nan"), dtype=torch.float32, device="cuda")
     dX = torch.full((m, k), float("nan"), dtype=torch.bfloat16, device="cuda")
@@ -109,3 +109,52 @@ def test_dropout_keep_none():
     out = run_dropout(t, shape, keep, 0.3)
     assert not out["U"].any() and not out["dA"].any() and not out["dB"].any()
     check(t, shape, keep, 0.3, out)
+
+
+# The keep mask drawn on the device (lora_dropout_keep_mask, Philox4x64-10)
+# against the oracle's evaluation of the same generator, bit for bit: ragged
+# byte counts (not a multiple of the 16 bytes a thread writes), a counter
+# that carries into its second word, p = 0, and the 7B q_proj input on
+# sampled rows.
+MASK_CASES = [(300, 1024, 1, 0, 0.05), (37, 72, 2**64 - 1, 2**64 - 5, 0.5), (3, 24, 7, 123, 0.3),
+              (1, 8, 0, 0, 0.0), (129, 4104, 42, 2**40, 0.05), (5, 40, 3, 2**64 - 2, 0.9)]
+
+
+def _device_mask(seed, offset, p, m, k):
+    import torch
+    import paper_2403_11366_amd as lora
+    keep = torch.full((m, k // 8), 0xA5, dtype=torch.uint8, device="cuda")
+    lora.lora_dropout_keep_mask(seed, offset, p, keep)
+    torch.cuda.synchronize()
+    return keep
+
+
+@pytest.mark.parametrize("m,k,seed,offset,p", MASK_CASES)
+def test_device_keep_mask_matches_oracle(m, k, seed, offset, p):
+    print(f"mask m={m} k={k} seed={seed} offset={offset} p={p}", flush=True)
+    got = _device_mask(seed, offset, p, m, k).cpu().numpy()
+    assert np.array_equal(got, oracle.dropout_keep_philox(seed, offset, p, m, k))
+
+
+def test_device_keep_mask_full_size_sampled_rows():
+    from gpu_harness import sample_rows
+    m, k, seed, offset, p = 2048, 4096, 2024, 2**33, 0.05
+    got = _device_mask(seed, offset, p, m, k).cpu().numpy()
+    rows = sample_rows(m, 7)
+    assert np.array_equal(got[rows], oracle.dropout_keep_philox(seed, offset, p, m, k, rows=rows))
+    bits = np.unpackbits(got, bitorder="little")
+    q = oracle.keep_threshold(p) / 2**16
+    assert abs(bits.mean() - q) <= 5 * np.sqrt(q * (1 - q) / bits.size)
+
+
+def test_dropout_step_with_device_mask():
+    """A training step whose mask never leaves the device: the forward and
+    backward read the generated mask, and match the oracle given the oracle's
+    mask of the same (seed, offset, p)."""
+    import torch
+    shape = Shape("drop_dev", 520, 1032, 640, 16, 32.0, 51)
+    p = 0.05
+    keep = oracle.dropout_keep_philox(77, 5000, p, shape.m, shape.k)
+    assert np.array_equal(_device_mask(77, 5000, p, shape.m, shape.k).cpu().numpy(), keep)
+    t = gen_inputs(shape, b_std=0.5)
+    check(t, shape, keep, p, run_dropout(t, shape, keep, p, device_keep=_device_mask(77, 5000, p, shape.m, shape.k)))
