@@ -7,7 +7,11 @@
                     synchronisation) and replayed several times, with eager
                     work and synchronisations between the replays; every
                     replay must reproduce the eager outputs bit for bit,
-                    including after the inputs are overwritten in place.
+                    including after the inputs are overwritten in place; the
+                    same for a dropout step whose mask is drawn on the device
+                    and for a grouped forward and backward.
+  * pending error  -- an HIP error left pending by an earlier call is
+                    reported before anything is enqueued.
 """
 import numpy as np
 import pytest
@@ -152,3 +156,80 @@ def test_pending_hip_error_is_reported_before_anything_is_enqueued():
     assert lib.lora_linear_fwd(*args) == 0
     torch.cuda.synchronize()
     assert not bool((U == -7.0).any())
+
+
+def _bits(x):
+    import torch
+    return x.view(torch.int16) if x.dtype == torch.bfloat16 else (x.view(torch.int32) if x.dtype == torch.float32
+                                                                   else x)
+
+
+def _graph_replays_match_eager(step, outputs, reps=3):
+    """Capture step() (which enqueues on the current stream) into a HIP graph
+    and replay it `reps` times, poisoning every output before each replay with
+    eager work; each replay must reproduce the eager outputs bit for bit."""
+    import torch
+    step()
+    torch.cuda.synchronize()
+    eager = [_bits(x).clone() for x in outputs]
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        with torch.cuda.graph(g, stream=side):
+            step()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    for rep in range(reps):
+        for x in outputs:
+            _bits(x).fill_(-1)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for i, (x, e) in enumerate(zip(outputs, eager)):
+            assert torch.equal(_bits(x), e), f"replay {rep}, output {i}"
+
+
+def test_graph_replays_match_eager_dropout_step_with_device_mask():
+    """A dropout step whose mask is drawn on the device, all three calls in
+    one captured graph."""
+    import torch
+    import paper_2403_11366_amd as lora
+    from paper_2403_11366_amd.device_io import bits_to_device
+    s = Shape("gdrop", 520, 1032, 640, 16, 32.0, 64)
+    t = gen_inputs(s, b_std=0.3)
+    d = {key: bits_to_device(v) for key, v in t.items()}
+    o = _alloc(s)
+    keep = torch.empty((s.m, s.k // 8), dtype=torch.uint8, device="cuda")
+    p = 0.1
+
+    def step():
+        lora.lora_dropout_keep_mask(5, 1 << 20, p, keep)
+        lora.lora_linear_fwd_dropout(d["X"], d["W"], d["A"], d["B"], keep, p, o["Y"], o["U"], s.alpha)
+        lora.lora_linear_bwd_dropout(d["dY"], d["X"], d["W"], d["A"], d["B"], o["U"], keep, p, o["dX"], o["dA"],
+                                     o["dB"], o["ws"], s.alpha)
+    _graph_replays_match_eager(step, [keep, o["Y"], o["U"], o["dX"], o["dA"], o["dB"]])
+
+
+def test_graph_replays_match_eager_grouped_step():
+    """A grouped forward and backward (q, k, v-like, stacked dA reduction) in
+    one captured graph."""
+    import torch
+    import paper_2403_11366_amd as lora
+    from paper_2403_11366_amd.device_io import bits_to_device
+    from lora_synth import gen_group_inputs
+    ns, m, k, r, alpha = [264, 520, 136], 300, 448, 13, 26.0
+    t = gen_group_inputs([Shape(f"gg{i}", m, n, k, r, alpha, 65 + i) for i, n in enumerate(ns)], b_std=0.3)
+    X = bits_to_device(t["X"])
+    dev = {key: [bits_to_device(v) for v in t[key]] for key in ("W", "A", "B", "dY")}
+    Y = [torch.empty((m, n), dtype=torch.bfloat16, device="cuda") for n in ns]
+    U = [torch.empty((m, r), dtype=torch.float32, device="cuda") for _ in ns]
+    dX = torch.empty((m, k), dtype=torch.bfloat16, device="cuda")
+    dA = [torch.empty((r, k), dtype=torch.float32, device="cuda") for _ in ns]
+    dB = [torch.empty((n, r), dtype=torch.float32, device="cuda") for n in ns]
+    ws = torch.empty((lora.lora_linear_group_bwd_workspace_size(ns, m, k, r),), dtype=torch.uint8, device="cuda")
+
+    def step():
+        lora.lora_linear_group_fwd(X, dev["W"], dev["A"], dev["B"], Y, U, alpha)
+        lora.lora_linear_group_bwd(dev["dY"], X, dev["W"], dev["A"], dev["B"], U, dX, dA, dB, ws, alpha)
+    _graph_replays_match_eager(step, Y + U + [dX] + dA + dB)
