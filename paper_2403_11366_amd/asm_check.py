@@ -148,7 +148,7 @@ def count_checked(paths) -> int:
         with open(p) as f:
             text = f.read()
         for chunk in re.split(r"\n(?=_Z\S+:)", text):
-            if re.search(r";;#ASMSTART\s*\n\s*ds_read", chunk):
+            if re.search(r";;#ASMSTART\n(?:(?!;;#ASMEND)[^\n]*\n)*?\s*ds_read", chunk):
                 n += 1
     return n
 

@@ -324,25 +324,91 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
     };
     dload(0, 0);
     copy_barrier<0>();
-    auto dstage = [&](int kb, auto bufc, bool load_next) LORA_INLINE {
-      constexpr int BUF = decltype(bufc)::value;
-      if (load_next) dload(kb + 1, BUF ^ 1);   // read in stage kb-1, free since its barrier
-      const char* sb = smem + BUF * STAGE;
-      read_frags(sb, 0, 0);
+    if constexpr (UPRE) {
+      // Fragment reads as inline assembly, two register sets deep: the reads
+      // of substep ks+1 are issued before the products of substep ks, which
+      // wait (s_waitcnt lgkmcnt) only for their own six reads.  (Left to
+      // itself the compiler folds the two sets into one and waits for each
+      // pair of reads right before its products.)  Chunk c of row p sits at
+      // p*128 | ((c ^ kc_swz(p)) << 4); for the lane's chunk 2ks + g that is
+      // base ^ (ks << 5) with base = p*128 | ((kc_swz(p) ^ g) << 4), and the
+      // fragments of a wave are 32 rows (4096 bytes) apart with the same
+      // swizzle, so one address register per operand and buffer suffices.
+      static_assert(FJ == 2 && FI == 4, "reads per substep");
+      const uint32_t sg = (uint32_t)((kc_swz(c32) ^ g) << 4);
+      const uint32_t wb0 = lds_addr(smem + BM * 128 + (wn * WTJ + c32) * 128) | sg;
+      const uint32_t xb0 = lds_addr(smem + (wm * WTI + c32) * 128) | sg;
+      auto areads = [&](int buf, int ks, int p) LORA_INLINE {   // (ks, buf, p: constants after inlining)
+        const uint32_t wb = wb0 + (uint32_t)buf * STAGE, xb = xb0 + (uint32_t)buf * STAGE;
+        uint32_t ta, tb;
+        asm volatile(
+            "v_xor_b32 %[ta], %[kx], %[wb]\n\t"
+            "v_xor_b32 %[tb], %[kx], %[xb]\n\t"
+            "ds_read_b128 %[w0], %[ta]\n\t"
+            "ds_read_b128 %[w1], %[ta] offset:4096\n\t"
+            "ds_read_b128 %[x0], %[tb]\n\t"
+            "ds_read_b128 %[x1], %[tb] offset:4096\n\t"
+            "ds_read_b128 %[x2], %[tb] offset:8192\n\t"
+            "ds_read_b128 %[x3], %[tb] offset:12288"
+            : [w0] "=v"(fw[p][0]), [w1] "=v"(fw[p][1]), [x0] "=v"(fx[p][0]), [x1] "=v"(fx[p][1]),
+              [x2] "=v"(fx[p][2]), [x3] "=v"(fx[p][3]), [ta] "=&v"(ta), [tb] "=&v"(tb)
+            : [wb] "v"(wb), [xb] "v"(xb), [kx] "i"(ks << 5));
+      };
+      auto amult = [&](int p, bool last) LORA_INLINE {
+        if (last)
+          asm volatile("s_waitcnt lgkmcnt(0)"
+                       : "+v"(fw[p][0]), "+v"(fw[p][1]), "+v"(fx[p][0]), "+v"(fx[p][1]), "+v"(fx[p][2]),
+                         "+v"(fx[p][3]));
+        else
+          asm volatile("s_waitcnt lgkmcnt(6)"
+                       : "+v"(fw[p][0]), "+v"(fw[p][1]), "+v"(fx[p][0]), "+v"(fx[p][1]), "+v"(fx[p][2]),
+                         "+v"(fx[p][3]));
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        if (ks < 3) read_frags(sb, ks + 1, (ks + 1) & 1);
-        multiply(ks & 1, ks);
+        for (int fi = 0; fi < FI; ++fi)
+#pragma unroll
+          for (int fj = 0; fj < FJ; ++fj) acc[fj][fi] = mfma32x32x16(fw[p][fj], fx[p][fi], acc[fj][fi]);
+      };
+      auto astage = [&](int kb, auto bufc, bool load_next) LORA_INLINE {
+        constexpr int BUF = decltype(bufc)::value;
+        if (load_next) dload(kb + 1, BUF ^ 1);   // read in stage kb-1, free since its barrier
+        areads(BUF, 0, 0);
+        areads(BUF, 1, 1);
+        amult(0, false);
+        areads(BUF, 2, 0);
+        amult(1, false);
+        areads(BUF, 3, 1);
+        amult(0, false);
+        amult(1, true);
+        copy_barrier<0>();
+      };
+      int kb = 0;
+      for (; kb + 2 < nkb; kb += 2) {
+        astage(kb, B0{}, true);
+        astage(kb + 1, B1{}, true);
       }
-      copy_barrier<0>();
-    };
-    int kb = 0;
-    for (; kb + 2 < nkb; kb += 2) {
-      dstage(kb, B0{}, true);
-      dstage(kb + 1, B1{}, true);
+      if (kb < nkb) astage(kb, B0{}, kb + 1 < nkb);
+      if (kb + 1 < nkb) astage(kb + 1, B1{}, false);
+    } else {
+      auto dstage = [&](int kb, auto bufc, bool load_next) LORA_INLINE {
+        constexpr int BUF = decltype(bufc)::value;
+        if (load_next) dload(kb + 1, BUF ^ 1);   // read in stage kb-1, free since its barrier
+        const char* sb = smem + BUF * STAGE;
+        read_frags(sb, 0, 0);
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) {
+          if (ks < 3) read_frags(sb, ks + 1, (ks + 1) & 1);
+          multiply(ks & 1, ks);
+        }
+        copy_barrier<0>();
+      };
+      int kb = 0;
+      for (; kb + 2 < nkb; kb += 2) {
+        dstage(kb, B0{}, true);
+        dstage(kb + 1, B1{}, true);
+      }
+      if (kb < nkb) dstage(kb, B0{}, kb + 1 < nkb);
+      if (kb + 1 < nkb) dstage(kb + 1, B1{}, false);
     }
-    if (kb < nkb) dstage(kb, B0{}, kb + 1 < nkb);
-    if (kb + 1 < nkb) dstage(kb + 1, B1{}, false);
   } else {
 #pragma unroll
     for (int pc = 0; pc < 4; ++pc) gload(0, pc);
