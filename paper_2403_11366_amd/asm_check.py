@@ -54,17 +54,7 @@ def _demangle(name: str) -> str:
 def check_function(name: str, lines: list) -> list:
     """Findings for one function's assembly lines (empty if it has no
     inline-asm LDS reads or passes)."""
-    in_asm = False
-    has_asm_reads = False
-    for ln in lines:
-        s = ln.strip()
-        if s.startswith(";;#ASMSTART"):
-            in_asm = True
-        elif s.startswith(";;#ASMEND"):
-            in_asm = False
-        elif in_asm and s.startswith("ds_read"):
-            has_asm_reads = True
-    if not has_asm_reads:
+    if not has_asm_reads(lines):
         return []
     errs = []
     # outstanding LDS operations in issue order: (line, destination registers,
@@ -141,6 +131,20 @@ def check_files(paths) -> list:
     return errs
 
 
+def has_asm_reads(lines) -> bool:
+    """True if an inline-asm block of these assembly lines issues an LDS read."""
+    in_asm = False
+    for ln in lines:
+        s = ln.strip()
+        if s.startswith(";;#ASMSTART"):
+            in_asm = True
+        elif s.startswith(";;#ASMEND"):
+            in_asm = False
+        elif in_asm and s.startswith("ds_read"):
+            return True
+    return False
+
+
 def count_checked(paths) -> int:
     """Number of functions with inline-asm LDS reads in these files."""
     n = 0
@@ -148,7 +152,7 @@ def count_checked(paths) -> int:
         with open(p) as f:
             text = f.read()
         for chunk in re.split(r"\n(?=_Z\S+:)", text):
-            if re.search(r";;#ASMSTART\n(?:(?!;;#ASMEND)[^\n]*\n)*?\s*ds_read", chunk):
+            if has_asm_reads(chunk.split("\n")):
                 n += 1
     return n
 
