@@ -3,6 +3,7 @@
 // call, so an invalid call launches nothing and leaves its outputs untouched.
 #include <cmath>
 #include <stdint.h>
+#include <string.h>
 
 #include <new>
 
@@ -84,7 +85,12 @@ bool all_aligned(const T* const* p, int64_t group) {
 extern "C" {
 
 const char* lora_status_string(lora_status s) {
-  switch (s) {
+  // A C caller may pass any int.  Its bits are read as an int: in C++, loading
+  // a lora_status object that holds a value past the enumerators is undefined.
+  static_assert(sizeof(lora_status) == sizeof(int), "lora_status is int-sized");
+  int code;
+  memcpy(&code, &s, sizeof code);
+  switch (code) {
     case LORA_OK: return "ok";
     case LORA_ERR_NULL: return "null pointer argument";
     case LORA_ERR_SHAPE: return "invalid shape (need m >= 1, n and k >= 8 and multiples of 8, r >= 1; merge sign +1 or -1)";
