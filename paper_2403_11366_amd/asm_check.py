@@ -145,15 +145,17 @@ def has_asm_reads(lines) -> bool:
     return False
 
 
+def count_checked_text(text: str) -> int:
+    """Number of functions with inline-asm LDS reads in one assembly listing."""
+    return sum(1 for chunk in re.split(r"\n(?=_Z\S+:)", text) if has_asm_reads(chunk.split("\n")))
+
+
 def count_checked(paths) -> int:
     """Number of functions with inline-asm LDS reads in these files."""
     n = 0
     for p in paths:
         with open(p) as f:
-            text = f.read()
-        for chunk in re.split(r"\n(?=_Z\S+:)", text):
-            if has_asm_reads(chunk.split("\n")):
-                n += 1
+            n += count_checked_text(f.read())
     return n
 
 

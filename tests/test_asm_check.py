@@ -72,3 +72,28 @@ def test_built_library_assembly_passes():
         pytest.skip("library not built here")
     assert asm_check.check_files(files) == []
     assert asm_check.count_checked(files) >= 1
+
+
+# One asm block that forms its addresses and then issues the reads (the form of
+# the 256x256 forward tile's reads): the reads inside the block are tracked.
+XOR_BLOCK = """
+	;;#ASMSTART
+	v_xor_b32 v2, 32, v1
+	v_xor_b32 v3, 32, v4
+	ds_read_b128 v[10:13], v2
+	ds_read_b128 v[14:17], v2 offset:4096
+	ds_read_b128 v[18:21], v3
+	;;#ASMEND
+	;;#ASMSTART
+	s_waitcnt lgkmcnt(0)
+	;;#ASMEND
+	v_mfma_f32_32x32x16_bf16 v[20:35], v[10:13], v[18:21], v[20:35]
+"""
+
+
+def test_reads_after_address_arithmetic_in_one_block():
+    assert asm_check.check_assembly(_fn(XOR_BLOCK)) == []
+    assert asm_check.count_checked_text(_fn(XOR_BLOCK)) == 1
+    bad = XOR_BLOCK.replace("\t;;#ASMSTART\n\ts_waitcnt lgkmcnt(0)", "\tv_mov_b32_e32 v50, v15\n\t;;#ASMSTART\n\ts_waitcnt lgkmcnt(0)", 1)
+    errs = asm_check.check_assembly(_fn(bad))
+    assert errs and "before its LDS read completed" in errs[0]
