@@ -263,3 +263,20 @@ def test_bench_prices_every_kernel_of_the_single_projection_plans(lora):
                         assert unit is None
                     else:
                         assert unit in ("flop", "byte") and amount > 0, (op, s.name, x["kernel"])
+
+
+def test_traffic_record_only_for_the_sources_it_was_taken_with(monkeypatch):
+    """bench.py reports the committed HBM-traffic record of the dominant
+    forward call only while the forward sources hash to the value the counter
+    runs were taken with; after any change of those sources it reports none."""
+    import json
+    import bench
+    path = bench.traffic_file("llama2_7b_shapes")
+    with open(path) as f:
+        rec = json.load(f)
+    monkeypatch.setattr(bench, "kernel_source_hash", lambda: rec["kernel_source_sha"])
+    got = bench.measured_traffic("llama2_7b_shapes")
+    assert got == pytest.approx(rec["hbm_bytes_per_launch"])
+    monkeypatch.setattr(bench, "kernel_source_hash", lambda: "0" * 16)
+    assert bench.measured_traffic("llama2_7b_shapes") is None
+
