@@ -56,7 +56,9 @@ namespace lora {
 // global memory straight into the free LDS buffer at the top of the stage
 // before it (one 16-byte chunk per lane per copy instruction, the swizzle
 // applied to the global addresses), with no staging registers; the stage's
-// closing barrier waits for those copies (copy_barrier).
+// closing barrier waits for those copies (copy_barrier).  With UPRE as well,
+// the fragment reads are issued as inline assembly, two register sets deep
+// (see the loop below).
 template <int BM, int BN, int WM, int WN, int RP, bool GRP, bool UPRE, bool KFULL, bool DMA>
 __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
     const u16* __restrict__ X, const u16* __restrict__ W, const u16* __restrict__ A,
