@@ -160,10 +160,22 @@ __global__ __launch_bounds__(512) void lora_bwd_du_kernel(
     process(1);
   }
 
-  // U^T of this workgroup's tokens in bf16 (tokens >= m are zero).
-  for (int e = tid; e < RP * TPW; e += 64 * NWV) {
-    const int t = e / TPW, i = i0 + e % TPW;
-    Ut2[(size_t)t * mp + i] = f32_to_bf16((i < m && t < r) ? U[(size_t)i * r + t] : 0.f);
+  // U^T of this workgroup's tokens in bf16 (tokens >= m are zero), all loads
+  // issued before the first store.
+  {
+    constexpr int UPT = (RP * TPW + 64 * NWV - 1) / (64 * NWV);
+    const __amdgpu_buffer_rsrc_t rsU = make_rsrc(U + (size_t)i0 * r, (uint64_t)max(0, min(TPW, m - i0)) * r * 4);
+    float uv[UPT];
+#pragma unroll
+    for (int q = 0; q < UPT; ++q) {
+      const int e = tid + q * 64 * NWV, t = e / TPW, il = e % TPW;
+      uv[q] = buf_load4f(rsU, (e < RP * TPW && t < r) ? (uint32_t)(il * r + t) * 4 : kOOB);
+    }
+#pragma unroll
+    for (int q = 0; q < UPT; ++q) {
+      const int e = tid + q * 64 * NWV, t = e / TPW, i = i0 + e % TPW;
+      if (e < RP * TPW) Ut2[(size_t)t * mp + i] = f32_to_bf16(uv[q]);
+    }
   }
 
   __syncthreads();
@@ -376,10 +388,22 @@ __global__ __launch_bounds__(256) void lora_bwd_du_dma_kernel(
   }
   wait_vmcnt<0>();   // the trailing copies (zeros) land before the LDS is reused
 
-  // U^T of this workgroup's tokens in bf16 (tokens >= m are zero).
-  for (int e = tid; e < RP * TPW; e += 64 * NWV) {
-    const int t = e / TPW, i = i0 + e % TPW;
-    Ut2[(size_t)t * mp + i] = f32_to_bf16((i < m && t < r) ? U[(size_t)i * r + t] : 0.f);
+  // U^T of this workgroup's tokens in bf16 (tokens >= m are zero), all loads
+  // issued before the first store.
+  {
+    constexpr int UPT = (RP * TPW + 64 * NWV - 1) / (64 * NWV);
+    const __amdgpu_buffer_rsrc_t rsU = make_rsrc(U + (size_t)i0 * r, (uint64_t)max(0, min(TPW, m - i0)) * r * 4);
+    float uv[UPT];
+#pragma unroll
+    for (int q = 0; q < UPT; ++q) {
+      const int e = tid + q * 64 * NWV, t = e / TPW, il = e % TPW;
+      uv[q] = buf_load4f(rsU, (e < RP * TPW && t < r) ? (uint32_t)(il * r + t) * 4 : kOOB);
+    }
+#pragma unroll
+    for (int q = 0; q < UPT; ++q) {
+      const int e = tid + q * 64 * NWV, t = e / TPW, i = i0 + e % TPW;
+      if (e < RP * TPW) Ut2[(size_t)t * mp + i] = f32_to_bf16(uv[q]);
+    }
   }
 
   __syncthreads();
@@ -1471,12 +1495,23 @@ __global__ __launch_bounds__(512) void lora_bwd_dxf_kernel(
   // U^T of the tile's tokens: high parts in rows 0..15, low parts in rows
   // 16..31 (zero beyond r and m), for the dB products.
   char* Uts = smem + UT_OFF;
-  for (int e = tid; e < BM * RP; e += NT) {
-    const int i = e / RP, t = e - i * RP;
-    const float v = (m0 + i < m && t < r) ? U[(size_t)(m0 + i) * r + t] : 0.f;
-    const u16 h = f32_to_bf16(v);
-    *reinterpret_cast<u16*>(Uts + t * UTP + i * 2) = h;
-    *reinterpret_cast<u16*>(Uts + (RP + t) * UTP + i * 2) = f32_to_bf16(v - bf16_to_f32(h));
+  {
+    constexpr int UPT = BM * RP / NT;   // all loads issued before the first store
+    static_assert(BM * RP % NT == 0, "U values per thread");
+    const __amdgpu_buffer_rsrc_t rsU = make_rsrc(U + (size_t)m0 * r, (uint64_t)min(BM, m - m0) * r * 4);
+    float uv[UPT];
+#pragma unroll
+    for (int q = 0; q < UPT; ++q) {
+      const int e = tid + q * NT, i = e / RP, t = e - i * RP;
+      uv[q] = buf_load4f(rsU, t < r ? (uint32_t)(i * r + t) * 4 : kOOB);
+    }
+#pragma unroll
+    for (int q = 0; q < UPT; ++q) {
+      const int e = tid + q * NT, i = e / RP, t = e - i * RP;
+      const u16 h = f32_to_bf16(uv[q]);
+      *reinterpret_cast<u16*>(Uts + t * UTP + i * 2) = h;
+      *reinterpret_cast<u16*>(Uts + (RP + t) * UTP + i * 2) = f32_to_bf16(uv[q] - bf16_to_f32(h));
+    }
   }
 
   // Staging registers, stored in pieces: 0 = the dY rows and (threads below

@@ -132,6 +132,11 @@ __device__ __forceinline__ void ds_read_b128_asm(short8& d, uint32_t addr) {
   asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(d) : "v"(addr), "i"(OFF));
 }
 
+// 4-byte load through a buffer resource; out-of-range offsets read as zero.
+__device__ __forceinline__ float buf_load4f(__amdgpu_buffer_rsrc_t rs, uint32_t byte_off) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, byte_off, 0, 0));
+}
+
 // 8-byte load through a buffer resource (byte_off a multiple of 8).
 __device__ __forceinline__ uint2 buf_load8(__amdgpu_buffer_rsrc_t rs, uint32_t byte_off) {
   const auto v = __builtin_amdgcn_raw_buffer_load_b64(rs, byte_off, 0, 0);

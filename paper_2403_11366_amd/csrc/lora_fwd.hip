@@ -453,10 +453,20 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
     const int q = tid + i * NT;
     bv[i] = buf_load16(rsB, q < nch ? (uint32_t)q * 16 : kOOB);
   }
-  if (UPRE) {   // U of the tile's tokens from the U pass (zero beyond r and m)
-    for (int e = tid; e < BM * RP; e += NT) {
-      const int il = e / RP, t = e - il * RP;
-      Us[il * RPU + t] = (m0 + il < m && t < r) ? U[(size_t)(m0 + il) * r + t] : 0.f;
+  if (UPRE) {   // U of the tile's tokens from the U pass (zero beyond r and m), all loads issued before the first use
+    constexpr int UPT = BM * RP / NT;
+    static_assert(BM * RP % NT == 0, "U values per thread");
+    const __amdgpu_buffer_rsrc_t rsU = make_rsrc(U + (size_t)m0 * r, (uint64_t)min(BM, m - m0) * r * 4);
+    float uv[UPT];
+#pragma unroll
+    for (int i = 0; i < UPT; ++i) {
+      const int e = tid + i * NT, il = e / RP, t = e - il * RP;
+      uv[i] = buf_load4f(rsU, t < r ? (uint32_t)(il * r + t) * 4 : kOOB);
+    }
+#pragma unroll
+    for (int i = 0; i < UPT; ++i) {
+      const int e = tid + i * NT, il = e / RP, t = e - il * RP;
+      Us[il * RPU + t] = uv[i];
     }
   } else if (U16) {   // lane holds token column c16 of its group, U rows t = 4 g16 .. +3
 #pragma unroll
@@ -1071,11 +1081,18 @@ __global__ __launch_bounds__(512) void lora_fwd_ks_kernel(
           }
         }
   }
-  if (UPRE) {   // U of the tile's tokens from the U pass (zero beyond r and m)
-    for (int e = tid; e < BM * RP; e += NT) {
-      const int il = e / RP, t = e - il * RP;
-      Us[e] = (m0 + il < m && t < r) ? U[(size_t)(m0 + il) * r + t] : 0.f;
+  if (UPRE) {   // U of the tile's tokens from the U pass (zero beyond r and m), all loads issued before the first use
+    constexpr int UPT = BM * RP / NT;
+    static_assert(BM * RP % NT == 0, "U values per thread");
+    const __amdgpu_buffer_rsrc_t rsU = make_rsrc(U + (size_t)m0 * r, (uint64_t)min(BM, m - m0) * r * 4);
+    float uv[UPT];
+#pragma unroll
+    for (int i = 0; i < UPT; ++i) {
+      const int e = tid + i * NT, il = e / RP, t = e - il * RP;
+      uv[i] = buf_load4f(rsU, t < r ? (uint32_t)(il * r + t) * 4 : kOOB);
     }
+#pragma unroll
+    for (int i = 0; i < UPT; ++i) Us[tid + i * NT] = uv[i];
   } else {
     // (the partial of half 1 is read here and written before the barrier above)
     for (int e = tid; e < BM * RP; e += NT) Us[e] = Us[e] + Us[BM * RP + e];
