@@ -586,22 +586,26 @@ __global__ __launch_bounds__(64 * WM * WN) void lora_fwd_kernel(
 // over its stages (16x16x32 products; under KEEP each X fragment of 8 k is
 // masked with its keep byte first); the four partial sums are added in wave
 // order through LDS at the end (bit-identical from run to run) and written
-// as fp32 U [m][r], scaled by inv_keep under KEEP.
+// as fp32 U [m][r], scaled by inv_keep under KEEP.  With TPW = 8 (launches
+// whose 16-token workgroups would leave compute units idle) a stage still
+// holds 16 X rows for the 16-token products; rows 8..15 are zeroed once and
+// never copied into, and only the first 8 tokens' U is written.
 template <int RP, int TPW, bool KEEP>
 __global__ __launch_bounds__(256) void lora_u_kernel(const u16* __restrict__ X, const u16* __restrict__ A,
                                                      const uint8_t* __restrict__ keep, float* __restrict__ U, int m,
                                                      int k, int r, float inv_keep) {
   constexpr int NWV = 4;
-  constexpr int ROWS = TPW + RP;                 // 128-byte rows per stage: X rows, then A rows
+  constexpr int XR = TPW < 16 ? 16 : TPW;        // X rows of a stage (rows TPW .. XR-1 stay zero)
+  constexpr int ROWS = XR + RP;                  // 128-byte rows per stage: X rows, then A rows
   constexpr int MOFF = ROWS * 128;               // keep bytes of the stage: [TPW][8]
   constexpr int STAGE = MOFF + (KEEP ? 256 : 0);
-  constexpr int CPS = ROWS / 8;                  // 1 KB copies per stage
+  constexpr int CPS = (TPW + RP) / 8;            // 1 KB copies per stage
   constexpr int CPW = CPS + (KEEP ? 1 : 0);      // copy instructions per stage (the wave's own)
   constexpr int NSW = (156 * 1024) / (NWV * STAGE) < 6 ? (156 * 1024) / (NWV * STAGE) : 6;   // ring stages per wave
-  constexpr int FT = RP / 16, TG = TPW / 16;
+  constexpr int FT = RP / 16, TG = XR / 16;
   constexpr int RED = NWV * FT * TG * 64 * 16;   // cross-wave sum: [NWV][FT][TG][64] float4
   constexpr int SMEM = NWV * NSW * STAGE > RED ? NWV * NSW * STAGE : RED;
-  static_assert(TPW == 16 || TPW == 32, "tokens per workgroup");
+  static_assert(TPW == 8 || TPW == 16 || TPW == 32, "tokens per workgroup");
   static_assert(NSW >= 3 && CPW * (NSW - 2) < 64, "copies in flight fit the wait counter");
   static_assert(FT * TG <= 8, "fragments per wave");
   __shared__ __attribute__((aligned(1024))) char smem[SMEM];
@@ -617,9 +621,11 @@ __global__ __launch_bounds__(256) void lora_u_kernel(const u16* __restrict__ X, 
       make_rsrc(KEEP ? (const void*)(keep + (size_t)i0 * kb8) : (const void*)X, KEEP ? (uint64_t)rows * kb8 : 0);
   char* ring = smem + wave * NSW * STAGE;
 
-  // Copy c of a stage fills its rows 8c .. 8c+7: this lane's row 8c + lane/8
-  // at physical chunk lane%8, which holds logical chunk (lane%8) ^ kc_swz(row).
-  // Rows past m or r, k past the end and stages past the wave's last read zero.
+  // Copy c of a stage fills 8 rows: X rows 8c .. 8c+7 (8c < TPW), else A rows
+  // 8c - TPW .. +7 at stage rows XR + 8c - TPW ..; this lane's row lane/8 of
+  // the eight at physical chunk lane%8, which holds logical chunk
+  // (lane%8) ^ kc_swz(stage row).  Rows past m or r, k past the end and stages
+  // past the wave's last read zero.
   const int c8 = lane & 7, r8 = lane >> 3;
   const int nst = (k + 63) / 64;
   auto issue = [&](int j, int buf) LORA_INLINE {   // the wave's j-th stage
@@ -629,12 +635,13 @@ __global__ __launch_bounds__(256) void lora_u_kernel(const u16* __restrict__ X, 
     char* sb = ring + buf * STAGE;
 #pragma unroll
     for (int c = 0; c < CPS; ++c) {
-      const int row = 8 * c + r8;
-      const int lc = c8 ^ kc_swz(row);
       const bool isx = 8 * c < TPW;   // uniform
+      const int row = 8 * c + r8;
+      const int srow = isx ? row : row + (XR - TPW);   // stage row
+      const int lc = c8 ^ kc_swz(srow);
       const int grow = isx ? row : row - TPW;
       const uint32_t off = live && k0 + 8 * lc < k ? (uint32_t)grow * rowbytes + (uint32_t)(k0 + 8 * lc) * 2 : kOOB;
-      dma16(isx ? rsX : rsA, off, 0, sb + c * 1024);
+      dma16(isx ? rsX : rsA, off, 0, sb + (isx ? c : c + (XR - TPW) / 8) * 1024);
     }
     if (KEEP)   // lane l: bytes 4 (l % 2) .. +3 of token l / 2's stage bits (lanes past TPW tokens: zero)
       dma4(rsK, live && (lane >> 1) < TPW ? (uint32_t)(lane >> 1) * kb8 + (uint32_t)k0 / 8 + 4 * (lane & 1) : kOOB,
@@ -657,7 +664,7 @@ __global__ __launch_bounds__(256) void lora_u_kernel(const u16* __restrict__ X, 
         if constexpr (KEEP) xf[tg] = keep_mask8(xf[tg], (uint32_t)(uint8_t)sb[MOFF + (16 * tg + c16) * 8 + ch]);
       }
 #pragma unroll
-      for (int ft = 0; ft < FT; ++ft) af[ft] = kc_read(sb, TPW + 16 * ft + c16, ch);
+      for (int ft = 0; ft < FT; ++ft) af[ft] = kc_read(sb, XR + 16 * ft + c16, ch);
 #pragma unroll
       for (int ft = 0; ft < FT; ++ft)
 #pragma unroll
@@ -666,6 +673,11 @@ __global__ __launch_bounds__(256) void lora_u_kernel(const u16* __restrict__ X, 
   };
 
   const int nsw = wave < nst ? (nst - wave + NWV - 1) / NWV : 0;   // this wave's stages
+  if constexpr (TPW < 16) {   // the zero X rows TPW .. 15 of every ring stage (8 rows: 16 bytes a lane)
+    static_assert(TPW == 8, "one 1 KB block of zero rows");
+#pragma unroll
+    for (int b = 0; b < NSW; ++b) *reinterpret_cast<int4v*>(ring + b * STAGE + TPW * 128 + lane * 16) = int4v{0, 0, 0, 0};
+  }
 #pragma unroll
   for (int j = 0; j < NSW - 1; ++j) issue(j, j);
   for (int j = 0; j < nsw; ++j) {
@@ -690,7 +702,7 @@ __global__ __launch_bounds__(256) void lora_u_kernel(const u16* __restrict__ X, 
 #pragma unroll
     for (int w = 1; w < NWV; ++w) v += red[((w * FT + ft) * TG + tg) * 64 + lane];
     const int i = i0 + 16 * tg + c16;
-    if (i < m) {
+    if (i < m && 16 * tg + c16 < TPW) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int t = 16 * ft + 4 * g + j;
@@ -1167,7 +1179,7 @@ static hipError_t run_fwd_launch(const Launch& L, const FwdArgs& a, const FwdGro
   const dim3 grid((unsigned)L.grid), block((unsigned)L.block);
   if (L.id == K_UPASS) {
     return with_int<16, 32, 64>(L.rp, [&](auto rc) {
-      return with_int<16, 32>(L.tpw, [&](auto tc) {
+      return with_int<8, 16, 32>(L.tpw, [&](auto tc) {
         return with_bool(L.drop, [&](auto kc) {
           hipLaunchKernelGGL((lora_u_kernel<decltype(rc)::value, decltype(tc)::value, decltype(kc)::value>), grid,
                              block, 0, st, a.X, a.A, a.keep, a.U, (int)a.m, (int)a.k, (int)a.r, a.inv_keep);

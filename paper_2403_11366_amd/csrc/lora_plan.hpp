@@ -100,8 +100,8 @@ inline void plan_fwd_part(Plan& p, GemmTile t, int64_t m, int64_t k, int64_t r, 
     u.rp = fwd_rank(r);
     u.drop = drop;
     // 32 tokens per workgroup (A read half as often) unless that leaves
-    // compute units idle
-    u.tpw = (m + 31) / 32 >= 256 ? 32 : 16;
+    // compute units idle, then 16, then 8
+    u.tpw = (m + 31) / 32 >= 256 ? 32 : ((m + 15) / 16 >= 256 ? 16 : 8);
     u.grid = (m + u.tpw - 1) / u.tpw;
     u.block = 256;
     p.add(u);

@@ -67,7 +67,10 @@ SHAPES = [Shape("drop_tiny", 256, 512, 512, 8, 16.0, 21), Shape("drop_ragged", 2
           Shape("drop_dx256_r33", 300, 136, 11008, 33, 66.0, 47),
           Shape("drop_dx256f_r33", 300, 64, 11008, 33, 66.0, 48),
           Shape("drop_dx256_r64", 300, 136, 11008, 64, 128.0, 49),
-          Shape("drop_dx256f_r64", 300, 64, 11008, 64, 128.0, 50)]
+          Shape("drop_dx256f_r64", 300, 64, 11008, 64, 128.0, 50),
+          # U pass with 16-token workgroups (4096 <= m < 8192; smaller m takes 8-token ones)
+          Shape("drop_m4100", 4100, 136, 128, 8, 16.0, 51), Shape("drop_m4100_r24", 4100, 136, 128, 24, 48.0, 52),
+          Shape("drop_m4096_r64", 4096, 128, 192, 64, 128.0, 53)]
 
 
 @pytest.mark.parametrize("shape", SHAPES, ids=lambda s: s.name)

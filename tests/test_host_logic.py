@@ -94,9 +94,11 @@ def test_dropout_forward_is_masked_u_pass_then_plain_tiles(lora, s):
 
 def test_dropout_suite_reaches_every_dropout_forward_variant(lora):
     seen = {x["kernel"] for s in DROP_SHAPES for x in lora.lora_linear_plan("fwd_dropout", s.m, s.n, s.k, s.r)}
-    for want in ("lora::lora_u_kernel<16, 16, true>", "lora::lora_u_kernel<16, 32, true>",
+    for want in ("lora::lora_u_kernel<16, 8, true>", "lora::lora_u_kernel<16, 16, true>",
+                 "lora::lora_u_kernel<16, 32, true>", "lora::lora_u_kernel<32, 8, true>",
                  "lora::lora_u_kernel<32, 16, true>", "lora::lora_u_kernel<32, 32, true>",
-                 "lora::lora_u_kernel<64, 16, true>", "lora::lora_u_kernel<64, 32, true>",
+                 "lora::lora_u_kernel<64, 8, true>", "lora::lora_u_kernel<64, 16, true>",
+                 "lora::lora_u_kernel<64, 32, true>",
                  "lora::lora_fwd_ks_kernel<false, true, true, true>",
                  "lora::lora_fwd_ks_kernel<false, true, false, true>",
                  "lora::lora_fwd_kernel<256, 256, 2, 4, 16, false, true, true, true>",
@@ -106,7 +108,8 @@ def test_dropout_suite_reaches_every_dropout_forward_variant(lora):
 
 def test_parity_suites_reach_every_plain_u_pass(lora):
     seen = {x["kernel"] for s in SINGLE for x in lora.lora_linear_plan("fwd", s.m, s.n, s.k, s.r)}
-    for want in ("lora::lora_u_kernel<32, 16, false>", "lora::lora_u_kernel<32, 32, false>",
+    for want in ("lora::lora_u_kernel<32, 8, false>", "lora::lora_u_kernel<32, 16, false>",
+                 "lora::lora_u_kernel<32, 32, false>", "lora::lora_u_kernel<64, 8, false>",
                  "lora::lora_u_kernel<64, 16, false>", "lora::lora_u_kernel<64, 32, false>"):
         assert want in seen, (want, sorted(x for x in seen if "u_kernel" in x))
 
