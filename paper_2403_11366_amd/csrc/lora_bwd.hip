@@ -42,6 +42,27 @@ __device__ __forceinline__ short8 tr16_read(const char* tile, int pitch, int col
                __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4v*)(p0 + 4 * pitch)));
 }
 
+// U^T of the tokens i0 .. i0+TPW-1 rounded to bf16 into Ut2 [RP][mp] (tokens
+// at or past m and ranks at or past r zero), by NTH threads; each thread
+// issues all of its loads before its first store.
+template <int RP, int TPW, int NTH>
+__device__ __forceinline__ void store_ut2(const float* __restrict__ U, u16* __restrict__ Ut2, int i0, int m, int r,
+                                          int mp, int tid) {
+  constexpr int UPT = (RP * TPW + NTH - 1) / NTH;
+  const __amdgpu_buffer_rsrc_t rsU = make_rsrc(U + (size_t)i0 * r, (uint64_t)max(0, min(TPW, m - i0)) * r * 4);
+  float uv[UPT];
+#pragma unroll
+  for (int q = 0; q < UPT; ++q) {
+    const int e = tid + q * NTH, t = e / TPW, il = e % TPW;
+    uv[q] = buf_load4f(rsU, (e < RP * TPW && t < r) ? (uint32_t)(il * r + t) * 4 : kOOB);
+  }
+#pragma unroll
+  for (int q = 0; q < UPT; ++q) {
+    const int e = tid + q * NTH, t = e / TPW;
+    if (e < RP * TPW) Ut2[(size_t)t * mp + i0 + e % TPW] = f32_to_bf16(uv[q]);
+  }
+}
+
 // ---------------------------------------------------------------------------
 // dU = s dY B for TPW (8, 16 or 32) tokens per workgroup, reducing over all
 // of n, plus the U^T high/low split of the same tokens.  The launch takes the
@@ -160,23 +181,7 @@ __global__ __launch_bounds__(512) void lora_bwd_du_kernel(
     process(1);
   }
 
-  // U^T of this workgroup's tokens in bf16 (tokens >= m are zero), all loads
-  // issued before the first store.
-  {
-    constexpr int UPT = (RP * TPW + 64 * NWV - 1) / (64 * NWV);
-    const __amdgpu_buffer_rsrc_t rsU = make_rsrc(U + (size_t)i0 * r, (uint64_t)max(0, min(TPW, m - i0)) * r * 4);
-    float uv[UPT];
-#pragma unroll
-    for (int q = 0; q < UPT; ++q) {
-      const int e = tid + q * 64 * NWV, t = e / TPW, il = e % TPW;
-      uv[q] = buf_load4f(rsU, (e < RP * TPW && t < r) ? (uint32_t)(il * r + t) * 4 : kOOB);
-    }
-#pragma unroll
-    for (int q = 0; q < UPT; ++q) {
-      const int e = tid + q * 64 * NWV, t = e / TPW, i = i0 + e % TPW;
-      if (e < RP * TPW) Ut2[(size_t)t * mp + i] = f32_to_bf16(uv[q]);
-    }
-  }
+  store_ut2<RP, TPW, 64 * NWV>(U, Ut2, i0, m, r, mp, tid);   // U^T of this workgroup's tokens in bf16
 
   __syncthreads();
   floatx4* red = reinterpret_cast<floatx4*>(sm);   // [NWV][TG][FT][64]
@@ -388,23 +393,7 @@ __global__ __launch_bounds__(256) void lora_bwd_du_dma_kernel(
   }
   wait_vmcnt<0>();   // the trailing copies (zeros) land before the LDS is reused
 
-  // U^T of this workgroup's tokens in bf16 (tokens >= m are zero), all loads
-  // issued before the first store.
-  {
-    constexpr int UPT = (RP * TPW + 64 * NWV - 1) / (64 * NWV);
-    const __amdgpu_buffer_rsrc_t rsU = make_rsrc(U + (size_t)i0 * r, (uint64_t)max(0, min(TPW, m - i0)) * r * 4);
-    float uv[UPT];
-#pragma unroll
-    for (int q = 0; q < UPT; ++q) {
-      const int e = tid + q * 64 * NWV, t = e / TPW, il = e % TPW;
-      uv[q] = buf_load4f(rsU, (e < RP * TPW && t < r) ? (uint32_t)(il * r + t) * 4 : kOOB);
-    }
-#pragma unroll
-    for (int q = 0; q < UPT; ++q) {
-      const int e = tid + q * 64 * NWV, t = e / TPW, i = i0 + e % TPW;
-      if (e < RP * TPW) Ut2[(size_t)t * mp + i] = f32_to_bf16(uv[q]);
-    }
-  }
+  store_ut2<RP, TPW, 64 * NWV>(U, Ut2, i0, m, r, mp, tid);   // U^T of this workgroup's tokens in bf16
 
   __syncthreads();
   floatx4* red = reinterpret_cast<floatx4*>(sm);   // [NWV][TG][FT][64]
